@@ -1,0 +1,206 @@
+/*
+ * fairy2i.h -- C ABI of the MI355X (gfx950) library for the Fairy2i
+ * quantised widely-linear layer (arXiv 2512.02901).
+ *
+ * The layer: a real linear map y~ = A x~ with A in R^{2N x 2K} (Sec. 3.1,
+ * real-layer equation) is rewritten exactly as y = U x + W conj(x) with
+ * U, W in C^{N x K} (Sec. 3.1, Eq. UW-from-R and the exact-equivalence
+ * theorem).  U and W are quantised independently (Sec. 3.3, last paragraph)
+ * by T stages of recursive residual PhaseQuant (Sec. 3.2 Eq. ifairy-proj,
+ * ifairy-scale, ifairy-dequant; Sec. 3.3 formal definition) to 2-bit codes
+ * over {+1, +i, -1, -i} with one (s_re, s_im) pair per matrix and stage.
+ * Inference computes y = sum_t (U^(t) x + W^(t) conj(x)) from the codes
+ * without multiplying by weights (Sec. 3.4, Algorithm 1, extended here with
+ * the W conj(x) term and a batch of tokens).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - N is the complex output dimension, K the complex input dimension; the
+ *    real layer is 2N x 2K.  Real vectors pair as stacked halves:
+ *    x~ = [Re x ; Im x] (Sec. 3.1).
+ *  - Every pointer argument is DEVICE memory, owned and allocated by the
+ *    caller; the library never keeps a pointer after the call returns and
+ *    never allocates, frees or synchronises.
+ *  - `stream` is a borrowed hipStream_t (NULL = the default stream); all
+ *    work is enqueued on it and the call returns without waiting.
+ *  - Argument checks run on the host before anything is enqueued; a failed
+ *    check returns its status and enqueues nothing.  A HIP launch error
+ *    returns FAIRY2I_ERR_HIP.  No exception or abort crosses the ABI.
+ *  - Complex arrays are interleaved (re, im) float pairs, row-major
+ *    (the memory of torch.complex64).
+ *  - Codes: code k in {0,1,2,3} stands for the codeword i^k
+ *    (0 -> +1, 1 -> +i, 2 -> -1, 3 -> -i).  Packed layout per matrix:
+ *    uint8 codes[T][N][K/4]; code (t, i, j) is in byte (i*K + j)/4 at bits
+ *    2*(j%4) and 2*(j%4)+1.  T*N*K/4 bytes per matrix, i.e. T bits per real
+ *    parameter for the pair (Sec. 3.4, storage paragraph).
+ *  - Scales: float32 scales[T][2] = (s_re, s_im) per matrix.
+ *  - Calls are stateless and may be issued from several host threads.
+ */
+#ifndef FAIRY2I_H
+#define FAIRY2I_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t fairy2i_status;
+
+enum {
+  FAIRY2I_OK = 0,
+  FAIRY2I_ERR_NULL = 1,        /* a required pointer is NULL               */
+  FAIRY2I_ERR_SHAPE = 2,       /* a dimension is out of range              */
+  FAIRY2I_ERR_STAGES = 3,      /* T outside [1, FAIRY2I_MAX_STAGES]        */
+  FAIRY2I_ERR_DTYPE = 4,       /* unknown activation dtype                 */
+  FAIRY2I_ERR_UNSUPPORTED = 5, /* valid but not implemented combination    */
+  FAIRY2I_ERR_WORKSPACE = 6,   /* workspace missing or too small           */
+  FAIRY2I_ERR_HIP = 7          /* a HIP runtime call or launch failed      */
+};
+
+/* Activation element types for fairy2i_wl_matmul / fairy2i_quantize_act_int8. */
+enum {
+  FAIRY2I_ACT_F32 = 0,  /* float32 pairs (re, im): B*K*2 floats            */
+  FAIRY2I_ACT_BF16 = 1, /* bf16 pairs (re, im): B*K*2 uint16 bf16 patterns  */
+  FAIRY2I_ACT_I8 = 2    /* int8 pairs (re, im): B*K*2 int8, plus a float32
+                           dequantisation factor per token                  */
+};
+
+#define FAIRY2I_MAX_STAGES 4
+/* Largest token count served by the decode kernels for float activations;
+ * larger batches need int8 activations (the prefill GEMM). */
+#define FAIRY2I_MAX_DECODE_BATCH 16
+/* Largest N*K (complex entries per matrix) the quantiser accepts. */
+#define FAIRY2I_MAX_QUANTIZE_ENTRIES ((int64_t)1 << 31)
+
+/* Human-readable name of a status code (static storage, never NULL). */
+const char* fairy2i_status_string(fairy2i_status status);
+
+/* Version of this ABI (incremented on any incompatible change). */
+int32_t fairy2i_abi_version(void);
+
+/*
+ * Real layer -> widely-linear pair.  Sec. 3.1, Eq. (UW-from-R):
+ *   R11 = A[:N,:K], R12 = A[:N,K:], R21 = A[N:,:K], R22 = A[N:,K:],
+ *   Re U = (R11+R22)/2, Im U = (R21-R12)/2, Re W = (R11-R22)/2, Im W = (R12+R21)/2.
+ * A: float32 [rows][cols] row-major, rows = 2N (outputs), cols = 2K (inputs).
+ * U, W: complex64 [N][K] outputs; each component is the exact value rounded
+ * once to float32.  rows and cols must be even and > 0 (the paper pads an odd
+ * dimension with a zero channel: Sec. 3.1 remarks; the caller does that).
+ * Errors: NULL pointer -> FAIRY2I_ERR_NULL; odd or non-positive dims ->
+ * FAIRY2I_ERR_SHAPE.
+ */
+fairy2i_status fairy2i_to_widely_linear(const float* A, int64_t rows, int64_t cols,
+                                        float* U, float* W, void* stream);
+
+/* Bytes of device workspace fairy2i_quantize needs for an N x K matrix. */
+size_t fairy2i_quantize_workspace_bytes(int64_t N, int64_t K, int32_t T);
+
+/*
+ * Recursive residual PhaseQuant of ONE complex matrix (call it once for U and
+ * once for W).  Sec. 3.3 formal definition, with Sec. 3.2:
+ *   R(0) = M;  for t < T:
+ *     k(t)  = code of the nearest codeword by angle (Eq. ifairy-proj; ties
+ *             take the floor form's counter-clockwise codeword, 0 -> +1),
+ *     s_re  = mean |Re r| over entries coded +-1, s_im = mean |Im r| over
+ *             entries coded +-i (Eq. ifairy-scale, per tensor); each mean is
+ *             computed exactly and rounded once to float32; 0 if empty,
+ *     R(t+1) = R(t) - (s_re b_re + i s_im b_im) with the stored float32
+ *             scales, carried in float64.
+ * M: complex64 [N][K] input.  codes: uint8 [T][N][K/4] output (packed
+ * layout above).  scales: float32 [T][2] output.  workspace: device buffer
+ * of at least fairy2i_quantize_workspace_bytes(N, K, T) bytes, contents
+ * ignored on entry.  Results are bitwise deterministic.
+ * Errors: FAIRY2I_ERR_NULL; FAIRY2I_ERR_SHAPE if N, K <= 0, K % 4 != 0 or
+ * N*K > FAIRY2I_MAX_QUANTIZE_ENTRIES; FAIRY2I_ERR_STAGES; FAIRY2I_ERR_WORKSPACE.
+ */
+fairy2i_status fairy2i_quantize(const float* M, int64_t N, int64_t K, int32_t T,
+                                uint8_t* codes, float* scales,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Per-token int8 activations (the paper names INT8 activations for its
+ * look-up-table inference paragraph in Sec. 3.4 without defining the
+ * quantiser; this is the library's definition).  For token b, in float32:
+ *   g = max over the 2K real components |x|,  inv = 127 / g (IEEE division),
+ *   q = clamp(rint(x * inv), -127, 127)  (round half to even),
+ *   x_scale[b] = g / 127;  g = 0 gives q = 0 and x_scale = 0.
+ * x: B*K*2 values of `dtype` (FAIRY2I_ACT_F32 or FAIRY2I_ACT_BF16),
+ * interleaved (re, im).  q: int8 [B][K][2] output.  x_scale: float32 [B].
+ * Errors: FAIRY2I_ERR_NULL; FAIRY2I_ERR_SHAPE if B or K <= 0;
+ * FAIRY2I_ERR_DTYPE for any other dtype.
+ */
+fairy2i_status fairy2i_quantize_act_int8(const void* x, int32_t dtype, int64_t B, int64_t K,
+                                         int8_t* q, float* x_scale, void* stream);
+
+/* Bytes of device workspace fairy2i_wl_matmul needs (0 if none). */
+size_t fairy2i_wl_matmul_workspace_bytes(int64_t N, int64_t K, int32_t T, int64_t B,
+                                         int32_t dtype);
+
+/*
+ * Quantised widely-linear product for a batch of B tokens (Sec. 3.4,
+ * Algorithm 1, read with the dequantisation of Eq. ifairy-dequant and the
+ * deployed sum of Eq. res-sum, and with the W conj(x) term of
+ * Eq. widely-linear):
+ *   y[b] = sum_t ( U^(t) x_b + W^(t) conj(x_b) ),
+ *   U^(t) = s^U_re(t) B_re(t) + i s^U_im(t) B_im(t)   (W^(t) likewise).
+ * codes_U, codes_W: uint8 [T][N][K/4]; scales_U, scales_W: float32 [T][2].
+ * x: B*K*2 activations of `dtype`, interleaved (re, im).  For
+ * FAIRY2I_ACT_I8, x_scale is float32 [B] (dequantisation factor per token,
+ * as produced by fairy2i_quantize_act_int8) and y[b] is multiplied by it;
+ * for the float dtypes x_scale must be NULL.
+ * y: complex64 [B][N] output.
+ * Accumulation is in float32 (float activations) or exact int32 (int8
+ * activations), with a fixed summation order: results are bitwise
+ * reproducible run to run.
+ * B <= FAIRY2I_MAX_DECODE_BATCH runs the decode kernel; larger B needs
+ * FAIRY2I_ACT_I8 and runs the int8-MFMA prefill kernel.
+ * workspace: at least fairy2i_wl_matmul_workspace_bytes(...) bytes of
+ * device memory (may be NULL when that is 0), contents ignored on entry.
+ * Errors: FAIRY2I_ERR_NULL; FAIRY2I_ERR_SHAPE if N, K, B <= 0 or K % 4;
+ * FAIRY2I_ERR_STAGES; FAIRY2I_ERR_DTYPE; FAIRY2I_ERR_UNSUPPORTED for
+ * B > FAIRY2I_MAX_DECODE_BATCH with float activations, or a non-NULL
+ * x_scale with float activations; FAIRY2I_ERR_WORKSPACE.
+ */
+fairy2i_status fairy2i_wl_matmul(const uint8_t* codes_U, const float* scales_U,
+                                 const uint8_t* codes_W, const float* scales_W,
+                                 int32_t T, int64_t N, int64_t K,
+                                 const void* x, const float* x_scale, int32_t dtype, int64_t B,
+                                 float* y, void* workspace, size_t workspace_bytes,
+                                 void* stream);
+
+/*
+ * The exact integer products behind the int8 path of fairy2i_wl_matmul,
+ * exported so they can be compared bit for bit:
+ *   acc[M][t][p][b][i][c] = sum_j B^{M,t}_p[i][j] * q[b][j][c]
+ * with M in {0 = U, 1 = W}, p in {0 = b_re plane, 1 = b_im plane} (entries in
+ * {-1, 0, +1}, the 2x2 real blocks of Eq. realify-ops split by axis) and
+ * c in {0 = re, 1 = im}.  acc: int32 [2][T][2][B][N][2] output.
+ * It runs the same kernels as fairy2i_wl_matmul with FAIRY2I_ACT_I8 and the
+ * same B (decode for B <= FAIRY2I_MAX_DECODE_BATCH, prefill above), with the
+ * epilogue replaced by a store of the accumulators.
+ * Errors: as fairy2i_wl_matmul.
+ */
+fairy2i_status fairy2i_wl_int8_accumulators(const uint8_t* codes_U, const uint8_t* codes_W,
+                                            int32_t T, int64_t N, int64_t K,
+                                            const int8_t* q, int64_t B, int32_t* acc,
+                                            void* workspace, size_t workspace_bytes,
+                                            void* stream);
+
+/*
+ * Host-side self-check of the exact-mean rounding used by fairy2i_quantize
+ * for the axis scales: *out = float32 nearest (ties to even) to
+ * (sum of |values[i]|) / n_values, with the sum taken exactly; 0 when
+ * n_values == 0.  values is HOST memory (n_values finite doubles).  Runs on
+ * the CPU with the same code the GPU uses; enqueues nothing.
+ * Errors: FAIRY2I_ERR_NULL; FAIRY2I_ERR_SHAPE if n_values < 0 or
+ * n_values > FAIRY2I_MAX_QUANTIZE_ENTRIES.
+ */
+fairy2i_status fairy2i_host_exact_mean_f32(const double* values, int64_t n_values, float* out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FAIRY2I_H */

@@ -1,0 +1,16 @@
+"""Fairy2i quantised widely-linear layer on MI355X (gfx950).
+
+The computation lives in libfairy2i.so (HIP kernels behind the C ABI of
+include/fairy2i.h); this package only marshals torch device tensors into it.
+Importing the package does not load the library; the first call does, and
+raises if it has not been built (there is no fallback path).
+"""
+from .binding import (ACT_BF16, ACT_F32, ACT_I8, MAX_DECODE_BATCH, MAX_STAGES,  # noqa: F401
+                      Fairy2iError, int8_accumulators, load, quantize, quantize_act_int8,
+                      to_widely_linear, wl_matmul, wl_matmul_workspace_bytes)
+
+__all__ = [
+    "to_widely_linear", "quantize", "quantize_act_int8", "wl_matmul", "int8_accumulators",
+    "wl_matmul_workspace_bytes", "load", "Fairy2iError",
+    "ACT_F32", "ACT_BF16", "ACT_I8", "MAX_STAGES", "MAX_DECODE_BATCH",
+]

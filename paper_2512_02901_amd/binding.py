@@ -1,0 +1,229 @@
+"""Thin ctypes binding of libfairy2i.so (declared in include/fairy2i.h).
+
+Argument marshalling only: torch tensors supply device pointers and the
+current HIP stream; every step of the computation runs in the library's
+kernels.  There is no fallback: if the library is missing, ``load()`` raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfairy2i.so")
+_lib = None
+
+OK, ERR_NULL, ERR_SHAPE, ERR_STAGES, ERR_DTYPE, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(8)
+ACT_F32, ACT_BF16, ACT_I8 = 0, 1, 2
+MAX_STAGES = 4
+MAX_DECODE_BATCH = 16
+
+_c_i32, _c_i64, _c_size, _c_p = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_void_p
+
+_SIGNATURES = {
+    "fairy2i_status_string": (ctypes.c_char_p, [_c_i32]),
+    "fairy2i_abi_version": (_c_i32, []),
+    "fairy2i_to_widely_linear": (_c_i32, [_c_p, _c_i64, _c_i64, _c_p, _c_p, _c_p]),
+    "fairy2i_quantize_workspace_bytes": (_c_size, [_c_i64, _c_i64, _c_i32]),
+    "fairy2i_quantize": (_c_i32, [_c_p, _c_i64, _c_i64, _c_i32, _c_p, _c_p, _c_p, _c_size, _c_p]),
+    "fairy2i_quantize_act_int8": (_c_i32, [_c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_p, _c_p]),
+    "fairy2i_wl_matmul_workspace_bytes": (_c_size, [_c_i64, _c_i64, _c_i32, _c_i64, _c_i32]),
+    "fairy2i_wl_matmul": (_c_i32, [_c_p, _c_p, _c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_p,
+                                   _c_i32, _c_i64, _c_p, _c_p, _c_size, _c_p]),
+    "fairy2i_wl_int8_accumulators": (_c_i32, [_c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_i64,
+                                              _c_p, _c_p, _c_size, _c_p]),
+    "fairy2i_host_exact_mean_f32": (_c_i32, [_c_p, _c_i64, _c_p]),
+}
+
+
+class Fairy2iError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        msg = _lib.fairy2i_status_string(status).decode() if _lib is not None else str(status)
+        super().__init__(f"{where}: status {status} ({msg})")
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def load():
+    """Load libfairy2i.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(f"{_LIB_PATH} is missing: build it with "
+                               "`python -m paper_2512_02901_amd.build`")
+        lib = ctypes.CDLL(_LIB_PATH)
+        for name, (res, args) in _SIGNATURES.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def _check(status: int, where: str):
+    if status != OK:
+        raise Fairy2iError(status, where)
+
+
+# --------------------------------------------------------------- helpers ---
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_ptr(tensor) -> int:
+    torch = _torch()
+    return torch.cuda.current_stream(tensor.device).cuda_stream
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _require(t, dtype, name, device=None):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+
+
+# ------------------------------------------------------------------ API ---
+
+def to_widely_linear(A):
+    """A: float32 [2N, 2K] device tensor -> (U, W) complex64 [N, K]."""
+    torch = _torch()
+    lib = load()
+    _require(A, torch.float32, "A")
+    rows, cols = A.shape
+    U = torch.empty((rows // 2, cols // 2), dtype=torch.complex64, device=A.device)
+    W = torch.empty_like(U)
+    _check(lib.fairy2i_to_widely_linear(_ptr(A), rows, cols, _ptr(U), _ptr(W), _stream_ptr(A)),
+           "fairy2i_to_widely_linear")
+    return U, W
+
+
+def quantize(M, T: int):
+    """M: complex64 [N, K] -> (codes uint8 [T, N, K/4], scales float32 [T, 2])."""
+    torch = _torch()
+    lib = load()
+    _require(M, torch.complex64, "M")
+    N, K = M.shape
+    codes = torch.empty((T, N, K // 4), dtype=torch.uint8, device=M.device)
+    scales = torch.empty((T, 2), dtype=torch.float32, device=M.device)
+    wsb = lib.fairy2i_quantize_workspace_bytes(N, K, T)
+    ws = torch.empty(max(int(wsb), 1), dtype=torch.uint8, device=M.device)
+    _check(lib.fairy2i_quantize(_ptr(M), N, K, T, _ptr(codes), _ptr(scales), _ptr(ws), wsb,
+                                _stream_ptr(M)), "fairy2i_quantize")
+    return codes, scales
+
+
+def _act_dtype(x):
+    torch = _torch()
+    if x.dtype == torch.complex64:
+        return ACT_F32
+    if x.dtype == torch.bfloat16:
+        return ACT_BF16
+    if x.dtype == torch.int8:
+        return ACT_I8
+    raise TypeError(f"unsupported activation dtype {x.dtype}")
+
+
+def _act_shape(x):
+    """(B, K) of an activation tensor: complex64 [B, K] or bf16/int8 [B, K, 2]."""
+    if x.dim() == 2:
+        return x.shape[0], x.shape[1]
+    if x.dim() == 3 and x.shape[2] == 2:
+        return x.shape[0], x.shape[1]
+    raise ValueError("activations must be complex64 [B, K] or bf16/int8 [B, K, 2]")
+
+
+def quantize_act_int8(x):
+    """x: complex64 [B, K] or bf16 [B, K, 2] -> (q int8 [B, K, 2], x_scale float32 [B])."""
+    torch = _torch()
+    lib = load()
+    _require(x, None, "x")
+    dt = _act_dtype(x)
+    B, K = _act_shape(x)
+    q = torch.empty((B, K, 2), dtype=torch.int8, device=x.device)
+    xs = torch.empty((B,), dtype=torch.float32, device=x.device)
+    _check(lib.fairy2i_quantize_act_int8(_ptr(x), dt, B, K, _ptr(q), _ptr(xs), _stream_ptr(x)),
+           "fairy2i_quantize_act_int8")
+    return q, xs
+
+
+def wl_matmul_workspace_bytes(N, K, T, B, dtype) -> int:
+    return int(load().fairy2i_wl_matmul_workspace_bytes(N, K, T, B, dtype))
+
+
+def wl_matmul(codes_U, scales_U, codes_W, scales_W, x, x_scale=None, out=None, workspace=None):
+    """y = sum_t U^(t) x + W^(t) conj(x) for each token; complex64 [B, N]."""
+    torch = _torch()
+    lib = load()
+    for t, n in ((codes_U, "codes_U"), (codes_W, "codes_W")):
+        _require(t, torch.uint8, n)
+    for t, n in ((scales_U, "scales_U"), (scales_W, "scales_W")):
+        _require(t, torch.float32, n)
+    _require(x, None, "x")
+    T, N, KB = codes_U.shape
+    if codes_W.shape != codes_U.shape or scales_U.shape != (T, 2) or scales_W.shape != (T, 2):
+        raise ValueError("codes/scales shapes disagree")
+    dt = _act_dtype(x)
+    B, K = _act_shape(x)
+    if K != 4 * KB:
+        raise ValueError(f"activations have K={K}, codes have K={4 * KB}")
+    if x_scale is not None:
+        _require(x_scale, torch.float32, "x_scale")
+    if out is None:
+        out = torch.empty((B, N), dtype=torch.complex64, device=x.device)
+    else:
+        _require(out, torch.complex64, "out")
+    wsb = lib.fairy2i_wl_matmul_workspace_bytes(N, K, T, B, dt)
+    if wsb and workspace is None:
+        workspace = torch.empty(int(wsb), dtype=torch.uint8, device=x.device)
+    _check(lib.fairy2i_wl_matmul(_ptr(codes_U), _ptr(scales_U), _ptr(codes_W), _ptr(scales_W), T, N, K,
+                                 _ptr(x), _ptr(x_scale), dt, B, _ptr(out), _ptr(workspace), wsb,
+                                 _stream_ptr(x)), "fairy2i_wl_matmul")
+    return out
+
+
+def int8_accumulators(codes_U, codes_W, q, workspace=None):
+    """Exact int32 products acc[M][t][p][b][i][c] behind the int8 path."""
+    torch = _torch()
+    lib = load()
+    _require(codes_U, torch.uint8, "codes_U")
+    _require(codes_W, torch.uint8, "codes_W")
+    _require(q, torch.int8, "q")
+    T, N, KB = codes_U.shape
+    B, K = _act_shape(q)
+    if K != 4 * KB:
+        raise ValueError("K mismatch")
+    acc = torch.empty((2, T, 2, B, N, 2), dtype=torch.int32, device=q.device)
+    wsb = lib.fairy2i_wl_matmul_workspace_bytes(N, K, T, B, ACT_I8)
+    if wsb and workspace is None:
+        workspace = torch.empty(int(wsb), dtype=torch.uint8, device=q.device)
+    _check(lib.fairy2i_wl_int8_accumulators(_ptr(codes_U), _ptr(codes_W), T, N, K, _ptr(q), B,
+                                            _ptr(acc), _ptr(workspace), wsb, _stream_ptr(q)),
+           "fairy2i_wl_int8_accumulators")
+    return acc
+
+
+def host_exact_mean_f32(values) -> np.float32:
+    """Host-side self-check of the scale rounding (no GPU involved)."""
+    lib = load()
+    v = np.ascontiguousarray(values, dtype=np.float64)
+    out = ctypes.c_float(0.0)
+    _check(lib.fairy2i_host_exact_mean_f32(v.ctypes.data_as(ctypes.c_void_p), v.size,
+                                           ctypes.byref(out)), "fairy2i_host_exact_mean_f32")
+    return np.float32(out.value)

@@ -1,0 +1,141 @@
+// Recursive residual PhaseQuant of one complex matrix (Sec. 3.3 formal
+// definition, with the projection, axis scales and dequantisation of
+// Sec. 3.2).
+//
+// Stage t runs two kernels on the caller's stream:
+//   qz_stage_kernel    one thread per packed byte (4 consecutive entries of a
+//                      row): rebuilds the float64 residual from M and the
+//                      codes/scales of stages < t, projects it, writes the
+//                      byte of stage-t codes, and adds |Re r| (k even) or
+//                      |Im r| (k odd) into an exact fixed-point accumulator
+//                      in LDS; each block stores its partial accumulator.
+//   qz_finalize_kernel one block: sums the partials (integer adds, so the
+//                      result does not depend on block order), then rounds
+//                      each exact mean once to float32 -> scales[t].
+// Stage t+1 reads scales[t] from device memory; nothing returns to the host.
+#include "common.h"
+#include "superacc.h"
+
+namespace fairy2i {
+
+namespace {
+
+constexpr int kPartWords = 2 * SA_LIMBS + 2;  // acc[2][SA_LIMBS], cnt[2]
+
+// Eq. (ifairy-proj) by exact comparisons (floor-form ties, 0 -> +1).
+__device__ inline uint32_t project_code(double a, double b) {
+  if (b > 0.0 && -b < a && a <= b) return 1u;
+  if (a < 0.0 && a < b && b <= -a) return 2u;
+  if (b < 0.0 && b <= a && a < -b) return 3u;
+  return 0u;
+}
+
+__device__ inline void sa_add_lds(unsigned long long* acc, double v) {
+  if (v == 0.0) return;
+  int limb;
+  uint32_t lo, mid, hi;
+  sa_split(v, &limb, &lo, &mid, &hi);
+  if (lo) atomicAdd(&acc[limb], (unsigned long long)lo);
+  if (mid) atomicAdd(&acc[limb + 1], (unsigned long long)mid);
+  if (hi) atomicAdd(&acc[limb + 2], (unsigned long long)hi);
+}
+
+__global__ __launch_bounds__(kQzThreads) void qz_stage_kernel(
+    const float2* __restrict__ M, int64_t nbytes, uint8_t* __restrict__ codes,
+    const float* __restrict__ scales, int t, unsigned long long* __restrict__ part) {
+  __shared__ unsigned long long acc[2][SA_LIMBS];
+  __shared__ unsigned long long cnt[2];
+  for (int i = threadIdx.x; i < 2 * SA_LIMBS; i += blockDim.x) (&acc[0][0])[i] = 0ull;
+  if (threadIdx.x < 2) cnt[threadIdx.x] = 0ull;
+  __syncthreads();
+
+  double s_re[FAIRY2I_MAX_STAGES], s_im[FAIRY2I_MAX_STAGES];
+  for (int tp = 0; tp < t; ++tp) {
+    s_re[tp] = (double)scales[2 * tp];
+    s_im[tp] = (double)scales[2 * tp + 1];
+  }
+  unsigned long long n_re = 0, n_im = 0;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t bi = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; bi < nbytes; bi += stride) {
+    uint32_t prev[FAIRY2I_MAX_STAGES];
+    for (int tp = 0; tp < t; ++tp) prev[tp] = codes[(int64_t)tp * nbytes + bi];
+    uint32_t out = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float2 m = M[4 * bi + e];
+      double re = (double)m.x, im = (double)m.y;
+      for (int tp = 0; tp < t; ++tp) {  // R(tp+1) = R(tp) - W^(tp)
+        const uint32_t k = (prev[tp] >> (2 * e)) & 3u;
+        if (k == 0u) re = re - s_re[tp];
+        else if (k == 2u) re = re + s_re[tp];
+        else if (k == 1u) im = im - s_im[tp];
+        else im = im + s_im[tp];
+      }
+      const uint32_t k = project_code(re, im);
+      out |= k << (2 * e);
+      if (k & 1u) {
+        sa_add_lds(acc[1], fabs(im));
+        ++n_im;
+      } else {
+        sa_add_lds(acc[0], fabs(re));
+        ++n_re;
+      }
+    }
+    codes[(int64_t)t * nbytes + bi] = (uint8_t)out;
+  }
+  if (n_re) atomicAdd(&cnt[0], n_re);
+  if (n_im) atomicAdd(&cnt[1], n_im);
+  __syncthreads();
+  unsigned long long* dst = part + (int64_t)blockIdx.x * kPartWords;
+  for (int i = threadIdx.x; i < 2 * SA_LIMBS; i += blockDim.x) dst[i] = (&acc[0][0])[i];
+  if (threadIdx.x < 2) dst[2 * SA_LIMBS + threadIdx.x] = cnt[threadIdx.x];
+}
+
+__global__ __launch_bounds__(256) void qz_finalize_kernel(const unsigned long long* __restrict__ part,
+                                                          int nblk, float* __restrict__ scales_t) {
+  __shared__ unsigned long long tot[kPartWords];
+  for (int i = threadIdx.x; i < kPartWords; i += blockDim.x) {
+    unsigned long long s = 0;
+    for (int b = 0; b < nblk; ++b) s += part[(int64_t)b * kPartWords + i];
+    tot[i] = s;
+  }
+  __syncthreads();
+  if (threadIdx.x < 2) {
+    const unsigned long long n = tot[2 * SA_LIMBS + threadIdx.x];
+    scales_t[threadIdx.x] =
+        n ? sa_mean_to_f32(reinterpret_cast<const uint64_t*>(&tot[threadIdx.x * SA_LIMBS]), n) : 0.0f;
+  }
+}
+
+int quantize_blocks(int64_t N, int64_t K) {
+  const int64_t nbytes = N * K / 4;
+  int64_t b = (nbytes + kQzThreads - 1) / kQzThreads;
+  if (b > kQzMaxBlocks) b = kQzMaxBlocks;
+  if (b < 1) b = 1;
+  return (int)b;
+}
+
+}  // namespace
+
+size_t quantize_workspace_bytes(int64_t N, int64_t K) {
+  return (size_t)quantize_blocks(N, K) * kPartWords * sizeof(unsigned long long);
+}
+
+hipError_t launch_quantize(const float2* M, int64_t N, int64_t K, int T, uint8_t* codes,
+                           float* scales, void* workspace, hipStream_t stream) {
+  const int nblk = quantize_blocks(N, K);
+  const int64_t nbytes = N * K / 4;
+  auto* part = static_cast<unsigned long long*>(workspace);
+  for (int t = 0; t < T; ++t) {
+    hipLaunchKernelGGL(qz_stage_kernel, dim3(nblk), dim3(kQzThreads), 0, stream, M, nbytes, codes,
+                       scales, t, part);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(qz_finalize_kernel, dim3(1), dim3(256), 0, stream, part, nblk, scales + 2 * t);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace fairy2i

@@ -1,0 +1,156 @@
+"""Host-side checks of the C ABI (no GPU): the library loads, exports every
+symbol the header declares, and rejects bad arguments before touching HIP."""
+import ctypes
+import os
+import re
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2512_02901_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fairy2i.h")
+
+# A non-null dummy device address: every call below fails validation before
+# the pointer could be used.
+P = ctypes.c_void_p(0x1000)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return binding.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fairy2i_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert len(names) >= 9
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(binding._SIGNATURES), "binding and header disagree"
+
+
+def test_status_strings(lib):
+    for s in range(8):
+        assert lib.fairy2i_status_string(s)
+    assert lib.fairy2i_status_string(99) == b"unknown status"
+    assert lib.fairy2i_abi_version() == 1
+
+
+def test_to_widely_linear_validation(lib):
+    f = lib.fairy2i_to_widely_linear
+    assert f(None, 4, 4, P, P, None) == binding.ERR_NULL
+    assert f(P, 4, 4, None, P, None) == binding.ERR_NULL
+    assert f(P, 3, 4, P, P, None) == binding.ERR_SHAPE
+    assert f(P, 4, 5, P, P, None) == binding.ERR_SHAPE
+    assert f(P, 0, 4, P, P, None) == binding.ERR_SHAPE
+    assert f(P, -2, 4, P, P, None) == binding.ERR_SHAPE
+
+
+def test_quantize_validation(lib):
+    f = lib.fairy2i_quantize
+    wsb = lib.fairy2i_quantize_workspace_bytes(8, 8, 2)
+    assert wsb > 0
+    assert f(None, 8, 8, 2, P, P, P, wsb, None) == binding.ERR_NULL
+    assert f(P, 8, 6, 2, P, P, P, wsb, None) == binding.ERR_SHAPE   # K % 4
+    assert f(P, 0, 8, 2, P, P, P, wsb, None) == binding.ERR_SHAPE
+    assert f(P, 1 << 20, 1 << 12, 2, P, P, P, 1 << 30, None) == binding.ERR_SHAPE  # N*K > 2^31
+    assert f(P, 8, 8, 0, P, P, P, wsb, None) == binding.ERR_STAGES
+    assert f(P, 8, 8, 5, P, P, P, wsb, None) == binding.ERR_STAGES
+    assert f(P, 8, 8, 2, P, P, None, wsb, None) == binding.ERR_WORKSPACE
+    assert f(P, 8, 8, 2, P, P, P, wsb - 1, None) == binding.ERR_WORKSPACE
+
+
+def test_act_quant_validation(lib):
+    f = lib.fairy2i_quantize_act_int8
+    assert f(None, 0, 1, 8, P, P, None) == binding.ERR_NULL
+    assert f(P, 0, 0, 8, P, P, None) == binding.ERR_SHAPE
+    assert f(P, 2, 1, 8, P, P, None) == binding.ERR_DTYPE
+    assert f(P, 7, 1, 8, P, P, None) == binding.ERR_DTYPE
+
+
+def test_wl_matmul_validation(lib):
+    f = lib.fairy2i_wl_matmul
+    ok = dict(cu=P, su=P, cw=P, sw=P, T=2, N=8, K=16, x=P, xs=None, dt=binding.ACT_F32, B=1, y=P)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return f(a["cu"], a["su"], a["cw"], a["sw"], a["T"], a["N"], a["K"], a["x"], a["xs"],
+                 a["dt"], a["B"], a["y"], None, 0, None)
+    assert call(cu=None) == binding.ERR_NULL
+    assert call(sw=None) == binding.ERR_NULL
+    assert call(y=None) == binding.ERR_NULL
+    assert call(K=18) == binding.ERR_SHAPE
+    assert call(N=0) == binding.ERR_SHAPE
+    assert call(B=0) == binding.ERR_SHAPE
+    assert call(T=0) == binding.ERR_STAGES
+    assert call(T=5) == binding.ERR_STAGES
+    assert call(dt=3) == binding.ERR_DTYPE
+    assert call(B=17) == binding.ERR_UNSUPPORTED                     # float needs decode batch
+    assert call(B=17, dt=binding.ACT_BF16) == binding.ERR_UNSUPPORTED
+    assert call(xs=P) == binding.ERR_UNSUPPORTED                     # x_scale with float acts
+    assert call(dt=binding.ACT_I8) == binding.ERR_NULL               # int8 needs x_scale
+    assert lib.fairy2i_wl_matmul_workspace_bytes(8, 16, 2, 1, 0) == 0
+
+
+def test_int8_accumulators_validation(lib):
+    f = lib.fairy2i_wl_int8_accumulators
+    assert f(None, P, 2, 8, 16, P, 1, P, None, 0, None) == binding.ERR_NULL
+    assert f(P, P, 2, 8, 16, P, 1, None, None, 0, None) == binding.ERR_NULL
+    assert f(P, P, 2, 8, 14, P, 1, P, None, 0, None) == binding.ERR_SHAPE
+    assert f(P, P, 9, 8, 16, P, 1, P, None, 0, None) == binding.ERR_STAGES
+
+
+def _host_mean(lib, v):
+    v = np.ascontiguousarray(v, dtype=np.float64)
+    out = ctypes.c_float(-1.0)
+    st = lib.fairy2i_host_exact_mean_f32(v.ctypes.data_as(ctypes.c_void_p), v.size, ctypes.byref(out))
+    assert st == binding.OK
+    return np.float32(out.value)
+
+
+def test_scale_rounding_matches_oracle_exact_rationals(lib):
+    """The library's exact-mean rounding (the code its GPU finalize kernel
+    runs, here on the host) against the oracle's rational arithmetic."""
+    rng = np.random.default_rng(0)
+    cases = [
+        np.abs(rng.standard_normal(1000)) * 0.02,
+        np.abs(rng.standard_normal(7)) * np.exp2(rng.integers(-140, 120, 7)),
+        np.array([5e-324] * 3),
+        np.array([1e-310, 3e-320, 7e-315]),
+        np.array([1.0, 1.0 + 2.0 ** -24]),                  # exact tie -> even
+        np.array([1.0 + 2.0 ** -23, 1.0 + 2.0 ** -22]),
+        np.array([3.0e38, 3.4e38]),                          # near float32 max
+        np.array([1e39, 1e39]),                              # overflow -> inf
+        np.array([1.0e-45, 2.0e-45, 0.0]),                   # float32 subnormal result
+        np.array([2.0 ** -150, 2.0 ** -150]),                # rounds to 0 (tie, even)
+        np.array([2.0 ** -150 * 1.5]),                       # rounds up to the smallest subnormal
+        np.abs(rng.standard_normal(5000)) * np.exp2(rng.integers(-1000, 1000, 5000)),
+    ]
+    for v in cases:
+        got = _host_mean(lib, v)
+        want = oracle.round_to_f32(oracle.exact_sum(np.abs(v)) / v.size)
+        assert (np.isinf(got) and np.isinf(want)) or got == want, (v[:4], got, want)
+    assert _host_mean(lib, np.zeros(0)) == 0
+
+
+def test_scale_rounding_random_ties(lib):
+    """Many means that land exactly on float32 rounding ties."""
+    rng = np.random.default_rng(1)
+    for _ in range(200):
+        base = np.float32(rng.uniform(0.001, 0.1))
+        ulp = float(np.nextafter(base, np.float32(1)) - base)
+        n = int(rng.integers(1, 40))
+        target = Fraction(float(base)) + Fraction(ulp) / 2   # exact midpoint
+        vals = np.full(n, float(target), dtype=np.float64)
+        assert Fraction(float(vals[0])) == target
+        got = _host_mean(lib, vals)
+        assert got == oracle.round_to_f32(target)
