@@ -197,13 +197,19 @@ __global__ __launch_bounds__(256) void gemv_valu_kernel(WlArgs a, bool aligned) 
   }
 }
 
-template <int DT, int T, bool EXPORT>
-hipError_t launch_t(const WlArgs& a, hipStream_t s) {
-  constexpr int TB = 4;
+template <int DT, int T, int TB, bool EXPORT>
+hipError_t launch_tb(const WlArgs& a, hipStream_t s) {
   const bool aligned = (a.K % 16) == 0;
   dim3 grid((unsigned)((a.N + 3) / 4), (unsigned)((a.B + TB - 1) / TB));
   hipLaunchKernelGGL((gemv_valu_kernel<DT, T, TB, EXPORT>), grid, dim3(256), 0, s, a, aligned);
   return hipGetLastError();
+}
+
+template <int DT, int T, bool EXPORT>
+hipError_t launch_t(const WlArgs& a, hipStream_t s) {
+  if (a.B == 1) return launch_tb<DT, T, 1, EXPORT>(a, s);
+  if (a.B == 2) return launch_tb<DT, T, 2, EXPORT>(a, s);
+  return launch_tb<DT, T, 4, EXPORT>(a, s);
 }
 
 template <int DT, bool EXPORT>
