@@ -151,11 +151,15 @@ size_t fairy2i_wl_matmul_workspace_bytes(int64_t N, int64_t K, int32_t T, int64_
  * as produced by fairy2i_quantize_act_int8) and y[b] is multiplied by it;
  * for the float dtypes x_scale must be NULL.
  * y: complex64 [B][N] output.
- * Accumulation is in float32 (float activations) or exact int32 (int8
- * activations), with a fixed summation order: results are bitwise
+ * Accumulation is exact integer arithmetic on the matrix cores, or float32
+ * in the vector kernel, always in a fixed order: results are bitwise
  * reproducible run to run.
- * B <= FAIRY2I_MAX_DECODE_BATCH runs the decode kernel; larger B needs
- * FAIRY2I_ACT_I8 and runs the int8-MFMA prefill kernel.
+ * B <= FAIRY2I_MAX_DECODE_BATCH runs the decode kernels: bf16 and int8
+ * activations with K % 64 == 0 go to the int8 matrix cores (bf16 tokens as
+ * a 23-bit block fixed point, exact for every value within 2^14 of the
+ * token's largest magnitude, smaller values rounded to that grid), other
+ * cases to a float32 / int32 vector kernel.  Larger B needs FAIRY2I_ACT_I8
+ * and runs the int8-MFMA prefill kernel.
  * workspace: at least fairy2i_wl_matmul_workspace_bytes(...) bytes of
  * device memory (may be NULL when that is 0), contents ignored on entry.
  * Errors: FAIRY2I_ERR_NULL; FAIRY2I_ERR_SHAPE if N, K, B <= 0 or K % 4;
@@ -187,6 +191,54 @@ fairy2i_status fairy2i_wl_int8_accumulators(const uint8_t* codes_U, const uint8_
                                             const int8_t* q, int64_t B, int32_t* acc,
                                             void* workspace, size_t workspace_bytes,
                                             void* stream);
+
+/*
+ * One layer of a grouped decode call (fairy2i_wl_matmul_group): the same
+ * arguments fairy2i_wl_matmul takes for one layer.  All pointers are device
+ * memory; x is B*K*2 activations of the group's dtype, x_scale is float32 [B]
+ * for FAIRY2I_ACT_I8 and NULL otherwise, y is complex64 [B][N].
+ */
+typedef struct fairy2i_wl_layer {
+  const uint8_t* codes_U;
+  const float* scales_U;
+  const uint8_t* codes_W;
+  const float* scales_W;
+  const void* x;
+  const float* x_scale;
+  float* y;
+  int64_t N;
+  int64_t K;
+} fairy2i_wl_layer;
+
+/*
+ * Grouped decode: the product of fairy2i_wl_matmul for many independent
+ * layers (for example every projection of a decoder stack, each with its own
+ * input) in a fixed number of kernel launches, so the weight stream of all
+ * layers runs back to back instead of paying a launch per layer.
+ * Restrictions: dtype FAIRY2I_ACT_BF16 or FAIRY2I_ACT_I8, 1 <= B <= 16,
+ * every K a multiple of 64.
+ *
+ * Use: size the workspace with fairy2i_wl_group_workspace_bytes and the
+ * table with fairy2i_wl_group_table_bytes; fairy2i_wl_group_build_table
+ * (host only, enqueues nothing) checks every layer and writes the table into
+ * HOST memory `table`; copy those bytes unchanged to device memory; then each
+ * fairy2i_wl_matmul_group(table, table_device, stream) computes every layer's
+ * y.  The workspace and both table copies must stay alive and unchanged while
+ * calls that use them run; calls sharing a workspace must not overlap.
+ * Results equal fairy2i_wl_matmul on each layer bit for bit.
+ * Errors: as fairy2i_wl_matmul, checked per layer by the build call;
+ * FAIRY2I_ERR_UNSUPPORTED for the restrictions above; FAIRY2I_ERR_SHAPE if
+ * n_layers < 1; fairy2i_wl_matmul_group returns FAIRY2I_ERR_NULL for a NULL
+ * table and FAIRY2I_ERR_UNSUPPORTED for bytes that are not a built table.
+ */
+size_t fairy2i_wl_group_workspace_bytes(const fairy2i_wl_layer* layers, int32_t n_layers,
+                                        int32_t T, int32_t dtype, int64_t B);
+size_t fairy2i_wl_group_table_bytes(int32_t n_layers);
+fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int32_t n_layers,
+                                            int32_t T, int32_t dtype, int64_t B,
+                                            void* workspace, size_t workspace_bytes,
+                                            void* table, size_t table_bytes);
+fairy2i_status fairy2i_wl_matmul_group(const void* table, const void* table_device, void* stream);
 
 /*
  * Host-side self-check of the exact-mean rounding used by fairy2i_quantize

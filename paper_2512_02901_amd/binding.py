@@ -34,7 +34,18 @@ _SIGNATURES = {
     "fairy2i_wl_int8_accumulators": (_c_i32, [_c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_i64,
                                               _c_p, _c_p, _c_size, _c_p]),
     "fairy2i_host_exact_mean_f32": (_c_i32, [_c_p, _c_i64, _c_p]),
+    "fairy2i_wl_group_workspace_bytes": (_c_size, [_c_p, _c_i32, _c_i32, _c_i32, _c_i64]),
+    "fairy2i_wl_group_table_bytes": (_c_size, [_c_i32]),
+    "fairy2i_wl_group_build_table": (_c_i32, [_c_p, _c_i32, _c_i32, _c_i32, _c_i64, _c_p, _c_size,
+                                              _c_p, _c_size]),
+    "fairy2i_wl_matmul_group": (_c_i32, [_c_p, _c_p, _c_p]),
 }
+
+
+class WlLayer(ctypes.Structure):
+    """fairy2i_wl_layer of include/fairy2i.h."""
+    _fields_ = [("codes_U", _c_p), ("scales_U", _c_p), ("codes_W", _c_p), ("scales_W", _c_p),
+                ("x", _c_p), ("x_scale", _c_p), ("y", _c_p), ("N", _c_i64), ("K", _c_i64)]
 
 
 class Fairy2iError(RuntimeError):
@@ -227,3 +238,43 @@ def host_exact_mean_f32(values) -> np.float32:
     _check(lib.fairy2i_host_exact_mean_f32(v.ctypes.data_as(ctypes.c_void_p), v.size,
                                            ctypes.byref(out)), "fairy2i_host_exact_mean_f32")
     return np.float32(out.value)
+
+
+class WlGroup:
+    """A table of independent layers decoded by one fairy2i_wl_matmul_group
+    call.  ``layers`` is a list of (codes_U, scales_U, codes_W, scales_W, x,
+    x_scale, y) device tensors (x_scale None for bf16); the object keeps them,
+    the workspace and both copies of the table alive."""
+
+    def __init__(self, layers, T: int, B: int):
+        torch = _torch()
+        lib = load()
+        if not layers:
+            raise ValueError("empty group")
+        dt = _act_dtype(layers[0][4])
+        self._keep = [t for layer in layers for t in layer if t is not None]
+        arr = (WlLayer * len(layers))()
+        for i, (cu, su, cw, sw, x, xs, y) in enumerate(layers):
+            Bx, K = _act_shape(x)
+            if Bx != B or _act_dtype(x) != dt:
+                raise ValueError("all layers of a group share B and the activation dtype")
+            arr[i] = WlLayer(cu.data_ptr(), su.data_ptr(), cw.data_ptr(), sw.data_ptr(), x.data_ptr(),
+                             None if xs is None else xs.data_ptr(), y.data_ptr(), cu.shape[1], K)
+        self.n = len(layers)
+        dev = layers[0][4].device
+        wsb = int(lib.fairy2i_wl_group_workspace_bytes(ctypes.byref(arr), self.n, T, dt, B))
+        self.workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+        tb = int(lib.fairy2i_wl_group_table_bytes(self.n))
+        self._table = (ctypes.c_uint8 * tb)()
+        _check(lib.fairy2i_wl_group_build_table(ctypes.byref(arr), self.n, T, dt, B,
+                                                _ptr(self.workspace), wsb, ctypes.byref(self._table), tb),
+               "fairy2i_wl_group_build_table")
+        host = torch.frombuffer(bytearray(bytes(self._table)), dtype=torch.uint8)
+        self.table_device = host.to(dev)
+        torch.cuda.synchronize(dev)
+        self._layers = arr
+
+    def run(self):
+        lib = load()
+        _check(lib.fairy2i_wl_matmul_group(ctypes.byref(self._table), _ptr(self.table_device),
+                                           _stream_ptr(self.table_device)), "fairy2i_wl_matmul_group")

@@ -5,6 +5,7 @@
 #include <vector>
 
 #include "common.h"
+#include "decode.h"
 #include "superacc.h"
 
 using namespace fairy2i;
@@ -25,6 +26,63 @@ fairy2i_status check_wl_common(const uint8_t* cu, const uint8_t* cw, int32_t T, 
   if (T < 1 || T > FAIRY2I_MAX_STAGES) return FAIRY2I_ERR_STAGES;
   return FAIRY2I_OK;
 }
+
+// Decode on the int8 matrix cores: bf16 / int8 activations, K % 64 == 0.
+bool use_mfma_decode(int32_t dtype, int64_t N, int64_t K, int64_t B) {
+  return (dtype == FAIRY2I_ACT_BF16 || dtype == FAIRY2I_ACT_I8) && (K % 64) == 0 &&
+         B <= FAIRY2I_MAX_DECODE_BATCH && N <= ((int64_t)1 << 26) &&
+         N * K / 4 < ((int64_t)1 << 31);  // 32-bit buffer ranges per code plane
+}
+
+int dec_mode(int32_t dtype) { return dtype == FAIRY2I_ACT_BF16 ? kModeBf16 : kModeI8; }
+
+int dec_ntile(int mode, int64_t B) { return mode == kModeBf16 ? (int)((B + 1) / 2) : (int)((B + 7) / 8); }
+
+DecLayer dec_layer(const uint8_t* cu, const float* su, const uint8_t* cw, const float* sw, int64_t N,
+                   int64_t K, const void* x, const float* xs, float* y) {
+  DecLayer l{};
+  l.codes[0] = cu;
+  l.codes[1] = cw;
+  l.scales[0] = su;
+  l.scales[1] = sw;
+  l.x = x;
+  l.x_scale_in = xs;
+  l.y = reinterpret_cast<float2*>(y);
+  l.N = (int32_t)N;
+  l.K = (int32_t)K;
+  return l;
+}
+
+fairy2i_status run_single_decode(DecLayer l, int32_t T, int32_t dtype, int64_t B, void* ws,
+                                 size_t ws_bytes, int32_t* acc, hipStream_t stream) {
+  const int mode = dec_mode(dtype);
+  const size_t need = dec_layer_setup(l, T, mode, (int)B, nullptr);
+  if (!ws || ws_bytes < need) return FAIRY2I_ERR_WORKSPACE;
+  dec_layer_setup(l, T, mode, (int)B, static_cast<char*>(ws));
+  l.acc = acc;
+  l.item0 = 0;
+  DecHeader h{};
+  h.n_layers = 1;
+  h.T = T;
+  h.mode = mode;
+  h.B = (int32_t)B;
+  h.ntile = dec_ntile(mode, B);
+  h.total_items = (int64_t)l.nrb * l.nkc;
+  const int64_t acc_elems = acc ? (int64_t)2 * T * 2 * B * l.N * 2 : 0;
+  return hip_status(launch_decode(h, l, nullptr, l.nkc > 1, B * (int64_t)l.N, acc != nullptr, acc_elems,
+                                  acc, stream));
+}
+
+// Group table: header followed by the layer descriptors (the device copy is
+// read by the kernels at the same offsets).
+constexpr uint32_t kGroupMagic = 0xFA112101u;
+struct GroupTableHeader {
+  uint32_t magic, abi;
+  DecHeader h;
+  int32_t any_split, pad0_;
+  int64_t max_BN, pad1_;
+};
+static_assert(sizeof(GroupTableHeader) % 16 == 0, "table header alignment");
 
 }  // namespace
 
@@ -80,8 +138,12 @@ fairy2i_status fairy2i_quantize_act_int8(const void* x, int32_t dtype, int64_t B
 }
 
 size_t fairy2i_wl_matmul_workspace_bytes(int64_t N, int64_t K, int32_t T, int64_t B, int32_t dtype) {
-  (void)N; (void)K; (void)T; (void)B; (void)dtype;
-  return 0;
+  if (N <= 0 || K <= 0 || B <= 0 || T < 1 || T > FAIRY2I_MAX_STAGES) return 0;
+  if (!use_mfma_decode(dtype, N, K, B)) return 0;
+  DecLayer l{};
+  l.N = (int32_t)N;
+  l.K = (int32_t)K;
+  return dec_layer_setup(l, T, dec_mode(dtype), (int)B, nullptr);
 }
 
 fairy2i_status fairy2i_wl_matmul(const uint8_t* codes_U, const float* scales_U,
@@ -100,6 +162,9 @@ fairy2i_status fairy2i_wl_matmul(const uint8_t* codes_U, const float* scales_U,
   if (workspace_bytes < fairy2i_wl_matmul_workspace_bytes(N, K, T, B, dtype) ||
       (fairy2i_wl_matmul_workspace_bytes(N, K, T, B, dtype) > 0 && !workspace))
     return FAIRY2I_ERR_WORKSPACE;
+  if (use_mfma_decode(dtype, N, K, B))
+    return run_single_decode(dec_layer(codes_U, scales_U, codes_W, scales_W, N, K, x, x_scale, y), T,
+                             dtype, B, workspace, workspace_bytes, nullptr, as_stream(stream));
   WlArgs a{};
   a.codes[0] = codes_U;
   a.codes[1] = codes_W;
@@ -128,6 +193,9 @@ fairy2i_status fairy2i_wl_int8_accumulators(const uint8_t* codes_U, const uint8_
   if (workspace_bytes < fairy2i_wl_matmul_workspace_bytes(N, K, T, B, FAIRY2I_ACT_I8) ||
       (fairy2i_wl_matmul_workspace_bytes(N, K, T, B, FAIRY2I_ACT_I8) > 0 && !workspace))
     return FAIRY2I_ERR_WORKSPACE;
+  if (use_mfma_decode(FAIRY2I_ACT_I8, N, K, B))
+    return run_single_decode(dec_layer(codes_U, nullptr, codes_W, nullptr, N, K, q, nullptr, nullptr), T,
+                             FAIRY2I_ACT_I8, B, workspace, workspace_bytes, acc, as_stream(stream));
   WlArgs a{};
   a.codes[0] = codes_U;
   a.codes[1] = codes_W;
@@ -141,6 +209,99 @@ fairy2i_status fairy2i_wl_int8_accumulators(const uint8_t* codes_U, const uint8_
   const hipError_t e = (B <= FAIRY2I_MAX_DECODE_BATCH) ? launch_gemv(a, as_stream(stream))
                                                        : launch_gemm_i8(a, as_stream(stream));
   return hip_status(e);
+}
+
+
+size_t fairy2i_wl_group_table_bytes(int32_t n_layers) {
+  if (n_layers < 1) return 0;
+  return sizeof(GroupTableHeader) + (size_t)n_layers * sizeof(DecLayer);
+}
+
+static fairy2i_status check_group(const fairy2i_wl_layer* layers, int32_t n_layers, int32_t T,
+                                  int32_t dtype, int64_t B) {
+  if (!layers) return FAIRY2I_ERR_NULL;
+  if (n_layers < 1) return FAIRY2I_ERR_SHAPE;
+  if (T < 1 || T > FAIRY2I_MAX_STAGES) return FAIRY2I_ERR_STAGES;
+  if (dtype != FAIRY2I_ACT_F32 && dtype != FAIRY2I_ACT_BF16 && dtype != FAIRY2I_ACT_I8)
+    return FAIRY2I_ERR_DTYPE;
+  if (B <= 0) return FAIRY2I_ERR_SHAPE;
+  for (int32_t i = 0; i < n_layers; ++i) {
+    const fairy2i_wl_layer& L = layers[i];
+    fairy2i_status st = check_wl_common(L.codes_U, L.codes_W, T, L.N, L.K, L.x, B, L.y);
+    if (st != FAIRY2I_OK) return st;
+    if (!L.scales_U || !L.scales_W) return FAIRY2I_ERR_NULL;
+    if (dtype == FAIRY2I_ACT_I8 && !L.x_scale) return FAIRY2I_ERR_NULL;
+    if (dtype != FAIRY2I_ACT_I8 && L.x_scale) return FAIRY2I_ERR_UNSUPPORTED;
+    if (!use_mfma_decode(dtype, L.N, L.K, B) || L.N > ((int64_t)1 << 30) || L.K > ((int64_t)1 << 24))
+      return FAIRY2I_ERR_UNSUPPORTED;
+  }
+  return FAIRY2I_OK;
+}
+
+size_t fairy2i_wl_group_workspace_bytes(const fairy2i_wl_layer* layers, int32_t n_layers, int32_t T,
+                                        int32_t dtype, int64_t B) {
+  if (check_group(layers, n_layers, T, dtype, B) != FAIRY2I_OK) return 0;
+  size_t total = 0;
+  for (int32_t i = 0; i < n_layers; ++i) {
+    DecLayer l{};
+    l.N = (int32_t)layers[i].N;
+    l.K = (int32_t)layers[i].K;
+    total += dec_layer_setup(l, T, dec_mode(dtype), (int)B, nullptr);
+  }
+  return total;
+}
+
+fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int32_t n_layers, int32_t T,
+                                            int32_t dtype, int64_t B, void* workspace,
+                                            size_t workspace_bytes, void* table, size_t table_bytes) {
+  fairy2i_status st = check_group(layers, n_layers, T, dtype, B);
+  if (st != FAIRY2I_OK) return st;
+  if (!table) return FAIRY2I_ERR_NULL;
+  if (table_bytes < fairy2i_wl_group_table_bytes(n_layers)) return FAIRY2I_ERR_WORKSPACE;
+  const size_t need = fairy2i_wl_group_workspace_bytes(layers, n_layers, T, dtype, B);
+  if (!workspace || workspace_bytes < need) return FAIRY2I_ERR_WORKSPACE;
+  auto* hdr = static_cast<GroupTableHeader*>(table);
+  auto* tab = reinterpret_cast<DecLayer*>(hdr + 1);
+  const int mode = dec_mode(dtype);
+  char* ws = static_cast<char*>(workspace);
+  int64_t items = 0;
+  int any_split = 0;
+  int64_t max_BN = 0;
+  for (int32_t i = 0; i < n_layers; ++i) {
+    const fairy2i_wl_layer& L = layers[i];
+    DecLayer l = dec_layer(L.codes_U, L.scales_U, L.codes_W, L.scales_W, L.N, L.K, L.x, L.x_scale, L.y);
+    ws += dec_layer_setup(l, T, mode, (int)B, ws);
+    l.acc = nullptr;
+    l.item0 = items;
+    items += (int64_t)l.nrb * l.nkc;
+    if (l.nkc > 1) any_split = 1;
+    if (B * (int64_t)l.N > max_BN) max_BN = B * (int64_t)l.N;
+    tab[i] = l;
+  }
+  *hdr = GroupTableHeader{};
+  hdr->magic = kGroupMagic;
+  hdr->abi = (uint32_t)fairy2i_abi_version();
+  hdr->h.n_layers = n_layers;
+  hdr->h.T = T;
+  hdr->h.mode = mode;
+  hdr->h.B = (int32_t)B;
+  hdr->h.ntile = dec_ntile(mode, B);
+  hdr->h.total_items = items;
+  hdr->any_split = any_split;
+  hdr->max_BN = max_BN;
+  return FAIRY2I_OK;
+}
+
+fairy2i_status fairy2i_wl_matmul_group(const void* table, const void* table_device, void* stream) {
+  if (!table || !table_device) return FAIRY2I_ERR_NULL;
+  const auto* hdr = static_cast<const GroupTableHeader*>(table);
+  if (hdr->magic != kGroupMagic || hdr->abi != (uint32_t)fairy2i_abi_version())
+    return FAIRY2I_ERR_UNSUPPORTED;
+  const auto* tab_dev = reinterpret_cast<const DecLayer*>(static_cast<const char*>(table_device) +
+                                                          sizeof(GroupTableHeader));
+  DecLayer none{};
+  return hip_status(launch_decode(hdr->h, none, tab_dev, hdr->any_split, hdr->max_BN, false, 0, nullptr,
+                                  as_stream(stream)));
 }
 
 fairy2i_status fairy2i_host_exact_mean_f32(const double* values, int64_t n_values, float* out) {

@@ -280,3 +280,76 @@ def test_prefill_llama_q_shape_sampled(gpu):
     toks[0], toks[-1] = 0, 2047
     np.testing.assert_array_equal(acc[:, :, :, toks], oracle.int8_accumulators(cu, cw, qo[toks]))
     assert rel_l2(y[toks], oracle.wl_matmul_int8(cu, su, cw, sw, qo[toks], fo[toks])) <= TOL_F32
+
+
+# ------------------------------------- decode on the int8 matrix cores ---
+
+@pytest.mark.parametrize("T", [1, 2, 3, 4])
+@pytest.mark.parametrize("B", [1, 2, 3, 8, 9, 16])
+@pytest.mark.parametrize("NK", [(64, 64), (100, 320), (48, 1088)])
+def test_mfma_decode_bf16_and_int8(gpu, T, B, NK):
+    """K % 64 == 0 routes bf16 and int8 decode to the matrix cores: ragged
+    row blocks (N % 16), K not a multiple of 256 or 512, several tiles."""
+    import paper_2512_02901_amd as f2
+    N, K = NK
+    A = synth.llama_weight(2 * N, 2 * K, (11, N, K))
+    _, _, cu, su, cw, sw = oracle_layer(A, T)
+    d = upload_layer(cu, su, cw, sw, gpu)
+    x = synth.activations(B, K, (12, B, K))
+    xb = synth.bf16_round_complex(x)
+    y = host(f2.wl_matmul(*d, bf16_dev(xb, gpu)))
+    assert rel_l2(y, oracle.wl_matmul(cu, su, cw, sw, xb)) <= TOL_F32
+    qo, fo = oracle.quantize_act_int8(x)
+    q, xs = dev(qo, gpu), dev(fo, gpu)
+    np.testing.assert_array_equal(host(f2.int8_accumulators(d[0], d[2], q)),
+                                  oracle.int8_accumulators(cu, cw, qo))
+    y = host(f2.wl_matmul(*d, q, xs))
+    assert rel_l2(y, oracle.wl_matmul_int8(cu, su, cw, sw, qo, fo)) <= TOL_F32
+
+
+def test_mfma_decode_bf16_wide_dynamic_range(gpu):
+    """A token whose values span 2^-40 .. 2^3: values more than 2^14 below the
+    token's largest magnitude are rounded to its 2^-E grid; the error stays
+    far inside the bf16 bar."""
+    import paper_2512_02901_amd as f2
+    N, K = 32, 256
+    A = synth.llama_weight(2 * N, 2 * K, (13, 0, 0))
+    _, _, cu, su, cw, sw = oracle_layer(A, 2)
+    d = upload_layer(cu, su, cw, sw, gpu)
+    rng = np.random.default_rng(13)
+    mag = np.exp2(rng.uniform(-40, 3, (1, K))) * np.sign(rng.standard_normal((1, K)))
+    x = synth.bf16_round_complex((mag + 1j * mag[:, ::-1]).astype(np.complex64))
+    y = host(f2.wl_matmul(*d, bf16_dev(x, gpu)))
+    assert rel_l2(y, oracle.wl_matmul(cu, su, cw, sw, x)) <= 1e-5
+
+
+def test_group_matches_single_layer_calls(gpu):
+    """One grouped call over layers of different shapes equals the per-layer
+    calls bit for bit, and the oracle within tolerance."""
+    import torch
+    import paper_2512_02901_amd as f2
+    shapes = [(128, 256), (200, 64), (48, 1088), (64, 2048)]
+    for B, mk in ((1, "bf16"), (4, "bf16"), (11, "i8")):
+        layers, refs = [], []
+        for i, (N, K) in enumerate(shapes):
+            A = synth.llama_weight(2 * N, 2 * K, (14, i, N))
+            _, _, cu, su, cw, sw = oracle_layer(A, 2)
+            d = upload_layer(cu, su, cw, sw, gpu)
+            x = synth.activations(B, K, (15, i, B))
+            if mk == "bf16":
+                xv = synth.bf16_round_complex(x)
+                xd, xs = bf16_dev(xv, gpu), None
+                yo = oracle.wl_matmul(cu, su, cw, sw, xv)
+            else:
+                qo, fo = oracle.quantize_act_int8(x)
+                xd, xs = dev(qo, gpu), dev(fo, gpu)
+                yo = oracle.wl_matmul_int8(cu, su, cw, sw, qo, fo)
+            y = torch.empty((B, N), dtype=torch.complex64, device=gpu)
+            layers.append((*d, xd, xs, y))
+            refs.append((host(f2.wl_matmul(*d, xd, xs)), yo))
+        grp = f2.WlGroup(layers, T=2, B=B)
+        grp.run()
+        grp.run()   # second call reuses workspace and table
+        for (cu, su, cw, sw, xd, xs, y), (ys, yo) in zip(layers, refs):
+            np.testing.assert_array_equal(host(y).view(np.uint32), ys.view(np.uint32))
+            assert rel_l2(host(y), yo) <= TOL_F32
