@@ -241,6 +241,17 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
 fairy2i_status fairy2i_wl_matmul_group(const void* table, const void* table_device, void* stream);
 
 /*
+ * fairy2i_wl_matmul_group with timing marks: records events[0] before the
+ * first launch, events[1] after the activation-operand kernel, events[2]
+ * after the product kernel and events[3] after the split-K reduction (each
+ * on `stream`, with hipEventRecord), so a caller can time each kernel of the
+ * call.  events: 4 hipEvent_t created by the caller.
+ * Errors: as fairy2i_wl_matmul_group; FAIRY2I_ERR_NULL for NULL events.
+ */
+fairy2i_status fairy2i_wl_matmul_group_timed(const void* table, const void* table_device,
+                                             void* stream, void* const* events);
+
+/*
  * Host-side self-check of the exact-mean rounding used by fairy2i_quantize
  * for the axis scales: *out = float32 nearest (ties to even) to
  * (sum of |values[i]|) / n_values, with the sum taken exactly; 0 when

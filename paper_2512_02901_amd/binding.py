@@ -39,6 +39,7 @@ _SIGNATURES = {
     "fairy2i_wl_group_build_table": (_c_i32, [_c_p, _c_i32, _c_i32, _c_i32, _c_i64, _c_p, _c_size,
                                               _c_p, _c_size]),
     "fairy2i_wl_matmul_group": (_c_i32, [_c_p, _c_p, _c_p]),
+    "fairy2i_wl_matmul_group_timed": (_c_i32, [_c_p, _c_p, _c_p, _c_p]),
 }
 
 
@@ -274,7 +275,16 @@ class WlGroup:
         torch.cuda.synchronize(dev)
         self._layers = arr
 
-    def run(self):
+    def run(self, events=None):
+        """One grouped call.  ``events``: optional 4 torch.cuda.Event already
+        recorded once (so they exist); the library re-records them around its
+        three kernels on the current stream."""
         lib = load()
-        _check(lib.fairy2i_wl_matmul_group(ctypes.byref(self._table), _ptr(self.table_device),
-                                           _stream_ptr(self.table_device)), "fairy2i_wl_matmul_group")
+        stream = _stream_ptr(self.table_device)
+        if events is None:
+            _check(lib.fairy2i_wl_matmul_group(ctypes.byref(self._table), _ptr(self.table_device), stream),
+                   "fairy2i_wl_matmul_group")
+            return
+        handles = (_c_p * 4)(*[e.cuda_event for e in events])
+        _check(lib.fairy2i_wl_matmul_group_timed(ctypes.byref(self._table), _ptr(self.table_device), stream,
+                                                 handles), "fairy2i_wl_matmul_group_timed")

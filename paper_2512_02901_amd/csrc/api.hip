@@ -292,7 +292,8 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
   return FAIRY2I_OK;
 }
 
-fairy2i_status fairy2i_wl_matmul_group(const void* table, const void* table_device, void* stream) {
+static fairy2i_status run_group(const void* table, const void* table_device, void* stream,
+                                void* const* events) {
   if (!table || !table_device) return FAIRY2I_ERR_NULL;
   const auto* hdr = static_cast<const GroupTableHeader*>(table);
   if (hdr->magic != kGroupMagic || hdr->abi != (uint32_t)fairy2i_abi_version())
@@ -301,7 +302,17 @@ fairy2i_status fairy2i_wl_matmul_group(const void* table, const void* table_devi
                                                           sizeof(GroupTableHeader));
   DecLayer none{};
   return hip_status(launch_decode(hdr->h, none, tab_dev, hdr->any_split, hdr->max_BN, false, 0, nullptr,
-                                  as_stream(stream)));
+                                  as_stream(stream), reinterpret_cast<hipEvent_t const*>(events)));
+}
+
+fairy2i_status fairy2i_wl_matmul_group(const void* table, const void* table_device, void* stream) {
+  return run_group(table, table_device, stream, nullptr);
+}
+
+fairy2i_status fairy2i_wl_matmul_group_timed(const void* table, const void* table_device, void* stream,
+                                             void* const* events) {
+  if (!events || !events[0] || !events[1] || !events[2] || !events[3]) return FAIRY2I_ERR_NULL;
+  return run_group(table, table_device, stream, events);
 }
 
 fairy2i_status fairy2i_host_exact_mean_f32(const double* values, int64_t n_values, float* out) {

@@ -43,6 +43,6 @@ size_t dec_layer_setup(DecLayer& l, int T, int mode, int B, char* ws);
 
 hipError_t launch_decode(const DecHeader& h, const DecLayer& inl, const DecLayer* tab,
                          int any_split, int64_t max_BN, bool export_acc, int64_t acc_elems,
-                         int32_t* acc, hipStream_t s);
+                         int32_t* acc, hipStream_t s, hipEvent_t const* events = nullptr);
 
 }  // namespace fairy2i

@@ -386,15 +386,17 @@ int dec_tiles_per_group(int T, int ntile) {
 
 hipError_t launch_decode(const DecHeader& h, const DecLayer& inl, const DecLayer* tab,
                          int any_split, int64_t max_BN, bool export_acc, int64_t acc_elems,
-                         int32_t* acc, hipStream_t s) {
+                         int32_t* acc, hipStream_t s, hipEvent_t const* events) {
   const int nl = h.n_layers;
+  auto mark = [&](int i) -> hipError_t { return events ? hipEventRecord(events[i], s) : hipSuccess; };
+  hipError_t e = mark(0);
+  if (e != hipSuccess) return e;
   // 1. activation operand
   if (h.mode == kModeBf16)
     hipLaunchKernelGGL(dec_prep_kernel<kModeBf16>, dim3(h.ntile * 16, nl), dim3(256), 0, s, h, inl, tab);
   else
     hipLaunchKernelGGL(dec_prep_kernel<kModeI8>, dim3(h.ntile * 16, nl), dim3(256), 0, s, h, inl, tab);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if ((e = hipGetLastError()) != hipSuccess || (e = mark(1)) != hipSuccess) return e;
   if (export_acc) {
     hipLaunchKernelGGL(fill_i32_kernel, dim3(1024), dim3(256), 0, s, acc, acc_elems);
     if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -409,7 +411,7 @@ hipError_t launch_decode(const DecHeader& h, const DecLayer& inl, const DecLayer
   } else {
     launch_dec_mode<kModeI8, false>(h, inl, tab, (int)blocks, s);
   }
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = hipGetLastError()) != hipSuccess || (e = mark(2)) != hipSuccess) return e;
   // 3. split-K partials, summed in slice order
   if (!export_acc && any_split) {
     int64_t rb = (max_BN + 255) / 256;
@@ -417,7 +419,7 @@ hipError_t launch_decode(const DecHeader& h, const DecLayer& inl, const DecLayer
     hipLaunchKernelGGL(dec_reduce_kernel, dim3((unsigned)rb, nl), dim3(256), 0, s, h, inl, tab);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  return hipSuccess;
+  return mark(3);
 }
 
 }  // namespace fairy2i

@@ -154,3 +154,45 @@ def test_scale_rounding_random_ties(lib):
         assert Fraction(float(vals[0])) == target
         got = _host_mean(lib, vals)
         assert got == oracle.round_to_f32(target)
+
+
+def _layer(**kw):
+    d = dict(codes_U=0x1000, scales_U=0x1000, codes_W=0x1000, scales_W=0x1000, x=0x1000, x_scale=None,
+             y=0x1000, N=64, K=128)
+    d.update(kw)
+    return binding.WlLayer(d["codes_U"], d["scales_U"], d["codes_W"], d["scales_W"], d["x"], d["x_scale"],
+                           d["y"], d["N"], d["K"])
+
+
+def test_group_build_validation(lib):
+    """fairy2i_wl_group_build_table checks every layer on the host."""
+    def build(layers, T=2, dt=binding.ACT_BF16, B=1, ws=P, wsb=1 << 30, tb=None):
+        arr = (binding.WlLayer * max(1, len(layers)))(*layers)
+        n = len(layers)
+        tbytes = lib.fairy2i_wl_group_table_bytes(max(n, 1)) if tb is None else tb
+        buf = (ctypes.c_uint8 * max(1, tbytes))()
+        return lib.fairy2i_wl_group_build_table(ctypes.byref(arr), n, T, dt, B, ws, wsb, ctypes.byref(buf), tbytes)
+    good = [_layer(), _layer(N=200, K=1088)]
+    assert build(good) == binding.OK
+    assert lib.fairy2i_wl_group_workspace_bytes(ctypes.byref((binding.WlLayer * 2)(*good)), 2, 2, 1, 1) > 0
+    assert build([]) == binding.ERR_SHAPE
+    assert build(good, T=5) == binding.ERR_STAGES
+    assert build(good, dt=7) == binding.ERR_DTYPE
+    assert build(good, dt=binding.ACT_F32) == binding.ERR_UNSUPPORTED     # float32 not on the matrix cores
+    assert build([_layer(K=100)]) == binding.ERR_UNSUPPORTED               # K % 64
+    assert build(good, B=17) == binding.ERR_UNSUPPORTED
+    assert build([_layer(codes_W=None)]) == binding.ERR_NULL
+    assert build([_layer(x_scale=0x1000)]) == binding.ERR_UNSUPPORTED      # x_scale with bf16
+    assert build([_layer()], dt=binding.ACT_I8) == binding.ERR_NULL        # int8 needs x_scale
+    assert build(good, ws=None) == binding.ERR_WORKSPACE
+    assert build(good, wsb=16) == binding.ERR_WORKSPACE
+    assert build(good, tb=8) == binding.ERR_WORKSPACE
+
+
+def test_group_call_validation(lib):
+    buf = (ctypes.c_uint8 * 256)()
+    assert lib.fairy2i_wl_matmul_group(None, P, None) == binding.ERR_NULL
+    assert lib.fairy2i_wl_matmul_group(ctypes.byref(buf), P, None) == binding.ERR_UNSUPPORTED  # not a table
+    ev = (ctypes.c_void_p * 4)(0x1000, 0x1000, None, 0x1000)
+    assert lib.fairy2i_wl_matmul_group_timed(ctypes.byref(buf), P, None, ev) == binding.ERR_NULL
+    assert lib.fairy2i_wl_matmul_group_timed(ctypes.byref(buf), P, None, None) == binding.ERR_NULL
