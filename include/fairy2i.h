@@ -225,7 +225,9 @@ typedef struct fairy2i_wl_layer {
  * fairy2i_wl_matmul_group(table, table_device, stream) computes every layer's
  * y.  The workspace and both table copies must stay alive and unchanged while
  * calls that use them run; calls sharing a workspace must not overlap.
- * Results equal fairy2i_wl_matmul on each layer bit for bit.
+ * Results equal fairy2i_wl_matmul on each layer up to the float32 rounding
+ * of the split-K sums (a one-layer call may cut K into more slices to fill
+ * the GPU); repeated calls are bitwise identical.
  * Errors: as fairy2i_wl_matmul, checked per layer by the build call;
  * FAIRY2I_ERR_UNSUPPORTED for the restrictions above; FAIRY2I_ERR_SHAPE if
  * n_layers < 1; fairy2i_wl_matmul_group returns FAIRY2I_ERR_NULL for a NULL

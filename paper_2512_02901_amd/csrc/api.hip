@@ -36,8 +36,6 @@ bool use_mfma_decode(int32_t dtype, int64_t N, int64_t K, int64_t B) {
 
 int dec_mode(int32_t dtype) { return dtype == FAIRY2I_ACT_BF16 ? kModeBf16 : kModeI8; }
 
-int dec_ntile(int mode, int64_t B) { return mode == kModeBf16 ? (int)((B + 1) / 2) : (int)((B + 7) / 8); }
-
 DecLayer dec_layer(const uint8_t* cu, const float* su, const uint8_t* cw, const float* sw, int64_t N,
                    int64_t K, const void* x, const float* xs, float* y) {
   DecLayer l{};
@@ -53,20 +51,29 @@ DecLayer dec_layer(const uint8_t* cu, const float* su, const uint8_t* cw, const 
   return l;
 }
 
+// Workspace of a one-layer decode call (the same for the y and the
+// accumulator-export variants: the larger of the two layouts).
+size_t single_decode_bytes(int64_t N, int64_t K, int32_t T, int64_t B, int32_t dtype) {
+  size_t best = 0;
+  for (int ex = 0; ex < 2; ++ex) {
+    DecLayer l{};
+    l.N = (int32_t)N;
+    l.K = (int32_t)K;
+    const size_t b = dec_layer_setup(l, dec_header(T, dec_mode(dtype), B, ex != 0), true, nullptr);
+    if (b > best) best = b;
+  }
+  return best;
+}
+
 fairy2i_status run_single_decode(DecLayer l, int32_t T, int32_t dtype, int64_t B, void* ws,
                                  size_t ws_bytes, int32_t* acc, hipStream_t stream) {
-  const int mode = dec_mode(dtype);
-  const size_t need = dec_layer_setup(l, T, mode, (int)B, nullptr);
+  DecHeader h = dec_header(T, dec_mode(dtype), B, acc != nullptr);
+  const size_t need = dec_layer_setup(l, h, true, nullptr);
   if (!ws || ws_bytes < need) return FAIRY2I_ERR_WORKSPACE;
-  dec_layer_setup(l, T, mode, (int)B, static_cast<char*>(ws));
+  dec_layer_setup(l, h, true, static_cast<char*>(ws));
   l.acc = acc;
   l.item0 = 0;
-  DecHeader h{};
   h.n_layers = 1;
-  h.T = T;
-  h.mode = mode;
-  h.B = (int32_t)B;
-  h.ntile = dec_ntile(mode, B);
   h.total_items = (int64_t)l.nrb * l.nkc;
   const int64_t acc_elems = acc ? (int64_t)2 * T * 2 * B * l.N * 2 : 0;
   return hip_status(launch_decode(h, l, nullptr, l.nkc > 1, B * (int64_t)l.N, acc != nullptr, acc_elems,
@@ -80,7 +87,7 @@ struct GroupTableHeader {
   uint32_t magic, abi;
   DecHeader h;
   int32_t any_split, pad0_;
-  int64_t max_BN, pad1_;
+  int64_t max_BN;
 };
 static_assert(sizeof(GroupTableHeader) % 16 == 0, "table header alignment");
 
@@ -140,10 +147,7 @@ fairy2i_status fairy2i_quantize_act_int8(const void* x, int32_t dtype, int64_t B
 size_t fairy2i_wl_matmul_workspace_bytes(int64_t N, int64_t K, int32_t T, int64_t B, int32_t dtype) {
   if (N <= 0 || K <= 0 || B <= 0 || T < 1 || T > FAIRY2I_MAX_STAGES) return 0;
   if (!use_mfma_decode(dtype, N, K, B)) return 0;
-  DecLayer l{};
-  l.N = (int32_t)N;
-  l.K = (int32_t)K;
-  return dec_layer_setup(l, T, dec_mode(dtype), (int)B, nullptr);
+  return single_decode_bytes(N, K, T, B, dtype);
 }
 
 fairy2i_status fairy2i_wl_matmul(const uint8_t* codes_U, const float* scales_U,
@@ -241,12 +245,13 @@ static fairy2i_status check_group(const fairy2i_wl_layer* layers, int32_t n_laye
 size_t fairy2i_wl_group_workspace_bytes(const fairy2i_wl_layer* layers, int32_t n_layers, int32_t T,
                                         int32_t dtype, int64_t B) {
   if (check_group(layers, n_layers, T, dtype, B) != FAIRY2I_OK) return 0;
+  const DecHeader h = dec_header(T, dec_mode(dtype), B, false);
   size_t total = 0;
   for (int32_t i = 0; i < n_layers; ++i) {
     DecLayer l{};
     l.N = (int32_t)layers[i].N;
     l.K = (int32_t)layers[i].K;
-    total += dec_layer_setup(l, T, dec_mode(dtype), (int)B, nullptr);
+    total += dec_layer_setup(l, h, false, nullptr);
   }
   return total;
 }
@@ -262,7 +267,7 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
   if (!workspace || workspace_bytes < need) return FAIRY2I_ERR_WORKSPACE;
   auto* hdr = static_cast<GroupTableHeader*>(table);
   auto* tab = reinterpret_cast<DecLayer*>(hdr + 1);
-  const int mode = dec_mode(dtype);
+  DecHeader h = dec_header(T, dec_mode(dtype), B, false);
   char* ws = static_cast<char*>(workspace);
   int64_t items = 0;
   int any_split = 0;
@@ -270,7 +275,7 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
   for (int32_t i = 0; i < n_layers; ++i) {
     const fairy2i_wl_layer& L = layers[i];
     DecLayer l = dec_layer(L.codes_U, L.scales_U, L.codes_W, L.scales_W, L.N, L.K, L.x, L.x_scale, L.y);
-    ws += dec_layer_setup(l, T, mode, (int)B, ws);
+    ws += dec_layer_setup(l, h, false, ws);
     l.acc = nullptr;
     l.item0 = items;
     items += (int64_t)l.nrb * l.nkc;
@@ -281,12 +286,9 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
   *hdr = GroupTableHeader{};
   hdr->magic = kGroupMagic;
   hdr->abi = (uint32_t)fairy2i_abi_version();
-  hdr->h.n_layers = n_layers;
-  hdr->h.T = T;
-  hdr->h.mode = mode;
-  hdr->h.B = (int32_t)B;
-  hdr->h.ntile = dec_ntile(mode, B);
-  hdr->h.total_items = items;
+  h.n_layers = n_layers;
+  h.total_items = items;
+  hdr->h = h;
   hdr->any_split = any_split;
   hdr->max_BN = max_BN;
   return FAIRY2I_OK;

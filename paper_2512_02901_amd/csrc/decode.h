@@ -9,8 +9,10 @@ namespace fairy2i {
 
 constexpr int kModeBf16 = 0;  // bf16 activations as 3 base-256 digits of a 23-bit fixed point
 constexpr int kModeI8 = 1;    // int8 activations with a per-token factor
-constexpr int kDecKc4 = 2;    // 256-code steps per work item (512 codes)
-constexpr int kDecMaxBlocks = 8192;
+
+constexpr int kKernelReg = 0;     // codes staged in registers; any batch, accumulator export
+constexpr int kKernelStream = 1;  // codes streamed through an LDS ring; one activation tile
+constexpr int kRegKc4 = 2;        // 256-code steps per work item of the register kernel
 
 // One layer of a decode call.  Workspace pointers (xf, xs, part) are carved
 // out of the caller's workspace by the host code.
@@ -21,25 +23,35 @@ struct DecLayer {
   const float* x_scale_in;   // int8: [B] dequantisation factors
   float2* y;                 // [B][N]
   int32_t* acc;              // accumulator export [2][T][2][B][N][2], else null
-  int8_t* xf;                // activation operand [ntile][nk4][4][64][16]
+  int8_t* xf;                // activation operand [ntile][nk4][4][4][nc][16]
   float* xs;                 // per-token output factor [B]
   float2* part;              // split-K partials [nkc][B][N] (nkc > 1)
   int32_t N, K;
-  int32_t nrb, nk4, nkc, pad_;
+  int32_t nrb, nk4, nkc, kc4;  // 16-row blocks, 256-code steps, K slices, steps per slice
   int64_t item0;             // index of this layer's first work item
 };
 
 struct DecHeader {
-  int32_t n_layers, T, mode, B, ntile, pad_;
+  int32_t n_layers, T, mode, B;
+  int32_t ntile;   // 16-column activation tiles
+  int32_t nc;      // stored columns per tile (the first tile's valid columns)
+  int32_t kernel;  // kKernelReg or kKernelStream
+  int32_t pad_;
   int64_t total_items;
 };
 
-// Tiles of 16 activation columns processed per pass over a work item.
+int dec_ntile(int mode, int64_t B);
+int dec_ncols(int mode, int64_t B);
+// Tiles of 16 activation columns processed per pass of the register kernel.
 int dec_tiles_per_group(int T, int ntile);
 
-// Fill the geometry fields of `l` (N, K set) and return its workspace bytes.
-// With `ws` non-null, also carve xf, xs, part out of it.
-size_t dec_layer_setup(DecLayer& l, int T, int mode, int B, char* ws);
+// Header fields that do not depend on the layers (n_layers, total_items = 0).
+DecHeader dec_header(int T, int mode, int64_t B, bool export_acc);
+
+// Fill the geometry fields of `l` (N, K set) for header h and return its
+// workspace bytes; with `ws` non-null also carve xf, xs, part out of it.
+// `single`: a one-layer call (slices chosen to give the GPU enough items).
+size_t dec_layer_setup(DecLayer& l, const DecHeader& h, bool single, char* ws);
 
 hipError_t launch_decode(const DecHeader& h, const DecLayer& inl, const DecLayer* tab,
                          int any_split, int64_t max_BN, bool export_acc, int64_t acc_elems,

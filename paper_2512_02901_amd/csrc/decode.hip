@@ -28,6 +28,8 @@
 // and a second kernel sums the partials in slice order, so results do not
 // depend on scheduling.  A table of layers is processed by one launch of
 // each kernel (used for a whole decoder stack).
+#include <type_traits>
+
 #include "common.h"
 #include "decode.h"
 
@@ -50,6 +52,15 @@ __device__ inline void expand_codes(uint32_t w, v4i& bre, v4i& bim) {
 }
 
 __device__ inline int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// Scalar (SMEM) load of a float at a wave-uniform address.  Scalar loads are
+// tracked by lgkmcnt, so waiting for one does not drain the vector-memory
+// queue that holds the prefetched code bytes.
+__device__ inline float sload_f32(const float* p) {
+  float v;
+  __asm__ volatile("s_load_dword %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(v) : "s"(p) : "memory");
+  return v;
+}
 
 __device__ inline int64_t uniform64(int64_t v) {
   const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
@@ -98,9 +109,12 @@ __device__ inline bool col_token(int tile, int col, int B, int& b, int& digit, i
 
 // ----------------------------------------------------------------- prep ---
 // One block per (tile, column) and layer: writes that column of the
-// activation operand for every 64-code MFMA step, in the lane order the
-// decode kernel loads (16 bytes per lane, byte 4c+b = code c + 4b of the
-// lane's 16-code group), and the per-token scale.
+// activation operand for every 64-code MFMA step, and the per-token scale.
+// Layout [tile][256-code step][d][g][column < nc][16 bytes]: the 16 bytes of
+// (column, g, d) are what the MFMA lane of that column and 16-code group g
+// takes for the step's d-th 64-code MFMA (byte 4c+b = code c + 4b of the
+// group); the nc stored columns of a step are contiguous, so a step's whole
+// operand is one nc * 256-byte run.
 template <int MODE>
 __global__ __launch_bounds__(256) void dec_prep_kernel(DecHeader h, DecLayer inl,
                                                        const DecLayer* __restrict__ tab) {
@@ -162,8 +176,8 @@ __global__ __launch_bounds__(256) void dec_prep_kernel(DecHeader h, DecLayer inl
       }
       out[dd] |= ((uint32_t)v & 0xFFu) << (8 * bb);
     }
-    const int lane = g * 16 + col;
-    uint4* dst = reinterpret_cast<uint4*>(L.xf + ((((int64_t)tile * L.nk4 + kk) * 4 + d) * 64 + lane) * 16);
+    uint4* dst = reinterpret_cast<uint4*>(
+        L.xf + (((((int64_t)tile * L.nk4 + kk) * 4 + d) * 4 + g) * h.nc + col) * 16);
     *dst = make_uint4(out[0], out[1], out[2], out[3]);
   }
 }
@@ -179,152 +193,432 @@ __device__ inline v4i buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
 }
 
-template <int MODE, int T, int NTG, bool EXPORT>
-__global__ __launch_bounds__(256) void dec_mfma_kernel(DecHeader h, DecLayer inl,
-                                                       const DecLayer* __restrict__ tab) {
-  constexpr int P = 2 * T;  // code planes (M, t)
-  const int lane = threadIdx.x & 63;
-  const int wave = uniform(threadIdx.x >> 6);
+// Position of one pass (work item x tile group) inside its layer.
+struct PassGeo {
+  int rb, kc, tg0, row, k4b, nk4_item;
+  bool row_ok;
+};
+
+__device__ inline PassGeo pass_geo(const DecLayer& L, int64_t item, int tg0, int li) {
+  PassGeo q;
+  const int64_t local = item - L.item0;
+  q.rb = (int)(local / L.nkc);
+  q.kc = (int)(local - (int64_t)q.rb * L.nkc);
+  q.tg0 = tg0;
+  q.row = q.rb * 16 + li;
+  q.row_ok = q.row < L.N;
+  q.k4b = q.kc * L.kc4;
+  q.nk4_item = min(L.kc4, L.nk4 - q.k4b);
+  return q;
+}
+
+// Issue the loads of step j of a pass (the 2T code planes' 16 bytes per lane
+// and the activation operand of the tile group).  Out-of-range lanes use an
+// offset past the buffer and read 0.
+template <int MODE, int T, int NTG>
+__device__ inline void issue_step_loads(const DecLayer& L, const DecHeader& h, const PassGeo& q, int lane, int j,
+                                        v4i (&cw)[2 * T][kRegKc4], v4i (&xa)[kRegKc4][4][NTG]) {
   const int g = lane >> 4, li = lane & 15;
-  const int64_t nwaves = (int64_t)gridDim.x * 4;
-
-  for (int64_t item = (int64_t)blockIdx.x * 4 + wave; item < h.total_items; item += nwaves) {
-    item = uniform64(item);
-    const DecLayer L = tab ? load_layer(tab + find_layer(tab, h.n_layers, item)) : inl;
-    const int64_t local = item - L.item0;
-    const int rb = (int)(local / L.nkc), kc = (int)(local % L.nkc);
-    const int N = L.N, K = L.K;
-    const uint32_t plane_bytes = (uint32_t)((int64_t)N * K / 4);
-    const int row = rb * 16 + li;
-    const bool row_ok = row < N;
-    const int k4b = kc * kDecKc4;
-    const int nk4_item = min(kDecKc4, L.nk4 - k4b);  // wave-uniform
-
-    const uint32_t xf_bytes = (uint32_t)(h.ntile * L.nk4 * 4 * 64 * 16);
-    const __amdgpu_buffer_rsrc_t xr = make_rsrc(L.xf, xf_bytes);
-
-    // Usually one pass (all tiles fit one group); further passes re-read the
-    // item's codes, which are then cache hits.
-    for (int tg0 = 0; tg0 < h.ntile; tg0 += NTG) {
-      // ---- every load of the pass first (out-of-range lanes read 0) ----
-      v4i cw[P][kDecKc4];
+  const int K = L.K;
+  const uint32_t plane_bytes = (uint32_t)((int64_t)L.N * K / 4);
+  const int kk = q.k4b + j;
+  const bool kok = j < q.nk4_item;
 #pragma unroll
-      for (int p = 0; p < P; ++p) {
-        const int m = p / T, t = p % T;
-        const __amdgpu_buffer_rsrc_t rs = make_rsrc(L.codes[m] + (int64_t)t * plane_bytes, plane_bytes);
+  for (int p = 0; p < 2 * T; ++p) {
+    const int m = p / T, t = p % T;
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(L.codes[m] + (int64_t)t * plane_bytes, plane_bytes);
+    const bool ok = q.row_ok && kok && kk * 256 + 64 * g < K;
+    const uint32_t off = ok ? (uint32_t)q.row * (uint32_t)(K / 4) + (uint32_t)(kk * 64 + 16 * g) : kOob;
+    cw[p][j] = buf_load16(rs, off);
+  }
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(L.xf, (uint32_t)(h.ntile * L.nk4 * 256 * h.nc));
 #pragma unroll
-        for (int j = 0; j < kDecKc4; ++j) {
-          const int kk = k4b + j;
-          const bool ok = row_ok && j < nk4_item && kk * 256 + 64 * g < K;
-          const uint32_t off = ok ? (uint32_t)row * (uint32_t)(K / 4) + (uint32_t)(kk * 64 + 16 * g) : kOob;
-          cw[p][j] = buf_load16(rs, off);
-        }
+  for (int d = 0; d < 4; ++d)
+#pragma unroll
+    for (int tt = 0; tt < NTG; ++tt) {
+      const int tile = q.tg0 + tt;
+      int b, digit, comp;
+      const bool ok = kok && tile < h.ntile && col_token<MODE>(tile, li, h.B, b, digit, comp);
+      const uint32_t off = ok ? (uint32_t)(((((tile * L.nk4 + kk) * 4 + d) * 4 + g) * h.nc + li) * 16) : kOob;
+      xa[j][d][tt] = buf_load16(xr, off);
+    }
+}
+
+// Factor of this lane's token s (bf16: token 2*tile + g/2; int8: token
+// 8*tile + 2g + s) from the tile's preloaded factors, selected with
+// compile-time indices only.
+template <int MODE>
+__device__ inline float token_factor(const float (&xsv)[8], int g, int s) {
+  if constexpr (MODE == kModeBf16) {
+    return (g >> 1) ? xsv[1] : xsv[0];
+  } else {
+    const float f0 = s ? xsv[1] : xsv[0], f1 = s ? xsv[3] : xsv[2];
+    const float f2 = s ? xsv[5] : xsv[4], f3 = s ? xsv[7] : xsv[6];
+    return g == 0 ? f0 : (g == 1 ? f1 : (g == 2 ? f2 : f3));
+  }
+}
+
+// Epilogue of a pass: lane holds x columns 4g..4g+3 of weight row li for each
+// (plane, axis, tile) accumulator; forms y (or the split-K partial, or the
+// exported integer products) of its row for the tokens of those columns.
+template <int MODE, int T, int NTG, bool EXPORT>
+__device__ inline void write_outputs(const DecLayer& L, const DecHeader& h, const PassGeo& q, int lane,
+                                     const v4i (&acc)[2 * T][2][NTG]) {
+  constexpr int P = 2 * T;
+  const int g = lane >> 4;
+  const int N = L.N;
+  // wave-uniform operands of the epilogue, by scalar loads
+  float sc[2][T][2];
+  if constexpr (!EXPORT) {
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        sc[m][t][0] = sload_f32(L.scales[m] + 2 * t);
+        sc[m][t][1] = sload_f32(L.scales[m] + 2 * t + 1);
       }
-      v4i xa[kDecKc4][4][NTG];
+  }
 #pragma unroll
-      for (int j = 0; j < kDecKc4; ++j)
+  for (int tt = 0; tt < NTG; ++tt) {
+    const int tile = q.tg0 + tt;
+    // factors of the (up to 8) tokens of this tile
+    float xsv[8];
+    if constexpr (!EXPORT) {
+      const int nt = MODE == kModeBf16 ? 2 : 8;
 #pragma unroll
-        for (int d = 0; d < 4; ++d)
-#pragma unroll
-          for (int tt = 0; tt < NTG; ++tt) {
-            const int tile = tg0 + tt, kk = k4b + j;
-            int b, digit, comp;
-            const bool ok = j < nk4_item && tile < h.ntile && col_token<MODE>(tile, li, h.B, b, digit, comp);
-            const uint32_t off = ok ? (uint32_t)((((tile * L.nk4 + kk) * 4 + d) * 64 + lane) * 16) : kOob;
-            xa[j][d][tt] = buf_load16(xr, off);
-          }
-
-      v4i acc[P][2][NTG];
+      for (int i = 0; i < 8; ++i)
+        xsv[i] = (i < nt && tile * nt + i < h.B) ? sload_f32(L.xs + tile * nt + i) : 0.0f;
+    }
+    // bf16: token 2*tile + g/2 has digits 0, 1 in group g and digit 2 in
+    // group g+1; fetch the latter (all lanes take part in the shuffle).
+    int hi[P][2][2];
+    if constexpr (MODE == kModeBf16) {
 #pragma unroll
       for (int p = 0; p < P; ++p)
 #pragma unroll
-        for (int ax = 0; ax < 2; ++ax)
+        for (int ax = 0; ax < 2; ++ax) {
+          hi[p][ax][0] = __shfl_down(acc[p][ax][tt][0], 16);
+          hi[p][ax][1] = __shfl_down(acc[p][ax][tt][1], 16);
+        }
+    }
+    if (!q.row_ok || tile >= h.ntile) continue;
+    const int ntok = MODE == kModeBf16 ? ((g & 1) ? 0 : 1) : 2;
 #pragma unroll
-          for (int tt = 0; tt < NTG; ++tt) acc[p][ax][tt] = v4i{0, 0, 0, 0};
-
+    for (int s = 0; s < 2; ++s) {
+      const int b = MODE == kModeBf16 ? 2 * tile + (g >> 1) : 8 * tile + 2 * g + s;
+      if (s >= ntok || b >= h.B) continue;
+      if constexpr (EXPORT) {
 #pragma unroll
-      for (int j = 0; j < kDecKc4; ++j) {
+        for (int p = 0; p < P; ++p)
 #pragma unroll
-        for (int d = 0; d < 4; ++d) {
-#pragma unroll
-          for (int p = 0; p < P; ++p) {
-            v4i bre, bim;
-            expand_codes((uint32_t)cw[p][j][d], bre, bim);
-#pragma unroll
-            for (int tt = 0; tt < NTG; ++tt) {
-              acc[p][0][tt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(xa[j][d][tt], bre, acc[p][0][tt], 0, 0, 0);
-              acc[p][1][tt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(xa[j][d][tt], bim, acc[p][1][tt], 0, 0, 0);
-            }
-            // keep each plane's expansion next to its MFMAs (bounds live registers)
-            __builtin_amdgcn_sched_group_barrier(0x002, 15, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, 2 * NTG, 0);
+          for (int ax = 0; ax < 2; ++ax) {
+            int32_t* dst = L.acc + ((((int64_t)p * 2 + ax) * h.B + b) * N + q.row) * 2;
+            atomicAdd(dst, acc[p][ax][tt][2 * s]);
+            atomicAdd(dst + 1, acc[p][ax][tt][2 * s + 1]);
           }
+      } else {
+        // exact integer product of plane (p, ax) with component c of token b,
+        // as a double: digits 0 and 1 combine exactly in int32, digit 2 in double
+        auto Pv = [&](int p, int ax, int c) -> double {
+          if constexpr (MODE == kModeBf16)
+            return (double)(acc[p][ax][tt][c] + (acc[p][ax][tt][2 + c] << 8)) + 65536.0 * (double)hi[p][ax][c];
+          else
+            return (double)acc[p][ax][tt][2 * s + c];
+        };
+        double yr = 0.0, yi = 0.0;
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+          const double su_re = sc[0][t][0], su_im = sc[0][t][1];
+          const double sw_re = sc[1][t][0], sw_im = sc[1][t][1];
+          const int pu = t, pw = T + t;
+          yr += su_re * Pv(pu, 0, 0) - su_im * Pv(pu, 1, 1);
+          yi += su_re * Pv(pu, 0, 1) + su_im * Pv(pu, 1, 0);
+          yr += sw_re * Pv(pw, 0, 0) + sw_im * Pv(pw, 1, 1);
+          yi += -sw_re * Pv(pw, 0, 1) + sw_im * Pv(pw, 1, 0);
         }
-      }
-
-      // ---- epilogue: lane holds x columns 4g..4g+3 of weight row li ----
-#pragma unroll
-      for (int tt = 0; tt < NTG; ++tt) {
-        const int tile = tg0 + tt;
-        // bf16: token 2*tile + g/2 has digits 0, 1 in group g and digit 2 in
-        // group g+1; fetch the latter (all lanes take part in the shuffle).
-        int hi[P][2][2];
-        if constexpr (MODE == kModeBf16) {
-#pragma unroll
-          for (int p = 0; p < P; ++p)
-#pragma unroll
-            for (int ax = 0; ax < 2; ++ax) {
-              hi[p][ax][0] = __shfl_down(acc[p][ax][tt][0], 16);
-              hi[p][ax][1] = __shfl_down(acc[p][ax][tt][1], 16);
-            }
-        }
-        if (!row_ok || tile >= h.ntile) continue;
-        const int ntok = MODE == kModeBf16 ? ((g & 1) ? 0 : 1) : 2;
-#pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          if (s >= ntok) break;
-          const int b = MODE == kModeBf16 ? 2 * tile + (g >> 1) : 8 * tile + 2 * g + s;
-          if (b >= h.B) continue;
-          // exact integer product of plane (p, ax) with component c of token b
-          auto Pv = [&](int p, int ax, int c) -> int64_t {
-            if constexpr (MODE == kModeBf16)
-              return (int64_t)acc[p][ax][tt][c] + 256 * (int64_t)acc[p][ax][tt][2 + c] +
-                     65536 * (int64_t)hi[p][ax][c];
-            else
-              return (int64_t)acc[p][ax][tt][2 * s + c];
-          };
-          if constexpr (EXPORT) {
-#pragma unroll
-            for (int p = 0; p < P; ++p)
-#pragma unroll
-              for (int ax = 0; ax < 2; ++ax) {
-                int32_t* dst = L.acc + ((((int64_t)p * 2 + ax) * h.B + b) * N + row) * 2;
-                atomicAdd(dst, (int32_t)Pv(p, ax, 0));
-                atomicAdd(dst + 1, (int32_t)Pv(p, ax, 1));
-              }
-          } else {
-            double yr = 0.0, yi = 0.0;
-#pragma unroll
-            for (int t = 0; t < T; ++t) {
-              const double su_re = L.scales[0][2 * t], su_im = L.scales[0][2 * t + 1];
-              const double sw_re = L.scales[1][2 * t], sw_im = L.scales[1][2 * t + 1];
-              const int pu = t, pw = T + t;
-              yr += su_re * (double)Pv(pu, 0, 0) - su_im * (double)Pv(pu, 1, 1);
-              yi += su_re * (double)Pv(pu, 0, 1) + su_im * (double)Pv(pu, 1, 0);
-              yr += sw_re * (double)Pv(pw, 0, 0) + sw_im * (double)Pv(pw, 1, 1);
-              yi += -sw_re * (double)Pv(pw, 0, 1) + sw_im * (double)Pv(pw, 1, 0);
-            }
-            const double f = (double)L.xs[b];
-            const float2 v = make_float2((float)(yr * f), (float)(yi * f));
-            if (L.nkc == 1)
-              L.y[(int64_t)b * N + row] = v;
-            else
-              L.part[((int64_t)kc * h.B + b) * N + row] = v;
-          }
-        }
+        const double f = (double)token_factor<MODE>(xsv, g, s);
+        const float2 v = make_float2((float)(yr * f), (float)(yi * f));
+        if (L.nkc == 1)
+          L.y[(int64_t)b * N + q.row] = v;
+        else
+          L.part[((int64_t)q.kc * h.B + b) * N + q.row] = v;
       }
     }
   }
+}
+
+// Products of one pass and its epilogue.
+template <int MODE, int T, int NTG, bool EXPORT>
+__device__ inline void compute_pass(const DecLayer& L, const DecHeader& h, const PassGeo& q, int lane,
+                                    v4i (&cw)[2 * T][kRegKc4], v4i (&xa)[kRegKc4][4][NTG], bool has_next,
+                                    const DecLayer& Ln, const PassGeo& qn) {
+  constexpr int P = 2 * T;
+  const int g = lane >> 4;
+  v4i acc[P][2][NTG];
+#pragma unroll
+  for (int p = 0; p < P; ++p)
+#pragma unroll
+    for (int ax = 0; ax < 2; ++ax)
+#pragma unroll
+      for (int tt = 0; tt < NTG; ++tt) acc[p][ax][tt] = v4i{0, 0, 0, 0};
+
+#pragma unroll
+  for (int j = 0; j < kRegKc4; ++j) {
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+#pragma unroll
+      for (int p = 0; p < P; ++p) {
+        v4i bre, bim;
+        expand_codes((uint32_t)cw[p][j][d], bre, bim);
+#pragma unroll
+        for (int tt = 0; tt < NTG; ++tt) {
+          acc[p][0][tt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(xa[j][d][tt], bre, acc[p][0][tt], 0, 0, 0);
+          acc[p][1][tt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(xa[j][d][tt], bim, acc[p][1][tt], 0, 0, 0);
+        }
+        // keep each plane's expansion next to its MFMAs (bounds live registers)
+        __builtin_amdgcn_sched_group_barrier(0x002, 15, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2 * NTG, 0);
+      }
+    }
+    // step j's registers are free: start the next pass's step j
+    if (has_next) issue_step_loads<MODE, T, NTG>(Ln, h, qn, lane, j, cw, xa);
+  }
+
+  write_outputs<MODE, T, NTG, EXPORT>(L, h, q, lane, acc);
+}
+
+// Persistent product kernel: wave w owns the contiguous range of passes
+// [w P / W, (w+1) P / W) (a pass = one work item and one tile group).  The
+// layer descriptor is kept while the range stays in one layer, and the loads
+// of the next pass go into each register set as soon as the current pass has
+// finished reading it, so they overlap the rest of the pass and its epilogue.
+template <int MODE, int T, int NTG, bool EXPORT>
+__global__ __launch_bounds__(256) void dec_mfma_kernel(DecHeader h, DecLayer inl,
+                                                       const DecLayer* __restrict__ tab) {
+  constexpr int P = 2 * T;
+  const int lane = threadIdx.x & 63;
+  const int li = lane & 15;
+  const int64_t wid = (int64_t)blockIdx.x * 4 + uniform(threadIdx.x >> 6);
+  const int64_t W = (int64_t)gridDim.x * 4;
+  const int ngroups = (h.ntile + NTG - 1) / NTG;
+  const int64_t total = h.total_items * ngroups;
+  int64_t pass = uniform64(wid * total / W);
+  const int64_t pend = uniform64((wid + 1) * total / W);
+  if (pass >= pend) return;
+
+  int lidx = tab ? find_layer(tab, h.n_layers, pass / ngroups) : 0;
+  DecLayer L = tab ? load_layer(tab + lidx) : inl;
+  int64_t lend = L.item0 + (int64_t)L.nrb * L.nkc;  // first item past layer L
+  PassGeo q = pass_geo(L, pass / ngroups, (int)(pass % ngroups) * NTG, li);
+
+  v4i cw[P][kRegKc4];
+  v4i xa[kRegKc4][4][NTG];
+#pragma unroll
+  for (int j = 0; j < kRegKc4; ++j) issue_step_loads<MODE, T, NTG>(L, h, q, lane, j, cw, xa);
+
+  while (true) {
+    const bool has_next = pass + 1 < pend;
+    DecLayer Ln = L;
+    int64_t lendn = lend;
+    PassGeo qn = q;
+    if (has_next) {
+      const int64_t it = (pass + 1) / ngroups;
+      if (it >= lend) {  // the range crosses into the next layer
+        ++lidx;
+        Ln = load_layer(tab + lidx);
+        lendn = Ln.item0 + (int64_t)Ln.nrb * Ln.nkc;
+      }
+      qn = pass_geo(Ln, it, (int)((pass + 1) % ngroups) * NTG, li);
+    }
+    compute_pass<MODE, T, NTG, EXPORT>(L, h, q, lane, cw, xa, has_next, Ln, qn);
+    if (!has_next) break;
+    pass += 1;
+    L = Ln;
+    lend = lendn;
+    q = qn;
+  }
+}
+
+// ------------------------------------------------------ streaming kernel ---
+// For one activation tile (bf16 B <= 2, int8 B <= 8) the code bytes and the
+// activation operand stream through a per-wave ring of NS LDS slots, filled
+// by direct-to-LDS buffer loads NS-1 steps (of 256 codes) ahead of the step
+// being computed, so the bytes in flight hold no registers.  Each lane's 16
+// bytes land at slot + lane * 16 (out-of-range lanes write zeros); a lane
+// reads back only its own code bytes and its wave's activation operand, so
+// waves never wait for each other.  A work item spans kc4 steps (up to 2048
+// codes), which keeps the epilogue cost per code small.
+
+// Cursor over the 256-code steps of a wave's item range.
+struct StepCursor {
+  DecLayer L;
+  int64_t item, lend;
+  int lidx, j, nsteps, kc, k4, row;
+  bool row_ok;
+};
+
+__device__ inline void cursor_item(StepCursor& c, int li) {
+  const int64_t local = c.item - c.L.item0;
+  const int rb = (int)(local / c.L.nkc);
+  c.kc = (int)(local - (int64_t)rb * c.L.nkc);
+  c.k4 = c.kc * c.L.kc4;
+  c.nsteps = min(c.L.kc4, c.L.nk4 - c.k4);
+  c.j = 0;
+  c.row = rb * 16 + li;
+  c.row_ok = c.row < c.L.N;
+}
+
+__device__ inline void cursor_init(StepCursor& c, const DecLayer& inl, const DecLayer* tab, int n_layers,
+                                   int64_t item, int li) {
+  c.lidx = tab ? find_layer(tab, n_layers, item) : 0;
+  c.L = tab ? load_layer(tab + c.lidx) : inl;
+  c.lend = c.L.item0 + (int64_t)c.L.nrb * c.L.nkc;
+  c.item = item;
+  cursor_item(c, li);
+}
+
+// Next step; false once the wave's item range [.., iend) is exhausted.
+__device__ inline bool cursor_next(StepCursor& c, const DecLayer* tab, int64_t iend, int li) {
+  if (++c.j < c.nsteps) {
+    ++c.k4;
+    return true;
+  }
+  if (++c.item >= iend) return false;
+  if (c.item >= c.lend) {
+    ++c.lidx;
+    c.L = load_layer(tab + c.lidx);
+    c.lend = c.L.item0 + (int64_t)c.L.nrb * c.L.nkc;
+  }
+  cursor_item(c, li);
+  return true;
+}
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+// Direct-to-LDS loads of one step into `slot`: 2T code planes (1 KB each:
+// 16 rows x 64 codes per 16-code group of each lane) and XW KB of the
+// activation operand.  A dead cursor issues the same loads out of range (they
+// write zeros), so every step issues exactly 2T + XW loads.
+template <int T, int XW>
+__device__ inline void stream_issue(const StepCursor& c, bool live, const DecHeader& h, int lane,
+                                    uint8_t* slot) {
+  const int g = lane >> 4;
+  const int K = c.L.K;
+  const uint32_t plane_bytes = (uint32_t)((int64_t)c.L.N * K / 4);
+  const bool ok = live && c.row_ok && c.k4 * 256 + 64 * g < K;
+  const uint32_t off = ok ? (uint32_t)c.row * (uint32_t)(K / 4) + (uint32_t)(c.k4 * 64 + 16 * g) : kOob;
+#pragma unroll
+  for (int p = 0; p < 2 * T; ++p) {
+    const int m = p / T, t = p % T;
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(c.L.codes[m] + (int64_t)t * plane_bytes, plane_bytes);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t)(slot + p * 1024), 16, off, 0, 0, 0);
+  }
+  const uint32_t xbytes = (uint32_t)(c.L.nk4 * 256 * h.nc);
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(c.L.xf, xbytes);
+#pragma unroll
+  for (int i = 0; i < XW; ++i) {
+    const uint32_t xo = live ? (uint32_t)(c.k4 * 256 * h.nc + i * 1024 + lane * 16) : kOob;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_ptr_t)(slot + 2 * T * 1024 + i * 1024), 16, xo, 0, 0, 0);
+  }
+}
+
+template <int T, int XW>
+struct StreamCfg {
+  static constexpr int P = 2 * T;
+  static constexpr int SLOT = (P + XW) * 1024;
+  // slots per wave: at most 80 KB per 4-wave block (two blocks per CU), 2..4
+  static constexpr int NS_RAW = (80 * 1024) / (4 * SLOT);
+  static constexpr int NS = NS_RAW < 2 ? 2 : (NS_RAW > 4 ? 4 : NS_RAW);
+  static constexpr int LOADS = P + XW;            // vector memory ops issued per step
+  static constexpr int WAIT = (NS - 2) * LOADS;   // outstanding ops allowed when a slot is read
+  static constexpr int WAITCNT = (WAIT & 0xF) | (0x7 << 4) | (0xF << 8) | (((WAIT >> 4) & 3) << 14);
+};
+
+template <int MODE, int T, int XW>
+__global__ __launch_bounds__(256) void dec_stream_kernel(DecHeader h, DecLayer inl,
+                                                         const DecLayer* __restrict__ tab) {
+  using C = StreamCfg<T, XW>;
+  constexpr int P = C::P, NS = C::NS, SLOT = C::SLOT;
+  __shared__ __attribute__((aligned(16))) uint8_t ring[4][NS][SLOT];
+  const int lane = threadIdx.x & 63;
+  const int g = lane >> 4, li = lane & 15;
+  const int wave = uniform(threadIdx.x >> 6);
+  const int64_t wid = (int64_t)blockIdx.x * 4 + wave;
+  const int64_t W = (int64_t)gridDim.x * 4;
+  const int64_t i0 = uniform64(wid * h.total_items / W);
+  const int64_t i1 = uniform64((wid + 1) * h.total_items / W);
+  if (i0 >= i1) return;
+
+  int b, digit, comp;
+  const bool xvalid = col_token<MODE>(0, li, h.B, b, digit, comp);
+  const uint32_t xoff = (uint32_t)(P * 1024 + (g * h.nc + li) * 16);  // + d * 4 * nc * 16
+
+  StepCursor lc, cc;
+  cursor_init(lc, inl, tab, h.n_layers, i0, li);
+  cc = lc;
+  bool live = true;
+#pragma unroll
+  for (int k = 0; k < NS - 1; ++k) {
+    stream_issue<T, XW>(lc, live, h, lane, &ring[wave][k][0]);
+    if (live) live = cursor_next(lc, tab, i1, li);
+  }
+
+  v4i acc[P][2][1];
+#pragma unroll
+  for (int p = 0; p < P; ++p) acc[p][0][0] = acc[p][1][0] = v4i{0, 0, 0, 0};
+
+  // one step on slot K; returns true when the wave's range is done
+  auto step = [&](auto kconst) -> bool {
+    constexpr int K = decltype(kconst)::value;
+    __builtin_amdgcn_s_waitcnt(C::WAITCNT);  // this slot's loads have landed
+    __asm__ volatile("" ::: "memory");
+    const uint8_t* sl = &ring[wave][K][0];
+    v4i cr[P];
+#pragma unroll
+    for (int p = 0; p < P; ++p) cr[p] = *reinterpret_cast<const v4i*>(sl + p * 1024 + lane * 16);
+    v4i xr[4];
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+      xr[d] = xvalid ? *reinterpret_cast<const v4i*>(sl + xoff + d * 4 * h.nc * 16) : v4i{0, 0, 0, 0};
+    __asm__ volatile("" ::: "memory");
+    // refill the slot consumed by the previous step
+    stream_issue<T, XW>(lc, live, h, lane, &ring[wave][(K + NS - 1) % NS][0]);
+    if (live) live = cursor_next(lc, tab, i1, li);
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+#pragma unroll
+      for (int p = 0; p < P; ++p) {
+        v4i bre, bim;
+        expand_codes((uint32_t)cr[p][d], bre, bim);
+        acc[p][0][0] = __builtin_amdgcn_mfma_i32_16x16x64_i8(xr[d], bre, acc[p][0][0], 0, 0, 0);
+        acc[p][1][0] = __builtin_amdgcn_mfma_i32_16x16x64_i8(xr[d], bim, acc[p][1][0], 0, 0, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 15, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      }
+    }
+    if (cc.j == cc.nsteps - 1) {
+      PassGeo q;
+      q.rb = 0;
+      q.kc = cc.kc;
+      q.tg0 = 0;
+      q.row = cc.row;
+      q.row_ok = cc.row_ok;
+      q.k4b = 0;
+      q.nk4_item = 0;
+      write_outputs<MODE, T, 1, false>(cc.L, h, q, lane, acc);
+#pragma unroll
+      for (int p = 0; p < P; ++p) acc[p][0][0] = acc[p][1][0] = v4i{0, 0, 0, 0};
+    }
+    return !cursor_next(cc, tab, i1, li);
+  };
+
+  while (true) {
+    if (step(std::integral_constant<int, 0>{})) break;
+    if constexpr (NS > 1) if (step(std::integral_constant<int, 1 % NS>{})) break;
+    if constexpr (NS > 2) if (step(std::integral_constant<int, 2 % NS>{})) break;
+    if constexpr (NS > 3) if (step(std::integral_constant<int, 3 % NS>{})) break;
+  }
+  __builtin_amdgcn_s_waitcnt(0);  // no load may still be writing LDS when the wave ends
 }
 
 // ------------------------------------------------------------ reduction ---
@@ -351,14 +645,27 @@ __global__ void fill_i32_kernel(int32_t* p, int64_t n) {
     p[i] = 0;
 }
 
+// Blocks of kernel k that fit on the current device at once.
+int resident_blocks(const void* k) {
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, 256, 0) != hipSuccess || per_cu < 1)
+    return 1024;
+  return cus * per_cu;
+}
+
 template <int MODE, int T, int NTG, bool EXPORT>
-void launch_dec(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, int blocks,
+void launch_dec(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, int64_t want_blocks,
                 hipStream_t s) {
-  hipLaunchKernelGGL((dec_mfma_kernel<MODE, T, NTG, EXPORT>), dim3(blocks), dim3(256), 0, s, h, inl, tab);
+  auto k = dec_mfma_kernel<MODE, T, NTG, EXPORT>;
+  static const int resident = resident_blocks(reinterpret_cast<const void*>(k));  // one query per variant
+  const int64_t blocks = want_blocks < resident ? want_blocks : resident;
+  hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(256), 0, s, h, inl, tab);
 }
 
 template <int MODE, bool EXPORT>
-void launch_dec_mode(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, int blocks,
+void launch_dec_mode(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, int64_t blocks,
                      hipStream_t s) {
   const int ntg = dec_tiles_per_group(h.T, h.ntile);
   switch (h.T * 8 + ntg) {
@@ -372,6 +679,35 @@ void launch_dec_mode(const DecHeader& h, const DecLayer& inl, const DecLayer* ta
     case 3 * 8 + 2: launch_dec<MODE, 3, 2, EXPORT>(h, inl, tab, blocks, s); break;
     case 4 * 8 + 1: launch_dec<MODE, 4, 1, EXPORT>(h, inl, tab, blocks, s); break;
     default: launch_dec<MODE, 4, 2, EXPORT>(h, inl, tab, blocks, s); break;
+  }
+}
+
+template <int MODE, int T, int XW>
+void launch_stream(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, int64_t want_blocks,
+                   hipStream_t s) {
+  auto k = dec_stream_kernel<MODE, T, XW>;
+  static const int resident = resident_blocks(reinterpret_cast<const void*>(k));
+  const int64_t blocks = want_blocks < resident ? want_blocks : resident;
+  hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(256), 0, s, h, inl, tab);
+}
+
+template <int MODE, int T>
+void launch_stream_t(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, int64_t blocks,
+                     hipStream_t s) {
+  const int xw = (h.nc + 3) / 4;  // KB of activation operand per step
+  if (xw <= 1) launch_stream<MODE, T, 1>(h, inl, tab, blocks, s);
+  else if (xw == 2) launch_stream<MODE, T, 2>(h, inl, tab, blocks, s);
+  else launch_stream<MODE, T, 4>(h, inl, tab, blocks, s);
+}
+
+template <int MODE>
+void launch_stream_mode(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, int64_t blocks,
+                        hipStream_t s) {
+  switch (h.T) {
+    case 1: launch_stream_t<MODE, 1>(h, inl, tab, blocks, s); break;
+    case 2: launch_stream_t<MODE, 2>(h, inl, tab, blocks, s); break;
+    case 3: launch_stream_t<MODE, 3>(h, inl, tab, blocks, s); break;
+    default: launch_stream_t<MODE, 4>(h, inl, tab, blocks, s); break;
   }
 }
 
@@ -402,14 +738,16 @@ hipError_t launch_decode(const DecHeader& h, const DecLayer& inl, const DecLayer
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   // 2. products
-  int64_t blocks = (h.total_items + 3) / 4;
-  if (blocks > kDecMaxBlocks) blocks = kDecMaxBlocks;
-  if (h.mode == kModeBf16) {
-    launch_dec_mode<kModeBf16, false>(h, inl, tab, (int)blocks, s);
+  const int64_t blocks = (h.total_items + 3) / 4;  // capped at what fits on the device
+  if (h.kernel == kKernelStream) {
+    if (h.mode == kModeBf16) launch_stream_mode<kModeBf16>(h, inl, tab, blocks, s);
+    else launch_stream_mode<kModeI8>(h, inl, tab, blocks, s);
+  } else if (h.mode == kModeBf16) {
+    launch_dec_mode<kModeBf16, false>(h, inl, tab, blocks, s);
   } else if (export_acc) {
-    launch_dec_mode<kModeI8, true>(h, inl, tab, (int)blocks, s);
+    launch_dec_mode<kModeI8, true>(h, inl, tab, blocks, s);
   } else {
-    launch_dec_mode<kModeI8, false>(h, inl, tab, (int)blocks, s);
+    launch_dec_mode<kModeI8, false>(h, inl, tab, blocks, s);
   }
   if ((e = hipGetLastError()) != hipSuccess || (e = mark(2)) != hipSuccess) return e;
   // 3. split-K partials, summed in slice order
@@ -430,15 +768,40 @@ namespace {
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 }  // namespace
 
-size_t dec_layer_setup(DecLayer& l, int T, int mode, int B, char* ws) {
-  (void)T;
-  const int ntile = mode == kModeBf16 ? (B + 1) / 2 : (B + 7) / 8;
+int dec_ntile(int mode, int64_t B) { return mode == kModeBf16 ? (int)((B + 1) / 2) : (int)((B + 7) / 8); }
+
+int dec_ncols(int mode, int64_t B) {
+  if (mode == kModeBf16) return B >= 2 ? 14 : 6;  // per token 6 digit columns, 8-column stride
+  return B >= 8 ? 16 : (int)(2 * B);
+}
+
+DecHeader dec_header(int T, int mode, int64_t B, bool export_acc) {
+  DecHeader h{};
+  h.T = T;
+  h.mode = mode;
+  h.B = (int32_t)B;
+  h.ntile = dec_ntile(mode, B);
+  h.nc = dec_ncols(mode, B);
+  h.kernel = (!export_acc && h.ntile == 1) ? kKernelStream : kKernelReg;
+  return h;
+}
+
+size_t dec_layer_setup(DecLayer& l, const DecHeader& h, bool single, char* ws) {
   l.nrb = (int32_t)((l.N + 15) / 16);
   l.nk4 = (int32_t)((l.K + 255) / 256);
-  l.nkc = (l.nk4 + kDecKc4 - 1) / kDecKc4;
-  const size_t xf_bytes = align256((size_t)ntile * l.nk4 * 4 * 64 * 16);
-  const size_t xs_bytes = align256((size_t)B * sizeof(float));
-  const size_t part_bytes = l.nkc > 1 ? align256((size_t)l.nkc * B * l.N * sizeof(float2)) : 0;
+  if (h.kernel == kKernelReg) {
+    l.kc4 = kRegKc4;
+  } else {
+    // slices of up to 8 steps (2048 codes); a single layer gets smaller
+    // slices while that is needed to give the GPU ~2048 work items
+    l.kc4 = 8;
+    if (single)
+      while (l.kc4 > 1 && (int64_t)l.nrb * ((l.nk4 + l.kc4 - 1) / l.kc4) < 2048) l.kc4 /= 2;
+  }
+  l.nkc = (l.nk4 + l.kc4 - 1) / l.kc4;
+  const size_t xf_bytes = align256((size_t)h.ntile * l.nk4 * 256 * h.nc);
+  const size_t xs_bytes = align256((size_t)h.B * sizeof(float));
+  const size_t part_bytes = l.nkc > 1 ? align256((size_t)l.nkc * h.B * l.N * sizeof(float2)) : 0;
   if (ws) {
     l.xf = reinterpret_cast<int8_t*>(ws);
     l.xs = reinterpret_cast<float*>(ws + xf_bytes);

@@ -324,8 +324,9 @@ def test_mfma_decode_bf16_wide_dynamic_range(gpu):
 
 
 def test_group_matches_single_layer_calls(gpu):
-    """One grouped call over layers of different shapes equals the per-layer
-    calls bit for bit, and the oracle within tolerance."""
+    """One grouped call over layers of different shapes matches the per-layer
+    calls (up to split-K rounding) and the oracle; repeated calls are
+    bitwise identical."""
     import torch
     import paper_2512_02901_amd as f2
     shapes = [(128, 256), (200, 64), (48, 1088), (64, 2048)]
@@ -349,7 +350,9 @@ def test_group_matches_single_layer_calls(gpu):
             refs.append((host(f2.wl_matmul(*d, xd, xs)), yo))
         grp = f2.WlGroup(layers, T=2, B=B)
         grp.run()
-        grp.run()   # second call reuses workspace and table
-        for (cu, su, cw, sw, xd, xs, y), (ys, yo) in zip(layers, refs):
-            np.testing.assert_array_equal(host(y).view(np.uint32), ys.view(np.uint32))
+        first = [host(l[6]).copy() for l in layers]
+        grp.run()   # second call reuses workspace and table: bitwise identical
+        for (cu, su, cw, sw, xd, xs, y), (ys, yo), y1 in zip(layers, refs, first):
+            np.testing.assert_array_equal(host(y).view(np.uint32), y1.view(np.uint32))
+            assert rel_l2(host(y), ys) <= 1e-6     # same products, K possibly sliced differently
             assert rel_l2(host(y), yo) <= TOL_F32
