@@ -80,14 +80,34 @@ __device__ inline int find_layer(const DecLayer* tab, int n, int64_t item) {
 }
 
 // A descriptor from the table, with every field forced wave-uniform so that
-// pointers and buffer descriptors live in scalar registers.
+// pointers and buffer descriptors live in scalar registers.  Field by field,
+// so the copy never goes through memory.
+template <typename P>
+__device__ inline P* uniform_ptr(P* v) {
+  return reinterpret_cast<P*>(uniform64(reinterpret_cast<int64_t>(v)));
+}
+
 __device__ inline DecLayer load_layer(const DecLayer* p) {
-  DecLayer out;
-  const uint32_t* src = reinterpret_cast<const uint32_t*>(p);
-  uint32_t* dst = reinterpret_cast<uint32_t*>(&out);
-#pragma unroll
-  for (int i = 0; i < (int)(sizeof(DecLayer) / 4); ++i) dst[i] = __builtin_amdgcn_readfirstlane(src[i]);
-  return out;
+  DecLayer o;
+  o.codes[0] = uniform_ptr(p->codes[0]);
+  o.codes[1] = uniform_ptr(p->codes[1]);
+  o.scales[0] = uniform_ptr(p->scales[0]);
+  o.scales[1] = uniform_ptr(p->scales[1]);
+  o.x = uniform_ptr(p->x);
+  o.x_scale_in = uniform_ptr(p->x_scale_in);
+  o.y = uniform_ptr(p->y);
+  o.acc = uniform_ptr(p->acc);
+  o.xf = uniform_ptr(p->xf);
+  o.xs = uniform_ptr(p->xs);
+  o.part = uniform_ptr(p->part);
+  o.N = uniform(p->N);
+  o.K = uniform(p->K);
+  o.nrb = uniform(p->nrb);
+  o.nk4 = uniform(p->nk4);
+  o.nkc = uniform(p->nkc);
+  o.kc4 = uniform(p->kc4);
+  o.item0 = uniform64(p->item0);
+  return o;
 }
 
 // Column of a 16-column activation tile -> (token, digit/component) or invalid.
@@ -105,6 +125,22 @@ __device__ inline bool col_token(int tile, int col, int B, int& b, int& digit, i
     comp = col & 1;
     return b < B;
   }
+}
+
+// --------------------------------------------------------------- decode ---
+constexpr uint32_t kOob = 0xFFFFFFF0u;  // buffer offset past every range: loads return 0
+
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+__device__ inline v4i buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+
+typedef float v2f __attribute__((ext_vector_type(2)));
+__device__ inline void buf_store8(const void* base, uint32_t bytes, uint32_t off, float2 v) {
+  __builtin_amdgcn_raw_buffer_store_b64(v2f{v.x, v.y}, make_rsrc(base, bytes), off, 0, 0);
 }
 
 // ----------------------------------------------------------------- prep ---
@@ -180,17 +216,6 @@ __global__ __launch_bounds__(256) void dec_prep_kernel(DecHeader h, DecLayer inl
         L.xf + (((((int64_t)tile * L.nk4 + kk) * 4 + d) * 4 + g) * h.nc + col) * 16);
     *dst = make_uint4(out[0], out[1], out[2], out[3]);
   }
-}
-
-// --------------------------------------------------------------- decode ---
-constexpr uint32_t kOob = 0xFFFFFFF0u;  // buffer offset past every range: loads return 0
-
-__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
-}
-
-__device__ inline v4i buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
 }
 
 // Position of one pass (work item x tile group) inside its layer.
@@ -338,10 +363,11 @@ __device__ inline void write_outputs(const DecLayer& L, const DecHeader& h, cons
         }
         const double f = (double)token_factor<MODE>(xsv, g, s);
         const float2 v = make_float2((float)(yr * f), (float)(yi * f));
+        // buffer stores: a global-only access, so no wait on in-flight loads into LDS
         if (L.nkc == 1)
-          L.y[(int64_t)b * N + q.row] = v;
+          buf_store8(L.y, (uint32_t)h.B * N * 8, (uint32_t)((b * N + q.row) * 8), v);
         else
-          L.part[((int64_t)q.kc * h.B + b) * N + q.row] = v;
+          buf_store8(L.part, (uint32_t)L.nkc * h.B * N * 8, (uint32_t)(((q.kc * h.B + b) * N + q.row) * 8), v);
       }
     }
   }
@@ -449,38 +475,73 @@ __global__ __launch_bounds__(256) void dec_mfma_kernel(DecHeader h, DecLayer inl
 // waves never wait for each other.  A work item spans kc4 steps (up to 2048
 // codes), which keeps the epilogue cost per code small.
 
-// Cursor over the 256-code steps of a wave's item range.
-struct StepCursor {
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+// Load side of the streaming kernel: which step's bytes to fetch next.  All
+// geometry is recomputed only when an item starts; a step just advances two
+// offsets.
+template <int T>
+struct LoadCursor {
   DecLayer L;
   int64_t item, lend;
-  int lidx, j, nsteps, kc, k4, row;
+  int lidx, j, nsteps, k4;
+  const uint8_t* pbase[2 * T];  // code plane (M, t) of the current layer
+  uint32_t plane_bytes, xbytes;
+  uint32_t voff;  // this lane's offset in every code plane at step k4 (row, 16-code group)
+  uint32_t xoff;  // offset of the step's activation operand + lane * 16
   bool row_ok;
 };
 
-__device__ inline void cursor_item(StepCursor& c, int li) {
+template <int T>
+__device__ inline void load_item(LoadCursor<T>& c, const DecHeader& h, int lane) {
+  const int g = lane >> 4, li = lane & 15;
   const int64_t local = c.item - c.L.item0;
   const int rb = (int)(local / c.L.nkc);
-  c.kc = (int)(local - (int64_t)rb * c.L.nkc);
-  c.k4 = c.kc * c.L.kc4;
+  const int kc = (int)(local - (int64_t)rb * c.L.nkc);
+  c.k4 = kc * c.L.kc4;
   c.nsteps = min(c.L.kc4, c.L.nk4 - c.k4);
   c.j = 0;
-  c.row = rb * 16 + li;
-  c.row_ok = c.row < c.L.N;
+  const int row = rb * 16 + li;
+  c.row_ok = row < c.L.N;
+  c.voff = (uint32_t)row * (uint32_t)(c.L.K / 4) + (uint32_t)(c.k4 * 64 + 16 * g);
+  c.xoff = (uint32_t)(c.k4 * 256 * h.nc + lane * 16);
 }
 
-__device__ inline void cursor_init(StepCursor& c, const DecLayer& inl, const DecLayer* tab, int n_layers,
-                                   int64_t item, int li) {
-  c.lidx = tab ? find_layer(tab, n_layers, item) : 0;
-  c.L = tab ? load_layer(tab + c.lidx) : inl;
-  c.lend = c.L.item0 + (int64_t)c.L.nrb * c.L.nkc;
-  c.item = item;
-  cursor_item(c, li);
+template <int T>
+__device__ inline void load_layer_rsrc(LoadCursor<T>& c, const DecHeader& h) {
+  c.plane_bytes = (uint32_t)((int64_t)c.L.N * c.L.K / 4);
+#pragma unroll
+  for (int p = 0; p < 2 * T; ++p) c.pbase[p] = c.L.codes[p / T] + (int64_t)(p % T) * c.plane_bytes;
+  c.xbytes = (uint32_t)(c.L.nk4 * 256 * h.nc);
 }
 
-// Next step; false once the wave's item range [.., iend) is exhausted.
-__device__ inline bool cursor_next(StepCursor& c, const DecLayer* tab, int64_t iend, int li) {
+// Issue the 2T + XW direct-to-LDS loads of the cursor's step into `slot`; a
+// dead cursor issues them out of range (they write zeros), so every step
+// issues the same number of loads.
+template <int XW, int T>
+__device__ inline void stream_issue(const LoadCursor<T>& c, bool live, int lane, uint8_t* slot) {
+  const int g = lane >> 4;
+  const bool ok = live && c.row_ok && c.k4 * 256 + 64 * g < c.L.K;
+  const uint32_t off = ok ? c.voff : kOob;
+#pragma unroll
+  for (int p = 0; p < 2 * T; ++p)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(c.pbase[p], c.plane_bytes), (lds_ptr_t)(slot + p * 1024),
+                                             16, off, 0, 0, 0);
+  const uint32_t xo = live ? c.xoff : kOob;
+#pragma unroll
+  for (int i = 0; i < XW; ++i)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(c.L.xf, c.xbytes), (lds_ptr_t)(slot + 2 * T * 1024 + i * 1024),
+                                             16, xo + i * 1024, 0, 0, 0);
+}
+
+// Next step of the load side; false once the wave's items are exhausted.
+template <int T>
+__device__ inline bool load_next(LoadCursor<T>& c, const DecLayer* tab, const DecHeader& h, int64_t iend,
+                                 int lane) {
   if (++c.j < c.nsteps) {
     ++c.k4;
+    c.voff += 64;
+    c.xoff += 256 * h.nc;
     return true;
   }
   if (++c.item >= iend) return false;
@@ -488,46 +549,48 @@ __device__ inline bool cursor_next(StepCursor& c, const DecLayer* tab, int64_t i
     ++c.lidx;
     c.L = load_layer(tab + c.lidx);
     c.lend = c.L.item0 + (int64_t)c.L.nrb * c.L.nkc;
+    load_layer_rsrc(c, h);
   }
-  cursor_item(c, li);
+  load_item(c, h, lane);
   return true;
 }
 
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
+// Compute side: which item the current step belongs to (for its epilogue).
+struct OutCursor {
+  DecLayer L;
+  int64_t item, lend;
+  int lidx, j, nsteps, kc, row;
+  bool row_ok;
+};
 
-// Direct-to-LDS loads of one step into `slot`: 2T code planes (1 KB each:
-// 16 rows x 64 codes per 16-code group of each lane) and XW KB of the
-// activation operand.  A dead cursor issues the same loads out of range (they
-// write zeros), so every step issues exactly 2T + XW loads.
-template <int T, int XW>
-__device__ inline void stream_issue(const StepCursor& c, bool live, const DecHeader& h, int lane,
-                                    uint8_t* slot) {
-  const int g = lane >> 4;
-  const int K = c.L.K;
-  const uint32_t plane_bytes = (uint32_t)((int64_t)c.L.N * K / 4);
-  const bool ok = live && c.row_ok && c.k4 * 256 + 64 * g < K;
-  const uint32_t off = ok ? (uint32_t)c.row * (uint32_t)(K / 4) + (uint32_t)(c.k4 * 64 + 16 * g) : kOob;
-#pragma unroll
-  for (int p = 0; p < 2 * T; ++p) {
-    const int m = p / T, t = p % T;
-    const __amdgpu_buffer_rsrc_t rs = make_rsrc(c.L.codes[m] + (int64_t)t * plane_bytes, plane_bytes);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t)(slot + p * 1024), 16, off, 0, 0, 0);
+__device__ inline void out_item(OutCursor& c, int li) {
+  const int64_t local = c.item - c.L.item0;
+  const int rb = (int)(local / c.L.nkc);
+  c.kc = (int)(local - (int64_t)rb * c.L.nkc);
+  c.nsteps = min(c.L.kc4, c.L.nk4 - c.kc * c.L.kc4);
+  c.j = 0;
+  c.row = rb * 16 + li;
+  c.row_ok = c.row < c.L.N;
+}
+
+__device__ inline bool out_next(OutCursor& c, const DecLayer* tab, int64_t iend, int li) {
+  if (++c.j < c.nsteps) return true;
+  if (++c.item >= iend) return false;
+  if (c.item >= c.lend) {
+    ++c.lidx;
+    c.L = load_layer(tab + c.lidx);
+    c.lend = c.L.item0 + (int64_t)c.L.nrb * c.L.nkc;
   }
-  const uint32_t xbytes = (uint32_t)(c.L.nk4 * 256 * h.nc);
-  const __amdgpu_buffer_rsrc_t xr = make_rsrc(c.L.xf, xbytes);
-#pragma unroll
-  for (int i = 0; i < XW; ++i) {
-    const uint32_t xo = live ? (uint32_t)(c.k4 * 256 * h.nc + i * 1024 + lane * 16) : kOob;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_ptr_t)(slot + 2 * T * 1024 + i * 1024), 16, xo, 0, 0, 0);
-  }
+  out_item(c, li);
+  return true;
 }
 
 template <int T, int XW>
 struct StreamCfg {
   static constexpr int P = 2 * T;
   static constexpr int SLOT = (P + XW) * 1024;
-  // slots per wave: at most 80 KB per 4-wave block (two blocks per CU), 2..4
-  static constexpr int NS_RAW = (80 * 1024) / (4 * SLOT);
+  // slots per wave: at most ~80 KB per 4-wave block (two blocks per CU), 2..4
+  static constexpr int NS_RAW = (80 * 1024 - 64) / (4 * SLOT);
   static constexpr int NS = NS_RAW < 2 ? 2 : (NS_RAW > 4 ? 4 : NS_RAW);
   static constexpr int LOADS = P + XW;            // vector memory ops issued per step
   static constexpr int WAIT = (NS - 2) * LOADS;   // outstanding ops allowed when a slot is read
@@ -537,37 +600,55 @@ struct StreamCfg {
 template <int MODE, int T, int XW>
 __global__ __launch_bounds__(256) void dec_stream_kernel(DecHeader h, DecLayer inl,
                                                          const DecLayer* __restrict__ tab) {
+#if defined(__HIP_DEVICE_COMPILE__)  // LDS-DMA and buffer-descriptor code: device pass only
   using C = StreamCfg<T, XW>;
   constexpr int P = C::P, NS = C::NS, SLOT = C::SLOT;
   __shared__ __attribute__((aligned(16))) uint8_t ring[4][NS][SLOT];
+  __shared__ __attribute__((aligned(16))) uint8_t zero16[16];
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4, li = lane & 15;
   const int wave = uniform(threadIdx.x >> 6);
+  if (threadIdx.x < 4) reinterpret_cast<uint32_t*>(zero16)[threadIdx.x] = 0u;
+  __syncthreads();
   const int64_t wid = (int64_t)blockIdx.x * 4 + wave;
   const int64_t W = (int64_t)gridDim.x * 4;
   const int64_t i0 = uniform64(wid * h.total_items / W);
   const int64_t i1 = uniform64((wid + 1) * h.total_items / W);
   if (i0 >= i1) return;
 
-  int b, digit, comp;
-  const bool xvalid = col_token<MODE>(0, li, h.B, b, digit, comp);
-  const uint32_t xoff = (uint32_t)(P * 1024 + (g * h.nc + li) * 16);  // + d * 4 * nc * 16
+  // activation operand: this lane's 16 bytes within a slot (or a zero area)
+  int b_, digit_, comp_;
+  const bool xvalid = col_token<MODE>(0, li, h.B, b_, digit_, comp_);
 
-  StepCursor lc, cc;
-  cursor_init(lc, inl, tab, h.n_layers, i0, li);
-  cc = lc;
+  LoadCursor<T> lc;
+  lc.lidx = tab ? find_layer(tab, h.n_layers, i0) : 0;
+  lc.L = tab ? load_layer(tab + lc.lidx) : inl;
+  lc.lend = lc.L.item0 + (int64_t)lc.L.nrb * lc.L.nkc;
+  lc.item = i0;
+  load_layer_rsrc(lc, h);
+  load_item(lc, h, lane);
+  OutCursor oc;
+  oc.L = lc.L;
+  oc.lidx = lc.lidx;
+  oc.lend = lc.lend;
+  oc.item = i0;
+  out_item(oc, li);
+
   bool live = true;
 #pragma unroll
   for (int k = 0; k < NS - 1; ++k) {
-    stream_issue<T, XW>(lc, live, h, lane, &ring[wave][k][0]);
-    if (live) live = cursor_next(lc, tab, i1, li);
+    stream_issue<XW>(lc, live, lane, &ring[wave][k][0]);
+    if (live) live = load_next(lc, tab, h, i1, lane);
   }
 
-  v4i acc[P][2][1];
+  // The accumulators are never reset: an item's products are acc - base,
+  // exact modulo 2^32 because each item's own sums fit in int32; base is
+  // updated only in the epilogue, so steps carry no conditional copies.
+  v4i acc[P][2][1], base[P][2][1];
 #pragma unroll
-  for (int p = 0; p < P; ++p) acc[p][0][0] = acc[p][1][0] = v4i{0, 0, 0, 0};
+  for (int p = 0; p < P; ++p)
+    acc[p][0][0] = acc[p][1][0] = base[p][0][0] = base[p][1][0] = v4i{0, 0, 0, 0};
 
-  // one step on slot K; returns true when the wave's range is done
   auto step = [&](auto kconst) -> bool {
     constexpr int K = decltype(kconst)::value;
     __builtin_amdgcn_s_waitcnt(C::WAITCNT);  // this slot's loads have landed
@@ -576,14 +657,15 @@ __global__ __launch_bounds__(256) void dec_stream_kernel(DecHeader h, DecLayer i
     v4i cr[P];
 #pragma unroll
     for (int p = 0; p < P; ++p) cr[p] = *reinterpret_cast<const v4i*>(sl + p * 1024 + lane * 16);
+    const uint8_t* xl = xvalid ? sl + P * 1024 + (g * h.nc + li) * 16 : zero16;
+    const int xstep = xvalid ? 4 * h.nc * 16 : 0;
     v4i xr[4];
 #pragma unroll
-    for (int d = 0; d < 4; ++d)
-      xr[d] = xvalid ? *reinterpret_cast<const v4i*>(sl + xoff + d * 4 * h.nc * 16) : v4i{0, 0, 0, 0};
+    for (int d = 0; d < 4; ++d) xr[d] = *reinterpret_cast<const v4i*>(xl + d * xstep);
     __asm__ volatile("" ::: "memory");
-    // refill the slot consumed by the previous step
-    stream_issue<T, XW>(lc, live, h, lane, &ring[wave][(K + NS - 1) % NS][0]);
-    if (live) live = cursor_next(lc, tab, i1, li);
+    // refill the slot the previous step consumed
+    stream_issue<XW>(lc, live, lane, &ring[wave][(K + NS - 1) % NS][0]);
+    if (live) live = load_next(lc, tab, h, i1, lane);
 #pragma unroll
     for (int d = 0; d < 4; ++d) {
 #pragma unroll
@@ -596,20 +678,26 @@ __global__ __launch_bounds__(256) void dec_stream_kernel(DecHeader h, DecLayer i
         __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
       }
     }
-    if (cc.j == cc.nsteps - 1) {
+    if (oc.j == oc.nsteps - 1) {
       PassGeo q;
       q.rb = 0;
-      q.kc = cc.kc;
+      q.kc = oc.kc;
       q.tg0 = 0;
-      q.row = cc.row;
-      q.row_ok = cc.row_ok;
+      q.row = oc.row;
+      q.row_ok = oc.row_ok;
       q.k4b = 0;
       q.nk4_item = 0;
-      write_outputs<MODE, T, 1, false>(cc.L, h, q, lane, acc);
+      v4i item_acc[P][2][1];
 #pragma unroll
-      for (int p = 0; p < P; ++p) acc[p][0][0] = acc[p][1][0] = v4i{0, 0, 0, 0};
+      for (int p = 0; p < P; ++p)
+#pragma unroll
+        for (int ax = 0; ax < 2; ++ax) {
+          item_acc[p][ax][0] = acc[p][ax][0] - base[p][ax][0];
+          base[p][ax][0] = acc[p][ax][0];
+        }
+      write_outputs<MODE, T, 1, false>(oc.L, h, q, lane, item_acc);
     }
-    return !cursor_next(cc, tab, i1, li);
+    return !out_next(oc, tab, i1, li);
   };
 
   while (true) {
@@ -619,6 +707,7 @@ __global__ __launch_bounds__(256) void dec_stream_kernel(DecHeader h, DecLayer i
     if constexpr (NS > 3) if (step(std::integral_constant<int, 3 % NS>{})) break;
   }
   __builtin_amdgcn_s_waitcnt(0);  // no load may still be writing LDS when the wave ends
+#endif
 }
 
 // ------------------------------------------------------------ reduction ---
