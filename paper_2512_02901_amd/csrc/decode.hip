@@ -144,77 +144,145 @@ __device__ inline void buf_store8(const void* base, uint32_t bytes, uint32_t off
 }
 
 // ----------------------------------------------------------------- prep ---
-// One block per (tile, column) and layer: writes that column of the
-// activation operand for every 64-code MFMA step, and the per-token scale.
-// Layout [tile][256-code step][d][g][column < nc][16 bytes]: the 16 bytes of
-// (column, g, d) are what the MFMA lane of that column and 16-code group g
-// takes for the step's d-th 64-code MFMA (byte 4c+b = code c + 4b of the
-// group); the nc stored columns of a step are contiguous, so a step's whole
-// operand is one nc * 256-byte run.
+// Layout of the activation operand: [tile][256-code step][d][g][column < nc]
+// [16 bytes].  The 16 bytes of (column, g, d) are what the MFMA lane of that
+// column and 16-code group g takes for the step's d-th 64-code MFMA (byte
+// 4c+b = code c + 4b of the group); the nc columns of a step are contiguous,
+// so a step's whole operand is one nc * 256-byte run.  Columns that hold no
+// token are written as zeros.
+
+// 16 consecutive complex activations x[b][k0 .. k0+15] of one component as
+// raw bits (bf16: 16-bit patterns, int8: sign-extended bytes).  Vector loads
+// when the activation pointer allows them.
+constexpr int kPrepSplit = 4;
+
+template <int MODE>
+__device__ inline void load_run16(const void* x, bool vec, int64_t e0, int comp, int (&v)[16]) {
+  if constexpr (MODE == kModeBf16) {
+    const uint16_t* p = static_cast<const uint16_t*>(x) + e0;
+    if (vec) {
+      const uint4* q = reinterpret_cast<const uint4*>(p);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint4 w = q[i];
+        const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[4 * i + j] = (int)(comp ? wd[j] >> 16 : wd[j] & 0xFFFFu);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) v[i] = p[2 * i + comp];
+    }
+  } else {
+    const int8_t* p = static_cast<const int8_t*>(x) + e0;
+    if (vec) {
+      const uint4* q = reinterpret_cast<const uint4*>(p);
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const uint4 w = q[i];
+        const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          v[8 * i + 2 * j] = (int)(int8_t)(wd[j] >> (8 * comp));
+          v[8 * i + 2 * j + 1] = (int)(int8_t)(wd[j] >> (16 + 8 * comp));
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) v[i] = p[2 * i + comp];
+    }
+  }
+}
+
+// kPrepSplit blocks per (activation tile, layer).  bf16: each block first
+// finds the block fixed-point exponent of the tile's two tokens (from their
+// largest magnitudes), then writes its share of the tile's 16-byte operand
+// chunks, one chunk per thread in storage order.  int8: the bytes are copied into place and the per-token
+// dequantisation factors passed on.
 template <int MODE>
 __global__ __launch_bounds__(256) void dec_prep_kernel(DecHeader h, DecLayer inl,
                                                        const DecLayer* __restrict__ tab) {
   const DecLayer L = tab ? load_layer(tab + blockIdx.y) : inl;
-  const int tile = blockIdx.x >> 4, col = blockIdx.x & 15;
-  int b, digit, comp;
-  if (!col_token<MODE>(tile, col, h.B, b, digit, comp)) return;
+  const int tile = blockIdx.x;
   const int64_t K = L.K;
-  __shared__ float red[4];
-  __shared__ int sh_E;
-  int E = 0;
+  const bool vec = (reinterpret_cast<uintptr_t>(L.x) & 15) == 0;
+  int E[2] = {0, 0};
   if constexpr (MODE == kModeBf16) {
-    const uint16_t* xb = static_cast<const uint16_t*>(L.x) + (int64_t)b * K * 2;
-    float m = 0.0f;
-    for (int64_t i = threadIdx.x; i < 2 * K; i += blockDim.x)
-      m = fmaxf(m, fabsf(__uint_as_float((uint32_t)xb[i] << 16)));
-    for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      const float g = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-      int ex = 0;
-      if (g > 0.0f) {
-        frexpf(g, &ex);       // g in [2^(ex-1), 2^ex)
-        E = 22 - ex;          // g * 2^E in [2^21, 2^22)
-        if (E > 149) E = 149; // keep 2^-E representable in float32
+    __shared__ float red[4][2];
+    __shared__ int sh_E[2];
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int b = 2 * tile + s;
+      float m = 0.0f;
+      if (b < h.B) {
+        const uint16_t* xb = static_cast<const uint16_t*>(L.x) + (int64_t)b * K * 2;
+        if (vec) {
+          const uint4* xv = reinterpret_cast<const uint4*>(xb);
+          for (int64_t i = threadIdx.x; i < K / 4; i += blockDim.x) {  // 8 bf16 (4 complex) per vector
+            const uint4 w = xv[i];
+            const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+              m = fmaxf(m, fmaxf(fabsf(__uint_as_float(wd[j] << 16)), fabsf(__uint_as_float(wd[j] & 0xFFFF0000u))));
+          }
+        } else {
+          for (int64_t i = threadIdx.x; i < 2 * K; i += blockDim.x)
+            m = fmaxf(m, fabsf(__uint_as_float((uint32_t)xb[i] << 16)));
+        }
       }
-      sh_E = E;
-      if (digit == 0 && comp == 0) L.xs[b] = g > 0.0f ? ldexpf(1.0f, -E) : 0.0f;
+      for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+      if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6][s] = m;
     }
     __syncthreads();
-    E = sh_E;
+    if (threadIdx.x < 2) {
+      const int s = threadIdx.x, b = 2 * tile + s;
+      const float g = fmaxf(fmaxf(red[0][s], red[1][s]), fmaxf(red[2][s], red[3][s]));
+      int ex = 0, e = 0;
+      if (g > 0.0f) {
+        frexpf(g, &ex);       // g in [2^(ex-1), 2^ex)
+        e = 22 - ex;          // g * 2^e in [2^21, 2^22)
+        if (e > 149) e = 149; // keep 2^-e representable in float32
+      }
+      sh_E[s] = e;
+      if (b < h.B && blockIdx.z == 0) L.xs[b] = g > 0.0f ? ldexpf(1.0f, -e) : 0.0f;
+    }
+    __syncthreads();
+    E[0] = sh_E[0];
+    E[1] = sh_E[1];
   } else {
-    // the accumulator export passes no factors (its epilogue does not use them)
-    if (threadIdx.x == 0 && comp == 0) L.xs[b] = L.x_scale_in ? L.x_scale_in[b] : 1.0f;
+    if (threadIdx.x < 8 && blockIdx.z == 0) {
+      // the accumulator export passes no factors (its epilogue does not use them)
+      const int b = 8 * tile + threadIdx.x;
+      if (b < h.B) L.xs[b] = L.x_scale_in ? L.x_scale_in[b] : 1.0f;
+    }
   }
-  const int nchunks = L.nk4 * 16;  // (k4, d, g)
-  for (int ch = threadIdx.x; ch < nchunks; ch += blockDim.x) {
-    const int kk = ch >> 4, d = (ch >> 2) & 3, g = ch & 3;
+  const int nch = L.nk4 * 16 * h.nc;
+  uint4* dst = reinterpret_cast<uint4*>(L.xf) + (int64_t)tile * nch;
+  for (int ch = blockIdx.z * blockDim.x + threadIdx.x; ch < nch; ch += gridDim.z * blockDim.x) {
+    const int col = ch % h.nc, r = ch / h.nc;
+    const int kk = r >> 4, d = (r >> 2) & 3, g = r & 3;
     const int64_t k0 = (int64_t)kk * 256 + 64 * g + 16 * d;
     uint32_t out[4] = {0u, 0u, 0u, 0u};
+    int b, digit, comp;
+    if (col_token<MODE>(tile, col, h.B, b, digit, comp) && k0 < K) {  // K % 64 == 0: whole run in range
+      int v[16];
+      load_run16<MODE>(L.x, vec, ((int64_t)b * K + k0) * 2, comp, v);
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int dd = e >> 2, bb = e & 3;
-      const int64_t k = k0 + dd + 4 * bb;
-      int v = 0;
-      if (k < K) {
+      for (int e = 0; e < 16; ++e) {
+        const int dd = e >> 2, bb = e & 3;  // byte 4dd+bb holds code dd + 4bb of the run
+        int q = v[dd + 4 * bb];
         if constexpr (MODE == kModeBf16) {
-          const uint16_t raw = static_cast<const uint16_t*>(L.x)[((int64_t)b * K + k) * 2 + comp];
-          const int X = (int)rintf(ldexpf(__uint_as_float((uint32_t)raw << 16), E));
+          const int X = (int)rintf(ldexpf(__uint_as_float((uint32_t)q << 16), (b & 1) ? E[1] : E[0]));
           const int d0 = ((X + 128) & 255) - 128;
           const int X1 = (X - d0) >> 8;
           const int d1 = ((X1 + 128) & 255) - 128;
           const int d2 = (X1 - d1) >> 8;
-          v = digit == 0 ? d0 : (digit == 1 ? d1 : d2);
-        } else {
-          v = static_cast<const int8_t*>(L.x)[((int64_t)b * K + k) * 2 + comp];
+          q = digit == 0 ? d0 : (digit == 1 ? d1 : d2);
         }
+        out[dd] |= ((uint32_t)q & 0xFFu) << (8 * bb);
       }
-      out[dd] |= ((uint32_t)v & 0xFFu) << (8 * bb);
     }
-    uint4* dst = reinterpret_cast<uint4*>(
-        L.xf + (((((int64_t)tile * L.nk4 + kk) * 4 + d) * 4 + g) * h.nc + col) * 16);
-    *dst = make_uint4(out[0], out[1], out[2], out[3]);
+    dst[ch] = make_uint4(out[0], out[1], out[2], out[3]);
   }
 }
 
@@ -585,33 +653,39 @@ __device__ inline bool out_next(OutCursor& c, const DecLayer* tab, int64_t iend,
   return true;
 }
 
+// waves per block and LDS bytes per wave of the streaming kernel
+constexpr int kStreamWaves = 4;
+constexpr int kStreamLdsPerWave = 20 * 1024 - 16;
+
 template <int T, int XW>
 struct StreamCfg {
   static constexpr int P = 2 * T;
   static constexpr int SLOT = (P + XW) * 1024;
-  // slots per wave: at most ~80 KB per 4-wave block (two blocks per CU), 2..4
-  static constexpr int NS_RAW = (80 * 1024 - 64) / (4 * SLOT);
-  static constexpr int NS = NS_RAW < 2 ? 2 : (NS_RAW > 4 ? 4 : NS_RAW);
+  static constexpr int WAVES = kStreamWaves;
+  // ring slots per wave within the LDS budget, 2..6
+  static constexpr int NS_RAW = kStreamLdsPerWave / SLOT;
+  static constexpr int NS = NS_RAW < 2 ? 2 : (NS_RAW > 6 ? 6 : NS_RAW);
   static constexpr int LOADS = P + XW;            // vector memory ops issued per step
   static constexpr int WAIT = (NS - 2) * LOADS;   // outstanding ops allowed when a slot is read
   static constexpr int WAITCNT = (WAIT & 0xF) | (0x7 << 4) | (0xF << 8) | (((WAIT >> 4) & 3) << 14);
 };
 
 template <int MODE, int T, int XW>
-__global__ __launch_bounds__(256) void dec_stream_kernel(DecHeader h, DecLayer inl,
-                                                         const DecLayer* __restrict__ tab) {
+__global__ __launch_bounds__(64 * kStreamWaves) void dec_stream_kernel(DecHeader h, DecLayer inl,
+                                                                       const DecLayer* __restrict__ tab) {
 #if defined(__HIP_DEVICE_COMPILE__)  // LDS-DMA and buffer-descriptor code: device pass only
   using C = StreamCfg<T, XW>;
   constexpr int P = C::P, NS = C::NS, SLOT = C::SLOT;
-  __shared__ __attribute__((aligned(16))) uint8_t ring[4][NS][SLOT];
+  constexpr int WAVES = C::WAVES;
+  __shared__ __attribute__((aligned(16))) uint8_t ring[WAVES][NS][SLOT];
   __shared__ __attribute__((aligned(16))) uint8_t zero16[16];
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4, li = lane & 15;
   const int wave = uniform(threadIdx.x >> 6);
   if (threadIdx.x < 4) reinterpret_cast<uint32_t*>(zero16)[threadIdx.x] = 0u;
   __syncthreads();
-  const int64_t wid = (int64_t)blockIdx.x * 4 + wave;
-  const int64_t W = (int64_t)gridDim.x * 4;
+  const int64_t wid = (int64_t)blockIdx.x * WAVES + wave;
+  const int64_t W = (int64_t)gridDim.x * WAVES;
   const int64_t i0 = uniform64(wid * h.total_items / W);
   const int64_t i1 = uniform64((wid + 1) * h.total_items / W);
   if (i0 >= i1) return;
@@ -735,11 +809,11 @@ __global__ void fill_i32_kernel(int32_t* p, int64_t n) {
 }
 
 // Blocks of kernel k that fit on the current device at once.
-int resident_blocks(const void* k) {
+int resident_blocks(const void* k, int threads) {
   int dev = 0, cus = 0, per_cu = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, 256, 0) != hipSuccess || per_cu < 1)
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, threads, 0) != hipSuccess || per_cu < 1)
     return 1024;
   return cus * per_cu;
 }
@@ -748,7 +822,7 @@ template <int MODE, int T, int NTG, bool EXPORT>
 void launch_dec(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, int64_t want_blocks,
                 hipStream_t s) {
   auto k = dec_mfma_kernel<MODE, T, NTG, EXPORT>;
-  static const int resident = resident_blocks(reinterpret_cast<const void*>(k));  // one query per variant
+  static const int resident = resident_blocks(reinterpret_cast<const void*>(k), 256);  // one query per variant
   const int64_t blocks = want_blocks < resident ? want_blocks : resident;
   hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(256), 0, s, h, inl, tab);
 }
@@ -775,9 +849,12 @@ template <int MODE, int T, int XW>
 void launch_stream(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, int64_t want_blocks,
                    hipStream_t s) {
   auto k = dec_stream_kernel<MODE, T, XW>;
-  static const int resident = resident_blocks(reinterpret_cast<const void*>(k));
-  const int64_t blocks = want_blocks < resident ? want_blocks : resident;
-  hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(256), 0, s, h, inl, tab);
+  constexpr int threads = 64 * kStreamWaves;
+  static const int resident = resident_blocks(reinterpret_cast<const void*>(k), threads);
+  const int64_t want = (h.total_items + kStreamWaves - 1) / kStreamWaves;
+  const int64_t blocks = want < resident ? want : resident;
+  (void)want_blocks;
+  hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(threads), 0, s, h, inl, tab);
 }
 
 template <int MODE, int T>
@@ -818,9 +895,9 @@ hipError_t launch_decode(const DecHeader& h, const DecLayer& inl, const DecLayer
   if (e != hipSuccess) return e;
   // 1. activation operand
   if (h.mode == kModeBf16)
-    hipLaunchKernelGGL(dec_prep_kernel<kModeBf16>, dim3(h.ntile * 16, nl), dim3(256), 0, s, h, inl, tab);
+    hipLaunchKernelGGL(dec_prep_kernel<kModeBf16>, dim3(h.ntile, nl, kPrepSplit), dim3(256), 0, s, h, inl, tab);
   else
-    hipLaunchKernelGGL(dec_prep_kernel<kModeI8>, dim3(h.ntile * 16, nl), dim3(256), 0, s, h, inl, tab);
+    hipLaunchKernelGGL(dec_prep_kernel<kModeI8>, dim3(h.ntile, nl, kPrepSplit), dim3(256), 0, s, h, inl, tab);
   if ((e = hipGetLastError()) != hipSuccess || (e = mark(1)) != hipSuccess) return e;
   if (export_acc) {
     hipLaunchKernelGGL(fill_i32_kernel, dim3(1024), dim3(256), 0, s, acc, acc_elems);

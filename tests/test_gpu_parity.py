@@ -307,6 +307,32 @@ def test_mfma_decode_bf16_and_int8(gpu, T, B, NK):
     assert rel_l2(y, oracle.wl_matmul_int8(cu, su, cw, sw, qo, fo)) <= TOL_F32
 
 
+@pytest.mark.parametrize("B", [1, 3, 9])
+def test_mfma_decode_misaligned_activations(gpu, B):
+    """Activations whose address is not 16-byte aligned take the element-wise
+    load path of the operand preparation; results are bitwise those of an
+    aligned copy."""
+    import torch
+    import paper_2512_02901_amd as f2
+    N, K = 48, 320
+    A = synth.llama_weight(2 * N, 2 * K, (14, N, K))
+    _, _, cu, su, cw, sw = oracle_layer(A, 2)
+    d = upload_layer(cu, su, cw, sw, gpu)
+    x = synth.activations(B, K, (15, B, K))
+    xb = synth.bf16_round_complex(x)
+    qo, fo = oracle.quantize_act_int8(x)
+    for xa, xs, want in ((bf16_dev(xb, gpu), None, oracle.wl_matmul(cu, su, cw, sw, xb)),
+                         (dev(qo, gpu), dev(fo, gpu), oracle.wl_matmul_int8(cu, su, cw, sw, qo, fo))):
+        buf = torch.zeros(xa.numel() + 8, dtype=xa.dtype, device=xa.device)
+        xm = buf[1:1 + xa.numel()].view(xa.shape)
+        xm.copy_(xa)
+        assert xm.data_ptr() % 16 != 0
+        y0 = host(f2.wl_matmul(*d, xa, xs))
+        y1 = host(f2.wl_matmul(*d, xm, xs))
+        np.testing.assert_array_equal(y1, y0)
+        assert rel_l2(y1, want) <= TOL_F32
+
+
 def test_mfma_decode_bf16_wide_dynamic_range(gpu):
     """A token whose values span 2^-40 .. 2^3: values more than 2^14 below the
     token's largest magnitude are rounded to its 2^-E grid; the error stays
