@@ -41,10 +41,13 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def build_stack(f2, synth, torch, dev, T, B=1, seed_base=1000):
+def build_stack(f2, synth, torch, dev, T, B=1, seed_base=1000, tiled=True):
     """32 x 7 widely-linear layers with T-stage codes, each with its own
-    bf16 activation token; returns (group, packed_bytes, algorithmic_bytes)."""
-    layers, packed, algo = [], 0, 0
+    bf16 activation token.  Returns (group, packed_bytes, algorithmic_bytes,
+    layers): the group decodes the tiled copies of the codes (made once by
+    fairy2i_repack_tiled, like the quantisation, outside any timing) unless
+    tiled is False; `layers` holds the D3 codes."""
+    layers, tiled_layers, packed, algo = [], [], 0, 0
     for layer in range(32):
         for p in synth.PROJ_ORDER:
             rows, cols = synth.LLAMA2_7B_PROJ[p]
@@ -60,12 +63,15 @@ def build_stack(f2, synth, torch, dev, T, B=1, seed_base=1000):
             x = torch.randn(B, K, 2, generator=g, device=dev).to(torch.bfloat16)
             y = torch.empty(B, N, dtype=torch.complex64, device=dev)
             layers.append((cu, su, cw, sw, x, None, y))
+            if tiled:
+                tiled_layers.append((f2.repack_tiled(cu), su, f2.repack_tiled(cw), sw, x, None, y))
             codes = 2 * T * N * K // 4
             packed += codes
             # codes + bf16 activations + complex64 outputs + scales
             algo += codes + B * K * 2 * 2 + B * N * 8 + 2 * T * 2 * 4
     torch.cuda.synchronize()
-    return f2.WlGroup(layers, T=T, B=B), packed, algo, layers
+    grp = f2.WlGroup(tiled_layers, T=T, B=B, tiled=True) if tiled else f2.WlGroup(layers, T=T, B=B)
+    return grp, packed, algo, layers
 
 
 def time_group(grp, torch, steps, warmup):
@@ -95,7 +101,7 @@ def traffic_record():
     """HBM bytes per launch of the product kernel from committed rocprofv3
     --pmc summaries, or None when absent or when the kernel source changed
     since the counters were taken."""
-    path = os.path.join(PROFILES, "dec_mfma_stack_T2_bf16_traffic.txt")
+    path = os.path.join(PROFILES, "dec_stream_stack_T2_bf16_traffic.txt")
     if not os.path.exists(path):
         return None
     rec = {}
@@ -181,7 +187,9 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-extras", action="store_true", help="skip prefill and T=3 measurements")
+    ap.add_argument("--no-extras", action="store_true", help="skip prefill, T=3 and D3-layout measurements")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run 5 plain 256 MiB device copies (reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -190,6 +198,14 @@ def main():
         sys.exit(2)
 
     import torch
+    if args.calibrate_copy:
+        src = torch.ones(256 << 20, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": src.numel(), "copies": 5}), flush=True)
+        return
     import paper_2512_02901_amd as f2
     import synth
 
@@ -209,7 +225,7 @@ def main():
     traffic = traffic_record()
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "kernel": "dec_mfma_kernel (int8 MFMA product, one launch per step)",
+                "kernel": "dec_stream_kernel<bf16, T=2> (int8 MFMA product over tiled codes, one launch per step)",
                 "algorithmic_bytes_per_launch": algo, "avg_launch_us": round(prod_ms * 1e3, 2)}
 
     result = {
@@ -233,6 +249,13 @@ def main():
                                          "reduce": round(red_ms * 1e3, 1)}},
         "roofline": roofline,
     }
+    if not args.no_extras:
+        # the same stack decoded straight from the canonical D3 codes
+        grp_d3 = f2.WlGroup(layers, T=T, B=1)
+        ms_d3, _, prod_d3, _ = time_group(grp_d3, torch, args.steps, args.warmup)
+        result["stack_d3_layout"] = {"ms_per_step": round(ms_d3, 4), "GBs": round(packed / (ms_d3 * 1e-3) / 1e9, 1),
+                                     "product_us": round(prod_d3 * 1e3, 1)}
+        del grp_d3
     del grp, layers
     torch.cuda.empty_cache()
 

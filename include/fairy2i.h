@@ -67,6 +67,14 @@ enum {
                            dequantisation factor per token                  */
 };
 
+/* Device layouts of packed codes.  D3 is the canonical one (what
+ * fairy2i_quantize writes and every call accepts); TILED is the decode
+ * layout written by fairy2i_repack_tiled, accepted by the grouped decode. */
+enum {
+  FAIRY2I_LAYOUT_D3 = 0,
+  FAIRY2I_LAYOUT_TILED = 1
+};
+
 #define FAIRY2I_MAX_STAGES 4
 /* Largest token count served by the decode kernels for float activations;
  * larger batches need int8 activations (the prefill GEMM). */
@@ -208,6 +216,9 @@ typedef struct fairy2i_wl_layer {
   float* y;
   int64_t N;
   int64_t K;
+  int32_t layout;    /* FAIRY2I_LAYOUT_D3 or FAIRY2I_LAYOUT_TILED, for both
+                        codes_U and codes_W (same T as the call)           */
+  int32_t reserved;  /* 0 */
 } fairy2i_wl_layer;
 
 /*
@@ -216,7 +227,8 @@ typedef struct fairy2i_wl_layer {
  * input) in a fixed number of kernel launches, so the weight stream of all
  * layers runs back to back instead of paying a launch per layer.
  * Restrictions: dtype FAIRY2I_ACT_BF16 or FAIRY2I_ACT_I8, 1 <= B <= 16,
- * every K a multiple of 64.
+ * every K a multiple of 64, reserved == 0.  Each layer's codes are in the
+ * layout its `layout` field names (same layout for U and W).
  *
  * Use: size the workspace with fairy2i_wl_group_workspace_bytes and the
  * table with fairy2i_wl_group_table_bytes; fairy2i_wl_group_build_table
@@ -233,6 +245,29 @@ typedef struct fairy2i_wl_layer {
  * n_layers < 1; fairy2i_wl_matmul_group returns FAIRY2I_ERR_NULL for a NULL
  * table and FAIRY2I_ERR_UNSUPPORTED for bytes that are not a built table.
  */
+/*
+ * Tiled decode layout of one matrix's packed codes (the code values and
+ * their packing into bytes are those of D3; only the byte order changes).
+ * Codes are cut into tiles of 16 rows x 256 codes (1024 bytes per stage);
+ * tile (row block rb, 256-code step s, stage t) is stored at byte offset
+ *     ((rb * ceil(K/256) + s) * T + t) * 1024
+ * and byte 16 * (16 g + r) + e of the tile is D3 byte 64 s + 16 g + e of
+ * row 16 rb + r of stage t (g < 4, r < 16, e < 16); bytes past row N - 1 or
+ * past the row's K/4 bytes are 0.  A 256-code step of one row block is then
+ * one contiguous 1024-byte run per stage, which is what one wave of the
+ * decode product loads at once.
+ * fairy2i_repack_tiled_bytes: bytes of the tiled copy, T * ceil(N/16) *
+ * ceil(K/256) * 1024 (0 for invalid sizes).
+ * fairy2i_repack_tiled: codes (D3, T*N*K/4 bytes) -> tiled (device memory,
+ * tiled_bytes >= fairy2i_repack_tiled_bytes); enqueued on `stream`.
+ * Errors: FAIRY2I_ERR_NULL; FAIRY2I_ERR_SHAPE for N < 1, K < 4, K % 4 != 0;
+ * FAIRY2I_ERR_STAGES; FAIRY2I_ERR_WORKSPACE if tiled_bytes is too small;
+ * FAIRY2I_ERR_HIP.
+ */
+size_t fairy2i_repack_tiled_bytes(int64_t N, int64_t K, int32_t T);
+fairy2i_status fairy2i_repack_tiled(const uint8_t* codes, int64_t N, int64_t K, int32_t T,
+                                    uint8_t* tiled, size_t tiled_bytes, void* stream);
+
 size_t fairy2i_wl_group_workspace_bytes(const fairy2i_wl_layer* layers, int32_t n_layers,
                                         int32_t T, int32_t dtype, int64_t B);
 size_t fairy2i_wl_group_table_bytes(int32_t n_layers);

@@ -16,6 +16,7 @@ _lib = None
 
 OK, ERR_NULL, ERR_SHAPE, ERR_STAGES, ERR_DTYPE, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(8)
 ACT_F32, ACT_BF16, ACT_I8 = 0, 1, 2
+LAYOUT_D3, LAYOUT_TILED = 0, 1
 MAX_STAGES = 4
 MAX_DECODE_BATCH = 16
 
@@ -27,6 +28,8 @@ _SIGNATURES = {
     "fairy2i_to_widely_linear": (_c_i32, [_c_p, _c_i64, _c_i64, _c_p, _c_p, _c_p]),
     "fairy2i_quantize_workspace_bytes": (_c_size, [_c_i64, _c_i64, _c_i32]),
     "fairy2i_quantize": (_c_i32, [_c_p, _c_i64, _c_i64, _c_i32, _c_p, _c_p, _c_p, _c_size, _c_p]),
+    "fairy2i_repack_tiled_bytes": (_c_size, [_c_i64, _c_i64, _c_i32]),
+    "fairy2i_repack_tiled": (_c_i32, [_c_p, _c_i64, _c_i64, _c_i32, _c_p, _c_size, _c_p]),
     "fairy2i_quantize_act_int8": (_c_i32, [_c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_p, _c_p]),
     "fairy2i_wl_matmul_workspace_bytes": (_c_size, [_c_i64, _c_i64, _c_i32, _c_i64, _c_i32]),
     "fairy2i_wl_matmul": (_c_i32, [_c_p, _c_p, _c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_p,
@@ -46,7 +49,8 @@ _SIGNATURES = {
 class WlLayer(ctypes.Structure):
     """fairy2i_wl_layer of include/fairy2i.h."""
     _fields_ = [("codes_U", _c_p), ("scales_U", _c_p), ("codes_W", _c_p), ("scales_W", _c_p),
-                ("x", _c_p), ("x_scale", _c_p), ("y", _c_p), ("N", _c_i64), ("K", _c_i64)]
+                ("x", _c_p), ("x_scale", _c_p), ("y", _c_p), ("N", _c_i64), ("K", _c_i64),
+                ("layout", _c_i32), ("reserved", _c_i32)]
 
 
 class Fairy2iError(RuntimeError):
@@ -210,6 +214,27 @@ def wl_matmul(codes_U, scales_U, codes_W, scales_W, x, x_scale=None, out=None, w
     return out
 
 
+def repack_tiled_bytes(N, K, T) -> int:
+    return int(load().fairy2i_repack_tiled_bytes(N, K, T))
+
+
+def repack_tiled(codes, out=None):
+    """D3 codes [T, N, K/4] -> the tiled decode layout (1-D uint8 tensor of
+    fairy2i_repack_tiled_bytes bytes)."""
+    torch = _torch()
+    lib = load()
+    _require(codes, torch.uint8, "codes")
+    T, N, KB = codes.shape
+    nb = repack_tiled_bytes(N, 4 * KB, T)
+    if out is None:
+        out = torch.empty(nb, dtype=torch.uint8, device=codes.device)
+    else:
+        _require(out, torch.uint8, "out")
+    _check(lib.fairy2i_repack_tiled(_ptr(codes), N, 4 * KB, T, _ptr(out), out.numel(), _stream_ptr(codes)),
+           "fairy2i_repack_tiled")
+    return out
+
+
 def int8_accumulators(codes_U, codes_W, q, workspace=None):
     """Exact int32 products acc[M][t][p][b][i][c] behind the int8 path."""
     torch = _torch()
@@ -245,9 +270,11 @@ class WlGroup:
     """A table of independent layers decoded by one fairy2i_wl_matmul_group
     call.  ``layers`` is a list of (codes_U, scales_U, codes_W, scales_W, x,
     x_scale, y) device tensors (x_scale None for bf16); the object keeps them,
-    the workspace and both copies of the table alive."""
+    the workspace and both copies of the table alive.  ``tiled``: the codes
+    are fairy2i_repack_tiled copies (a 1-D uint8 tensor per matrix) rather
+    than D3 [T, N, K/4] tensors; N is then taken from y."""
 
-    def __init__(self, layers, T: int, B: int):
+    def __init__(self, layers, T: int, B: int, tiled: bool = False):
         torch = _torch()
         lib = load()
         if not layers:
@@ -259,8 +286,14 @@ class WlGroup:
             Bx, K = _act_shape(x)
             if Bx != B or _act_dtype(x) != dt:
                 raise ValueError("all layers of a group share B and the activation dtype")
+            N = y.shape[1] if tiled else cu.shape[1]
+            if tiled:
+                need = repack_tiled_bytes(N, K, T)
+                if cu.numel() < need or cw.numel() < need:
+                    raise ValueError("tiled codes smaller than fairy2i_repack_tiled_bytes")
             arr[i] = WlLayer(cu.data_ptr(), su.data_ptr(), cw.data_ptr(), sw.data_ptr(), x.data_ptr(),
-                             None if xs is None else xs.data_ptr(), y.data_ptr(), cu.shape[1], K)
+                             None if xs is None else xs.data_ptr(), y.data_ptr(), N, K,
+                             LAYOUT_TILED if tiled else LAYOUT_D3, 0)
         self.n = len(layers)
         dev = layers[0][4].device
         wsb = int(lib.fairy2i_wl_group_workspace_bytes(ctypes.byref(arr), self.n, T, dt, B))

@@ -109,7 +109,7 @@ const char* fairy2i_status_string(fairy2i_status s) {
   }
 }
 
-int32_t fairy2i_abi_version(void) { return 1; }
+int32_t fairy2i_abi_version(void) { return 2; }
 
 fairy2i_status fairy2i_to_widely_linear(const float* A, int64_t rows, int64_t cols, float* U,
                                         float* W, void* stream) {
@@ -134,6 +134,24 @@ fairy2i_status fairy2i_quantize(const float* M, int64_t N, int64_t K, int32_t T,
   if (!workspace || workspace_bytes < quantize_workspace_bytes(N, K)) return FAIRY2I_ERR_WORKSPACE;
   return hip_status(launch_quantize(reinterpret_cast<const float2*>(M), N, K, T, codes, scales,
                                     workspace, as_stream(stream)));
+}
+
+static bool repack_shape_ok(int64_t N, int64_t K) {
+  return N >= 1 && K >= 4 && (K % 4) == 0 && N <= FAIRY2I_MAX_QUANTIZE_ENTRIES / K;
+}
+
+size_t fairy2i_repack_tiled_bytes(int64_t N, int64_t K, int32_t T) {
+  if (!repack_shape_ok(N, K) || T < 1 || T > FAIRY2I_MAX_STAGES) return 0;
+  return repack_tiled_bytes(N, K, T);
+}
+
+fairy2i_status fairy2i_repack_tiled(const uint8_t* codes, int64_t N, int64_t K, int32_t T, uint8_t* tiled,
+                                    size_t tiled_bytes, void* stream) {
+  if (!codes || !tiled) return FAIRY2I_ERR_NULL;
+  if (!repack_shape_ok(N, K)) return FAIRY2I_ERR_SHAPE;
+  if (T < 1 || T > FAIRY2I_MAX_STAGES) return FAIRY2I_ERR_STAGES;
+  if (tiled_bytes < repack_tiled_bytes(N, K, T)) return FAIRY2I_ERR_WORKSPACE;
+  return hip_status(launch_repack_tiled(codes, N, K, T, tiled, as_stream(stream)));
 }
 
 fairy2i_status fairy2i_quantize_act_int8(const void* x, int32_t dtype, int64_t B, int64_t K,
@@ -238,6 +256,11 @@ static fairy2i_status check_group(const fairy2i_wl_layer* layers, int32_t n_laye
     if (dtype != FAIRY2I_ACT_I8 && L.x_scale) return FAIRY2I_ERR_UNSUPPORTED;
     if (!use_mfma_decode(dtype, L.N, L.K, B) || L.N > ((int64_t)1 << 30) || L.K > ((int64_t)1 << 24))
       return FAIRY2I_ERR_UNSUPPORTED;
+    if (L.reserved != 0) return FAIRY2I_ERR_UNSUPPORTED;
+    if (L.layout != FAIRY2I_LAYOUT_D3 && L.layout != FAIRY2I_LAYOUT_TILED) return FAIRY2I_ERR_UNSUPPORTED;
+    // the decode kernels address a matrix with 32-bit offsets
+    if (L.layout == FAIRY2I_LAYOUT_TILED && repack_tiled_bytes(L.N, L.K, T) >= ((size_t)1 << 31))
+      return FAIRY2I_ERR_UNSUPPORTED;
   }
   return FAIRY2I_OK;
 }
@@ -275,6 +298,7 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
   for (int32_t i = 0; i < n_layers; ++i) {
     const fairy2i_wl_layer& L = layers[i];
     DecLayer l = dec_layer(L.codes_U, L.scales_U, L.codes_W, L.scales_W, L.N, L.K, L.x, L.x_scale, L.y);
+    l.tiled = L.layout == FAIRY2I_LAYOUT_TILED ? 1 : 0;
     ws += dec_layer_setup(l, h, false, ws);
     l.acc = nullptr;
     l.item0 = items;

@@ -20,6 +20,11 @@ size_t quantize_workspace_bytes(int64_t N, int64_t K);
 hipError_t launch_quantize(const float2* M, int64_t N, int64_t K, int T, uint8_t* codes,
                            float* scales, void* workspace, hipStream_t stream);
 
+// --------------------------------------------------------------- repack ---
+size_t repack_tiled_bytes(int64_t N, int64_t K, int T);
+hipError_t launch_repack_tiled(const uint8_t* codes, int64_t N, int64_t K, int T, uint8_t* tiled,
+                               hipStream_t stream);
+
 // ----------------------------------------------------------- act quant ---
 hipError_t launch_quantize_act_int8(const void* x, int dtype, int64_t B, int64_t K, int8_t* q,
                                     float* x_scale, hipStream_t stream);

@@ -28,6 +28,8 @@ struct DecLayer {
   float2* part;              // split-K partials [nkc][B][N] (nkc > 1)
   int32_t N, K;
   int32_t nrb, nk4, nkc, kc4;  // 16-row blocks, 256-code steps, K slices, steps per slice
+  int32_t tiled;             // codes in the tiled layout (else D3)
+  int32_t pad_;
   int64_t item0;             // index of this layer's first work item
 };
 

@@ -106,6 +106,8 @@ __device__ inline DecLayer load_layer(const DecLayer* p) {
   o.nk4 = uniform(p->nk4);
   o.nkc = uniform(p->nkc);
   o.kc4 = uniform(p->kc4);
+  o.tiled = uniform(p->tiled);
+  o.pad_ = 0;
   o.item0 = uniform64(p->item0);
   return o;
 }
@@ -313,16 +315,26 @@ __device__ inline void issue_step_loads(const DecLayer& L, const DecHeader& h, c
                                         v4i (&cw)[2 * T][kRegKc4], v4i (&xa)[kRegKc4][4][NTG]) {
   const int g = lane >> 4, li = lane & 15;
   const int K = L.K;
-  const uint32_t plane_bytes = (uint32_t)((int64_t)L.N * K / 4);
   const int kk = q.k4b + j;
   const bool kok = j < q.nk4_item;
+  const bool ok = q.row_ok && kok && kk * 256 + 64 * g < K;
+  if (L.tiled) {
+    // tile (rb, kk, t) is one 1024-byte run; this lane's 16 bytes sit at lane * 16
+    const uint32_t mat_bytes = (uint32_t)(T * L.nrb * L.nk4 * 1024);
+    const uint32_t off = ok ? (uint32_t)((q.rb * L.nk4 + kk) * T) * 1024u + (uint32_t)lane * 16u : kOob;
 #pragma unroll
-  for (int p = 0; p < 2 * T; ++p) {
-    const int m = p / T, t = p % T;
-    const __amdgpu_buffer_rsrc_t rs = make_rsrc(L.codes[m] + (int64_t)t * plane_bytes, plane_bytes);
-    const bool ok = q.row_ok && kok && kk * 256 + 64 * g < K;
+    for (int p = 0; p < 2 * T; ++p) {
+      const int m = p / T, t = p % T;
+      cw[p][j] = buf_load16(make_rsrc(L.codes[m] + t * 1024, mat_bytes - t * 1024), off);
+    }
+  } else {
+    const uint32_t plane_bytes = (uint32_t)((int64_t)L.N * K / 4);
     const uint32_t off = ok ? (uint32_t)q.row * (uint32_t)(K / 4) + (uint32_t)(kk * 64 + 16 * g) : kOob;
-    cw[p][j] = buf_load16(rs, off);
+#pragma unroll
+    for (int p = 0; p < 2 * T; ++p) {
+      const int m = p / T, t = p % T;
+      cw[p][j] = buf_load16(make_rsrc(L.codes[m] + (int64_t)t * plane_bytes, plane_bytes), off);
+    }
   }
   const __amdgpu_buffer_rsrc_t xr = make_rsrc(L.xf, (uint32_t)(h.ntile * L.nk4 * 256 * h.nc));
 #pragma unroll
@@ -555,7 +567,8 @@ struct LoadCursor {
   int lidx, j, nsteps, k4;
   const uint8_t* pbase[2 * T];  // code plane (M, t) of the current layer
   uint32_t plane_bytes, xbytes;
-  uint32_t voff;  // this lane's offset in every code plane at step k4 (row, 16-code group)
+  uint32_t voff;   // this lane's offset in every code plane at step k4 (row, 16-code group)
+  uint32_t vstep;  // voff advance per step: 64 (D3) or T * 1024 (tiled)
   uint32_t xoff;  // offset of the step's activation operand + lane * 16
   bool row_ok;
 };
@@ -571,15 +584,25 @@ __device__ inline void load_item(LoadCursor<T>& c, const DecHeader& h, int lane)
   c.j = 0;
   const int row = rb * 16 + li;
   c.row_ok = row < c.L.N;
-  c.voff = (uint32_t)row * (uint32_t)(c.L.K / 4) + (uint32_t)(c.k4 * 64 + 16 * g);
+  c.voff = c.L.tiled ? (uint32_t)((rb * c.L.nk4 + c.k4) * T) * 1024u + (uint32_t)lane * 16u
+                     : (uint32_t)row * (uint32_t)(c.L.K / 4) + (uint32_t)(c.k4 * 64 + 16 * g);
   c.xoff = (uint32_t)(c.k4 * 256 * h.nc + lane * 16);
 }
 
 template <int T>
 __device__ inline void load_layer_rsrc(LoadCursor<T>& c, const DecHeader& h) {
-  c.plane_bytes = (uint32_t)((int64_t)c.L.N * c.L.K / 4);
+  if (c.L.tiled) {
+    // every stage's tiles are addressed from the matrix base + t * 1024
+    c.plane_bytes = (uint32_t)(T * c.L.nrb * c.L.nk4 * 1024) - (uint32_t)(T - 1) * 1024u;
 #pragma unroll
-  for (int p = 0; p < 2 * T; ++p) c.pbase[p] = c.L.codes[p / T] + (int64_t)(p % T) * c.plane_bytes;
+    for (int p = 0; p < 2 * T; ++p) c.pbase[p] = c.L.codes[p / T] + (p % T) * 1024;
+    c.vstep = (uint32_t)T * 1024u;
+  } else {
+    c.plane_bytes = (uint32_t)((int64_t)c.L.N * c.L.K / 4);
+#pragma unroll
+    for (int p = 0; p < 2 * T; ++p) c.pbase[p] = c.L.codes[p / T] + (int64_t)(p % T) * c.plane_bytes;
+    c.vstep = 64u;
+  }
   c.xbytes = (uint32_t)(c.L.nk4 * 256 * h.nc);
 }
 
@@ -608,7 +631,7 @@ __device__ inline bool load_next(LoadCursor<T>& c, const DecLayer* tab, const De
                                  int lane) {
   if (++c.j < c.nsteps) {
     ++c.k4;
-    c.voff += 64;
+    c.voff += c.vstep;
     c.xoff += 256 * h.nc;
     return true;
   }
@@ -774,11 +797,15 @@ __global__ __launch_bounds__(64 * kStreamWaves) void dec_stream_kernel(DecHeader
     return !out_next(oc, tab, i1, li);
   };
 
+  // one pass of the loop body visits every slot once, in ring order
+  static_assert(NS >= 2 && NS <= 6, "the ring loop below is unrolled for 2..6 slots");
   while (true) {
     if (step(std::integral_constant<int, 0>{})) break;
-    if constexpr (NS > 1) if (step(std::integral_constant<int, 1 % NS>{})) break;
+    if (step(std::integral_constant<int, 1>{})) break;
     if constexpr (NS > 2) if (step(std::integral_constant<int, 2 % NS>{})) break;
     if constexpr (NS > 3) if (step(std::integral_constant<int, 3 % NS>{})) break;
+    if constexpr (NS > 4) if (step(std::integral_constant<int, 4 % NS>{})) break;
+    if constexpr (NS > 5) if (step(std::integral_constant<int, 5 % NS>{})) break;
   }
   __builtin_amdgcn_s_waitcnt(0);  // no load may still be writing LDS when the wave ends
 #endif

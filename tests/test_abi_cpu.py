@@ -42,7 +42,7 @@ def test_status_strings(lib):
     for s in range(8):
         assert lib.fairy2i_status_string(s)
     assert lib.fairy2i_status_string(99) == b"unknown status"
-    assert lib.fairy2i_abi_version() == 1
+    assert lib.fairy2i_abi_version() == 2
 
 
 def test_to_widely_linear_validation(lib):
@@ -158,10 +158,10 @@ def test_scale_rounding_random_ties(lib):
 
 def _layer(**kw):
     d = dict(codes_U=0x1000, scales_U=0x1000, codes_W=0x1000, scales_W=0x1000, x=0x1000, x_scale=None,
-             y=0x1000, N=64, K=128)
+             y=0x1000, N=64, K=128, layout=binding.LAYOUT_D3, reserved=0)
     d.update(kw)
     return binding.WlLayer(d["codes_U"], d["scales_U"], d["codes_W"], d["scales_W"], d["x"], d["x_scale"],
-                           d["y"], d["N"], d["K"])
+                           d["y"], d["N"], d["K"], d["layout"], d["reserved"])
 
 
 def test_group_build_validation(lib):
@@ -187,6 +187,24 @@ def test_group_build_validation(lib):
     assert build(good, ws=None) == binding.ERR_WORKSPACE
     assert build(good, wsb=16) == binding.ERR_WORKSPACE
     assert build(good, tb=8) == binding.ERR_WORKSPACE
+    assert build([_layer(layout=binding.LAYOUT_TILED), _layer(N=200, K=1088)]) == binding.OK
+    assert build([_layer(layout=2)]) == binding.ERR_UNSUPPORTED
+    assert build([_layer(reserved=1)]) == binding.ERR_UNSUPPORTED
+
+
+def test_repack_validation_and_size(lib):
+    b = lib.fairy2i_repack_tiled_bytes
+    assert b(16, 256, 1) == 1024
+    assert b(17, 256, 2) == 2 * 2 * 1024             # 2 row blocks
+    assert b(2048, 5504, 2) == 2 * 128 * 22 * 1024   # K = 5504: 21.5 steps -> 22
+    assert b(0, 256, 1) == 0 and b(16, 6, 1) == 0 and b(16, 256, 5) == 0
+    f = lib.fairy2i_repack_tiled
+    assert f(None, 16, 256, 1, P, 1024, None) == binding.ERR_NULL
+    assert f(P, 16, 256, 1, None, 1024, None) == binding.ERR_NULL
+    assert f(P, 16, 258, 1, P, 1 << 20, None) == binding.ERR_SHAPE
+    assert f(P, 0, 256, 1, P, 1 << 20, None) == binding.ERR_SHAPE
+    assert f(P, 16, 256, 0, P, 1 << 20, None) == binding.ERR_STAGES
+    assert f(P, 16, 256, 1, P, 1023, None) == binding.ERR_WORKSPACE
 
 
 def test_group_call_validation(lib):

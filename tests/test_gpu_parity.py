@@ -382,3 +382,76 @@ def test_group_matches_single_layer_calls(gpu):
             np.testing.assert_array_equal(host(y).view(np.uint32), y1.view(np.uint32))
             assert rel_l2(host(y), ys) <= 1e-6     # same products, K possibly sliced differently
             assert rel_l2(host(y), yo) <= TOL_F32
+
+
+# ------------------------------------------------------ tiled layout ---
+
+def tile_reference(packed, N, K):
+    """The tiled decode layout of D3 bytes [T, N, K/4], written out with
+    numpy: tile (row block, 256-code step, stage) of 1024 bytes holds, at
+    byte 16 (16 g + r) + e, D3 byte 64 s + 16 g + e of row 16 rb + r."""
+    T = packed.shape[0]
+    nrb, nk4, rowbytes = -(-N // 16), -(-K // 256), K // 4
+    pad = np.zeros((T, nrb * 16, nk4 * 64), np.uint8)
+    pad[:, :N, :rowbytes] = packed
+    a = pad.reshape(T, nrb, 16, nk4, 4, 16)            # t, rb, r, s, g, e
+    return np.ascontiguousarray(a.transpose(1, 3, 0, 4, 2, 5)).reshape(-1)
+
+
+@pytest.mark.parametrize("NKT", [(16, 256, 1), (100, 320, 2), (48, 1088, 3), (37, 100, 2), (5, 4, 4),
+                                 (2048, 5504, 2)])
+def test_repack_tiled_bit_exact(gpu, NKT):
+    """fairy2i_repack_tiled is a byte permutation of D3 with zero padding:
+    ragged row blocks, K not a multiple of 256 or of 64 (byte path), and an
+    unaligned source."""
+    import torch
+    import paper_2512_02901_amd as f2
+    N, K, T = NKT
+    rng = np.random.default_rng(N * 7 + K)
+    packed = rng.integers(0, 256, (T, N, K // 4), dtype=np.uint8)
+    want = tile_reference(packed, N, K)
+    got = host(f2.repack_tiled(dev(packed, gpu)))
+    assert got.shape == want.shape == (f2.repack_tiled_bytes(N, K, T),)
+    np.testing.assert_array_equal(got, want)
+    buf = torch.zeros(packed.size + 16, dtype=torch.uint8, device=gpu)
+    src = buf[3:3 + packed.size].view(packed.shape)
+    src.copy_(dev(packed, gpu))
+    np.testing.assert_array_equal(host(f2.repack_tiled(src)), want)
+
+
+def test_group_tiled_matches_d3(gpu):
+    """A grouped call over tiled copies of the codes gives bitwise the same y
+    as over the D3 codes (same kernels and K slicing, other addresses), for
+    the streaming (one activation tile) and the register (several tiles)
+    product kernels; both match the oracle."""
+    import torch
+    import paper_2512_02901_amd as f2
+    shapes = [(128, 256), (200, 64), (48, 1088), (64, 2048), (37, 5504)]
+    for T in (1, 2, 3):
+        qlayers = []
+        for i, (N, K) in enumerate(shapes):
+            _, _, cu, su, cw, sw = oracle_layer(synth.llama_weight(2 * N, 2 * K, (16, i, N)), T)
+            d = upload_layer(cu, su, cw, sw, gpu)
+            qlayers.append((cu, su, cw, sw, d, (f2.repack_tiled(d[0]), d[1], f2.repack_tiled(d[2]), d[3])))
+        for B, mk in ((1, "bf16"), (2, "bf16"), (3, "bf16"), (16, "bf16"), (1, "i8"), (8, "i8"), (9, "i8")):
+            d3, tl, refs = [], [], []
+            for i, ((N, K), (cu, su, cw, sw, d, dt)) in enumerate(zip(shapes, qlayers)):
+                x = synth.activations(B, K, (17, i, B))
+                if mk == "bf16":
+                    xv = synth.bf16_round_complex(x)
+                    xd, xs = bf16_dev(xv, gpu), None
+                    yo = oracle.wl_matmul(cu, su, cw, sw, xv)
+                else:
+                    qo, fo = oracle.quantize_act_int8(x)
+                    xd, xs = dev(qo, gpu), dev(fo, gpu)
+                    yo = oracle.wl_matmul_int8(cu, su, cw, sw, qo, fo)
+                y0 = torch.empty((B, N), dtype=torch.complex64, device=gpu)
+                y1 = torch.empty((B, N), dtype=torch.complex64, device=gpu)
+                d3.append((*d, xd, xs, y0))
+                tl.append((*dt, xd, xs, y1))
+                refs.append(yo)
+            f2.WlGroup(d3, T=T, B=B).run()
+            f2.WlGroup(tl, T=T, B=B, tiled=True).run()
+            for a, b, yo in zip(d3, tl, refs):
+                np.testing.assert_array_equal(host(b[6]).view(np.uint32), host(a[6]).view(np.uint32))
+                assert rel_l2(host(b[6]), yo) <= TOL_F32
