@@ -53,13 +53,70 @@ __device__ inline void expand_codes(uint32_t w, v4i& bre, v4i& bim) {
 
 __device__ inline int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
-// Scalar (SMEM) load of a float at a wave-uniform address.  Scalar loads are
-// tracked by lgkmcnt, so waiting for one does not drain the vector-memory
-// queue that holds the prefetched code bytes.
-__device__ inline float sload_f32(const float* p) {
-  float v;
-  __asm__ volatile("s_load_dword %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(v) : "s"(p) : "memory");
-  return v;
+// Scalar (SMEM) loads of wave-uniform operands.  Scalar loads are tracked by
+// lgkmcnt, so waiting for them does not drain the vector-memory queue that
+// holds the prefetched code bytes.
+
+typedef float sf2 __attribute__((ext_vector_type(2)));
+typedef float sf4 __attribute__((ext_vector_type(4)));
+typedef float sf8 __attribute__((ext_vector_type(8)));
+
+// Axis scales of both matrices, sc[m][t][axis], by scalar loads that are all
+// in flight before one wait.  The arrays hold exactly 2T floats each.
+template <int T>
+__device__ inline void sload_scales(const float* pu, const float* pw, float (&sc)[2][T][2]) {
+  float a[2][2 * T];
+  if constexpr (T == 1) {
+    sf2 u, w;
+    __asm__ volatile("s_load_dwordx2 %0, %2, 0x0\n\ts_load_dwordx2 %1, %3, 0x0\n\ts_waitcnt lgkmcnt(0)"
+                     : "=&s"(u), "=&s"(w) : "s"(pu), "s"(pw) : "memory");
+    for (int i = 0; i < 2; ++i) { a[0][i] = u[i]; a[1][i] = w[i]; }
+  } else if constexpr (T == 2) {
+    sf4 u, w;
+    __asm__ volatile("s_load_dwordx4 %0, %2, 0x0\n\ts_load_dwordx4 %1, %3, 0x0\n\ts_waitcnt lgkmcnt(0)"
+                     : "=&s"(u), "=&s"(w) : "s"(pu), "s"(pw) : "memory");
+    for (int i = 0; i < 4; ++i) { a[0][i] = u[i]; a[1][i] = w[i]; }
+  } else if constexpr (T == 3) {
+    sf4 u, w;
+    sf2 u2, w2;
+    __asm__ volatile(
+        "s_load_dwordx4 %0, %4, 0x0\n\ts_load_dwordx2 %1, %4, 0x10\n\t"
+        "s_load_dwordx4 %2, %5, 0x0\n\ts_load_dwordx2 %3, %5, 0x10\n\ts_waitcnt lgkmcnt(0)"
+        : "=&s"(u), "=&s"(u2), "=&s"(w), "=&s"(w2) : "s"(pu), "s"(pw) : "memory");
+    for (int i = 0; i < 4; ++i) { a[0][i] = u[i]; a[1][i] = w[i]; }
+    for (int i = 0; i < 2; ++i) { a[0][4 + i] = u2[i]; a[1][4 + i] = w2[i]; }
+  } else {
+    static_assert(T == 4, "1 <= T <= 4");
+    sf8 u, w;
+    __asm__ volatile("s_load_dwordx8 %0, %2, 0x0\n\ts_load_dwordx8 %1, %3, 0x0\n\ts_waitcnt lgkmcnt(0)"
+                     : "=&s"(u), "=&s"(w) : "s"(pu), "s"(pw) : "memory");
+    for (int i = 0; i < 8; ++i) { a[0][i] = u[i]; a[1][i] = w[i]; }
+  }
+#pragma unroll
+  for (int m = 0; m < 2; ++m)
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      sc[m][t][0] = a[m][2 * t];
+      sc[m][t][1] = a[m][2 * t + 1];
+    }
+}
+
+// NT consecutive floats (2 or 8) at a wave-uniform address, one scalar load.
+// The caller guarantees the NT floats lie inside the allocation.
+template <int NT>
+__device__ inline void sload_run(const float* p, float (&v)[NT]) {
+  if constexpr (NT == 2) {
+    sf2 r;
+    __asm__ volatile("s_load_dwordx2 %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=&s"(r) : "s"(p) : "memory");
+    v[0] = r[0];
+    v[1] = r[1];
+  } else {
+    static_assert(NT == 8, "2 or 8 floats");
+    sf8 r;
+    __asm__ volatile("s_load_dwordx8 %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=&s"(r) : "s"(p) : "memory");
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = r[i];
+  }
 }
 
 __device__ inline int64_t uniform64(int64_t v) {
@@ -374,25 +431,20 @@ __device__ inline void write_outputs(const DecLayer& L, const DecHeader& h, cons
   const int N = L.N;
   // wave-uniform operands of the epilogue, by scalar loads
   float sc[2][T][2];
-  if constexpr (!EXPORT) {
-#pragma unroll
-    for (int m = 0; m < 2; ++m)
-#pragma unroll
-      for (int t = 0; t < T; ++t) {
-        sc[m][t][0] = sload_f32(L.scales[m] + 2 * t);
-        sc[m][t][1] = sload_f32(L.scales[m] + 2 * t + 1);
-      }
-  }
+  if constexpr (!EXPORT) sload_scales<T>(L.scales[0], L.scales[1], sc);
 #pragma unroll
   for (int tt = 0; tt < NTG; ++tt) {
     const int tile = q.tg0 + tt;
     // factors of the (up to 8) tokens of this tile
     float xsv[8];
     if constexpr (!EXPORT) {
-      const int nt = MODE == kModeBf16 ? 2 : 8;
+      // the factor array is padded to 256 bytes, so the tile's full run of
+      // nt floats is always inside it
+      constexpr int nt = MODE == kModeBf16 ? 2 : 8;
+      float run[nt];
+      sload_run<nt>(L.xs + tile * nt, run);
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
-        xsv[i] = (i < nt && tile * nt + i < h.B) ? sload_f32(L.xs + tile * nt + i) : 0.0f;
+      for (int i = 0; i < 8; ++i) xsv[i] = (i < nt && tile * nt + i < h.B) ? run[i < nt ? i : 0] : 0.0f;
     }
     // bf16: token 2*tile + g/2 has digits 0, 1 in group g and digit 2 in
     // group g+1; fetch the latter (all lanes take part in the shuffle).
@@ -557,53 +609,89 @@ __global__ __launch_bounds__(256) void dec_mfma_kernel(DecHeader h, DecLayer inl
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
+// Geometry of one layer as the streaming kernel needs it (all wave-uniform).
+struct StreamLayer {
+  int64_t item0, lend;  // first work item of the layer and one past its last
+  int32_t N, K, nkc, kc4, nk4, tiled;
+};
+
+__device__ inline StreamLayer stream_layer(const DecLayer& L) {
+  StreamLayer g;
+  g.item0 = L.item0;
+  g.lend = L.item0 + (int64_t)L.nrb * L.nkc;
+  g.N = L.N;
+  g.K = L.K;
+  g.nkc = L.nkc;
+  g.kc4 = L.kc4;
+  g.nk4 = L.nk4;
+  g.tiled = L.tiled;
+  return g;
+}
+
 // Load side of the streaming kernel: which step's bytes to fetch next.  All
 // geometry is recomputed only when an item starts; a step just advances two
-// offsets.
+// offsets.  Only addressing state is kept (a layer descriptor is read from
+// the table when the range enters a new layer).
 template <int T>
 struct LoadCursor {
-  DecLayer L;
-  int64_t item, lend;
-  int lidx, j, nsteps, k4;
+  StreamLayer G;
+  int64_t item;
+  int lidx, rb, kc, j, nsteps, k4;  // item = (row block rb, K slice kc) of layer lidx
   const uint8_t* pbase[2 * T];  // code plane (M, t) of the current layer
+  const int8_t* xf;             // the layer's activation operand
   uint32_t plane_bytes, xbytes;
   uint32_t voff;   // this lane's offset in every code plane at step k4 (row, 16-code group)
   uint32_t vstep;  // voff advance per step: 64 (D3) or T * 1024 (tiled)
-  uint32_t xoff;  // offset of the step's activation operand + lane * 16
+  uint32_t xoff;   // offset of the step's activation operand + lane * 16
   bool row_ok;
 };
+
+// (row block, K slice) of an item inside its layer (a layer has < 2^31 items)
+__device__ inline void split_item(int64_t item, const StreamLayer& G, int& rb, int& kc) {
+  const int local = (int)(item - G.item0);
+  rb = local / G.nkc;
+  kc = local - rb * G.nkc;
+}
+
+// The next item of a cursor: the next K slice, else the next row block.
+__device__ inline void advance_item(int& rb, int& kc, int nkc) {
+  if (++kc == nkc) {
+    kc = 0;
+    ++rb;
+  }
+}
 
 template <int T>
 __device__ inline void load_item(LoadCursor<T>& c, const DecHeader& h, int lane) {
   const int g = lane >> 4, li = lane & 15;
-  const int64_t local = c.item - c.L.item0;
-  const int rb = (int)(local / c.L.nkc);
-  const int kc = (int)(local - (int64_t)rb * c.L.nkc);
-  c.k4 = kc * c.L.kc4;
-  c.nsteps = min(c.L.kc4, c.L.nk4 - c.k4);
+  const int rb = c.rb, kc = c.kc;
+  c.k4 = kc * c.G.kc4;
+  c.nsteps = min(c.G.kc4, c.G.nk4 - c.k4);
   c.j = 0;
   const int row = rb * 16 + li;
-  c.row_ok = row < c.L.N;
-  c.voff = c.L.tiled ? (uint32_t)((rb * c.L.nk4 + c.k4) * T) * 1024u + (uint32_t)lane * 16u
-                     : (uint32_t)row * (uint32_t)(c.L.K / 4) + (uint32_t)(c.k4 * 64 + 16 * g);
+  c.row_ok = row < c.G.N;
+  c.voff = c.G.tiled ? (uint32_t)((rb * c.G.nk4 + c.k4) * T) * 1024u + (uint32_t)lane * 16u
+                     : (uint32_t)row * (uint32_t)(c.G.K / 4) + (uint32_t)(c.k4 * 64 + 16 * g);
   c.xoff = (uint32_t)(c.k4 * 256 * h.nc + lane * 16);
 }
 
 template <int T>
-__device__ inline void load_layer_rsrc(LoadCursor<T>& c, const DecHeader& h) {
-  if (c.L.tiled) {
+__device__ inline void load_enter_layer(LoadCursor<T>& c, const DecLayer& L, const DecHeader& h) {
+  c.G = stream_layer(L);
+  if (L.tiled) {
     // every stage's tiles are addressed from the matrix base + t * 1024
-    c.plane_bytes = (uint32_t)(T * c.L.nrb * c.L.nk4 * 1024) - (uint32_t)(T - 1) * 1024u;
+    c.plane_bytes = (uint32_t)(T * L.nrb * L.nk4 * 1024) - (uint32_t)(T - 1) * 1024u;
 #pragma unroll
-    for (int p = 0; p < 2 * T; ++p) c.pbase[p] = c.L.codes[p / T] + (p % T) * 1024;
+    for (int p = 0; p < 2 * T; ++p) c.pbase[p] = L.codes[p / T] + (p % T) * 1024;
     c.vstep = (uint32_t)T * 1024u;
   } else {
-    c.plane_bytes = (uint32_t)((int64_t)c.L.N * c.L.K / 4);
+    c.plane_bytes = (uint32_t)((int64_t)L.N * L.K / 4);
 #pragma unroll
-    for (int p = 0; p < 2 * T; ++p) c.pbase[p] = c.L.codes[p / T] + (int64_t)(p % T) * c.plane_bytes;
+    for (int p = 0; p < 2 * T; ++p) c.pbase[p] = L.codes[p / T] + (int64_t)(p % T) * c.plane_bytes;
     c.vstep = 64u;
   }
-  c.xbytes = (uint32_t)(c.L.nk4 * 256 * h.nc);
+  c.xf = L.xf;
+  c.xbytes = (uint32_t)(L.nk4 * 256 * h.nc);
 }
 
 // Issue the 2T + XW direct-to-LDS loads of the cursor's step into `slot`; a
@@ -612,16 +700,21 @@ __device__ inline void load_layer_rsrc(LoadCursor<T>& c, const DecHeader& h) {
 template <int XW, int T>
 __device__ inline void stream_issue(const LoadCursor<T>& c, bool live, int lane, uint8_t* slot) {
   const int g = lane >> 4;
-  const bool ok = live && c.row_ok && c.k4 * 256 + 64 * g < c.L.K;
+  const bool ok = live && c.row_ok && c.k4 * 256 + 64 * g < c.G.K;
   const uint32_t off = ok ? c.voff : kOob;
+  // descriptor fields stated wave-uniform, so the descriptors stay in scalar
+  // registers (no per-load waterfall over lanes)
+  const int pb = __builtin_amdgcn_readfirstlane((int)c.plane_bytes);
 #pragma unroll
   for (int p = 0; p < 2 * T; ++p)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(c.pbase[p], c.plane_bytes), (lds_ptr_t)(slot + p * 1024),
-                                             16, off, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(uniform_ptr(c.pbase[p]), (uint32_t)pb),
+                                             (lds_ptr_t)(slot + p * 1024), 16, off, 0, 0, 0);
   const uint32_t xo = live ? c.xoff : kOob;
+  const int xb = __builtin_amdgcn_readfirstlane((int)c.xbytes);
+  const int8_t* xf = uniform_ptr(c.xf);
 #pragma unroll
   for (int i = 0; i < XW; ++i)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(c.L.xf, c.xbytes), (lds_ptr_t)(slot + 2 * T * 1024 + i * 1024),
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(xf, (uint32_t)xb), (lds_ptr_t)(slot + 2 * T * 1024 + i * 1024),
                                              16, xo + i * 1024, 0, 0, 0);
 }
 
@@ -636,49 +729,76 @@ __device__ inline bool load_next(LoadCursor<T>& c, const DecLayer* tab, const De
     return true;
   }
   if (++c.item >= iend) return false;
-  if (c.item >= c.lend) {
+  if (c.item >= c.G.lend) {
     ++c.lidx;
-    c.L = load_layer(tab + c.lidx);
-    c.lend = c.L.item0 + (int64_t)c.L.nrb * c.L.nkc;
-    load_layer_rsrc(c, h);
+    load_enter_layer(c, load_layer(tab + c.lidx), h);
+    c.rb = c.kc = 0;
+  } else {
+    advance_item(c.rb, c.kc, c.G.nkc);
   }
   load_item(c, h, lane);
   return true;
 }
 
-// Compute side: which item the current step belongs to (for its epilogue).
+// Compute side: which item the current step belongs to, and what its
+// epilogue writes.
 struct OutCursor {
-  DecLayer L;
-  int64_t item, lend;
-  int lidx, j, nsteps, kc, row;
+  StreamLayer G;
+  const float* scales[2];
+  float* xs;
+  float2* y;
+  float2* part;
+  int64_t item;
+  int lidx, rb, kc, j, nsteps, row;
   bool row_ok;
 };
 
+__device__ inline void out_enter_layer(OutCursor& c, const DecLayer& L) {
+  c.G = stream_layer(L);
+  c.scales[0] = L.scales[0];
+  c.scales[1] = L.scales[1];
+  c.xs = L.xs;
+  c.y = L.y;
+  c.part = L.part;
+}
+
 __device__ inline void out_item(OutCursor& c, int li) {
-  const int64_t local = c.item - c.L.item0;
-  const int rb = (int)(local / c.L.nkc);
-  c.kc = (int)(local - (int64_t)rb * c.L.nkc);
-  c.nsteps = min(c.L.kc4, c.L.nk4 - c.kc * c.L.kc4);
+  c.nsteps = min(c.G.kc4, c.G.nk4 - c.kc * c.G.kc4);
   c.j = 0;
-  c.row = rb * 16 + li;
-  c.row_ok = c.row < c.L.N;
+  c.row = c.rb * 16 + li;
+  c.row_ok = c.row < c.G.N;
 }
 
 __device__ inline bool out_next(OutCursor& c, const DecLayer* tab, int64_t iend, int li) {
   if (++c.j < c.nsteps) return true;
   if (++c.item >= iend) return false;
-  if (c.item >= c.lend) {
+  if (c.item >= c.G.lend) {
     ++c.lidx;
-    c.L = load_layer(tab + c.lidx);
-    c.lend = c.L.item0 + (int64_t)c.L.nrb * c.L.nkc;
+    out_enter_layer(c, load_layer(tab + c.lidx));
+    c.rb = c.kc = 0;
+  } else {
+    advance_item(c.rb, c.kc, c.G.nkc);
   }
   out_item(c, li);
   return true;
 }
 
+// The fields write_outputs reads, from the compute cursor.
+__device__ inline DecLayer out_layer(const OutCursor& c) {
+  DecLayer L{};
+  L.scales[0] = uniform_ptr(c.scales[0]);
+  L.scales[1] = uniform_ptr(c.scales[1]);
+  L.xs = uniform_ptr(c.xs);
+  L.y = uniform_ptr(c.y);
+  L.part = uniform_ptr(c.part);
+  L.N = c.G.N;
+  L.nkc = c.G.nkc;
+  return L;
+}
+
 // waves per block and LDS bytes per wave of the streaming kernel
 constexpr int kStreamWaves = 4;
-constexpr int kStreamLdsPerWave = 20 * 1024 - 16;
+constexpr int kStreamLdsPerWave = 12 * 1024;
 
 template <int T, int XW>
 struct StreamCfg {
@@ -718,17 +838,19 @@ __global__ __launch_bounds__(64 * kStreamWaves) void dec_stream_kernel(DecHeader
   const bool xvalid = col_token<MODE>(0, li, h.B, b_, digit_, comp_);
 
   LoadCursor<T> lc;
-  lc.lidx = tab ? find_layer(tab, h.n_layers, i0) : 0;
-  lc.L = tab ? load_layer(tab + lc.lidx) : inl;
-  lc.lend = lc.L.item0 + (int64_t)lc.L.nrb * lc.L.nkc;
-  lc.item = i0;
-  load_layer_rsrc(lc, h);
-  load_item(lc, h, lane);
   OutCursor oc;
-  oc.L = lc.L;
-  oc.lidx = lc.lidx;
-  oc.lend = lc.lend;
-  oc.item = i0;
+  {
+    const int lidx = tab ? find_layer(tab, h.n_layers, i0) : 0;
+    const DecLayer L0 = tab ? load_layer(tab + lidx) : inl;
+    lc.lidx = oc.lidx = lidx;
+    lc.item = oc.item = i0;
+    load_enter_layer(lc, L0, h);
+    out_enter_layer(oc, L0);
+    split_item(i0, lc.G, lc.rb, lc.kc);
+    oc.rb = lc.rb;
+    oc.kc = lc.kc;
+  }
+  load_item(lc, h, lane);
   out_item(oc, li);
 
   bool live = true;
@@ -792,7 +914,7 @@ __global__ __launch_bounds__(64 * kStreamWaves) void dec_stream_kernel(DecHeader
           item_acc[p][ax][0] = acc[p][ax][0] - base[p][ax][0];
           base[p][ax][0] = acc[p][ax][0];
         }
-      write_outputs<MODE, T, 1, false>(oc.L, h, q, lane, item_acc);
+      write_outputs<MODE, T, 1, false>(out_layer(oc), h, q, lane, item_acc);
     }
     return !out_next(oc, tab, i1, li);
   };
