@@ -167,7 +167,10 @@ size_t fairy2i_wl_matmul_workspace_bytes(int64_t N, int64_t K, int32_t T, int64_
  * a 23-bit block fixed point, exact for every value within 2^14 of the
  * token's largest magnitude, smaller values rounded to that grid), other
  * cases to a float32 / int32 vector kernel.  Larger B needs FAIRY2I_ACT_I8
- * and runs the int8-MFMA prefill kernel.
+ * and runs the int8-MFMA prefill GEMM: with K % 64 == 0 (and sizes within
+ * 32-bit offsets) a workspace holds the activations in the matrix-core
+ * operand layout and the GEMM streams operands through LDS; otherwise a
+ * direct kernel runs without workspace.
  * workspace: at least fairy2i_wl_matmul_workspace_bytes(...) bytes of
  * device memory (may be NULL when that is 0), contents ignored on entry.
  * Errors: FAIRY2I_ERR_NULL; FAIRY2I_ERR_SHAPE if N, K, B <= 0 or K % 4;

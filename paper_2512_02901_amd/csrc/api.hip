@@ -164,8 +164,9 @@ fairy2i_status fairy2i_quantize_act_int8(const void* x, int32_t dtype, int64_t B
 
 size_t fairy2i_wl_matmul_workspace_bytes(int64_t N, int64_t K, int32_t T, int64_t B, int32_t dtype) {
   if (N <= 0 || K <= 0 || B <= 0 || T < 1 || T > FAIRY2I_MAX_STAGES) return 0;
-  if (!use_mfma_decode(dtype, N, K, B)) return 0;
-  return single_decode_bytes(N, K, T, B, dtype);
+  if (use_mfma_decode(dtype, N, K, B)) return single_decode_bytes(N, K, T, B, dtype);
+  if (dtype == FAIRY2I_ACT_I8 && B > FAIRY2I_MAX_DECODE_BATCH) return gemm_workspace_bytes(N, K, B);
+  return 0;
 }
 
 fairy2i_status fairy2i_wl_matmul(const uint8_t* codes_U, const float* scales_U,
@@ -202,7 +203,7 @@ fairy2i_status fairy2i_wl_matmul(const uint8_t* codes_U, const float* scales_U,
   a.y = reinterpret_cast<float2*>(y);
   a.acc = nullptr;
   const hipError_t e = (B <= FAIRY2I_MAX_DECODE_BATCH) ? launch_gemv(a, as_stream(stream))
-                                                       : launch_gemm_i8(a, as_stream(stream));
+                                                       : launch_gemm_i8(a, workspace, as_stream(stream));
   return hip_status(e);
 }
 
@@ -229,7 +230,7 @@ fairy2i_status fairy2i_wl_int8_accumulators(const uint8_t* codes_U, const uint8_
   a.dtype = FAIRY2I_ACT_I8;
   a.acc = acc;
   const hipError_t e = (B <= FAIRY2I_MAX_DECODE_BATCH) ? launch_gemv(a, as_stream(stream))
-                                                       : launch_gemm_i8(a, as_stream(stream));
+                                                       : launch_gemm_i8(a, workspace, as_stream(stream));
   return hip_status(e);
 }
 

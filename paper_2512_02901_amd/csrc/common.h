@@ -43,6 +43,10 @@ struct WlArgs {
 };
 
 hipError_t launch_gemv(const WlArgs& a, hipStream_t stream);       // B <= 16
-hipError_t launch_gemm_i8(const WlArgs& a, hipStream_t stream);    // int8, any B
+// int8, any B.  With a workspace of gemm_workspace_bytes (> 0 only when
+// K % 64 == 0 and sizes fit 32-bit offsets) the pipelined kernel runs, else
+// the direct one.
+size_t gemm_workspace_bytes(int64_t N, int64_t K, int64_t B);
+hipError_t launch_gemm_i8(const WlArgs& a, void* workspace, hipStream_t stream);
 
 }  // namespace fairy2i

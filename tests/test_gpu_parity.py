@@ -191,7 +191,7 @@ def test_decode_float_paths(gpu, T, B, NK):
 
 @pytest.mark.parametrize("T", [1, 2, 3, 4])
 @pytest.mark.parametrize("B", [1, 5, 16, 17, 64, 100, 130])
-@pytest.mark.parametrize("NK", [(128, 128), (48, 68), (96, 1040)])
+@pytest.mark.parametrize("NK", [(128, 128), (48, 68), (96, 1040), (100, 192), (37, 1088)])
 def test_int8_paths_bit_exact(gpu, T, B, NK):
     """Decode (B <= 16) and prefill (B > 16) int8 products: accumulators
     bit-exact, y within 1e-5."""
@@ -331,6 +331,26 @@ def test_mfma_decode_misaligned_activations(gpu, B):
         y1 = host(f2.wl_matmul(*d, xm, xs))
         np.testing.assert_array_equal(y1, y0)
         assert rel_l2(y1, want) <= TOL_F32
+
+
+def test_prefill_misaligned_activations(gpu):
+    """int8 activations at an address that is not 16-byte aligned take the
+    element-wise path of the prefill operand preparation: bitwise the same."""
+    import torch
+    import paper_2512_02901_amd as f2
+    N, K, B = 40, 192, 37
+    A = synth.llama_weight(2 * N, 2 * K, (18, N, K))
+    _, _, cu, su, cw, sw = oracle_layer(A, 2)
+    d = upload_layer(cu, su, cw, sw, gpu)
+    qo, fo = oracle.quantize_act_int8(synth.activations(B, K, (19, B, K)))
+    q, xs = dev(qo, gpu), dev(fo, gpu)
+    buf = torch.zeros(q.numel() + 16, dtype=torch.int8, device=gpu)
+    qm = buf[5:5 + q.numel()].view(q.shape)
+    qm.copy_(q)
+    y0 = host(f2.wl_matmul(*d, q, xs))
+    np.testing.assert_array_equal(host(f2.wl_matmul(*d, qm, xs)), y0)
+    np.testing.assert_array_equal(host(f2.int8_accumulators(d[0], d[2], qm)), oracle.int8_accumulators(cu, cw, qo))
+    assert rel_l2(y0, oracle.wl_matmul_int8(cu, su, cw, sw, qo, fo)) <= TOL_F32
 
 
 def test_mfma_decode_bf16_wide_dynamic_range(gpu):
