@@ -271,7 +271,7 @@ __global__ __launch_bounds__(256) void prefill_prep_kernel(const int8_t* __restr
 }
 
 template <int T, bool EXPORT>
-__global__ __launch_bounds__(256) void gemm_i8_pipe_kernel(WlArgs a, const int8_t* __restrict__ xp) {
+__global__ __launch_bounds__(256, (T <= 3) ? 2 : 1) void gemm_i8_pipe_kernel(WlArgs a, const int8_t* __restrict__ xp) {
 #if defined(__HIP_DEVICE_COMPILE__)  // LDS-DMA and buffer-descriptor code: device pass only
   constexpr int P = 2 * T;
   constexpr int CL = (P + 3) / 4;  // code tiles loaded per wave and stage
