@@ -224,7 +224,11 @@ def main():
     achieved = algo / (prod_ms * 1e-3) / 1e9
     traffic = traffic_record()
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "frac": round(achieved / HBM_PEAK_GBS, 4),
+                # calibrated rocprofv3 FETCH_SIZE + WRITE_SIZE bytes per launch (null when the
+                # committed counters were taken for another kernel source)
+                "traffic": None if traffic is None else int(traffic),
+                "traffic_over_algorithmic": None if traffic is None else round(traffic / algo, 3),
                 "kernel": "dec_stream_kernel<bf16, T=2> (int8 MFMA product over tiled codes, one launch per step)",
                 "algorithmic_bytes_per_launch": algo, "avg_launch_us": round(prod_ms * 1e3, 2)}
 
