@@ -173,7 +173,7 @@ def cpu_baseline(f2, synth, torch, dev, layers, T, budget_s=12.0):
         oracle.wl_matmul(cu_h, su_h, cw_h, sw_h, xh)
         reps += 1
         el = time.perf_counter() - t0
-        if el >= budget_s or reps >= 50:
+        if el >= budget_s or reps >= 400:
             break
     gbs = packed * reps / el / 1e9
     return {"value": round(gbs, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",

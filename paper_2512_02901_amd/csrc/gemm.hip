@@ -275,8 +275,6 @@ __global__ __launch_bounds__(256, (T <= 3) ? 2 : 1) void gemm_i8_pipe_kernel(WlA
 #if defined(__HIP_DEVICE_COMPILE__)  // LDS-DMA and buffer-descriptor code: device pass only
   constexpr int P = 2 * T;
   constexpr int CL = (P + 3) / 4;  // code tiles loaded per wave and stage
-  constexpr int LOADS = 4 + CL;    // loads per wave and stage
-  constexpr int WAITCNT = (LOADS & 0xF) | (0x7 << 4) | (0xF << 8);
   __shared__ __attribute__((aligned(16))) uint8_t lx0[4][2][2][1024];  // [fragment][step][component]
   __shared__ __attribute__((aligned(16))) uint8_t lx1[4][2][2][1024];
   __shared__ __attribute__((aligned(16))) uint8_t lc0[P][1024];        // [plane][row (32) x 32 bytes]
@@ -361,27 +359,20 @@ __global__ __launch_bounds__(256, (T <= 3) ? 2 : 1) void gemm_i8_pipe_kernel(WlA
 
   // stages alternate between the two buffers; the buffer index is a
   // compile-time choice so loads into one buffer never order reads of the other
+  // One barrier per stage: after it, every wave has both received stage st
+  // (each waited for its own loads) and finished stage st-1, whose buffer
+  // the loads of stage st+1 then refill while stage st is multiplied.
   issue(0, lx0, lc0);
   for (int st = 0; st < nst; st += 2) {
-    if (st + 1 < nst) {
-      issue(st + 1, lx1, lc1);
-      __builtin_amdgcn_s_waitcnt(WAITCNT);  // stage st has landed (stage st+1 may be in flight)
-    } else {
-      __builtin_amdgcn_s_waitcnt(0);
-    }
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
+    if (st + 1 < nst) issue(st + 1, lx1, lc1);
     compute(st, lx0, lc0);
-    __syncthreads();
     if (st + 1 >= nst) break;
-    if (st + 2 < nst) {
-      issue(st + 2, lx0, lc0);
-      __builtin_amdgcn_s_waitcnt(WAITCNT);
-    } else {
-      __builtin_amdgcn_s_waitcnt(0);
-    }
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
+    if (st + 2 < nst) issue(st + 2, lx0, lc0);
     compute(st + 1, lx1, lc1);
-    __syncthreads();
   }
 
   // ---- epilogue: lane holds rows 4*(lane/16)+r, token column lane%16 ----
