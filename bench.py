@@ -118,7 +118,7 @@ def traffic_record():
         return None
 
 
-def prefill_bench(f2, synth, torch, dev, T=2, tokens=2048, reps=10):
+def prefill_bench(f2, synth, torch, dev, T=2, tokens=2048, reps=20):
     out = {}
     for name, (rows, cols) in (("q", synth.LLAMA2_7B_PROJ["q"]), ("gate", synth.LLAMA2_7B_PROJ["gate"])):
         N, K = rows // 2, cols // 2
@@ -133,7 +133,7 @@ def prefill_bench(f2, synth, torch, dev, T=2, tokens=2048, reps=10):
         x = torch.randn(tokens, K, dtype=torch.complex64, device=dev, generator=g)
         q, xs = f2.quantize_act_int8(x)
         y = torch.empty(tokens, N, dtype=torch.complex64, device=dev)
-        for _ in range(3):
+        for _ in range(10):
             f2.wl_matmul(cu, su, cw, sw, q, xs, out=y)
         torch.cuda.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
@@ -184,8 +184,8 @@ def cpu_baseline(f2, synth, torch, dev, layers, T, budget_s=12.0):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=30)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true", help="skip prefill, T=3 and D3-layout measurements")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -265,7 +265,7 @@ def main():
 
     if not args.no_extras:
         grp3, packed3, _, layers3 = build_stack(f2, synth, torch, dev, 3, seed_base=2000)
-        ms3, _, _, _ = time_group(grp3, torch, max(5, args.steps // 2), 2)
+        ms3, _, _, _ = time_group(grp3, torch, max(5, args.steps // 2), args.warmup)
         result["stack_T3"] = {"ms_per_step": round(ms3, 4), "packed_bytes": packed3,
                               "GBs": round(packed3 / (ms3 * 1e-3) / 1e9, 1),
                               "time_ratio_T3_over_T2": round(ms3 / ms, 3)}
