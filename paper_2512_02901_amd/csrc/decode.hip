@@ -598,14 +598,16 @@ __global__ __launch_bounds__(256) void dec_mfma_kernel(DecHeader h, DecLayer inl
 }
 
 // ------------------------------------------------------ streaming kernel ---
-// For one activation tile (bf16 B <= 2, int8 B <= 8) the code bytes and the
-// activation operand stream through a per-wave ring of NS LDS slots, filled
-// by direct-to-LDS buffer loads NS-1 steps (of 256 codes) ahead of the step
-// being computed, so the bytes in flight hold no registers.  Each lane's 16
-// bytes land at slot + lane * 16 (out-of-range lanes write zeros); a lane
-// reads back only its own code bytes and its wave's activation operand, so
-// waves never wait for each other.  A work item spans kc4 steps (up to 2048
-// codes), which keeps the epilogue cost per code small.
+// For one activation tile (bf16 B <= 2, int8 B <= 8) each wave streams its
+// range of work items through a ring of NS slots, filled NS-1 steps (of 256
+// codes) ahead of the step being computed.  A slot holds the step's code
+// bytes in registers (16 bytes per lane and plane, non-temporal loads: the
+// codes are read once) and its activation operand in LDS (a direct-to-LDS
+// load of the layer's prepared operand, which stays cached: every row block
+// of the layer reads it).  Out-of-range lanes load zeros.  A lane only ever
+// reads its own wave's slots, so waves never wait for each other.  A work
+// item spans kc4 steps (up to 2048 codes), which keeps the epilogue cost per
+// code small.
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
@@ -694,11 +696,15 @@ __device__ inline void load_enter_layer(LoadCursor<T>& c, const DecLayer& L, con
   c.xbytes = (uint32_t)(L.nk4 * 256 * h.nc);
 }
 
-// Issue the 2T + XW direct-to-LDS loads of the cursor's step into `slot`; a
-// dead cursor issues them out of range (they write zeros), so every step
+constexpr int kNonTemporal = 2;  // buffer-load cache policy: streaming (nt)
+
+// Issue the loads of the cursor's step: its 2T x 16 code bytes per lane into
+// registers cq, and its activation operand (XW KiB) into the LDS slot xslot.
+// A dead cursor issues them out of range (they return zeros), so every step
 // issues the same number of loads.
 template <int XW, int T>
-__device__ inline void stream_issue(const LoadCursor<T>& c, bool live, int lane, uint8_t* slot) {
+__device__ inline void stream_issue(const LoadCursor<T>& c, bool live, int lane, v4i (&cq)[2 * T],
+                                    uint8_t* xslot) {
   const int g = lane >> 4;
   const bool ok = live && c.row_ok && c.k4 * 256 + 64 * g < c.G.K;
   const uint32_t off = ok ? c.voff : kOob;
@@ -707,15 +713,33 @@ __device__ inline void stream_issue(const LoadCursor<T>& c, bool live, int lane,
   const int pb = __builtin_amdgcn_readfirstlane((int)c.plane_bytes);
 #pragma unroll
   for (int p = 0; p < 2 * T; ++p)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(uniform_ptr(c.pbase[p]), (uint32_t)pb),
-                                             (lds_ptr_t)(slot + p * 1024), 16, off, 0, 0, 0);
+    cq[p] = __builtin_amdgcn_raw_buffer_load_b128(make_rsrc(uniform_ptr(c.pbase[p]), (uint32_t)pb), off, 0,
+                                                  kNonTemporal);
   const uint32_t xo = live ? c.xoff : kOob;
   const int xb = __builtin_amdgcn_readfirstlane((int)c.xbytes);
   const int8_t* xf = uniform_ptr(c.xf);
 #pragma unroll
   for (int i = 0; i < XW; ++i)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(xf, (uint32_t)xb), (lds_ptr_t)(slot + 2 * T * 1024 + i * 1024),
-                                             16, xo + i * 1024, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(xf, (uint32_t)xb), (lds_ptr_t)(xslot + i * 1024), 16,
+                                             xo + i * 1024, 0, 0, 0);
+}
+
+// LDS address (byte offset) of a pointer into shared memory.
+__device__ inline uint32_t lds_addr(const void* p) {
+  return (uint32_t)reinterpret_cast<uintptr_t>((lds_ptr_t)const_cast<void*>(p));
+}
+
+// Four 16-byte LDS reads and the wait for them, as one unit.  The ring's
+// loads into LDS are ordered by the caller's explicit vmcnt wait; written
+// this way the compiler adds no wait of its own for the loads still in
+// flight into the ring's other slots.
+__device__ inline void lds_read4(uint32_t a0, uint32_t a1, uint32_t a2, uint32_t a3, v4i (&x)[4]) {
+  __asm__ volatile(
+      "ds_read_b128 %0, %4\n\tds_read_b128 %1, %5\n\tds_read_b128 %2, %6\n\tds_read_b128 %3, %7\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(x[0]), "=&v"(x[1]), "=&v"(x[2]), "=&v"(x[3])
+      : "v"(a0), "v"(a1), "v"(a2), "v"(a3)
+      : "memory");
 }
 
 // Next step of the load side; false once the wave's items are exhausted.
@@ -796,20 +820,18 @@ __device__ inline DecLayer out_layer(const OutCursor& c) {
   return L;
 }
 
-// waves per block and LDS bytes per wave of the streaming kernel
+// waves per block of the streaming kernel
 constexpr int kStreamWaves = 4;
-constexpr int kStreamLdsPerWave = 12 * 1024;
 
 template <int T, int XW>
 struct StreamCfg {
   static constexpr int P = 2 * T;
-  static constexpr int SLOT = (P + XW) * 1024;
+  static constexpr int XSLOT = XW * 1024;         // LDS bytes of a slot's activation operand
   static constexpr int WAVES = kStreamWaves;
-  // ring slots per wave within the LDS budget, 2..6
-  static constexpr int NS_RAW = kStreamLdsPerWave / SLOT;
-  static constexpr int NS = NS_RAW < 2 ? 2 : (NS_RAW > 6 ? 6 : NS_RAW);
+  // ring depth: about 48 code registers per lane
+  static constexpr int NS = T <= 1 ? 4 : (T == 2 ? 3 : 2);
   static constexpr int LOADS = P + XW;            // vector memory ops issued per step
-  static constexpr int WAIT = (NS - 2) * LOADS;   // outstanding ops allowed when a slot is read
+  static constexpr int WAIT = (NS - 1) * LOADS;   // outstanding ops allowed when a slot is read
   static constexpr int WAITCNT = (WAIT & 0xF) | (0x7 << 4) | (0xF << 8) | (((WAIT >> 4) & 3) << 14);
 };
 
@@ -818,9 +840,9 @@ __global__ __launch_bounds__(64 * kStreamWaves) void dec_stream_kernel(DecHeader
                                                                        const DecLayer* __restrict__ tab) {
 #if defined(__HIP_DEVICE_COMPILE__)  // LDS-DMA and buffer-descriptor code: device pass only
   using C = StreamCfg<T, XW>;
-  constexpr int P = C::P, NS = C::NS, SLOT = C::SLOT;
+  constexpr int P = C::P, NS = C::NS, XSLOT = C::XSLOT;
   constexpr int WAVES = C::WAVES;
-  __shared__ __attribute__((aligned(16))) uint8_t ring[WAVES][NS][SLOT];
+  __shared__ __attribute__((aligned(16))) uint8_t ring[WAVES][NS][XSLOT];
   __shared__ __attribute__((aligned(16))) uint8_t zero16[16];
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4, li = lane & 15;
@@ -853,38 +875,32 @@ __global__ __launch_bounds__(64 * kStreamWaves) void dec_stream_kernel(DecHeader
   load_item(lc, h, lane);
   out_item(oc, li);
 
+  v4i cq[NS][P];  // code bytes of each ring slot
   bool live = true;
 #pragma unroll
   for (int k = 0; k < NS - 1; ++k) {
-    stream_issue<XW>(lc, live, lane, &ring[wave][k][0]);
+    stream_issue<XW>(lc, live, lane, cq[k], &ring[wave][k][0]);
     if (live) live = load_next(lc, tab, h, i1, lane);
   }
 
-  // The accumulators are never reset: an item's products are acc - base,
-  // exact modulo 2^32 because each item's own sums fit in int32; base is
-  // updated only in the epilogue, so steps carry no conditional copies.
-  v4i acc[P][2][1], base[P][2][1];
+  v4i acc[P][2][1];
 #pragma unroll
-  for (int p = 0; p < P; ++p)
-    acc[p][0][0] = acc[p][1][0] = base[p][0][0] = base[p][1][0] = v4i{0, 0, 0, 0};
+  for (int p = 0; p < P; ++p) acc[p][0][0] = acc[p][1][0] = v4i{0, 0, 0, 0};
 
   auto step = [&](auto kconst) -> bool {
     constexpr int K = decltype(kconst)::value;
-    __builtin_amdgcn_s_waitcnt(C::WAITCNT);  // this slot's loads have landed
-    __asm__ volatile("" ::: "memory");
-    const uint8_t* sl = &ring[wave][K][0];
-    v4i cr[P];
-#pragma unroll
-    for (int p = 0; p < P; ++p) cr[p] = *reinterpret_cast<const v4i*>(sl + p * 1024 + lane * 16);
-    const uint8_t* xl = xvalid ? sl + P * 1024 + (g * h.nc + li) * 16 : zero16;
-    const int xstep = xvalid ? 4 * h.nc * 16 : 0;
-    v4i xr[4];
-#pragma unroll
-    for (int d = 0; d < 4; ++d) xr[d] = *reinterpret_cast<const v4i*>(xl + d * xstep);
-    __asm__ volatile("" ::: "memory");
-    // refill the slot the previous step consumed
-    stream_issue<XW>(lc, live, lane, &ring[wave][(K + NS - 1) % NS][0]);
+    constexpr int KN = (K + NS - 1) % NS;  // the slot the previous step consumed
+    // refill the slot the previous step consumed, then wait for this one
+    stream_issue<XW>(lc, live, lane, cq[KN], &ring[wave][KN][0]);
     if (live) live = load_next(lc, tab, h, i1, lane);
+    __builtin_amdgcn_s_waitcnt(C::WAITCNT);  // this slot's loads have landed
+    v4i xr[4];
+    {
+      const uint32_t xa = xvalid ? lds_addr(&ring[wave][K][0]) + (uint32_t)((g * h.nc + li) * 16) : lds_addr(zero16);
+      const uint32_t xs = xvalid ? (uint32_t)(4 * h.nc * 16) : 0u;
+      lds_read4(xa, xa + xs, xa + 2 * xs, xa + 3 * xs, xr);
+    }
+    const v4i* cr = cq[K];
 #pragma unroll
     for (int d = 0; d < 4; ++d) {
 #pragma unroll
@@ -906,15 +922,9 @@ __global__ __launch_bounds__(64 * kStreamWaves) void dec_stream_kernel(DecHeader
       q.row_ok = oc.row_ok;
       q.k4b = 0;
       q.nk4_item = 0;
-      v4i item_acc[P][2][1];
+      write_outputs<MODE, T, 1, false>(out_layer(oc), h, q, lane, acc);
 #pragma unroll
-      for (int p = 0; p < P; ++p)
-#pragma unroll
-        for (int ax = 0; ax < 2; ++ax) {
-          item_acc[p][ax][0] = acc[p][ax][0] - base[p][ax][0];
-          base[p][ax][0] = acc[p][ax][0];
-        }
-      write_outputs<MODE, T, 1, false>(out_layer(oc), h, q, lane, item_acc);
+      for (int p = 0; p < P; ++p) acc[p][0][0] = acc[p][1][0] = v4i{0, 0, 0, 0};
     }
     return !out_next(oc, tab, i1, li);
   };
