@@ -41,7 +41,7 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def build_stack(f2, synth, torch, dev, T, B=1, seed_base=1000, tiled=True):
+def build_stack(f2, synth, torch, dev, T, B=1, seed_base=1000, tiled=True, random_codes=False):
     """32 x 7 widely-linear layers with T-stage codes, each with its own
     bf16 activation token.  Returns (group, packed_bytes, algorithmic_bytes,
     layers): the group decodes the tiled copies of the codes (made once by
@@ -52,14 +52,22 @@ def build_stack(f2, synth, torch, dev, T, B=1, seed_base=1000, tiled=True):
         for p in synth.PROJ_ORDER:
             rows, cols = synth.LLAMA2_7B_PROJ[p]
             N, K = rows // 2, cols // 2
-            A = synth.torch_llama_weight(rows, cols, seed_base + 7 * layer + synth.PROJ_ORDER.index(p), dev)
-            U, W = f2.to_widely_linear(A)
-            del A
-            cu, su = f2.quantize(U, T)
-            cw, sw = f2.quantize(W, T)
-            del U, W
             g = torch.Generator(device=dev)
             g.manual_seed(seed_base * 31 + len(layers))
+            if random_codes:
+                # counter collection only: uniform random 2-bit codes and unit-range scales of the
+                # same shapes (the product kernel's memory traffic does not depend on code values)
+                cu = torch.randint(0, 256, (T, N, K // 4), dtype=torch.uint8, device=dev, generator=g)
+                cw = torch.randint(0, 256, (T, N, K // 4), dtype=torch.uint8, device=dev, generator=g)
+                su = torch.rand(T, 2, device=dev, generator=g) + 0.5
+                sw = torch.rand(T, 2, device=dev, generator=g) + 0.5
+            else:
+                A = synth.torch_llama_weight(rows, cols, seed_base + 7 * layer + synth.PROJ_ORDER.index(p), dev)
+                U, W = f2.to_widely_linear(A)
+                del A
+                cu, su = f2.quantize(U, T)
+                cw, sw = f2.quantize(W, T)
+                del U, W
             x = torch.randn(B, K, 2, generator=g, device=dev).to(torch.bfloat16)
             y = torch.empty(B, N, dtype=torch.complex64, device=dev)
             layers.append((cu, su, cw, sw, x, None, y))
@@ -188,6 +196,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=30)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true", help="skip prefill, T=3 and D3-layout measurements")
+    ap.add_argument("--random-codes", action="store_true",
+                    help="random codes instead of quantised weights (for hardware-counter runs only; "
+                         "the JSON line then says so in `data`)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run 5 plain 256 MiB device copies (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -213,7 +224,7 @@ def main():
     f2.load()
     T = 2
     t0 = time.time()
-    grp, packed, algo, layers = build_stack(f2, synth, torch, dev, T)
+    grp, packed, algo, layers = build_stack(f2, synth, torch, dev, T, random_codes=args.random_codes)
     log(f"stack T={T}: {len(layers)} layers, {packed / 1e9:.3f} GB packed, setup {time.time() - t0:.1f} s")
 
     ms, prep_ms, prod_ms, red_ms = time_group(grp, torch, args.steps, args.warmup)
@@ -244,7 +255,9 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16 activations, int8 MFMA with exact integer accumulation",
-        "data": "synthetic: seeded Student-t(4) weights with 1% outlier input channels, N(0,1) bf16 tokens",
+        "data": ("synthetic: seeded uniform random 2-bit codes (counter run), N(0,1) bf16 tokens"
+                 if args.random_codes else
+                 "synthetic: seeded Student-t(4) weights with 1% outlier input channels, N(0,1) bf16 tokens"),
         "config": {"workload": "LLaMA-2-7B linear stack, 32 layers x 7 projections, widely-linear T=2, "
                                "one decode token (bs=1) per projection, bf16 activations",
                    "layers": len(layers), "T": T, "batch": 1, "packed_bytes": packed,
