@@ -105,6 +105,36 @@ def time_group(grp, torch, steps, warmup):
     return total_ms / steps, prep, prod, red
 
 
+def quantizer_bench(f2, synth, torch, dev, T=2, reps=5):
+    """Offline preparation wall time (real -> widely-linear, then the T-stage
+    quantiser on U and W) for the q and gate shapes, on the GPU."""
+    out = {}
+    for name in ("q", "gate"):
+        rows, cols = synth.LLAMA2_7B_PROJ[name]
+        A = synth.torch_llama_weight(rows, cols, 5000 + len(out), dev)
+        for _ in range(2):
+            U, W = f2.to_widely_linear(A)
+            f2.quantize(U, T)
+        torch.cuda.synchronize()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        t_wl = t_q = 0.0
+        for _ in range(reps):
+            e[0].record()
+            U, W = f2.to_widely_linear(A)
+            e[1].record()
+            f2.quantize(U, T)
+            f2.quantize(W, T)
+            e[2].record()
+            torch.cuda.synchronize()
+            t_wl += e[0].elapsed_time(e[1])
+            t_q += e[1].elapsed_time(e[2])
+        out[name] = {"real_shape": [rows, cols], "T": T, "to_widely_linear_us": round(t_wl / reps * 1e3, 1),
+                     "quantize_U_and_W_us": round(t_q / reps * 1e3, 1)}
+        del A, U, W
+    torch.cuda.empty_cache()
+    return out
+
+
 def traffic_record():
     """HBM bytes per launch of the product kernel from committed rocprofv3
     --pmc summaries, or None when absent or when the kernel source changed
@@ -285,6 +315,7 @@ def main():
         del grp3, layers3
         torch.cuda.empty_cache()
         result["prefill"] = prefill_bench(f2, synth, torch, dev)
+        result["quantizer"] = quantizer_bench(f2, synth, torch, dev)
 
     if not args.no_cpu_baseline:
         # a fresh single-layer copy of the stack's first projection

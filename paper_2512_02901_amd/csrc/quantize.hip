@@ -2,16 +2,17 @@
 // definition, with the projection, axis scales and dequantisation of
 // Sec. 3.2).
 //
-// Stage t runs two kernels on the caller's stream:
+// A fill kernel clears the per-stage totals; then stage t runs two kernels on
+// the caller's stream:
 //   qz_stage_kernel    one thread per packed byte (4 consecutive entries of a
 //                      row): rebuilds the float64 residual from M and the
 //                      codes/scales of stages < t, projects it, writes the
 //                      byte of stage-t codes, and adds |Re r| (k even) or
 //                      |Im r| (k odd) into an exact fixed-point accumulator
-//                      in LDS; each block stores its partial accumulator.
-//   qz_finalize_kernel one block: sums the partials (integer adds, so the
-//                      result does not depend on block order), then rounds
-//                      each exact mean once to float32 -> scales[t].
+//                      in LDS.  Each block then adds its accumulator words into the
+//                      stage total with 64-bit integer atomics (exact, so the
+//                      total does not depend on the order blocks arrive in).
+//   qz_finalize_kernel rounds each exact mean once to float32 -> scales[t].
 // Stage t+1 reads scales[t] from device memory; nothing returns to the host.
 #include "common.h"
 #include "superacc.h"
@@ -42,7 +43,7 @@ __device__ inline void sa_add_lds(unsigned long long* acc, double v) {
 
 __global__ __launch_bounds__(kQzThreads) void qz_stage_kernel(
     const float2* __restrict__ M, int64_t nbytes, uint8_t* __restrict__ codes,
-    const float* __restrict__ scales, int t, unsigned long long* __restrict__ part) {
+    const float* __restrict__ scales, int t, unsigned long long* __restrict__ tot) {
   __shared__ unsigned long long acc[2][SA_LIMBS];
   __shared__ unsigned long long cnt[2];
   for (int i = threadIdx.x; i < 2 * SA_LIMBS; i += blockDim.x) (&acc[0][0])[i] = 0ull;
@@ -86,25 +87,25 @@ __global__ __launch_bounds__(kQzThreads) void qz_stage_kernel(
   if (n_re) atomicAdd(&cnt[0], n_re);
   if (n_im) atomicAdd(&cnt[1], n_im);
   __syncthreads();
-  unsigned long long* dst = part + (int64_t)blockIdx.x * kPartWords;
-  for (int i = threadIdx.x; i < 2 * SA_LIMBS; i += blockDim.x) dst[i] = (&acc[0][0])[i];
-  if (threadIdx.x < 2) dst[2 * SA_LIMBS + threadIdx.x] = cnt[threadIdx.x];
+  // the block's words into the stage total: 64-bit integer additions, exact
+  // and independent of the order in which blocks arrive
+  for (int i = threadIdx.x; i < kPartWords; i += blockDim.x) {
+    const unsigned long long v = i < 2 * SA_LIMBS ? (&acc[0][0])[i] : cnt[i - 2 * SA_LIMBS];
+    if (v) atomicAdd(&tot[i], v);
+  }
 }
 
-__global__ __launch_bounds__(256) void qz_finalize_kernel(const unsigned long long* __restrict__ part,
-                                                          int nblk, float* __restrict__ scales_t) {
-  __shared__ unsigned long long tot[kPartWords];
-  for (int i = threadIdx.x; i < kPartWords; i += blockDim.x) {
-    unsigned long long s = 0;
-    for (int b = 0; b < nblk; ++b) s += part[(int64_t)b * kPartWords + i];
-    tot[i] = s;
-  }
-  __syncthreads();
+__global__ __launch_bounds__(64) void qz_finalize_kernel(const unsigned long long* __restrict__ tot,
+                                                         float* __restrict__ scales_t) {
   if (threadIdx.x < 2) {
     const unsigned long long n = tot[2 * SA_LIMBS + threadIdx.x];
     scales_t[threadIdx.x] =
-        n ? sa_mean_to_f32(reinterpret_cast<const uint64_t*>(&tot[threadIdx.x * SA_LIMBS]), n) : 0.0f;
+        n ? sa_mean_to_f32(reinterpret_cast<const uint64_t*>(tot + threadIdx.x * SA_LIMBS), n) : 0.0f;
   }
+}
+
+__global__ __launch_bounds__(256) void qz_zero_kernel(unsigned long long* __restrict__ p, int n) {
+  for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = 0ull;
 }
 
 int quantize_blocks(int64_t N, int64_t K) {
@@ -118,22 +119,26 @@ int quantize_blocks(int64_t N, int64_t K) {
 }  // namespace
 
 size_t quantize_workspace_bytes(int64_t N, int64_t K) {
-  return (size_t)quantize_blocks(N, K) * kPartWords * sizeof(unsigned long long);
+  (void)N;
+  (void)K;
+  return (size_t)FAIRY2I_MAX_STAGES * kPartWords * sizeof(unsigned long long);  // one total per stage
 }
 
 hipError_t launch_quantize(const float2* M, int64_t N, int64_t K, int T, uint8_t* codes,
                            float* scales, void* workspace, hipStream_t stream) {
   const int nblk = quantize_blocks(N, K);
   const int64_t nbytes = N * K / 4;
-  auto* part = static_cast<unsigned long long*>(workspace);
+  auto* tot = static_cast<unsigned long long*>(workspace);
+  hipLaunchKernelGGL(qz_zero_kernel, dim3(1), dim3(256), 0, stream, tot, T * kPartWords);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   for (int t = 0; t < T; ++t) {
+    unsigned long long* tot_t = tot + (int64_t)t * kPartWords;
     hipLaunchKernelGGL(qz_stage_kernel, dim3(nblk), dim3(kQzThreads), 0, stream, M, nbytes, codes,
-                       scales, t, part);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(qz_finalize_kernel, dim3(1), dim3(256), 0, stream, part, nblk, scales + 2 * t);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
+                       scales, t, tot_t);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(qz_finalize_kernel, dim3(1), dim3(64), 0, stream, tot_t, scales + 2 * t);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   return hipSuccess;
 }
