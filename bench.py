@@ -41,6 +41,23 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+stack_codes = []   # (N, K, tiled codes_U, scales_U, tiled codes_W, scales_W) of the last stack built
+
+
+def batch_stack(f2, torch, dev, T, B, steps, warmup, seed=3000):
+    """The last stack's codes decoding B bf16 tokens per layer; returns
+    time_group's (ms per step, prep ms, product ms, reduce ms)."""
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed + B)
+    layers = []
+    for (N, K, cu, su, cw, sw) in stack_codes:
+        x = torch.randn(B, K, 2, generator=g, device=dev).to(torch.bfloat16)
+        y = torch.empty(B, N, dtype=torch.complex64, device=dev)
+        layers.append((cu, su, cw, sw, x, None, y))
+    grp = f2.WlGroup(layers, T=T, B=B, tiled=True)
+    return time_group(grp, torch, steps, warmup)
+
+
 def build_stack(f2, synth, torch, dev, T, B=1, seed_base=1000, tiled=True, random_codes=False):
     """32 x 7 widely-linear layers with T-stage codes, each with its own
     bf16 activation token.  Returns (group, packed_bytes, algorithmic_bytes,
@@ -48,6 +65,7 @@ def build_stack(f2, synth, torch, dev, T, B=1, seed_base=1000, tiled=True, rando
     fairy2i_repack_tiled, like the quantisation, outside any timing) unless
     tiled is False; `layers` holds the D3 codes."""
     layers, tiled_layers, packed, algo = [], [], 0, 0
+    stack_codes.clear()
     for layer in range(32):
         for p in synth.PROJ_ORDER:
             rows, cols = synth.LLAMA2_7B_PROJ[p]
@@ -73,6 +91,7 @@ def build_stack(f2, synth, torch, dev, T, B=1, seed_base=1000, tiled=True, rando
             layers.append((cu, su, cw, sw, x, None, y))
             if tiled:
                 tiled_layers.append((f2.repack_tiled(cu), su, f2.repack_tiled(cw), sw, x, None, y))
+                stack_codes.append((N, K) + tiled_layers[-1][:4])
             codes = 2 * T * N * K // 4
             packed += codes
             # codes + bf16 activations + complex64 outputs + scales
@@ -297,6 +316,11 @@ def main():
         "roofline": roofline,
     }
     if not args.no_extras:
+        # batches of 4 and 16 tokens per layer over the same codes
+        for Bb in (4, 16):
+            msb, _, prodb, _ = batch_stack(f2, torch, dev, T, Bb, max(10, args.steps // 2), args.warmup)
+            result[f"stack_B{Bb}"] = {"ms_per_step": round(msb, 4), "GBs": round(packed / (msb * 1e-3) / 1e9, 1),
+                                      "product_us": round(prodb * 1e3, 1)}
         # the same stack decoded straight from the canonical D3 codes
         grp_d3 = f2.WlGroup(layers, T=T, B=1)
         ms_d3, _, prod_d3, _ = time_group(grp_d3, torch, args.steps, args.warmup)

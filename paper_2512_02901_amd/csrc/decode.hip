@@ -188,6 +188,7 @@ __device__ inline bool col_token(int tile, int col, int B, int& b, int& digit, i
 
 // --------------------------------------------------------------- decode ---
 constexpr uint32_t kOob = 0xFFFFFFF0u;  // buffer offset past every range: loads return 0
+constexpr int kNonTemporal = 2;         // buffer-load cache policy: streaming (nt), for bytes read once
 
 __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
@@ -382,7 +383,8 @@ __device__ inline void issue_step_loads(const DecLayer& L, const DecHeader& h, c
 #pragma unroll
     for (int p = 0; p < 2 * T; ++p) {
       const int m = p / T, t = p % T;
-      cw[p][j] = buf_load16(make_rsrc(L.codes[m] + t * 1024, mat_bytes - t * 1024), off);
+      cw[p][j] = __builtin_amdgcn_raw_buffer_load_b128(make_rsrc(L.codes[m] + t * 1024, mat_bytes - t * 1024), off, 0,
+                                                       kNonTemporal);
     }
   } else {
     const uint32_t plane_bytes = (uint32_t)((int64_t)L.N * K / 4);
@@ -390,7 +392,8 @@ __device__ inline void issue_step_loads(const DecLayer& L, const DecHeader& h, c
 #pragma unroll
     for (int p = 0; p < 2 * T; ++p) {
       const int m = p / T, t = p % T;
-      cw[p][j] = buf_load16(make_rsrc(L.codes[m] + (int64_t)t * plane_bytes, plane_bytes), off);
+      cw[p][j] = __builtin_amdgcn_raw_buffer_load_b128(make_rsrc(L.codes[m] + (int64_t)t * plane_bytes, plane_bytes),
+                                                       off, 0, kNonTemporal);
     }
   }
   const __amdgpu_buffer_rsrc_t xr = make_rsrc(L.xf, (uint32_t)(h.ntile * L.nk4 * 256 * h.nc));
@@ -695,8 +698,6 @@ __device__ inline void load_enter_layer(LoadCursor<T>& c, const DecLayer& L, con
   c.xf = L.xf;
   c.xbytes = (uint32_t)(L.nk4 * 256 * h.nc);
 }
-
-constexpr int kNonTemporal = 2;  // buffer-load cache policy: streaming (nt)
 
 // Issue the loads of the cursor's step: its 2T x 16 code bytes per lane into
 // registers cq, and its activation operand (XW KiB) into the LDS slot xslot.
