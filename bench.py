@@ -252,8 +252,8 @@ def main():
                     help="only run 5 plain 256 MiB device copies (reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(the layer would shard by output rows with an all-gather of y; see the design notes)",
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(a layer would shard by output rows, with one all-gather of y per layer)",
               file=sys.stderr)
         sys.exit(2)
 
