@@ -58,13 +58,28 @@ def batch_stack(f2, torch, dev, T, B, steps, warmup, seed=3000):
     return time_group(grp, torch, steps, warmup)
 
 
-def build_stack(f2, synth, torch, dev, T, B=1, seed_base=1000, tiled=True, random_codes=False):
+def batch_stack_fp4(f2, torch, dev, T, layers, B, steps, warmup, seed=4000):
+    """The stack's fp4 tiled codes decoding B <= 2 bf16 tokens per layer."""
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed + B)
+    grp_layers = []
+    for (cu, su, cw, sw, x1, _, y1) in layers:
+        N, K = y1.shape[1], x1.shape[1]
+        x = torch.randn(B, K, 2, generator=g, device=dev).to(torch.bfloat16)
+        y = torch.empty(B, N, dtype=torch.complex64, device=dev)
+        grp_layers.append((f2.repack_tiled_fp4(cu), su, f2.repack_tiled_fp4(cw), sw, x, None, y))
+    grp = f2.WlGroup(grp_layers, T=T, B=B, layout=f2.LAYOUT_TILED_FP4)
+    return time_group(grp, torch, steps, warmup)
+
+
+def build_stack(f2, synth, torch, dev, T, B=1, seed_base=1000, random_codes=False, with_tiled=False):
     """32 x 7 widely-linear layers with T-stage codes, each with its own
     bf16 activation token.  Returns (group, packed_bytes, algorithmic_bytes,
-    layers): the group decodes the tiled copies of the codes (made once by
-    fairy2i_repack_tiled, like the quantisation, outside any timing) unless
-    tiled is False; `layers` holds the D3 codes."""
-    layers, tiled_layers, packed, algo = [], [], 0, 0
+    layers, tiled_group): the group decodes the fp4 tiled copies of the codes
+    (made once by fairy2i_repack_tiled_fp4, like the quantisation, outside
+    any timing); with_tiled also makes the tiled copies and a group over them
+    (the int8 matrix-core path); `layers` holds the D3 codes."""
+    layers, fp4_layers, tiled_layers, packed, algo = [], [], [], 0, 0
     stack_codes.clear()
     for layer in range(32):
         for p in synth.PROJ_ORDER:
@@ -89,7 +104,8 @@ def build_stack(f2, synth, torch, dev, T, B=1, seed_base=1000, tiled=True, rando
             x = torch.randn(B, K, 2, generator=g, device=dev).to(torch.bfloat16)
             y = torch.empty(B, N, dtype=torch.complex64, device=dev)
             layers.append((cu, su, cw, sw, x, None, y))
-            if tiled:
+            fp4_layers.append((f2.repack_tiled_fp4(cu), su, f2.repack_tiled_fp4(cw), sw, x, None, y))
+            if with_tiled:
                 tiled_layers.append((f2.repack_tiled(cu), su, f2.repack_tiled(cw), sw, x, None, y))
                 stack_codes.append((N, K) + tiled_layers[-1][:4])
             codes = 2 * T * N * K // 4
@@ -97,31 +113,38 @@ def build_stack(f2, synth, torch, dev, T, B=1, seed_base=1000, tiled=True, rando
             # codes + bf16 activations + complex64 outputs + scales
             algo += codes + B * K * 2 * 2 + B * N * 8 + 2 * T * 2 * 4
     torch.cuda.synchronize()
-    grp = f2.WlGroup(tiled_layers, T=T, B=B, tiled=True) if tiled else f2.WlGroup(layers, T=T, B=B)
-    return grp, packed, algo, layers
+    grp = f2.WlGroup(fp4_layers, T=T, B=B, layout=f2.LAYOUT_TILED_FP4)
+    grp_tiled = f2.WlGroup(tiled_layers, T=T, B=B, tiled=True) if with_tiled else None
+    return grp, packed, algo, layers, grp_tiled
 
 
 def time_group(grp, torch, steps, warmup):
+    """(ms per step, prep ms, product ms, reduce ms): the step time from a
+    loop of plain calls; the per-kernel split from a second loop in which
+    the library records events around its three launches."""
     for _ in range(warmup):
         grp.run()
     torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(steps):
+        grp.run()
+    t1.record()
+    torch.cuda.synchronize()
+    step_ms = t0.elapsed_time(t1) / steps
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
     for es in ev:
         for e in es:
             e.record()        # create the events before handing them to the library
     torch.cuda.synchronize()
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
-    t0.record()
     for es in ev:
         grp.run(events=es)
-    t1.record()
     torch.cuda.synchronize()
-    total_ms = t0.elapsed_time(t1)
     prep = sum(es[0].elapsed_time(es[1]) for es in ev) / steps
     prod = sum(es[1].elapsed_time(es[2]) for es in ev) / steps
     red = sum(es[2].elapsed_time(es[3]) for es in ev) / steps
-    return total_ms / steps, prep, prod, red
+    return step_ms, prep, prod, red
 
 
 def quantizer_bench(f2, synth, torch, dev, T=2, reps=5):
@@ -273,7 +296,8 @@ def main():
     f2.load()
     T = 2
     t0 = time.time()
-    grp, packed, algo, layers = build_stack(f2, synth, torch, dev, T, random_codes=args.random_codes)
+    grp, packed, algo, layers, grp_tiled = build_stack(f2, synth, torch, dev, T, random_codes=args.random_codes,
+                                                       with_tiled=not args.no_extras)
     log(f"stack T={T}: {len(layers)} layers, {packed / 1e9:.3f} GB packed, setup {time.time() - t0:.1f} s")
 
     ms, prep_ms, prod_ms, red_ms = time_group(grp, torch, args.steps, args.warmup)
@@ -289,7 +313,8 @@ def main():
                 # committed counters were taken for another kernel source)
                 "traffic": None if traffic is None else int(traffic),
                 "traffic_over_algorithmic": None if traffic is None else round(traffic / algo, 3),
-                "kernel": "dec_stream_kernel<bf16, T=2> (int8 MFMA product over tiled codes, one launch per step)",
+                "kernel": "dec_stream_f4_kernel<T=2> (fp8 x fp4 MFMA product over fp4-tiled codes, "
+                          "one launch per step)",
                 "algorithmic_bytes_per_launch": algo, "avg_launch_us": round(prod_ms * 1e3, 2)}
 
     result = {
@@ -303,7 +328,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16 activations, int8 MFMA with exact integer accumulation",
+        "dtype": "bf16 activations as 15-bit fixed point, fp8 x fp4 MFMA with exact integer accumulation",
         "data": ("synthetic: seeded uniform random 2-bit codes (counter run), N(0,1) bf16 tokens"
                  if args.random_codes else
                  "synthetic: seeded Student-t(4) weights with 1% outlier input channels, N(0,1) bf16 tokens"),
@@ -316,7 +341,16 @@ def main():
         "roofline": roofline,
     }
     if not args.no_extras:
-        # batches of 4 and 16 tokens per layer over the same codes
+        # the same stack on the int8 matrix cores over the tiled copies
+        ms_t, _, prod_t, _ = time_group(grp_tiled, torch, args.steps, args.warmup)
+        result["stack_tiled_int8"] = {"ms_per_step": round(ms_t, 4), "GBs": round(packed / (ms_t * 1e-3) / 1e9, 1),
+                                      "product_us": round(prod_t * 1e3, 1)}
+        del grp_tiled
+        # two tokens per layer on the fp4 path
+        ms2, _, prod2, _ = batch_stack_fp4(f2, torch, dev, T, layers, 2, args.steps, args.warmup)
+        result["stack_B2"] = {"ms_per_step": round(ms2, 4), "GBs": round(packed / (ms2 * 1e-3) / 1e9, 1),
+                              "product_us": round(prod2 * 1e3, 1)}
+        # batches of 4 and 16 tokens per layer over the same codes (int8 path, tiled copies)
         for Bb in (4, 16):
             msb, _, prodb, _ = batch_stack(f2, torch, dev, T, Bb, max(10, args.steps // 2), args.warmup)
             result[f"stack_B{Bb}"] = {"ms_per_step": round(msb, 4), "GBs": round(packed / (msb * 1e-3) / 1e9, 1),
@@ -328,10 +362,11 @@ def main():
                                      "product_us": round(prod_d3 * 1e3, 1)}
         del grp_d3
     del grp, layers
+    stack_codes.clear()
     torch.cuda.empty_cache()
 
     if not args.no_extras:
-        grp3, packed3, _, layers3 = build_stack(f2, synth, torch, dev, 3, seed_base=2000)
+        grp3, packed3, _, layers3, _ = build_stack(f2, synth, torch, dev, 3, seed_base=2000)
         ms3, _, _, _ = time_group(grp3, torch, max(5, args.steps // 2), args.warmup)
         result["stack_T3"] = {"ms_per_step": round(ms3, 4), "packed_bytes": packed3,
                               "GBs": round(packed3 / (ms3 * 1e-3) / 1e9, 1),

@@ -68,11 +68,13 @@ enum {
 };
 
 /* Device layouts of packed codes.  D3 is the canonical one (what
- * fairy2i_quantize writes and every call accepts); TILED is the decode
- * layout written by fairy2i_repack_tiled, accepted by the grouped decode. */
+ * fairy2i_quantize writes and every call accepts); TILED and TILED_FP4 are
+ * the decode layouts written by fairy2i_repack_tiled and
+ * fairy2i_repack_tiled_fp4, accepted by the grouped decode. */
 enum {
   FAIRY2I_LAYOUT_D3 = 0,
-  FAIRY2I_LAYOUT_TILED = 1
+  FAIRY2I_LAYOUT_TILED = 1,
+  FAIRY2I_LAYOUT_TILED_FP4 = 2
 };
 
 #define FAIRY2I_MAX_STAGES 4
@@ -219,7 +221,7 @@ typedef struct fairy2i_wl_layer {
   float* y;
   int64_t N;
   int64_t K;
-  int32_t layout;    /* FAIRY2I_LAYOUT_D3 or FAIRY2I_LAYOUT_TILED, for both
+  int32_t layout;    /* FAIRY2I_LAYOUT_D3, _TILED or _TILED_FP4, for both
                         codes_U and codes_W (same T as the call)           */
   int32_t reserved;  /* 0 */
 } fairy2i_wl_layer;
@@ -231,7 +233,13 @@ typedef struct fairy2i_wl_layer {
  * layers runs back to back instead of paying a launch per layer.
  * Restrictions: dtype FAIRY2I_ACT_BF16 or FAIRY2I_ACT_I8, 1 <= B <= 16,
  * every K a multiple of 64, reserved == 0.  Each layer's codes are in the
- * layout its `layout` field names (same layout for U and W).
+ * layout its `layout` field names (same layout for U and W).  With
+ * FAIRY2I_LAYOUT_TILED_FP4 every layer of the group must use it, with dtype
+ * FAIRY2I_ACT_BF16 and B <= 2; the product then runs on the fp8 x fp4
+ * matrix cores, each token taken as a 15-bit block fixed point
+ * X = rint(x * 2^E) with 2^14 <= max |X| < 2^15 (every bf16 value within a
+ * factor 2^7 of the token's largest magnitude exactly, smaller ones rounded
+ * to the 2^-E grid), and the integer products are exact.
  *
  * Use: size the workspace with fairy2i_wl_group_workspace_bytes and the
  * table with fairy2i_wl_group_table_bytes; fairy2i_wl_group_build_table
@@ -270,6 +278,26 @@ typedef struct fairy2i_wl_layer {
 size_t fairy2i_repack_tiled_bytes(int64_t N, int64_t K, int32_t T);
 fairy2i_status fairy2i_repack_tiled(const uint8_t* codes, int64_t N, int64_t K, int32_t T,
                                     uint8_t* tiled, size_t tiled_bytes, void* stream);
+
+/*
+ * Fp4 tiled decode layout of one matrix's packed codes (Sec. 3.4 codes
+ * i^k; same tiles and size as the tiled layout, fairy2i_repack_tiled_bytes).
+ * Lane (g, r) (g < 4, r < 16) owns bytes 16 * (16 g + r) .. + 15 of tile
+ * (rb, s, t), read as four little-endian 32-bit words; it holds codes
+ * 256 s + 128 kb + 32 g + n (kb < 2, n < 32) of row 16 rb + r of stage t.
+ * Writing n = 16 h + 8 a + m (h, a < 2, m < 8), code n is in word 2 kb + h,
+ * nibble m (bits 4m .. 4m+3), with its bits p = k & 1 and q = k >> 1 at
+ * nibble bits (1, 3) for a = 0 and (0, 2) for a = 1.  Codes past row N - 1 or
+ * past K are 0.  A nibble masked to bits (3, 1), or to bit 3 with bit 1 set,
+ * is then an e2m1 value of (1 - 2q) p or 1 - 2q, which the decode product
+ * feeds to v_mfma_f32_16x16x128_f8f6f4 with five ALU instructions per
+ * 16 codes.
+ * fairy2i_repack_tiled_fp4: codes (D3, T*N*K/4 bytes) -> out (device memory,
+ * out_bytes >= fairy2i_repack_tiled_bytes(N, K, T)); enqueued on `stream`.
+ * Errors: as fairy2i_repack_tiled.
+ */
+fairy2i_status fairy2i_repack_tiled_fp4(const uint8_t* codes, int64_t N, int64_t K, int32_t T,
+                                        uint8_t* out, size_t out_bytes, void* stream);
 
 size_t fairy2i_wl_group_workspace_bytes(const fairy2i_wl_layer* layers, int32_t n_layers,
                                         int32_t T, int32_t dtype, int64_t B);

@@ -16,7 +16,7 @@ _lib = None
 
 OK, ERR_NULL, ERR_SHAPE, ERR_STAGES, ERR_DTYPE, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(8)
 ACT_F32, ACT_BF16, ACT_I8 = 0, 1, 2
-LAYOUT_D3, LAYOUT_TILED = 0, 1
+LAYOUT_D3, LAYOUT_TILED, LAYOUT_TILED_FP4 = 0, 1, 2
 MAX_STAGES = 4
 MAX_DECODE_BATCH = 16
 
@@ -30,6 +30,7 @@ _SIGNATURES = {
     "fairy2i_quantize": (_c_i32, [_c_p, _c_i64, _c_i64, _c_i32, _c_p, _c_p, _c_p, _c_size, _c_p]),
     "fairy2i_repack_tiled_bytes": (_c_size, [_c_i64, _c_i64, _c_i32]),
     "fairy2i_repack_tiled": (_c_i32, [_c_p, _c_i64, _c_i64, _c_i32, _c_p, _c_size, _c_p]),
+    "fairy2i_repack_tiled_fp4": (_c_i32, [_c_p, _c_i64, _c_i64, _c_i32, _c_p, _c_size, _c_p]),
     "fairy2i_quantize_act_int8": (_c_i32, [_c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_p, _c_p]),
     "fairy2i_wl_matmul_workspace_bytes": (_c_size, [_c_i64, _c_i64, _c_i32, _c_i64, _c_i32]),
     "fairy2i_wl_matmul": (_c_i32, [_c_p, _c_p, _c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_p,
@@ -218,9 +219,7 @@ def repack_tiled_bytes(N, K, T) -> int:
     return int(load().fairy2i_repack_tiled_bytes(N, K, T))
 
 
-def repack_tiled(codes, out=None):
-    """D3 codes [T, N, K/4] -> the tiled decode layout (1-D uint8 tensor of
-    fairy2i_repack_tiled_bytes bytes)."""
+def _repack(fn, codes, out):
     torch = _torch()
     lib = load()
     _require(codes, torch.uint8, "codes")
@@ -230,9 +229,20 @@ def repack_tiled(codes, out=None):
         out = torch.empty(nb, dtype=torch.uint8, device=codes.device)
     else:
         _require(out, torch.uint8, "out")
-    _check(lib.fairy2i_repack_tiled(_ptr(codes), N, 4 * KB, T, _ptr(out), out.numel(), _stream_ptr(codes)),
-           "fairy2i_repack_tiled")
+    _check(getattr(lib, fn)(_ptr(codes), N, 4 * KB, T, _ptr(out), out.numel(), _stream_ptr(codes)), fn)
     return out
+
+
+def repack_tiled(codes, out=None):
+    """D3 codes [T, N, K/4] -> the tiled decode layout (1-D uint8 tensor of
+    fairy2i_repack_tiled_bytes bytes)."""
+    return _repack("fairy2i_repack_tiled", codes, out)
+
+
+def repack_tiled_fp4(codes, out=None):
+    """D3 codes [T, N, K/4] -> the fp4 tiled decode layout (1-D uint8 tensor
+    of fairy2i_repack_tiled_bytes bytes)."""
+    return _repack("fairy2i_repack_tiled_fp4", codes, out)
 
 
 def int8_accumulators(codes_U, codes_W, q, workspace=None):
@@ -270,11 +280,15 @@ class WlGroup:
     """A table of independent layers decoded by one fairy2i_wl_matmul_group
     call.  ``layers`` is a list of (codes_U, scales_U, codes_W, scales_W, x,
     x_scale, y) device tensors (x_scale None for bf16); the object keeps them,
-    the workspace and both copies of the table alive.  ``tiled``: the codes
-    are fairy2i_repack_tiled copies (a 1-D uint8 tensor per matrix) rather
-    than D3 [T, N, K/4] tensors; N is then taken from y."""
+    the workspace and both copies of the table alive.  ``layout``: LAYOUT_D3
+    (codes [T, N, K/4]), LAYOUT_TILED or LAYOUT_TILED_FP4 (repacked copies,
+    a 1-D uint8 tensor per matrix; N is then taken from y); ``tiled=True``
+    is LAYOUT_TILED."""
 
-    def __init__(self, layers, T: int, B: int, tiled: bool = False):
+    def __init__(self, layers, T: int, B: int, tiled: bool = False, layout=None):
+        if layout is None:
+            layout = LAYOUT_TILED if tiled else LAYOUT_D3
+        tiled = layout != LAYOUT_D3
         torch = _torch()
         lib = load()
         if not layers:
@@ -293,7 +307,7 @@ class WlGroup:
                     raise ValueError("tiled codes smaller than fairy2i_repack_tiled_bytes")
             arr[i] = WlLayer(cu.data_ptr(), su.data_ptr(), cw.data_ptr(), sw.data_ptr(), x.data_ptr(),
                              None if xs is None else xs.data_ptr(), y.data_ptr(), N, K,
-                             LAYOUT_TILED if tiled else LAYOUT_D3, 0)
+                             layout, 0)
         self.n = len(layers)
         dev = layers[0][4].device
         wsb = int(lib.fairy2i_wl_group_workspace_bytes(ctypes.byref(arr), self.n, T, dt, B))

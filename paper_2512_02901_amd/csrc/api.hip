@@ -109,7 +109,7 @@ const char* fairy2i_status_string(fairy2i_status s) {
   }
 }
 
-int32_t fairy2i_abi_version(void) { return 2; }
+int32_t fairy2i_abi_version(void) { return 3; }
 
 fairy2i_status fairy2i_to_widely_linear(const float* A, int64_t rows, int64_t cols, float* U,
                                         float* W, void* stream) {
@@ -152,6 +152,15 @@ fairy2i_status fairy2i_repack_tiled(const uint8_t* codes, int64_t N, int64_t K, 
   if (T < 1 || T > FAIRY2I_MAX_STAGES) return FAIRY2I_ERR_STAGES;
   if (tiled_bytes < repack_tiled_bytes(N, K, T)) return FAIRY2I_ERR_WORKSPACE;
   return hip_status(launch_repack_tiled(codes, N, K, T, tiled, as_stream(stream)));
+}
+
+fairy2i_status fairy2i_repack_tiled_fp4(const uint8_t* codes, int64_t N, int64_t K, int32_t T, uint8_t* out,
+                                        size_t out_bytes, void* stream) {
+  if (!codes || !out) return FAIRY2I_ERR_NULL;
+  if (!repack_shape_ok(N, K)) return FAIRY2I_ERR_SHAPE;
+  if (T < 1 || T > FAIRY2I_MAX_STAGES) return FAIRY2I_ERR_STAGES;
+  if (out_bytes < repack_tiled_bytes(N, K, T)) return FAIRY2I_ERR_WORKSPACE;
+  return hip_status(launch_repack_fp4(codes, N, K, T, out, as_stream(stream)));
 }
 
 fairy2i_status fairy2i_quantize_act_int8(const void* x, int32_t dtype, int64_t B, int64_t K,
@@ -258,18 +267,29 @@ static fairy2i_status check_group(const fairy2i_wl_layer* layers, int32_t n_laye
     if (!use_mfma_decode(dtype, L.N, L.K, B) || L.N > ((int64_t)1 << 30) || L.K > ((int64_t)1 << 24))
       return FAIRY2I_ERR_UNSUPPORTED;
     if (L.reserved != 0) return FAIRY2I_ERR_UNSUPPORTED;
-    if (L.layout != FAIRY2I_LAYOUT_D3 && L.layout != FAIRY2I_LAYOUT_TILED) return FAIRY2I_ERR_UNSUPPORTED;
+    if (L.layout != FAIRY2I_LAYOUT_D3 && L.layout != FAIRY2I_LAYOUT_TILED && L.layout != FAIRY2I_LAYOUT_TILED_FP4)
+      return FAIRY2I_ERR_UNSUPPORTED;
     // the decode kernels address a matrix with 32-bit offsets
-    if (L.layout == FAIRY2I_LAYOUT_TILED && repack_tiled_bytes(L.N, L.K, T) >= ((size_t)1 << 31))
+    if (L.layout != FAIRY2I_LAYOUT_D3 && repack_tiled_bytes(L.N, L.K, T) >= ((size_t)1 << 31))
+      return FAIRY2I_ERR_UNSUPPORTED;
+    // fp4 tiled codes: every layer, bf16 activations, one activation tile
+    if ((L.layout == FAIRY2I_LAYOUT_TILED_FP4) != (layers[0].layout == FAIRY2I_LAYOUT_TILED_FP4))
+      return FAIRY2I_ERR_UNSUPPORTED;
+    if (L.layout == FAIRY2I_LAYOUT_TILED_FP4 && (dtype != FAIRY2I_ACT_BF16 || B > 2))
       return FAIRY2I_ERR_UNSUPPORTED;
   }
   return FAIRY2I_OK;
 }
 
+// Decode mode of a checked group.
+static int group_mode(const fairy2i_wl_layer* layers, int32_t dtype) {
+  return layers[0].layout == FAIRY2I_LAYOUT_TILED_FP4 ? kModeBf16F4 : dec_mode(dtype);
+}
+
 size_t fairy2i_wl_group_workspace_bytes(const fairy2i_wl_layer* layers, int32_t n_layers, int32_t T,
                                         int32_t dtype, int64_t B) {
   if (check_group(layers, n_layers, T, dtype, B) != FAIRY2I_OK) return 0;
-  const DecHeader h = dec_header(T, dec_mode(dtype), B, false);
+  const DecHeader h = dec_header(T, group_mode(layers, dtype), B, false);
   size_t total = 0;
   for (int32_t i = 0; i < n_layers; ++i) {
     DecLayer l{};
@@ -291,7 +311,7 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
   if (!workspace || workspace_bytes < need) return FAIRY2I_ERR_WORKSPACE;
   auto* hdr = static_cast<GroupTableHeader*>(table);
   auto* tab = reinterpret_cast<DecLayer*>(hdr + 1);
-  DecHeader h = dec_header(T, dec_mode(dtype), B, false);
+  DecHeader h = dec_header(T, group_mode(layers, dtype), B, false);
   char* ws = static_cast<char*>(workspace);
   int64_t items = 0;
   int any_split = 0;
@@ -299,7 +319,7 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
   for (int32_t i = 0; i < n_layers; ++i) {
     const fairy2i_wl_layer& L = layers[i];
     DecLayer l = dec_layer(L.codes_U, L.scales_U, L.codes_W, L.scales_W, L.N, L.K, L.x, L.x_scale, L.y);
-    l.tiled = L.layout == FAIRY2I_LAYOUT_TILED ? 1 : 0;
+    l.tiled = L.layout != FAIRY2I_LAYOUT_D3 ? 1 : 0;
     ws += dec_layer_setup(l, h, false, ws);
     l.acc = nullptr;
     l.item0 = items;

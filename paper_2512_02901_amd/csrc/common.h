@@ -24,6 +24,8 @@ hipError_t launch_quantize(const float2* M, int64_t N, int64_t K, int T, uint8_t
 size_t repack_tiled_bytes(int64_t N, int64_t K, int T);
 hipError_t launch_repack_tiled(const uint8_t* codes, int64_t N, int64_t K, int T, uint8_t* tiled,
                                hipStream_t stream);
+hipError_t launch_repack_fp4(const uint8_t* codes, int64_t N, int64_t K, int T, uint8_t* out,
+                             hipStream_t stream);
 
 // ----------------------------------------------------------- act quant ---
 hipError_t launch_quantize_act_int8(const void* x, int dtype, int64_t B, int64_t K, int8_t* q,

@@ -9,6 +9,8 @@ namespace fairy2i {
 
 constexpr int kModeBf16 = 0;  // bf16 activations as 3 base-256 digits of a 23-bit fixed point
 constexpr int kModeI8 = 1;    // int8 activations with a per-token factor
+constexpr int kModeBf16F4 = 2;  // bf16 activations as 4 base-16 digits of a 15-bit fixed point,
+                                // codes in the fp4 tiled layout (fp8 x fp4 matrix cores)
 
 constexpr int kKernelReg = 0;     // codes staged in registers; any batch, accumulator export
 constexpr int kKernelStream = 1;  // codes streamed through an LDS ring; one activation tile
@@ -28,7 +30,7 @@ struct DecLayer {
   float2* part;              // split-K partials [nkc][B][N] (nkc > 1)
   int32_t N, K;
   int32_t nrb, nk4, nkc, kc4;  // 16-row blocks, 256-code steps, K slices, steps per slice
-  int32_t tiled;             // codes in the tiled layout (else D3)
+  int32_t tiled;             // codes in a tiled layout (tiled or fp4 tiled; else D3)
   int32_t pad_;
   int64_t item0;             // index of this layer's first work item
 };

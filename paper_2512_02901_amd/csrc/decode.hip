@@ -38,6 +38,8 @@ namespace fairy2i {
 namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
 
 constexpr uint32_t kTableRe = 0x00FF0001u;  // code 0 -> +1, 1 -> 0, 2 -> -1, 3 -> 0
 constexpr uint32_t kTableIm = 0xFF000100u;  // code 0 -> 0, 1 -> +1, 2 -> 0, 3 -> -1
@@ -178,6 +180,11 @@ __device__ inline bool col_token(int tile, int col, int B, int& b, int& digit, i
     digit = ci >> 1;
     comp = ci & 1;
     return ci < 6 && b < B;
+  } else if constexpr (MODE == kModeBf16F4) {
+    b = 2 * tile + (col >> 3);  // columns 8b' .. 8b'+7: (digit, component) of token b'
+    digit = (col >> 1) & 3;
+    comp = col & 1;
+    return b < B;
   } else {
     b = 8 * tile + (col >> 1);
     digit = 0;
@@ -205,16 +212,41 @@ __device__ inline void buf_store8(const void* base, uint32_t bytes, uint32_t off
 
 // ----------------------------------------------------------------- prep ---
 // Layout of the activation operand: [tile][256-code step][d][g][column < nc]
-// [16 bytes].  The 16 bytes of (column, g, d) are what the MFMA lane of that
-// column and 16-code group g takes for the step's d-th 64-code MFMA (byte
-// 4c+b = code c + 4b of the group); the nc columns of a step are contiguous,
-// so a step's whole operand is one nc * 256-byte run.  Columns that hold no
-// token are written as zeros.
+// [16 bytes].  Int8 operand: the 16 bytes of (column, g, d) are what the
+// MFMA lane of that column and 16-code group g takes for the step's d-th
+// 64-code MFMA (byte 4c+b = code c + 4b of the group).  Fp8 operand (the fp4
+// code layout): they are bytes 16 (d % 2) .. +15 of what the lane of that
+// column and lane group g takes for the step's (d / 2)-th 128-code MFMA, the
+// activations of codes 64 d + 16 g .. +15 of the step.  The nc columns of a
+// step are contiguous, so a step's whole operand is one nc * 256-byte run.
+// Columns that hold no token are written as zeros.
 
 // 16 consecutive complex activations x[b][k0 .. k0+15] of one component as
 // raw bits (bf16: 16-bit patterns, int8: sign-extended bytes).  Vector loads
 // when the activation pointer allows them.
 constexpr int kPrepSplit = 4;
+
+// Balanced base-16 digit i (i < 4) of X, |X| <= 2^15: X = sum_i d_i 16^i with
+// d_0..d_2 in [-8, 7] and |d_3| <= 9.
+__device__ inline int f4_digit(int X, int i) {
+  int d = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    d = j < 3 ? ((X + 8) & 15) - 8 : X;
+    if (j == i) break;
+    X = (X - d) >> 4;
+  }
+  return d;
+}
+
+// The e4m3 (OCP fp8: 1 sign, 4 exponent bits with bias 7, 3 mantissa bits)
+// encoding of an integer |d| <= 16, which it represents exactly.
+__device__ inline uint32_t e4m3_of_int(int d) {
+  const uint32_t a = (uint32_t)(d < 0 ? -d : d);
+  if (a == 0) return 0u;
+  const int ex = 31 - __builtin_clz(a);  // a = 1.m * 2^ex
+  return (d < 0 ? 0x80u : 0u) | ((uint32_t)(ex + 7) << 3) | (((a << 3) >> ex) & 7u);
+}
 
 template <int MODE>
 __device__ inline void load_run16(const void* x, bool vec, int64_t e0, int comp, int (&v)[16]) {
@@ -267,7 +299,7 @@ __global__ __launch_bounds__(256) void dec_prep_kernel(DecHeader h, DecLayer inl
   const int64_t K = L.K;
   const bool vec = (reinterpret_cast<uintptr_t>(L.x) & 15) == 0;
   int E[2] = {0, 0};
-  if constexpr (MODE == kModeBf16) {
+  if constexpr (MODE == kModeBf16 || MODE == kModeBf16F4) {
     __shared__ float red[4][2];
     __shared__ int sh_E[2];
 #pragma unroll
@@ -300,7 +332,8 @@ __global__ __launch_bounds__(256) void dec_prep_kernel(DecHeader h, DecLayer inl
       int ex = 0, e = 0;
       if (g > 0.0f) {
         frexpf(g, &ex);       // g in [2^(ex-1), 2^ex)
-        e = 22 - ex;          // g * 2^e in [2^21, 2^22)
+        // g * 2^e in [2^21, 2^22) (3 base-256 digits) or [2^14, 2^15) (4 base-16 digits)
+        e = (MODE == kModeBf16 ? 22 : 15) - ex;
         if (e > 149) e = 149; // keep 2^-e representable in float32
       }
       sh_E[s] = e;
@@ -321,25 +354,37 @@ __global__ __launch_bounds__(256) void dec_prep_kernel(DecHeader h, DecLayer inl
   for (int ch = blockIdx.z * blockDim.x + threadIdx.x; ch < nch; ch += gridDim.z * blockDim.x) {
     const int col = ch % h.nc, r = ch / h.nc;
     const int kk = r >> 4, d = (r >> 2) & 3, g = r & 3;
-    const int64_t k0 = (int64_t)kk * 256 + 64 * g + 16 * d;
+    // int8 operand: chunk (d, g) feeds dword d of lane group g; fp8 operand:
+    // chunk (d, g) is half d % 2 of lane group g's operand of MFMA d / 2
+    const int64_t k0 = MODE == kModeBf16F4 ? (int64_t)kk * 256 + 64 * d + 16 * g
+                                           : (int64_t)kk * 256 + 64 * g + 16 * d;
     uint32_t out[4] = {0u, 0u, 0u, 0u};
     int b, digit, comp;
     if (col_token<MODE>(tile, col, h.B, b, digit, comp) && k0 < K) {  // K % 64 == 0: whole run in range
       int v[16];
-      load_run16<MODE>(L.x, vec, ((int64_t)b * K + k0) * 2, comp, v);
+      load_run16<MODE == kModeBf16F4 ? kModeBf16 : MODE>(L.x, vec, ((int64_t)b * K + k0) * 2, comp, v);
+      if constexpr (MODE == kModeBf16F4) {
+        // byte e = base-16 digit `digit` of X = rint(x[k0 + e] * 2^E), as an e4m3 value
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int dd = e >> 2, bb = e & 3;  // byte 4dd+bb holds code dd + 4bb of the run
-        int q = v[dd + 4 * bb];
-        if constexpr (MODE == kModeBf16) {
-          const int X = (int)rintf(ldexpf(__uint_as_float((uint32_t)q << 16), (b & 1) ? E[1] : E[0]));
-          const int d0 = ((X + 128) & 255) - 128;
-          const int X1 = (X - d0) >> 8;
-          const int d1 = ((X1 + 128) & 255) - 128;
-          const int d2 = (X1 - d1) >> 8;
-          q = digit == 0 ? d0 : (digit == 1 ? d1 : d2);
+        for (int e = 0; e < 16; ++e) {
+          const int X = (int)rintf(ldexpf(__uint_as_float((uint32_t)v[e] << 16), (b & 1) ? E[1] : E[0]));
+          out[e >> 2] |= e4m3_of_int(f4_digit(X, digit)) << (8 * (e & 3));
         }
-        out[dd] |= ((uint32_t)q & 0xFFu) << (8 * bb);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int dd = e >> 2, bb = e & 3;  // byte 4dd+bb holds code dd + 4bb of the run
+          int q = v[dd + 4 * bb];
+          if constexpr (MODE == kModeBf16) {
+            const int X = (int)rintf(ldexpf(__uint_as_float((uint32_t)q << 16), (b & 1) ? E[1] : E[0]));
+            const int d0 = ((X + 128) & 255) - 128;
+            const int X1 = (X - d0) >> 8;
+            const int d1 = ((X1 + 128) & 255) - 128;
+            const int d2 = (X1 - d1) >> 8;
+            q = digit == 0 ? d0 : (digit == 1 ? d1 : d2);
+          }
+          out[dd] |= ((uint32_t)q & 0xFFu) << (8 * bb);
+        }
       }
     }
     dst[ch] = make_uint4(out[0], out[1], out[2], out[3]);
@@ -702,12 +747,14 @@ __device__ inline void load_enter_layer(LoadCursor<T>& c, const DecLayer& L, con
 // Issue the loads of the cursor's step: its 2T x 16 code bytes per lane into
 // registers cq, and its activation operand (XW KiB) into the LDS slot xslot.
 // A dead cursor issues them out of range (they return zeros), so every step
-// issues the same number of loads.
-template <int XW, int T>
+// issues the same number of loads.  Lane group g's first code of the step is
+// code 64 g (D3 and tiled layouts) or 32 g (fp4 tiled layout, G0 = 32); a
+// group whose codes all lie past K loads zeros.
+template <int XW, int T, int G0 = 64>
 __device__ inline void stream_issue(const LoadCursor<T>& c, bool live, int lane, v4i (&cq)[2 * T],
                                     uint8_t* xslot) {
   const int g = lane >> 4;
-  const bool ok = live && c.row_ok && c.k4 * 256 + 64 * g < c.G.K;
+  const bool ok = live && c.row_ok && c.k4 * 256 + G0 * g < c.G.K;
   const uint32_t off = ok ? c.voff : kOob;
   // descriptor fields stated wave-uniform, so the descriptors stay in scalar
   // registers (no per-load waterfall over lanes)
@@ -824,13 +871,15 @@ __device__ inline DecLayer out_layer(const OutCursor& c) {
 // waves per block of the streaming kernel
 constexpr int kStreamWaves = 4;
 
-template <int T, int XW>
+// ring depth: about 48 code registers per lane
+constexpr int ring_slots(int T) { return T <= 1 ? 4 : (T == 2 ? 3 : 2); }
+
+template <int T, int XW, int NSLOTS = ring_slots(T)>
 struct StreamCfg {
   static constexpr int P = 2 * T;
   static constexpr int XSLOT = XW * 1024;         // LDS bytes of a slot's activation operand
   static constexpr int WAVES = kStreamWaves;
-  // ring depth: about 48 code registers per lane
-  static constexpr int NS = T <= 1 ? 4 : (T == 2 ? 3 : 2);
+  static constexpr int NS = NSLOTS;
   static constexpr int LOADS = P + XW;            // vector memory ops issued per step
   static constexpr int WAIT = (NS - 1) * LOADS;   // outstanding ops allowed when a slot is read
   static constexpr int WAITCNT = (WAIT & 0xF) | (0x7 << 4) | (0xF << 8) | (((WAIT >> 4) & 3) << 14);
@@ -944,6 +993,194 @@ __global__ __launch_bounds__(64 * kStreamWaves) void dec_stream_kernel(DecHeader
 #endif
 }
 
+// ------------------------------------------- streaming kernel, fp4 codes ---
+// The same ring, cursors and work items as above, for codes in the fp4 tiled
+// layout and bf16 activations as 4 base-16 digits (e4m3 integers).  With the
+// code bits (p, q) = (bit 0, bit 1) of code k, i^k = (1 - 2q)(1 - p) +
+// i (1 - 2q) p (Eq. realify-ops: b_re = (1 - 2q)(1 - p), b_im = (1 - 2q) p),
+// the kernel contracts two e2m1 operands with v_mfma_f32_16x16x128_f8f6f4:
+//     S = 1 - 2q  (every code: +-1)     and     I = (1 - 2q) p  (0 or +-1),
+// and forms b_re = S - I in the epilogue.  In the fp4 layout a nibble holds
+// the bits of two codes at (q_A, q_B, p_A, p_B) = bits (3, 2, 1, 0), so per
+// 32-bit word of 16 codes
+//     I_A = w & 0xAAAAAAAA,          S_A = I_A | 0x22222222,
+//     I_B = (w << 1) & 0xAAAAAAAA,   S_B = I_B | 0x22222222
+// (e2m1 0b0010 = 1, 0b1010 = -1, 0b0000 / 0b1000 = +-0): five VALU
+// instructions per 16 codes.  Every product is a digit (|d| <= 9) times 0 or
+// +-1, so the float32 sums are exact integers (|sum| < 2^24 for K < 2^20).
+
+// S and I operands of one 128-code MFMA from the lane's two code words
+// (S = I | 0x22222222: I keeps only bits 3 and 1 of each nibble).
+__device__ inline void expand_f4(uint32_t w0, uint32_t w1, v8i& bs, v8i& bi) {
+  const uint32_t ia0 = w0 & 0xAAAAAAAAu, ib0 = (w0 << 1) & 0xAAAAAAAAu;
+  const uint32_t ia1 = w1 & 0xAAAAAAAAu, ib1 = (w1 << 1) & 0xAAAAAAAAu;
+  bi = v8i{(int)ia0, (int)ib0, (int)ia1, (int)ib1, 0, 0, 0, 0};
+  bs = v8i{(int)(ia0 | 0x22222222u), (int)(ib0 | 0x22222222u), (int)(ia1 | 0x22222222u),
+           (int)(ib1 | 0x22222222u), 0, 0, 0, 0};
+}
+
+constexpr int kFmtFp8 = 0;  // MFMA operand format codes: e4m3
+constexpr int kFmtFp4 = 4;  // e2m1
+
+// Epilogue of a work item: lane (g, li) holds activation columns 4g..4g+3
+// of weight row li, i.e. digits 2(g % 2), 2(g % 2) + 1 of both components of
+// token g / 2; even lane groups take the other two digits from the next
+// group and write the token's output.
+template <int T>
+__device__ inline void write_outputs_f4(const DecLayer& L, const DecHeader& h, int kc, int row, bool row_ok,
+                                        int lane, const v4f (&aS)[2 * T], const v4f (&aI)[2 * T]) {
+  constexpr int P = 2 * T;
+  const int g = lane >> 4;
+  float sc[2][T][2];
+  sload_scales<T>(L.scales[0], L.scales[1], sc);
+  float run[2];
+  sload_run<2>(L.xs, run);
+  float hS[P][4], hI[P][4];
+#pragma unroll
+  for (int p = 0; p < P; ++p)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      hS[p][r] = __shfl_down(aS[p][r], 16);
+      hI[p][r] = __shfl_down(aI[p][r], 16);
+    }
+  const int b = g >> 1;
+  if ((g & 1) || !row_ok || b >= h.B) return;
+  // exact integer products of plane p with component c: axis re (b_re = S - I), im (b_im = I)
+  auto digits = [](const float (&a)[4], const float (&hh)[4], int c) -> double {
+    return (double)a[c] + 16.0 * (double)a[2 + c] + 256.0 * (double)hh[c] + 4096.0 * (double)hh[2 + c];
+  };
+  double yr = 0.0, yi = 0.0;
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    double Pre[2][2], Pim[2][2];  // [matrix][component]
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {
+      const int p = m * T + t;
+      const float s4[4] = {aS[p][0], aS[p][1], aS[p][2], aS[p][3]};
+      const float i4[4] = {aI[p][0], aI[p][1], aI[p][2], aI[p][3]};
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const double vi = digits(i4, hI[p], c);
+        Pre[m][c] = digits(s4, hS[p], c) - vi;
+        Pim[m][c] = vi;
+      }
+    }
+    const double su_re = sc[0][t][0], su_im = sc[0][t][1];
+    const double sw_re = sc[1][t][0], sw_im = sc[1][t][1];
+    yr += su_re * Pre[0][0] - su_im * Pim[0][1];
+    yi += su_re * Pre[0][1] + su_im * Pim[0][0];
+    yr += sw_re * Pre[1][0] + sw_im * Pim[1][1];
+    yi += -sw_re * Pre[1][1] + sw_im * Pim[1][0];
+  }
+  const double f = (double)(b ? run[1] : run[0]);
+  const float2 v = make_float2((float)(yr * f), (float)(yi * f));
+  if (L.nkc == 1)
+    buf_store8(L.y, (uint32_t)h.B * L.N * 8, (uint32_t)((b * L.N + row) * 8), v);
+  else
+    buf_store8(L.part, (uint32_t)L.nkc * h.B * L.N * 8, (uint32_t)(((kc * h.B + b) * L.N + row) * 8), v);
+}
+
+constexpr int f4_ring_slots(int T) { return ring_slots(T); }
+
+template <int T, int XW>
+__global__ __launch_bounds__(64 * kStreamWaves) void dec_stream_f4_kernel(DecHeader h, DecLayer inl,
+                                                                          const DecLayer* __restrict__ tab) {
+#if defined(__HIP_DEVICE_COMPILE__)  // LDS-DMA and buffer-descriptor code: device pass only
+  using C = StreamCfg<T, XW, f4_ring_slots(T)>;
+  constexpr int P = C::P, NS = C::NS, XSLOT = C::XSLOT;
+  constexpr int WAVES = C::WAVES;
+  __shared__ __attribute__((aligned(16))) uint8_t ring[WAVES][NS][XSLOT];
+  __shared__ __attribute__((aligned(16))) uint8_t zero16[16];
+  const int lane = threadIdx.x & 63;
+  const int g = lane >> 4, li = lane & 15;
+  const int wave = uniform(threadIdx.x >> 6);
+  if (threadIdx.x < 4) reinterpret_cast<uint32_t*>(zero16)[threadIdx.x] = 0u;
+  __syncthreads();
+  const int64_t wid = (int64_t)blockIdx.x * WAVES + wave;
+  const int64_t W = (int64_t)gridDim.x * WAVES;
+  const int64_t i0 = uniform64(wid * h.total_items / W);
+  const int64_t i1 = uniform64((wid + 1) * h.total_items / W);
+  if (i0 >= i1) return;
+
+  int b_, digit_, comp_;
+  const bool xvalid = col_token<kModeBf16F4>(0, li, h.B, b_, digit_, comp_);
+
+  LoadCursor<T> lc;
+  OutCursor oc;
+  {
+    const int lidx = tab ? find_layer(tab, h.n_layers, i0) : 0;
+    const DecLayer L0 = tab ? load_layer(tab + lidx) : inl;
+    lc.lidx = oc.lidx = lidx;
+    lc.item = oc.item = i0;
+    load_enter_layer(lc, L0, h);
+    out_enter_layer(oc, L0);
+    split_item(i0, lc.G, lc.rb, lc.kc);
+    oc.rb = lc.rb;
+    oc.kc = lc.kc;
+  }
+  load_item(lc, h, lane);
+  out_item(oc, li);
+
+  v4i cq[NS][P];
+  bool live = true;
+#pragma unroll
+  for (int k = 0; k < NS - 1; ++k) {
+    stream_issue<XW, T, 32>(lc, live, lane, cq[k], &ring[wave][k][0]);
+    if (live) live = load_next(lc, tab, h, i1, lane);
+  }
+
+  v4f aS[P], aI[P];
+#pragma unroll
+  for (int p = 0; p < P; ++p) aS[p] = aI[p] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  auto step = [&](auto kconst) -> bool {
+    constexpr int K = decltype(kconst)::value;
+    constexpr int KN = (K + NS - 1) % NS;
+    stream_issue<XW, T, 32>(lc, live, lane, cq[KN], &ring[wave][KN][0]);
+    if (live) live = load_next(lc, tab, h, i1, lane);
+    __builtin_amdgcn_s_waitcnt(C::WAITCNT);
+    v4i xr[4];
+    {
+      const uint32_t xa = xvalid ? lds_addr(&ring[wave][K][0]) + (uint32_t)((g * h.nc + li) * 16) : lds_addr(zero16);
+      const uint32_t xs = xvalid ? (uint32_t)(4 * h.nc * 16) : 0u;
+      lds_read4(xa, xa + xs, xa + 2 * xs, xa + 3 * xs, xr);
+    }
+    const v4i* cr = cq[K];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const v4i x0 = xr[2 * kb], x1 = xr[2 * kb + 1];
+      const v8i a = v8i{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+#pragma unroll
+      for (int p = 0; p < P; ++p) {
+        v8i bs, bi;
+        expand_f4((uint32_t)cr[p][2 * kb], (uint32_t)cr[p][2 * kb + 1], bs, bi);
+        aS[p] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bs, aS[p], kFmtFp8, kFmtFp4, 0, 0, 0, 0);
+        aI[p] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bi, aI[p], kFmtFp8, kFmtFp4, 0, 0, 0, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 10, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      }
+    }
+    if (oc.j == oc.nsteps - 1) {
+      write_outputs_f4<T>(out_layer(oc), h, oc.kc, oc.row, oc.row_ok, lane, aS, aI);
+#pragma unroll
+      for (int p = 0; p < P; ++p) aS[p] = aI[p] = v4f{0.f, 0.f, 0.f, 0.f};
+    }
+    return !out_next(oc, tab, i1, li);
+  };
+
+  static_assert(NS >= 2 && NS <= 6, "the ring loop below is unrolled for 2..6 slots");
+  while (true) {
+    if (step(std::integral_constant<int, 0>{})) break;
+    if (step(std::integral_constant<int, 1>{})) break;
+    if constexpr (NS > 2) if (step(std::integral_constant<int, 2 % NS>{})) break;
+    if constexpr (NS > 3) if (step(std::integral_constant<int, 3 % NS>{})) break;
+    if constexpr (NS > 4) if (step(std::integral_constant<int, 4 % NS>{})) break;
+    if constexpr (NS > 5) if (step(std::integral_constant<int, 5 % NS>{})) break;
+  }
+  __builtin_amdgcn_s_waitcnt(0);  // no load may still be writing LDS when the wave ends
+#endif
+}
+
 // ------------------------------------------------------------ reduction ---
 __global__ __launch_bounds__(256) void dec_reduce_kernel(DecHeader h, DecLayer inl,
                                                          const DecLayer* __restrict__ tab) {
@@ -1017,6 +1254,22 @@ void launch_stream(const DecHeader& h, const DecLayer& inl, const DecLayer* tab,
   hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(threads), 0, s, h, inl, tab);
 }
 
+template <int T, int XW>
+void launch_stream_f4(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
+  auto k = dec_stream_f4_kernel<T, XW>;
+  constexpr int threads = 64 * kStreamWaves;
+  static const int resident = resident_blocks(reinterpret_cast<const void*>(k), threads);
+  const int64_t want = (h.total_items + kStreamWaves - 1) / kStreamWaves;
+  const int64_t blocks = want < resident ? want : resident;
+  hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(threads), 0, s, h, inl, tab);
+}
+
+template <int T>
+void launch_stream_f4_t(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
+  if (h.nc <= 8) launch_stream_f4<T, 2>(h, inl, tab, s);   // one token: 8 columns, 2 KB per step
+  else launch_stream_f4<T, 4>(h, inl, tab, s);
+}
+
 template <int MODE, int T>
 void launch_stream_t(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, int64_t blocks,
                      hipStream_t s) {
@@ -1056,6 +1309,9 @@ hipError_t launch_decode(const DecHeader& h, const DecLayer& inl, const DecLayer
   // 1. activation operand
   if (h.mode == kModeBf16)
     hipLaunchKernelGGL(dec_prep_kernel<kModeBf16>, dim3(h.ntile, nl, kPrepSplit), dim3(256), 0, s, h, inl, tab);
+  else if (h.mode == kModeBf16F4)
+    hipLaunchKernelGGL(dec_prep_kernel<kModeBf16F4>, dim3(h.ntile, nl, kPrepSplit), dim3(256), 0, s, h, inl,
+                       tab);
   else
     hipLaunchKernelGGL(dec_prep_kernel<kModeI8>, dim3(h.ntile, nl, kPrepSplit), dim3(256), 0, s, h, inl, tab);
   if ((e = hipGetLastError()) != hipSuccess || (e = mark(1)) != hipSuccess) return e;
@@ -1065,7 +1321,15 @@ hipError_t launch_decode(const DecHeader& h, const DecLayer& inl, const DecLayer
   }
   // 2. products
   const int64_t blocks = (h.total_items + 3) / 4;  // capped at what fits on the device
-  if (h.kernel == kKernelStream) {
+  if (h.mode == kModeBf16F4) {
+    // one activation tile (B <= 2), codes in the fp4 tiled layout: checked by the host code
+    switch (h.T) {
+      case 1: launch_stream_f4_t<1>(h, inl, tab, s); break;
+      case 2: launch_stream_f4_t<2>(h, inl, tab, s); break;
+      case 3: launch_stream_f4_t<3>(h, inl, tab, s); break;
+      default: launch_stream_f4_t<4>(h, inl, tab, s); break;
+    }
+  } else if (h.kernel == kKernelStream) {
     if (h.mode == kModeBf16) launch_stream_mode<kModeBf16>(h, inl, tab, blocks, s);
     else launch_stream_mode<kModeI8>(h, inl, tab, blocks, s);
   } else if (h.mode == kModeBf16) {
@@ -1094,10 +1358,11 @@ namespace {
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 }  // namespace
 
-int dec_ntile(int mode, int64_t B) { return mode == kModeBf16 ? (int)((B + 1) / 2) : (int)((B + 7) / 8); }
+int dec_ntile(int mode, int64_t B) { return mode == kModeI8 ? (int)((B + 7) / 8) : (int)((B + 1) / 2); }
 
 int dec_ncols(int mode, int64_t B) {
   if (mode == kModeBf16) return B >= 2 ? 14 : 6;  // per token 6 digit columns, 8-column stride
+  if (mode == kModeBf16F4) return B >= 2 ? 16 : 8;  // per token 8 digit columns
   return B >= 8 ? 16 : (int)(2 * B);
 }
 

@@ -42,7 +42,7 @@ def test_status_strings(lib):
     for s in range(8):
         assert lib.fairy2i_status_string(s)
     assert lib.fairy2i_status_string(99) == b"unknown status"
-    assert lib.fairy2i_abi_version() == 2
+    assert lib.fairy2i_abi_version() == 3
 
 
 def test_to_widely_linear_validation(lib):
@@ -188,7 +188,14 @@ def test_group_build_validation(lib):
     assert build(good, wsb=16) == binding.ERR_WORKSPACE
     assert build(good, tb=8) == binding.ERR_WORKSPACE
     assert build([_layer(layout=binding.LAYOUT_TILED), _layer(N=200, K=1088)]) == binding.OK
-    assert build([_layer(layout=2)]) == binding.ERR_UNSUPPORTED
+    fp4 = binding.LAYOUT_TILED_FP4
+    assert build([_layer(layout=fp4), _layer(layout=fp4, N=200, K=1088)]) == binding.OK
+    assert build([_layer(layout=fp4)], B=2) == binding.OK
+    assert build([_layer(layout=fp4)], B=3) == binding.ERR_UNSUPPORTED      # one activation tile
+    assert build([_layer(layout=fp4, x_scale=0x1000)], dt=binding.ACT_I8) == binding.ERR_UNSUPPORTED
+    assert build([_layer(layout=fp4), _layer()]) == binding.ERR_UNSUPPORTED  # fp4 for every layer or none
+    assert build([_layer(), _layer(layout=fp4)]) == binding.ERR_UNSUPPORTED
+    assert build([_layer(layout=3)]) == binding.ERR_UNSUPPORTED
     assert build([_layer(reserved=1)]) == binding.ERR_UNSUPPORTED
 
 
@@ -205,6 +212,12 @@ def test_repack_validation_and_size(lib):
     assert f(P, 0, 256, 1, P, 1 << 20, None) == binding.ERR_SHAPE
     assert f(P, 16, 256, 0, P, 1 << 20, None) == binding.ERR_STAGES
     assert f(P, 16, 256, 1, P, 1023, None) == binding.ERR_WORKSPACE
+    f4 = lib.fairy2i_repack_tiled_fp4
+    assert f4(None, 16, 256, 1, P, 1024, None) == binding.ERR_NULL
+    assert f4(P, 16, 256, 1, None, 1024, None) == binding.ERR_NULL
+    assert f4(P, 16, 258, 1, P, 1 << 20, None) == binding.ERR_SHAPE
+    assert f4(P, 16, 256, 5, P, 1 << 20, None) == binding.ERR_STAGES
+    assert f4(P, 16, 256, 1, P, 1023, None) == binding.ERR_WORKSPACE
 
 
 def test_group_call_validation(lib):

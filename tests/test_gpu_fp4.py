@@ -1,0 +1,209 @@
+"""GPU parity of the fp4 decode path (codes in the fp4 tiled layout, bf16
+activations on the fp8 x fp4 matrix cores) against the CPU oracle.
+
+Bars: the repacked bytes bit-exact against the layout's definition written
+out with numpy; y against the oracle within relative L2 TOL_FP4.  The path
+takes each token as a 15-bit block fixed point X = rint(x 2^E) with
+2^14 <= max|X| < 2^15 and forms exact integer products, so its only error is
+the rounding of bf16 values more than a factor 2^7 below the token's largest
+magnitude to the 2^-E grid (at most 2^-16 of that magnitude per value).  For
+N(0,1) tokens about 1.4 % of the values are that small, which puts the
+expected relative L2 error near 1e-5; TOL_FP4 = 1e-4 leaves a factor 10 and
+stays a factor 10 inside the 1e-3 bar for bf16 activations.  Tokens whose
+values all lie within a factor 2^7 of their largest magnitude are exact
+(y to float32 rounding, 1e-6).
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+TOL_FP4 = 1e-4
+TOL_EXACT = 1e-6
+
+
+def rel_l2(got, want):
+    got = np.asarray(got, dtype=np.complex128)
+    want = np.asarray(want, dtype=np.complex128)
+    den = np.linalg.norm(want)
+    return np.linalg.norm(got - want) / (den if den > 0 else 1.0)
+
+
+def dev(a, gpu):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).to(gpu)
+
+
+def host(t):
+    return t.detach().cpu().numpy()
+
+
+def bf16_dev(x, gpu):
+    import torch
+    bits = np.stack([synth.bf16_bits(x.real.astype(np.float32)),
+                     synth.bf16_bits(x.imag.astype(np.float32))], axis=-1)
+    return dev(bits.view(np.int16), gpu).view(torch.bfloat16)
+
+
+def quantized_layer(N, K, T, key):
+    A = synth.llama_weight(2 * N, 2 * K, key)
+    U, W = oracle.to_widely_linear(A)
+    cu, su = oracle.quantize(U, T)
+    cw, sw = oracle.quantize(W, T)
+    return cu, su, cw, sw
+
+
+def fp4_reference(packed, N, K):
+    """The fp4 tiled layout of D3 bytes [T, N, K/4], written out from its
+    definition: lane (g, r) of tile (rb, s, t) holds codes
+    256 s + 128 kb + 32 g + n of row 16 rb + r; n = 16 h + 8 a + m goes to
+    word 2 kb + h, nibble m, bits (q, p) at (3, 1) for a = 0, (2, 0) for a = 1."""
+    T = packed.shape[0]
+    nrb, nk4 = -(-N // 16), -(-K // 256)
+    codes = np.zeros((T, nrb * 16, nk4 * 256), np.uint32)
+    unpacked = (packed[..., None] >> (2 * np.arange(4, dtype=np.uint8))) & 3   # [T, N, K/4, 4]
+    codes[:, :N, :K] = unpacked.reshape(T, N, K)
+    p, q = codes & 1, codes >> 1
+    out = np.zeros((nrb, nk4, T, 4, 16, 4), np.uint32)          # rb, s, t, g, r, word
+    for kb in range(2):
+        for n in range(32):
+            h, a, m = n // 16, (n // 8) % 2, n % 8
+            k = np.arange(nk4)[:, None] * 256 + 128 * kb + 32 * np.arange(4)[None, :] + n   # [s, g]
+            pk = p[:, :, k]          # [T, rows, s, g]
+            qk = q[:, :, k]
+            nib = (qk << 3) | (pk << 1) if a == 0 else (qk << 2) | pk
+            nib = nib.reshape(T, nrb, 16, nk4, 4).transpose(1, 3, 0, 4, 2)   # rb, s, t, g, r
+            out[..., 2 * kb + h] |= nib << (4 * m)
+    return out.astype("<u4").view(np.uint8).reshape(-1)
+
+
+@pytest.mark.parametrize("NKT", [(16, 256, 1), (100, 320, 2), (48, 1088, 3), (37, 100, 2), (5, 4, 4),
+                                 (2048, 5504, 2)])
+def test_repack_tiled_fp4_bit_exact(gpu, NKT):
+    """fairy2i_repack_tiled_fp4 against the layout's definition: ragged row
+    blocks, K not a multiple of 256 or of 32, an unaligned source."""
+    import torch
+    import paper_2512_02901_amd as f2
+    N, K, T = NKT
+    rng = np.random.default_rng(N * 11 + K)
+    packed = rng.integers(0, 256, (T, N, K // 4), dtype=np.uint8)
+    want = fp4_reference(packed, N, K)
+    got = host(f2.repack_tiled_fp4(dev(packed, gpu)))
+    assert got.shape == want.shape == (f2.repack_tiled_bytes(N, K, T),)
+    np.testing.assert_array_equal(got, want)
+    buf = torch.zeros(packed.size + 16, dtype=torch.uint8, device=gpu)
+    src = buf[3:3 + packed.size].view(packed.shape)
+    src.copy_(dev(packed, gpu))
+    np.testing.assert_array_equal(host(f2.repack_tiled_fp4(src)), want)
+
+
+SHAPES = [(128, 256), (200, 64), (48, 1088), (64, 2048), (37, 5504), (1, 64)]
+
+
+def run_fp4_group(layers, T, B, gpu, x_of):
+    """layers: [(N, K, cu, su, cw, sw)]; x_of(i, N, K) -> bf16-exact complex
+    activations [B, K].  Returns (y list, oracle list, group)."""
+    import torch
+    import paper_2512_02901_amd as f2
+    args, refs = [], []
+    for i, (N, K, cu, su, cw, sw) in enumerate(layers):
+        x = x_of(i, N, K)
+        d_cu, d_cw = dev(oracle.pack(cu), gpu), dev(oracle.pack(cw), gpu)
+        y = torch.empty((B, N), dtype=torch.complex64, device=gpu)
+        args.append((f2.repack_tiled_fp4(d_cu), dev(su, gpu), f2.repack_tiled_fp4(d_cw), dev(sw, gpu),
+                     bf16_dev(x, gpu), None, y))
+        refs.append(oracle.wl_matmul(cu, su, cw, sw, x))
+    grp = f2.WlGroup(args, T=T, B=B, layout=f2.LAYOUT_TILED_FP4)
+    grp.run()
+    return [a[6] for a in args], refs, grp
+
+
+@pytest.mark.parametrize("T", [1, 2, 3, 4])
+def test_group_fp4_matches_oracle(gpu, T):
+    """One grouped fp4 call over layers of several shapes (ragged row blocks,
+    K with a partial 256-code step, one row), 1 and 2 tokens, against the
+    oracle; a repeated call is bitwise identical."""
+    layers = [(N, K, *quantized_layer(N, K, T, (40, i, N))) for i, (N, K) in enumerate(SHAPES)]
+    for B in (1, 2):
+        ys, refs, grp = run_fp4_group(layers, T, B, gpu,
+                                      lambda i, N, K: synth.bf16_round_complex(synth.activations(B, K, (41, i, B))))
+        first = [host(y).copy() for y in ys]
+        errs = [rel_l2(host(y), yo) for y, yo in zip(ys, refs)]
+        print(f"T={T} B={B} rel-L2 per layer:", " ".join(f"{e:.2e}" for e in errs))
+        assert max(errs) <= TOL_FP4
+        grp.run()
+        for y, y1 in zip(ys, first):
+            np.testing.assert_array_equal(host(y).view(np.uint32), y1.view(np.uint32))
+
+
+def representable_tokens(B, K, key):
+    """bf16 tokens whose values all lie within a factor 2^7 of the token's
+    largest magnitude (magnitudes in [1, 128), random signs)."""
+    rng = np.random.default_rng(key)
+    mag = np.exp2(rng.uniform(0.0, 7.0, (B, K, 2)))
+    v = mag * np.where(rng.random((B, K, 2)) < 0.5, -1.0, 1.0)
+    return synth.bf16_round_complex((v[..., 0] + 1j * v[..., 1]).astype(np.complex64))
+
+
+def test_group_fp4_exact_for_representable_tokens(gpu):
+    """Tokens on the 15-bit grid: the integer products are exact, y matches
+    the oracle to float32 rounding and the int8 tiled path to double
+    rounding."""
+    import torch
+    import paper_2512_02901_amd as f2
+    T = 2
+    layers = [(N, K, *quantized_layer(N, K, T, (42, i, N))) for i, (N, K) in enumerate(SHAPES)]
+    for B in (1, 2):
+        xs = {}
+
+        def x_of(i, N, K):
+            xs[i] = representable_tokens(B, K, 43 * 100 + 10 * i + B)
+            return xs[i]
+        ys, refs, _ = run_fp4_group(layers, T, B, gpu, x_of)
+        for y, yo in zip(ys, refs):
+            assert rel_l2(host(y), yo) <= TOL_EXACT
+        # the same products through the int8 matrix cores (tiled layout)
+        args = []
+        for i, (N, K, cu, su, cw, sw) in enumerate(layers):
+            y = torch.empty((B, N), dtype=torch.complex64, device=gpu)
+            args.append((f2.repack_tiled(dev(oracle.pack(cu), gpu)), dev(su, gpu),
+                         f2.repack_tiled(dev(oracle.pack(cw), gpu)), dev(sw, gpu), bf16_dev(xs[i], gpu), None, y))
+        f2.WlGroup(args, T=T, B=B, tiled=True).run()
+        for y, a in zip(ys, args):
+            assert rel_l2(host(y), host(a[6])) <= 1e-7
+
+
+def test_group_fp4_edge_tokens(gpu):
+    """A zero token gives y = 0 (and does not disturb its neighbour); a token
+    spanning 2^-40 .. 2^3 stays inside the bf16 bar; a single huge or tiny
+    token is scaled without overflow."""
+    T = 2
+    N, K = 48, 1088
+    layer = [(N, K, *quantized_layer(N, K, T, (44, 0, N)))]
+    rng = np.random.default_rng(45)
+    mag = np.exp2(rng.uniform(-40, 3, (1, K))) * np.sign(rng.standard_normal((1, K)))
+    wide = synth.bf16_round_complex((mag + 1j * mag[:, ::-1]).astype(np.complex64))
+    normal = synth.bf16_round_complex(synth.activations(1, K, (46,)))
+    cases = {
+        "zero+normal": np.concatenate([np.zeros((1, K), np.complex64), normal]),
+        "wide": wide,
+        "huge": synth.bf16_round_complex((normal * np.float32(2.0 ** 100)).astype(np.complex64)),
+        "tiny": synth.bf16_round_complex((normal * np.float32(2.0 ** -100)).astype(np.complex64)),
+    }
+    for name, x in cases.items():
+        B = x.shape[0]
+        ys, refs, _ = run_fp4_group(layer, T, B, gpu, lambda i, N_, K_: x)
+        y, yo = host(ys[0]), refs[0]
+        err = rel_l2(y, yo)
+        print(f"{name}: rel-L2 {err:.2e}")
+        assert np.all(np.isfinite(y.view(np.float32)))
+        if name == "zero+normal":
+            assert np.all(y[0] == 0)
+            assert rel_l2(y[1], yo[1]) <= TOL_FP4
+        elif name == "wide":
+            assert err <= 1e-3
+        else:
+            assert err <= TOL_FP4
