@@ -181,7 +181,7 @@ def traffic_record():
     """HBM bytes per launch of the product kernel from committed rocprofv3
     --pmc summaries, or None when absent or when the kernel source changed
     since the counters were taken."""
-    path = os.path.join(PROFILES, "dec_stream_stack_T2_bf16_traffic.txt")
+    path = os.path.join(PROFILES, "dec_stream_f4_stack_T2_bf16_traffic.txt")
     if not os.path.exists(path):
         return None
     rec = {}

@@ -1024,8 +1024,11 @@ constexpr int kFmtFp4 = 4;  // e2m1
 
 // Epilogue of a work item: lane (g, li) holds activation columns 4g..4g+3
 // of weight row li, i.e. digits 2(g % 2), 2(g % 2) + 1 of both components of
-// token g / 2; even lane groups take the other two digits from the next
-// group and write the token's output.
+// token g / 2.  Each lane first joins its two digits (the sums are exact
+// integers: an item spans at most 2048 codes, so |sum| < 2^26); odd lane
+// groups pass theirs to the even group below, which forms the token's
+// integer products and applies the axis scales and the token factor in
+// float32.
 template <int T>
 __device__ inline void write_outputs_f4(const DecLayer& L, const DecHeader& h, int kc, int row, bool row_ok,
                                         int lane, const v4f (&aS)[2 * T], const v4f (&aI)[2 * T]) {
@@ -1035,45 +1038,41 @@ __device__ inline void write_outputs_f4(const DecLayer& L, const DecHeader& h, i
   sload_scales<T>(L.scales[0], L.scales[1], sc);
   float run[2];
   sload_run<2>(L.xs, run);
-  float hS[P][4], hI[P][4];
+  int vS[P][2], vI[P][2], hS[P][2], hI[P][2];
 #pragma unroll
   for (int p = 0; p < P; ++p)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      hS[p][r] = __shfl_down(aS[p][r], 16);
-      hI[p][r] = __shfl_down(aI[p][r], 16);
+    for (int c = 0; c < 2; ++c) {
+      vS[p][c] = (int)aS[p][c] + 16 * (int)aS[p][2 + c];
+      vI[p][c] = (int)aI[p][c] + 16 * (int)aI[p][2 + c];
+      hS[p][c] = __shfl_down(vS[p][c], 16);
+      hI[p][c] = __shfl_down(vI[p][c], 16);
     }
   const int b = g >> 1;
   if ((g & 1) || !row_ok || b >= h.B) return;
-  // exact integer products of plane p with component c: axis re (b_re = S - I), im (b_im = I)
-  auto digits = [](const float (&a)[4], const float (&hh)[4], int c) -> double {
-    return (double)a[c] + 16.0 * (double)a[2 + c] + 256.0 * (double)hh[c] + 4096.0 * (double)hh[2 + c];
-  };
-  double yr = 0.0, yi = 0.0;
+  float yr = 0.0f, yi = 0.0f;
 #pragma unroll
   for (int t = 0; t < T; ++t) {
-    double Pre[2][2], Pim[2][2];  // [matrix][component]
+    float Pre[2][2], Pim[2][2];  // [matrix][component]: products with b_re = S - I and b_im = I
 #pragma unroll
     for (int m = 0; m < 2; ++m) {
       const int p = m * T + t;
-      const float s4[4] = {aS[p][0], aS[p][1], aS[p][2], aS[p][3]};
-      const float i4[4] = {aI[p][0], aI[p][1], aI[p][2], aI[p][3]};
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
-        const double vi = digits(i4, hI[p], c);
-        Pre[m][c] = digits(s4, hS[p], c) - vi;
-        Pim[m][c] = vi;
+        const int ii = vI[p][c] + 256 * hI[p][c];
+        Pre[m][c] = (float)(vS[p][c] + 256 * hS[p][c] - ii);
+        Pim[m][c] = (float)ii;
       }
     }
-    const double su_re = sc[0][t][0], su_im = sc[0][t][1];
-    const double sw_re = sc[1][t][0], sw_im = sc[1][t][1];
+    const float su_re = sc[0][t][0], su_im = sc[0][t][1];
+    const float sw_re = sc[1][t][0], sw_im = sc[1][t][1];
     yr += su_re * Pre[0][0] - su_im * Pim[0][1];
     yi += su_re * Pre[0][1] + su_im * Pim[0][0];
     yr += sw_re * Pre[1][0] + sw_im * Pim[1][1];
     yi += -sw_re * Pre[1][1] + sw_im * Pim[1][0];
   }
-  const double f = (double)(b ? run[1] : run[0]);
-  const float2 v = make_float2((float)(yr * f), (float)(yi * f));
+  const float f = b ? run[1] : run[0];
+  const float2 v = make_float2(yr * f, yi * f);
   if (L.nkc == 1)
     buf_store8(L.y, (uint32_t)h.B * L.N * 8, (uint32_t)((b * L.N + row) * 8), v);
   else
