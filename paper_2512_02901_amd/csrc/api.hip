@@ -328,6 +328,8 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
     if (B * (int64_t)l.N > max_BN) max_BN = B * (int64_t)l.N;
     tab[i] = l;
   }
+  // the decode kernels index a call's work items with 32-bit offsets
+  if (items >= ((int64_t)1 << 31)) return FAIRY2I_ERR_UNSUPPORTED;
   *hdr = GroupTableHeader{};
   hdr->magic = kGroupMagic;
   hdr->abi = (uint32_t)fairy2i_abi_version();

@@ -226,19 +226,6 @@ __device__ inline void buf_store8(const void* base, uint32_t bytes, uint32_t off
 // when the activation pointer allows them.
 constexpr int kPrepSplit = 4;
 
-// Balanced base-16 digit i (i < 4) of X, |X| <= 2^15: X = sum_i d_i 16^i with
-// d_0..d_2 in [-8, 7] and |d_3| <= 9.
-__device__ inline int f4_digit(int X, int i) {
-  int d = 0;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    d = j < 3 ? ((X + 8) & 15) - 8 : X;
-    if (j == i) break;
-    X = (X - d) >> 4;
-  }
-  return d;
-}
-
 // The e4m3 (OCP fp8: 1 sign, 4 exponent bits with bias 7, 3 mantissa bits)
 // encoding of an integer |d| <= 16, which it represents exactly.
 __device__ inline uint32_t e4m3_of_int(int d) {
@@ -351,40 +338,60 @@ __global__ __launch_bounds__(256) void dec_prep_kernel(DecHeader h, DecLayer inl
   }
   const int nch = L.nk4 * 16 * h.nc;
   uint4* dst = reinterpret_cast<uint4*>(L.xf) + (int64_t)tile * nch;
+  if constexpr (MODE == kModeBf16F4) {
+    // one thread per run of 16 values of one component of one token: it
+    // writes the run's four digit chunks (columns 8 tk + 2 digit + comp)
+    const int ntok = h.nc / 8;
+    const int nrun = L.nk4 * 16 * ntok * 2;
+    for (int ri = blockIdx.z * blockDim.x + threadIdx.x; ri < nrun; ri += gridDim.z * blockDim.x) {
+      const int comp = ri & 1, tk = (ri >> 1) % ntok, r = (ri >> 1) / ntok;
+      const int kk = r >> 4, d = (r >> 2) & 3, g = r & 3;
+      const int64_t k0 = (int64_t)kk * 256 + 64 * d + 16 * g;
+      const int b = 2 * tile + tk;
+      uint32_t out[4][4] = {};
+      if (b < h.B && k0 < K) {  // K % 64 == 0: the whole run is in range
+        int v[16];
+        load_run16<kModeBf16>(L.x, vec, ((int64_t)b * K + k0) * 2, comp, v);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          int X = (int)rintf(ldexpf(__uint_as_float((uint32_t)v[e] << 16), tk ? E[1] : E[0]));
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            // balanced base-16 digits of |X| <= 2^15: d_0..d_2 in [-8, 7], |d_3| <= 9
+            const int dj = j < 3 ? ((X + 8) & 15) - 8 : X;
+            X = (X - dj) >> 4;
+            out[j][e >> 2] |= e4m3_of_int(dj) << (8 * (e & 3));
+          }
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        dst[(int64_t)r * h.nc + 8 * tk + 2 * j + comp] = make_uint4(out[j][0], out[j][1], out[j][2], out[j][3]);
+    }
+    return;
+  }
   for (int ch = blockIdx.z * blockDim.x + threadIdx.x; ch < nch; ch += gridDim.z * blockDim.x) {
     const int col = ch % h.nc, r = ch / h.nc;
     const int kk = r >> 4, d = (r >> 2) & 3, g = r & 3;
-    // int8 operand: chunk (d, g) feeds dword d of lane group g; fp8 operand:
-    // chunk (d, g) is half d % 2 of lane group g's operand of MFMA d / 2
-    const int64_t k0 = MODE == kModeBf16F4 ? (int64_t)kk * 256 + 64 * d + 16 * g
-                                           : (int64_t)kk * 256 + 64 * g + 16 * d;
+    const int64_t k0 = (int64_t)kk * 256 + 64 * g + 16 * d;  // chunk (d, g) feeds dword d of lane group g
     uint32_t out[4] = {0u, 0u, 0u, 0u};
     int b, digit, comp;
     if (col_token<MODE>(tile, col, h.B, b, digit, comp) && k0 < K) {  // K % 64 == 0: whole run in range
       int v[16];
-      load_run16<MODE == kModeBf16F4 ? kModeBf16 : MODE>(L.x, vec, ((int64_t)b * K + k0) * 2, comp, v);
-      if constexpr (MODE == kModeBf16F4) {
-        // byte e = base-16 digit `digit` of X = rint(x[k0 + e] * 2^E), as an e4m3 value
+      load_run16<MODE>(L.x, vec, ((int64_t)b * K + k0) * 2, comp, v);
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int X = (int)rintf(ldexpf(__uint_as_float((uint32_t)v[e] << 16), (b & 1) ? E[1] : E[0]));
-          out[e >> 2] |= e4m3_of_int(f4_digit(X, digit)) << (8 * (e & 3));
+      for (int e = 0; e < 16; ++e) {
+        const int dd = e >> 2, bb = e & 3;  // byte 4dd+bb holds code dd + 4bb of the run
+        int q = v[dd + 4 * bb];
+        if constexpr (MODE == kModeBf16) {
+          const int X = (int)rintf(ldexpf(__uint_as_float((uint32_t)q << 16), (b & 1) ? E[1] : E[0]));
+          const int d0 = ((X + 128) & 255) - 128;
+          const int X1 = (X - d0) >> 8;
+          const int d1 = ((X1 + 128) & 255) - 128;
+          const int d2 = (X1 - d1) >> 8;
+          q = digit == 0 ? d0 : (digit == 1 ? d1 : d2);
         }
-      } else {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int dd = e >> 2, bb = e & 3;  // byte 4dd+bb holds code dd + 4bb of the run
-          int q = v[dd + 4 * bb];
-          if constexpr (MODE == kModeBf16) {
-            const int X = (int)rintf(ldexpf(__uint_as_float((uint32_t)q << 16), (b & 1) ? E[1] : E[0]));
-            const int d0 = ((X + 128) & 255) - 128;
-            const int X1 = (X - d0) >> 8;
-            const int d1 = ((X1 + 128) & 255) - 128;
-            const int d2 = (X1 - d1) >> 8;
-            q = digit == 0 ? d0 : (digit == 1 ? d1 : d2);
-          }
-          out[dd] |= ((uint32_t)q & 0xFFu) << (8 * bb);
-        }
+        out[dd] |= ((uint32_t)q & 0xFFu) << (8 * bb);
       }
     }
     dst[ch] = make_uint4(out[0], out[1], out[2], out[3]);
@@ -868,25 +875,31 @@ __device__ inline DecLayer out_layer(const OutCursor& c) {
   return L;
 }
 
-// waves per block of the streaming kernel
+// waves per block of the streaming kernel (fewer when the ring would not
+// fit the LDS)
 constexpr int kStreamWaves = 4;
+constexpr int stream_waves(int NS, int XW, int base = kStreamWaves) {
+  int w = base;
+  while (w > 1 && w * NS * XW * 1024 > 150 * 1024) w /= 2;
+  return w;
+}
 
 // ring depth: about 48 code registers per lane
 constexpr int ring_slots(int T) { return T <= 1 ? 4 : (T == 2 ? 3 : 2); }
 
-template <int T, int XW, int NSLOTS = ring_slots(T)>
+template <int T, int XW, int NSLOTS = ring_slots(T), int BASE_WAVES = kStreamWaves>
 struct StreamCfg {
   static constexpr int P = 2 * T;
   static constexpr int XSLOT = XW * 1024;         // LDS bytes of a slot's activation operand
-  static constexpr int WAVES = kStreamWaves;
   static constexpr int NS = NSLOTS;
+  static constexpr int WAVES = stream_waves(NS, XW, BASE_WAVES);
   static constexpr int LOADS = P + XW;            // vector memory ops issued per step
   static constexpr int WAIT = (NS - 1) * LOADS;   // outstanding ops allowed when a slot is read
   static constexpr int WAITCNT = (WAIT & 0xF) | (0x7 << 4) | (0xF << 8) | (((WAIT >> 4) & 3) << 14);
 };
 
 template <int MODE, int T, int XW>
-__global__ __launch_bounds__(64 * kStreamWaves) void dec_stream_kernel(DecHeader h, DecLayer inl,
+__global__ __launch_bounds__((64 * StreamCfg<T, XW>::WAVES)) void dec_stream_kernel(DecHeader h, DecLayer inl,
                                                                        const DecLayer* __restrict__ tab) {
 #if defined(__HIP_DEVICE_COMPILE__)  // LDS-DMA and buffer-descriptor code: device pass only
   using C = StreamCfg<T, XW>;
@@ -1064,15 +1077,22 @@ __device__ inline void write_outputs_f4(const DecLayer& L, const DecHeader& h, i
         Pim[m][c] = (float)ii;
       }
     }
+    // explicit fused multiply-adds in a fixed order: every inlined copy of
+    // this epilogue rounds alike, so y does not depend on which wave or ring
+    // slot finishes the item
     const float su_re = sc[0][t][0], su_im = sc[0][t][1];
     const float sw_re = sc[1][t][0], sw_im = sc[1][t][1];
-    yr += su_re * Pre[0][0] - su_im * Pim[0][1];
-    yi += su_re * Pre[0][1] + su_im * Pim[0][0];
-    yr += sw_re * Pre[1][0] + sw_im * Pim[1][1];
-    yi += -sw_re * Pre[1][1] + sw_im * Pim[1][0];
+    yr = fmaf(su_re, Pre[0][0], yr);
+    yr = fmaf(-su_im, Pim[0][1], yr);
+    yr = fmaf(sw_re, Pre[1][0], yr);
+    yr = fmaf(sw_im, Pim[1][1], yr);
+    yi = fmaf(su_re, Pre[0][1], yi);
+    yi = fmaf(su_im, Pim[0][0], yi);
+    yi = fmaf(-sw_re, Pre[1][1], yi);
+    yi = fmaf(sw_im, Pim[1][0], yi);
   }
   const float f = b ? run[1] : run[0];
-  const float2 v = make_float2(yr * f, yi * f);
+  const float2 v = make_float2(__fmul_rn(yr, f), __fmul_rn(yi, f));
   if (L.nkc == 1)
     buf_store8(L.y, (uint32_t)h.B * L.N * 8, (uint32_t)((b * L.N + row) * 8), v);
   else
@@ -1080,32 +1100,110 @@ __device__ inline void write_outputs_f4(const DecLayer& L, const DecHeader& h, i
 }
 
 constexpr int f4_ring_slots(int T) { return ring_slots(T); }
+// one block per CU: the waves that share a SIMD are served in age order, so
+// a static split of the items across them leaves the youngest wave of each
+// SIMD working long after the oldest has finished.  The block's waves
+// therefore claim their items one at a time from a counter in LDS.  Three
+// waves per SIMD for T <= 2; two for T >= 3, whose accumulators and ring need
+// more than 168 registers.
+constexpr int f4_waves(int T) { return T <= 2 ? 12 : 8; }
+
+// Items the load cursor has entered and the output cursor has not reached
+// (the load side runs at most NS - 1 <= 3 steps ahead, an item has >= 1 step),
+// as offsets from the block's first item.
+struct ItemQueue {
+  int q0, q1, q2, q3;
+  int n;
+  __device__ void push(int v) {
+    if (n == 0) q0 = v;
+    else if (n == 1) q1 = v;
+    else if (n == 2) q2 = v;
+    else q3 = v;
+    ++n;
+  }
+  __device__ int pop() {
+    const int v = q0;
+    q0 = q1;
+    q1 = q2;
+    q2 = q3;
+    --n;
+    return v;
+  }
+};
+
+// Offset of this wave's next item in its block's range of n items, or -1:
+// lane 0 takes a ticket from the block's LDS counter.  Written as one asm
+// block so that the compiler adds no wait for the loads still in flight into
+// the LDS ring.
+__device__ inline int claim_item(uint32_t ctr_addr, int n, int lane) {
+  int off = 0;
+  if (lane == 0) {
+    __asm__ volatile("ds_add_rtn_u32 %0, %1, %2\n\ts_waitcnt lgkmcnt(0)"
+                     : "=v"(off)
+                     : "v"(ctr_addr), "v"(1)
+                     : "memory");
+  }
+  off = uniform(off);
+  return off < n ? off : -1;
+}
+
+// Move a cursor to `item` (>= its current item) of the layer table.
+template <int T>
+__device__ inline void load_goto(LoadCursor<T>& c, int64_t item, const DecLayer* tab, const DecHeader& h,
+                                 int lane) {
+  while (item >= c.G.lend) {
+    ++c.lidx;
+    load_enter_layer(c, load_layer(tab + c.lidx), h);
+  }
+  c.item = item;
+  split_item(item, c.G, c.rb, c.kc);
+  load_item(c, h, lane);
+}
+
+__device__ inline void out_goto(OutCursor& c, int64_t item, const DecLayer* tab, int li) {
+  while (item >= c.G.lend) {
+    ++c.lidx;
+    out_enter_layer(c, load_layer(tab + c.lidx));
+  }
+  c.item = item;
+  split_item(item, c.G, c.rb, c.kc);
+  out_item(c, li);
+}
 
 template <int T, int XW>
-__global__ __launch_bounds__(64 * kStreamWaves) void dec_stream_f4_kernel(DecHeader h, DecLayer inl,
-                                                                          const DecLayer* __restrict__ tab) {
+using F4Cfg = StreamCfg<T, XW, f4_ring_slots(T), f4_waves(T)>;
+
+template <int T, int XW>
+__global__ __launch_bounds__((64 * F4Cfg<T, XW>::WAVES)) void dec_stream_f4_kernel(DecHeader h, DecLayer inl,
+                                                                                  const DecLayer* __restrict__ tab) {
 #if defined(__HIP_DEVICE_COMPILE__)  // LDS-DMA and buffer-descriptor code: device pass only
-  using C = StreamCfg<T, XW, f4_ring_slots(T)>;
+  using C = F4Cfg<T, XW>;
   constexpr int P = C::P, NS = C::NS, XSLOT = C::XSLOT;
   constexpr int WAVES = C::WAVES;
+  static_assert(NS <= 4, "the item queue holds the items of up to NS - 1 steps ahead");
   __shared__ __attribute__((aligned(16))) uint8_t ring[WAVES][NS][XSLOT];
   __shared__ __attribute__((aligned(16))) uint8_t zero16[16];
+  __shared__ uint32_t claim_ctr;
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4, li = lane & 15;
   const int wave = uniform(threadIdx.x >> 6);
   if (threadIdx.x < 4) reinterpret_cast<uint32_t*>(zero16)[threadIdx.x] = 0u;
+  if (threadIdx.x == 0) claim_ctr = (uint32_t)WAVES;  // wave w starts with item b0 + w
   __syncthreads();
-  const int64_t wid = (int64_t)blockIdx.x * WAVES + wave;
-  const int64_t W = (int64_t)gridDim.x * WAVES;
-  const int64_t i0 = uniform64(wid * h.total_items / W);
-  const int64_t i1 = uniform64((wid + 1) * h.total_items / W);
-  if (i0 >= i1) return;
+  // the block's items: an equal share of the call's
+  const int64_t b0 = uniform64((int64_t)blockIdx.x * h.total_items / gridDim.x);
+  const int nb = uniform((int)(uniform64(((int64_t)blockIdx.x + 1) * h.total_items / gridDim.x) - b0));
+  if (wave >= nb) return;
+  const int64_t i0 = b0 + wave;
+  const uint32_t ctr_addr = lds_addr(&claim_ctr);
 
   int b_, digit_, comp_;
   const bool xvalid = col_token<kModeBf16F4>(0, li, h.B, b_, digit_, comp_);
 
   LoadCursor<T> lc;
   OutCursor oc;
+  ItemQueue iq;
+  iq.n = 0;
   {
     const int lidx = tab ? find_layer(tab, h.n_layers, i0) : 0;
     const DecLayer L0 = tab ? load_layer(tab + lidx) : inl;
@@ -1120,12 +1218,34 @@ __global__ __launch_bounds__(64 * kStreamWaves) void dec_stream_f4_kernel(DecHea
   load_item(lc, h, lane);
   out_item(oc, li);
 
+  // next step of the load side: the next step of its item, else a claimed
+  // item (queued for the output side); false once the block's items are gone
+  auto load_advance = [&]() -> bool {
+    if (++lc.j < lc.nsteps) {
+      ++lc.k4;
+      lc.voff += lc.vstep;
+      lc.xoff += 256 * h.nc;
+      return true;
+    }
+    const int off = claim_item(ctr_addr, nb, lane);
+    if (off < 0) return false;
+    load_goto(lc, b0 + off, tab, h, lane);
+    iq.push(off);
+    return true;
+  };
+  auto out_advance = [&]() -> bool {
+    if (++oc.j < oc.nsteps) return true;
+    if (iq.n == 0) return false;
+    out_goto(oc, b0 + iq.pop(), tab, li);
+    return true;
+  };
+
   v4i cq[NS][P];
   bool live = true;
 #pragma unroll
   for (int k = 0; k < NS - 1; ++k) {
     stream_issue<XW, T, 32>(lc, live, lane, cq[k], &ring[wave][k][0]);
-    if (live) live = load_next(lc, tab, h, i1, lane);
+    if (live) live = load_advance();
   }
 
   v4f aS[P], aI[P];
@@ -1136,7 +1256,7 @@ __global__ __launch_bounds__(64 * kStreamWaves) void dec_stream_f4_kernel(DecHea
     constexpr int K = decltype(kconst)::value;
     constexpr int KN = (K + NS - 1) % NS;
     stream_issue<XW, T, 32>(lc, live, lane, cq[KN], &ring[wave][KN][0]);
-    if (live) live = load_next(lc, tab, h, i1, lane);
+    if (live) live = load_advance();
     __builtin_amdgcn_s_waitcnt(C::WAITCNT);
     v4i xr[4];
     {
@@ -1164,7 +1284,7 @@ __global__ __launch_bounds__(64 * kStreamWaves) void dec_stream_f4_kernel(DecHea
 #pragma unroll
       for (int p = 0; p < P; ++p) aS[p] = aI[p] = v4f{0.f, 0.f, 0.f, 0.f};
     }
-    return !out_next(oc, tab, i1, li);
+    return !out_advance();
   };
 
   static_assert(NS >= 2 && NS <= 6, "the ring loop below is unrolled for 2..6 slots");
@@ -1245,9 +1365,10 @@ template <int MODE, int T, int XW>
 void launch_stream(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, int64_t want_blocks,
                    hipStream_t s) {
   auto k = dec_stream_kernel<MODE, T, XW>;
-  constexpr int threads = 64 * kStreamWaves;
+  constexpr int waves = StreamCfg<T, XW>::WAVES;
+  constexpr int threads = 64 * waves;
   static const int resident = resident_blocks(reinterpret_cast<const void*>(k), threads);
-  const int64_t want = (h.total_items + kStreamWaves - 1) / kStreamWaves;
+  const int64_t want = (h.total_items + waves - 1) / waves;
   const int64_t blocks = want < resident ? want : resident;
   (void)want_blocks;
   hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(threads), 0, s, h, inl, tab);
@@ -1256,9 +1377,10 @@ void launch_stream(const DecHeader& h, const DecLayer& inl, const DecLayer* tab,
 template <int T, int XW>
 void launch_stream_f4(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
   auto k = dec_stream_f4_kernel<T, XW>;
-  constexpr int threads = 64 * kStreamWaves;
+  constexpr int waves = F4Cfg<T, XW>::WAVES;
+  constexpr int threads = 64 * waves;
   static const int resident = resident_blocks(reinterpret_cast<const void*>(k), threads);
-  const int64_t want = (h.total_items + kStreamWaves - 1) / kStreamWaves;
+  const int64_t want = (h.total_items + waves - 1) / waves;
   const int64_t blocks = want < resident ? want : resident;
   hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(threads), 0, s, h, inl, tab);
 }
