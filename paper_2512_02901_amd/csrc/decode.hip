@@ -1042,15 +1042,14 @@ constexpr int kFmtFp4 = 4;  // e2m1
 // groups pass theirs to the even group below, which forms the token's
 // integer products and applies the axis scales and the token factor in
 // float32.
+// The layer's axis scales sc[m][t][axis] and token factors xf[b] are the
+// caller's (loaded once per layer).
 template <int T>
 __device__ inline void write_outputs_f4(const DecLayer& L, const DecHeader& h, int kc, int row, bool row_ok,
-                                        int lane, const v4f (&aS)[2 * T], const v4f (&aI)[2 * T]) {
+                                        int lane, const v4f (&aS)[2 * T], const v4f (&aI)[2 * T],
+                                        const float (&sc)[2][T][2], const float (&xf)[2]) {
   constexpr int P = 2 * T;
   const int g = lane >> 4;
-  float sc[2][T][2];
-  sload_scales<T>(L.scales[0], L.scales[1], sc);
-  float run[2];
-  sload_run<2>(L.xs, run);
   int vS[P][2], vI[P][2], hS[P][2], hI[P][2];
 #pragma unroll
   for (int p = 0; p < P; ++p)
@@ -1091,7 +1090,7 @@ __device__ inline void write_outputs_f4(const DecLayer& L, const DecHeader& h, i
     yi = fmaf(-sw_re, Pre[1][1], yi);
     yi = fmaf(sw_im, Pim[1][0], yi);
   }
-  const float f = b ? run[1] : run[0];
+  const float f = b ? xf[1] : xf[0];
   const float2 v = make_float2(__fmul_rn(yr, f), __fmul_rn(yi, f));
   if (L.nkc == 1)
     buf_store8(L.y, (uint32_t)h.B * L.N * 8, (uint32_t)((b * L.N + row) * 8), v);
@@ -1160,14 +1159,18 @@ __device__ inline void load_goto(LoadCursor<T>& c, int64_t item, const DecLayer*
   load_item(c, h, lane);
 }
 
-__device__ inline void out_goto(OutCursor& c, int64_t item, const DecLayer* tab, int li) {
+// Returns whether the cursor entered another layer.
+__device__ inline bool out_goto(OutCursor& c, int64_t item, const DecLayer* tab, int li) {
+  bool moved = false;
   while (item >= c.G.lend) {
     ++c.lidx;
     out_enter_layer(c, load_layer(tab + c.lidx));
+    moved = true;
   }
   c.item = item;
   split_item(item, c.G, c.rb, c.kc);
   out_item(c, li);
+  return moved;
 }
 
 template <int T, int XW>
@@ -1217,6 +1220,13 @@ __global__ __launch_bounds__((64 * F4Cfg<T, XW>::WAVES)) void dec_stream_f4_kern
   }
   load_item(lc, h, lane);
   out_item(oc, li);
+  // the epilogue's per-layer constants, reloaded when the output side changes layer
+  float esc[2][T][2], exf[2];
+  auto load_epilogue_consts = [&]() {
+    sload_scales<T>(uniform_ptr(oc.scales[0]), uniform_ptr(oc.scales[1]), esc);
+    sload_run<2>(uniform_ptr(oc.xs), exf);
+  };
+  load_epilogue_consts();
 
   // next step of the load side: the next step of its item, else a claimed
   // item (queued for the output side); false once the block's items are gone
@@ -1236,7 +1246,7 @@ __global__ __launch_bounds__((64 * F4Cfg<T, XW>::WAVES)) void dec_stream_f4_kern
   auto out_advance = [&]() -> bool {
     if (++oc.j < oc.nsteps) return true;
     if (iq.n == 0) return false;
-    out_goto(oc, b0 + iq.pop(), tab, li);
+    if (out_goto(oc, b0 + iq.pop(), tab, li)) load_epilogue_consts();
     return true;
   };
 
@@ -1280,7 +1290,7 @@ __global__ __launch_bounds__((64 * F4Cfg<T, XW>::WAVES)) void dec_stream_f4_kern
       }
     }
     if (oc.j == oc.nsteps - 1) {
-      write_outputs_f4<T>(out_layer(oc), h, oc.kc, oc.row, oc.row_ok, lane, aS, aI);
+      write_outputs_f4<T>(out_layer(oc), h, oc.kc, oc.row, oc.row_ok, lane, aS, aI, esc, exf);
 #pragma unroll
       for (int p = 0; p < P; ++p) aS[p] = aI[p] = v4f{0.f, 0.f, 0.f, 0.f};
     }
