@@ -346,15 +346,17 @@ def main():
         result["stack_tiled_int8"] = {"ms_per_step": round(ms_t, 4), "GBs": round(packed / (ms_t * 1e-3) / 1e9, 1),
                                       "product_us": round(prod_t * 1e3, 1)}
         del grp_tiled
-        # two tokens per layer on the fp4 path
-        ms2, _, prod2, _ = batch_stack_fp4(f2, torch, dev, T, layers, 2, args.steps, args.warmup)
-        result["stack_B2"] = {"ms_per_step": round(ms2, 4), "GBs": round(packed / (ms2 * 1e-3) / 1e9, 1),
-                              "product_us": round(prod2 * 1e3, 1)}
-        # batches of 4 and 16 tokens per layer over the same codes (int8 path, tiled copies)
-        for Bb in (4, 16):
-            msb, _, prodb, _ = batch_stack(f2, torch, dev, T, Bb, max(10, args.steps // 2), args.warmup)
+        # two and four tokens per layer on the fp4 path (one and two activation tiles)
+        for Bb in (2, 4):
+            msb, _, prodb, _ = batch_stack_fp4(f2, torch, dev, T, layers, Bb, args.steps, args.warmup)
             result[f"stack_B{Bb}"] = {"ms_per_step": round(msb, 4), "GBs": round(packed / (msb * 1e-3) / 1e9, 1),
                                       "product_us": round(prodb * 1e3, 1)}
+        # 4 and 16 tokens per layer on the int8 matrix cores (tiled copies)
+        for Bb in (4, 16):
+            msb, _, prodb, _ = batch_stack(f2, torch, dev, T, Bb, max(10, args.steps // 2), args.warmup)
+            result[f"stack_B{Bb}_int8"] = {"ms_per_step": round(msb, 4),
+                                           "GBs": round(packed / (msb * 1e-3) / 1e9, 1),
+                                           "product_us": round(prodb * 1e3, 1)}
         # the same stack decoded straight from the canonical D3 codes
         grp_d3 = f2.WlGroup(layers, T=T, B=1)
         ms_d3, _, prod_d3, _ = time_group(grp_d3, torch, args.steps, args.warmup)

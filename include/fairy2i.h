@@ -235,7 +235,7 @@ typedef struct fairy2i_wl_layer {
  * every K a multiple of 64, reserved == 0.  Each layer's codes are in the
  * layout its `layout` field names (same layout for U and W).  With
  * FAIRY2I_LAYOUT_TILED_FP4 every layer of the group must use it, with dtype
- * FAIRY2I_ACT_BF16 and B <= 2; the product then runs on the fp8 x fp4
+ * FAIRY2I_ACT_BF16 and B <= 2 (B <= 4 for T <= 3); the product then runs on the fp8 x fp4
  * matrix cores, each token taken as a 15-bit block fixed point
  * X = rint(x * 2^E) with 2^14 <= max |X| < 2^15 (every bf16 value within a
  * factor 2^7 of the token's largest magnitude exactly, smaller ones rounded

@@ -697,6 +697,7 @@ struct LoadCursor {
   const uint8_t* pbase[2 * T];  // code plane (M, t) of the current layer
   const int8_t* xf;             // the layer's activation operand
   uint32_t plane_bytes, xbytes;
+  uint32_t xtile;  // bytes of one activation tile's operand
   uint32_t voff;   // this lane's offset in every code plane at step k4 (row, 16-code group)
   uint32_t vstep;  // voff advance per step: 64 (D3) or T * 1024 (tiled)
   uint32_t xoff;   // offset of the step's activation operand + lane * 16
@@ -748,16 +749,18 @@ __device__ inline void load_enter_layer(LoadCursor<T>& c, const DecLayer& L, con
     c.vstep = 64u;
   }
   c.xf = L.xf;
-  c.xbytes = (uint32_t)(L.nk4 * 256 * h.nc);
+  c.xtile = (uint32_t)(L.nk4 * 256 * h.nc);
+  c.xbytes = (uint32_t)h.ntile * c.xtile;
 }
 
 // Issue the loads of the cursor's step: its 2T x 16 code bytes per lane into
-// registers cq, and its activation operand (XW KiB) into the LDS slot xslot.
+// registers cq, and its activation operand (XW KiB for each of NT tiles) into
+// the LDS slot xslot.
 // A dead cursor issues them out of range (they return zeros), so every step
 // issues the same number of loads.  Lane group g's first code of the step is
 // code 64 g (D3 and tiled layouts) or 32 g (fp4 tiled layout, G0 = 32); a
 // group whose codes all lie past K loads zeros.
-template <int XW, int T, int G0 = 64>
+template <int XW, int T, int G0 = 64, int NT = 1>
 __device__ inline void stream_issue(const LoadCursor<T>& c, bool live, int lane, v4i (&cq)[2 * T],
                                     uint8_t* xslot) {
   const int g = lane >> 4;
@@ -770,13 +773,14 @@ __device__ inline void stream_issue(const LoadCursor<T>& c, bool live, int lane,
   for (int p = 0; p < 2 * T; ++p)
     cq[p] = __builtin_amdgcn_raw_buffer_load_b128(make_rsrc(uniform_ptr(c.pbase[p]), (uint32_t)pb), off, 0,
                                                   kNonTemporal);
-  const uint32_t xo = live ? c.xoff : kOob;
   const int xb = __builtin_amdgcn_readfirstlane((int)c.xbytes);
   const int8_t* xf = uniform_ptr(c.xf);
 #pragma unroll
-  for (int i = 0; i < XW; ++i)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(xf, (uint32_t)xb), (lds_ptr_t)(xslot + i * 1024), 16,
-                                             xo + i * 1024, 0, 0, 0);
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int i = 0; i < XW; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(xf, (uint32_t)xb), (lds_ptr_t)(xslot + (t * XW + i) * 1024),
+                                               16, live ? c.xoff + t * c.xtile + i * 1024 : kOob, 0, 0, 0);
 }
 
 // LDS address (byte offset) of a pointer into shared memory.
@@ -1046,7 +1050,7 @@ constexpr int kFmtFp4 = 4;  // e2m1
 // caller's (loaded once per layer).
 template <int T>
 __device__ inline void write_outputs_f4(const DecLayer& L, const DecHeader& h, int kc, int row, bool row_ok,
-                                        int lane, const v4f (&aS)[2 * T], const v4f (&aI)[2 * T],
+                                        int lane, int tile, const v4f (&aS)[2 * T], const v4f (&aI)[2 * T],
                                         const float (&sc)[2][T][2], const float (&xf)[2]) {
   constexpr int P = 2 * T;
   const int g = lane >> 4;
@@ -1060,7 +1064,7 @@ __device__ inline void write_outputs_f4(const DecLayer& L, const DecHeader& h, i
       hS[p][c] = __shfl_down(vS[p][c], 16);
       hI[p][c] = __shfl_down(vI[p][c], 16);
     }
-  const int b = g >> 1;
+  const int b = 2 * tile + (g >> 1);
   if ((g & 1) || !row_ok || b >= h.B) return;
   float yr = 0.0f, yi = 0.0f;
 #pragma unroll
@@ -1090,7 +1094,7 @@ __device__ inline void write_outputs_f4(const DecLayer& L, const DecHeader& h, i
     yi = fmaf(-sw_re, Pre[1][1], yi);
     yi = fmaf(sw_im, Pim[1][0], yi);
   }
-  const float f = b ? xf[1] : xf[0];
+  const float f = (g >> 1) ? xf[1] : xf[0];
   const float2 v = make_float2(__fmul_rn(yr, f), __fmul_rn(yi, f));
   if (L.nkc == 1)
     buf_store8(L.y, (uint32_t)h.B * L.N * 8, (uint32_t)((b * L.N + row) * 8), v);
@@ -1176,11 +1180,12 @@ __device__ inline bool out_goto(OutCursor& c, int64_t item, const DecLayer* tab,
 template <int T, int XW>
 using F4Cfg = StreamCfg<T, XW, f4_ring_slots(T), f4_waves(T)>;
 
-template <int T, int XW>
-__global__ __launch_bounds__((64 * F4Cfg<T, XW>::WAVES)) void dec_stream_f4_kernel(DecHeader h, DecLayer inl,
-                                                                                  const DecLayer* __restrict__ tab) {
+// NT activation tiles (2 tokens each); a ring slot holds XW KiB per tile.
+template <int T, int XW, int NT>
+__global__ __launch_bounds__((64 * F4Cfg<T, NT * XW>::WAVES)) void dec_stream_f4_kernel(DecHeader h, DecLayer inl,
+                                                                                       const DecLayer* __restrict__ tab) {
 #if defined(__HIP_DEVICE_COMPILE__)  // LDS-DMA and buffer-descriptor code: device pass only
-  using C = F4Cfg<T, XW>;
+  using C = F4Cfg<T, NT * XW>;
   constexpr int P = C::P, NS = C::NS, XSLOT = C::XSLOT;
   constexpr int WAVES = C::WAVES;
   static_assert(NS <= 4, "the item queue holds the items of up to NS - 1 steps ahead");
@@ -1200,8 +1205,12 @@ __global__ __launch_bounds__((64 * F4Cfg<T, XW>::WAVES)) void dec_stream_f4_kern
   const int64_t i0 = b0 + wave;
   const uint32_t ctr_addr = lds_addr(&claim_ctr);
 
-  int b_, digit_, comp_;
-  const bool xvalid = col_token<kModeBf16F4>(0, li, h.B, b_, digit_, comp_);
+  bool xvalid[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    int b_, digit_, comp_;
+    xvalid[t] = col_token<kModeBf16F4>(t, li, h.B, b_, digit_, comp_);
+  }
 
   LoadCursor<T> lc;
   OutCursor oc;
@@ -1221,10 +1230,12 @@ __global__ __launch_bounds__((64 * F4Cfg<T, XW>::WAVES)) void dec_stream_f4_kern
   load_item(lc, h, lane);
   out_item(oc, li);
   // the epilogue's per-layer constants, reloaded when the output side changes layer
-  float esc[2][T][2], exf[2];
+  float esc[2][T][2], exf[NT][2];
   auto load_epilogue_consts = [&]() {
     sload_scales<T>(uniform_ptr(oc.scales[0]), uniform_ptr(oc.scales[1]), esc);
-    sload_run<2>(uniform_ptr(oc.xs), exf);
+    // the factor array is padded to 256 bytes: both floats of every tile are inside it
+#pragma unroll
+    for (int t = 0; t < NT; ++t) sload_run<2>(uniform_ptr(oc.xs) + 2 * t, exf[t]);
   };
   load_epilogue_consts();
 
@@ -1254,45 +1265,56 @@ __global__ __launch_bounds__((64 * F4Cfg<T, XW>::WAVES)) void dec_stream_f4_kern
   bool live = true;
 #pragma unroll
   for (int k = 0; k < NS - 1; ++k) {
-    stream_issue<XW, T, 32>(lc, live, lane, cq[k], &ring[wave][k][0]);
+    stream_issue<XW, T, 32, NT>(lc, live, lane, cq[k], &ring[wave][k][0]);
     if (live) live = load_advance();
   }
 
-  v4f aS[P], aI[P];
+  v4f aS[NT][P], aI[NT][P];
 #pragma unroll
-  for (int p = 0; p < P; ++p) aS[p] = aI[p] = v4f{0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int p = 0; p < P; ++p) aS[t][p] = aI[t][p] = v4f{0.f, 0.f, 0.f, 0.f};
 
   auto step = [&](auto kconst) -> bool {
     constexpr int K = decltype(kconst)::value;
     constexpr int KN = (K + NS - 1) % NS;
-    stream_issue<XW, T, 32>(lc, live, lane, cq[KN], &ring[wave][KN][0]);
+    stream_issue<XW, T, 32, NT>(lc, live, lane, cq[KN], &ring[wave][KN][0]);
     if (live) live = load_advance();
     __builtin_amdgcn_s_waitcnt(C::WAITCNT);
-    v4i xr[4];
-    {
-      const uint32_t xa = xvalid ? lds_addr(&ring[wave][K][0]) + (uint32_t)((g * h.nc + li) * 16) : lds_addr(zero16);
-      const uint32_t xs = xvalid ? (uint32_t)(4 * h.nc * 16) : 0u;
-      lds_read4(xa, xa + xs, xa + 2 * xs, xa + 3 * xs, xr);
+    v4i xr[NT][4];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const uint32_t xa = xvalid[t] ? lds_addr(&ring[wave][K][t * XW * 1024]) + (uint32_t)((g * h.nc + li) * 16)
+                                    : lds_addr(zero16);
+      const uint32_t xs = xvalid[t] ? (uint32_t)(4 * h.nc * 16) : 0u;
+      lds_read4(xa, xa + xs, xa + 2 * xs, xa + 3 * xs, xr[t]);
     }
     const v4i* cr = cq[K];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
-      const v4i x0 = xr[2 * kb], x1 = xr[2 * kb + 1];
-      const v8i a = v8i{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
 #pragma unroll
       for (int p = 0; p < P; ++p) {
         v8i bs, bi;
         expand_f4((uint32_t)cr[p][2 * kb], (uint32_t)cr[p][2 * kb + 1], bs, bi);
-        aS[p] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bs, aS[p], kFmtFp8, kFmtFp4, 0, 0, 0, 0);
-        aI[p] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bi, aI[p], kFmtFp8, kFmtFp4, 0, 0, 0, 0);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          const v4i x0 = xr[t][2 * kb], x1 = xr[t][2 * kb + 1];
+          const v8i a = v8i{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+          aS[t][p] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bs, aS[t][p], kFmtFp8, kFmtFp4, 0, 0, 0, 0);
+          aI[t][p] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bi, aI[t][p], kFmtFp8, kFmtFp4, 0, 0, 0, 0);
+        }
         __builtin_amdgcn_sched_group_barrier(0x002, 10, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2 * NT, 0);
       }
     }
     if (oc.j == oc.nsteps - 1) {
-      write_outputs_f4<T>(out_layer(oc), h, oc.kc, oc.row, oc.row_ok, lane, aS, aI, esc, exf);
+      const DecLayer Lo = out_layer(oc);
 #pragma unroll
-      for (int p = 0; p < P; ++p) aS[p] = aI[p] = v4f{0.f, 0.f, 0.f, 0.f};
+      for (int t = 0; t < NT; ++t) {
+        write_outputs_f4<T>(Lo, h, oc.kc, oc.row, oc.row_ok, lane, t, aS[t], aI[t], esc, exf[t]);
+#pragma unroll
+        for (int p = 0; p < P; ++p) aS[t][p] = aI[t][p] = v4f{0.f, 0.f, 0.f, 0.f};
+      }
     }
     return !out_advance();
   };
@@ -1384,10 +1406,10 @@ void launch_stream(const DecHeader& h, const DecLayer& inl, const DecLayer* tab,
   hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(threads), 0, s, h, inl, tab);
 }
 
-template <int T, int XW>
+template <int T, int XW, int NT>
 void launch_stream_f4(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
-  auto k = dec_stream_f4_kernel<T, XW>;
-  constexpr int waves = F4Cfg<T, XW>::WAVES;
+  auto k = dec_stream_f4_kernel<T, XW, NT>;
+  constexpr int waves = F4Cfg<T, NT * XW>::WAVES;
   constexpr int threads = 64 * waves;
   static const int resident = resident_blocks(reinterpret_cast<const void*>(k), threads);
   const int64_t want = (h.total_items + waves - 1) / waves;
@@ -1397,8 +1419,9 @@ void launch_stream_f4(const DecHeader& h, const DecLayer& inl, const DecLayer* t
 
 template <int T>
 void launch_stream_f4_t(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
-  if (h.nc <= 8) launch_stream_f4<T, 2>(h, inl, tab, s);   // one token: 8 columns, 2 KB per step
-  else launch_stream_f4<T, 4>(h, inl, tab, s);
+  if (h.ntile >= 2) launch_stream_f4<T, 4, 2>(h, inl, tab, s);  // 3-4 tokens: two tiles
+  else if (h.nc <= 8) launch_stream_f4<T, 2, 1>(h, inl, tab, s);  // one token: 8 columns, 2 KB per step
+  else launch_stream_f4<T, 4, 1>(h, inl, tab, s);
 }
 
 template <int MODE, int T>
@@ -1453,7 +1476,7 @@ hipError_t launch_decode(const DecHeader& h, const DecLayer& inl, const DecLayer
   // 2. products
   const int64_t blocks = (h.total_items + 3) / 4;  // capped at what fits on the device
   if (h.mode == kModeBf16F4) {
-    // one activation tile (B <= 2), codes in the fp4 tiled layout: checked by the host code
+    // one or two activation tiles (B <= 4), codes in the fp4 tiled layout: checked by the host code
     switch (h.T) {
       case 1: launch_stream_f4_t<1>(h, inl, tab, s); break;
       case 2: launch_stream_f4_t<2>(h, inl, tab, s); break;

@@ -124,10 +124,11 @@ def run_fp4_group(layers, T, B, gpu, x_of):
 @pytest.mark.parametrize("T", [1, 2, 3, 4])
 def test_group_fp4_matches_oracle(gpu, T):
     """One grouped fp4 call over layers of several shapes (ragged row blocks,
-    K with a partial 256-code step, one row), 1 and 2 tokens, against the
-    oracle; a repeated call is bitwise identical."""
+    K with a partial 256-code step, one row), 1 to 4 tokens (one or two
+    activation tiles), against the oracle; a repeated call is bitwise
+    identical."""
     layers = [(N, K, *quantized_layer(N, K, T, (40, i, N))) for i, (N, K) in enumerate(SHAPES)]
-    for B in (1, 2):
+    for B in ((1, 2, 3, 4) if T <= 3 else (1, 2)):   # B > 2: two activation tiles (T <= 3)
         ys, refs, grp = run_fp4_group(layers, T, B, gpu,
                                       lambda i, N, K: synth.bf16_round_complex(synth.activations(B, K, (41, i, B))))
         first = [host(y).copy() for y in ys]
@@ -156,7 +157,7 @@ def test_group_fp4_exact_for_representable_tokens(gpu):
     import paper_2512_02901_amd as f2
     T = 2
     layers = [(N, K, *quantized_layer(N, K, T, (42, i, N))) for i, (N, K) in enumerate(SHAPES)]
-    for B in (1, 2):
+    for B in (1, 2, 3, 4):
         xs = {}
 
         def x_of(i, N, K):
