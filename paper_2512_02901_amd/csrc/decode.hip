@@ -481,6 +481,9 @@ __device__ inline float token_factor(const float (&xsv)[8], int g, int s) {
 template <int MODE, int T, int NTG, bool EXPORT>
 __device__ inline void write_outputs(const DecLayer& L, const DecHeader& h, const PassGeo& q, int lane,
                                      const v4i (&acc)[2 * T][2][NTG]) {
+  // no fused multiply-adds: every inlined copy rounds alike, so y does not
+  // depend on which wave or ring slot finishes an item
+#pragma clang fp contract(off)
   constexpr int P = 2 * T;
   const int g = lane >> 4;
   const int N = L.N;
@@ -801,28 +804,6 @@ __device__ inline void lds_read4(uint32_t a0, uint32_t a1, uint32_t a2, uint32_t
       : "memory");
 }
 
-// Next step of the load side; false once the wave's items are exhausted.
-template <int T>
-__device__ inline bool load_next(LoadCursor<T>& c, const DecLayer* tab, const DecHeader& h, int64_t iend,
-                                 int lane) {
-  if (++c.j < c.nsteps) {
-    ++c.k4;
-    c.voff += c.vstep;
-    c.xoff += 256 * h.nc;
-    return true;
-  }
-  if (++c.item >= iend) return false;
-  if (c.item >= c.G.lend) {
-    ++c.lidx;
-    load_enter_layer(c, load_layer(tab + c.lidx), h);
-    c.rb = c.kc = 0;
-  } else {
-    advance_item(c.rb, c.kc, c.G.nkc);
-  }
-  load_item(c, h, lane);
-  return true;
-}
-
 // Compute side: which item the current step belongs to, and what its
 // epilogue writes.
 struct OutCursor {
@@ -852,20 +833,6 @@ __device__ inline void out_item(OutCursor& c, int li) {
   c.row_ok = c.row < c.G.N;
 }
 
-__device__ inline bool out_next(OutCursor& c, const DecLayer* tab, int64_t iend, int li) {
-  if (++c.j < c.nsteps) return true;
-  if (++c.item >= iend) return false;
-  if (c.item >= c.G.lend) {
-    ++c.lidx;
-    out_enter_layer(c, load_layer(tab + c.lidx));
-    c.rb = c.kc = 0;
-  } else {
-    advance_item(c.rb, c.kc, c.G.nkc);
-  }
-  out_item(c, li);
-  return true;
-}
-
 // The fields write_outputs reads, from the compute cursor.
 __device__ inline DecLayer out_layer(const OutCursor& c) {
   DecLayer L{};
@@ -879,6 +846,80 @@ __device__ inline DecLayer out_layer(const OutCursor& c) {
   return L;
 }
 
+// Items the load cursor has entered and the output cursor has not reached
+// (the load side runs at most NS - 1 <= 3 steps ahead, an item has >= 1 step),
+// as offsets from the block's first item.
+struct ItemQueue {
+  int q0, q1, q2, q3;
+  int n;
+  __device__ void push(int v) {
+    if (n == 0) q0 = v;
+    else if (n == 1) q1 = v;
+    else if (n == 2) q2 = v;
+    else q3 = v;
+    ++n;
+  }
+  __device__ int pop() {
+    const int v = q0;
+    q0 = q1;
+    q1 = q2;
+    q2 = q3;
+    --n;
+    return v;
+  }
+};
+
+// Offset of this wave's next item in its block's range of n items, or -1:
+// lane 0 takes a ticket from the block's LDS counter.  Written as one asm
+// block so that the compiler adds no wait for the loads still in flight into
+// the LDS ring.
+__device__ inline int claim_item(uint32_t ctr_addr, int n, int lane) {
+  int off = 0;
+  if (lane == 0) {
+    __asm__ volatile("ds_add_rtn_u32 %0, %1, %2\n\ts_waitcnt lgkmcnt(0)"
+                     : "=v"(off)
+                     : "v"(ctr_addr), "v"(1)
+                     : "memory");
+  }
+  off = uniform(off);
+  return off < n ? off : -1;
+}
+
+// Move a cursor to `item` (>= its current item) of the layer table.
+template <int T>
+__device__ inline void load_goto(LoadCursor<T>& c, int64_t item, const DecLayer* tab, const DecHeader& h,
+                                 int lane) {
+  while (item >= c.G.lend) {
+    ++c.lidx;
+    load_enter_layer(c, load_layer(tab + c.lidx), h);
+  }
+  c.item = item;
+  split_item(item, c.G, c.rb, c.kc);
+  load_item(c, h, lane);
+}
+
+// Returns whether the cursor entered another layer.
+__device__ inline bool out_goto(OutCursor& c, int64_t item, const DecLayer* tab, int li) {
+  bool moved = false;
+  while (item >= c.G.lend) {
+    ++c.lidx;
+    out_enter_layer(c, load_layer(tab + c.lidx));
+    moved = true;
+  }
+  c.item = item;
+  split_item(item, c.G, c.rb, c.kc);
+  out_item(c, li);
+  return moved;
+}
+
+// One block per CU for both streaming kernels: the waves that share a SIMD
+// are served in age order, so a static split of the items across them leaves
+// the youngest wave of each SIMD working long after the oldest has finished.
+// The block's waves therefore claim their items one at a time from a counter
+// in LDS.  Three waves per SIMD for T <= 2; two for T >= 3, whose
+// accumulators and ring need more than 168 registers.
+constexpr int block_waves(int T) { return T <= 2 ? 12 : 8; }
+
 // waves per block of the streaming kernel (fewer when the ring would not
 // fit the LDS)
 constexpr int kStreamWaves = 4;
@@ -891,7 +932,7 @@ constexpr int stream_waves(int NS, int XW, int base = kStreamWaves) {
 // ring depth: about 48 code registers per lane
 constexpr int ring_slots(int T) { return T <= 1 ? 4 : (T == 2 ? 3 : 2); }
 
-template <int T, int XW, int NSLOTS = ring_slots(T), int BASE_WAVES = kStreamWaves>
+template <int T, int XW, int NSLOTS = ring_slots(T), int BASE_WAVES = block_waves(T)>
 struct StreamCfg {
   static constexpr int P = 2 * T;
   static constexpr int XSLOT = XW * 1024;         // LDS bytes of a slot's activation operand
@@ -909,18 +950,22 @@ __global__ __launch_bounds__((64 * StreamCfg<T, XW>::WAVES)) void dec_stream_ker
   using C = StreamCfg<T, XW>;
   constexpr int P = C::P, NS = C::NS, XSLOT = C::XSLOT;
   constexpr int WAVES = C::WAVES;
+  static_assert(NS <= 4, "the item queue holds the items of up to NS - 1 steps ahead");
   __shared__ __attribute__((aligned(16))) uint8_t ring[WAVES][NS][XSLOT];
   __shared__ __attribute__((aligned(16))) uint8_t zero16[16];
+  __shared__ uint32_t claim_ctr;
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4, li = lane & 15;
   const int wave = uniform(threadIdx.x >> 6);
   if (threadIdx.x < 4) reinterpret_cast<uint32_t*>(zero16)[threadIdx.x] = 0u;
+  if (threadIdx.x == 0) claim_ctr = (uint32_t)WAVES;  // wave w starts with item b0 + w
   __syncthreads();
-  const int64_t wid = (int64_t)blockIdx.x * WAVES + wave;
-  const int64_t W = (int64_t)gridDim.x * WAVES;
-  const int64_t i0 = uniform64(wid * h.total_items / W);
-  const int64_t i1 = uniform64((wid + 1) * h.total_items / W);
-  if (i0 >= i1) return;
+  // the block's items: an equal share of the call's
+  const int64_t b0 = uniform64((int64_t)blockIdx.x * h.total_items / gridDim.x);
+  const int nb = uniform((int)(uniform64(((int64_t)blockIdx.x + 1) * h.total_items / gridDim.x) - b0));
+  if (wave >= nb) return;
+  const int64_t i0 = b0 + wave;
+  const uint32_t ctr_addr = lds_addr(&claim_ctr);
 
   // activation operand: this lane's 16 bytes within a slot (or a zero area)
   int b_, digit_, comp_;
@@ -928,6 +973,8 @@ __global__ __launch_bounds__((64 * StreamCfg<T, XW>::WAVES)) void dec_stream_ker
 
   LoadCursor<T> lc;
   OutCursor oc;
+  ItemQueue iq;
+  iq.n = 0;
   {
     const int lidx = tab ? find_layer(tab, h.n_layers, i0) : 0;
     const DecLayer L0 = tab ? load_layer(tab + lidx) : inl;
@@ -942,12 +989,33 @@ __global__ __launch_bounds__((64 * StreamCfg<T, XW>::WAVES)) void dec_stream_ker
   load_item(lc, h, lane);
   out_item(oc, li);
 
+  // as in the fp4 kernel: the load side claims items, the output side follows
+  auto load_advance = [&]() -> bool {
+    if (++lc.j < lc.nsteps) {
+      ++lc.k4;
+      lc.voff += lc.vstep;
+      lc.xoff += 256 * h.nc;
+      return true;
+    }
+    const int off = claim_item(ctr_addr, nb, lane);
+    if (off < 0) return false;
+    load_goto(lc, b0 + off, tab, h, lane);
+    iq.push(off);
+    return true;
+  };
+  auto out_advance = [&]() -> bool {
+    if (++oc.j < oc.nsteps) return true;
+    if (iq.n == 0) return false;
+    out_goto(oc, b0 + iq.pop(), tab, li);
+    return true;
+  };
+
   v4i cq[NS][P];  // code bytes of each ring slot
   bool live = true;
 #pragma unroll
   for (int k = 0; k < NS - 1; ++k) {
     stream_issue<XW>(lc, live, lane, cq[k], &ring[wave][k][0]);
-    if (live) live = load_next(lc, tab, h, i1, lane);
+    if (live) live = load_advance();
   }
 
   v4i acc[P][2][1];
@@ -959,7 +1027,7 @@ __global__ __launch_bounds__((64 * StreamCfg<T, XW>::WAVES)) void dec_stream_ker
     constexpr int KN = (K + NS - 1) % NS;  // the slot the previous step consumed
     // refill the slot the previous step consumed, then wait for this one
     stream_issue<XW>(lc, live, lane, cq[KN], &ring[wave][KN][0]);
-    if (live) live = load_next(lc, tab, h, i1, lane);
+    if (live) live = load_advance();
     __builtin_amdgcn_s_waitcnt(C::WAITCNT);  // this slot's loads have landed
     v4i xr[4];
     {
@@ -993,7 +1061,7 @@ __global__ __launch_bounds__((64 * StreamCfg<T, XW>::WAVES)) void dec_stream_ker
 #pragma unroll
       for (int p = 0; p < P; ++p) acc[p][0][0] = acc[p][1][0] = v4i{0, 0, 0, 0};
     }
-    return !out_next(oc, tab, i1, li);
+    return !out_advance();
   };
 
   // one pass of the loop body visits every slot once, in ring order
@@ -1103,82 +1171,10 @@ __device__ inline void write_outputs_f4(const DecLayer& L, const DecHeader& h, i
 }
 
 constexpr int f4_ring_slots(int T) { return ring_slots(T); }
-// one block per CU: the waves that share a SIMD are served in age order, so
-// a static split of the items across them leaves the youngest wave of each
-// SIMD working long after the oldest has finished.  The block's waves
-// therefore claim their items one at a time from a counter in LDS.  Three
-// waves per SIMD for T <= 2; two for T >= 3, whose accumulators and ring need
-// more than 168 registers.
-constexpr int f4_waves(int T) { return T <= 2 ? 12 : 8; }
 
-// Items the load cursor has entered and the output cursor has not reached
-// (the load side runs at most NS - 1 <= 3 steps ahead, an item has >= 1 step),
-// as offsets from the block's first item.
-struct ItemQueue {
-  int q0, q1, q2, q3;
-  int n;
-  __device__ void push(int v) {
-    if (n == 0) q0 = v;
-    else if (n == 1) q1 = v;
-    else if (n == 2) q2 = v;
-    else q3 = v;
-    ++n;
-  }
-  __device__ int pop() {
-    const int v = q0;
-    q0 = q1;
-    q1 = q2;
-    q2 = q3;
-    --n;
-    return v;
-  }
-};
-
-// Offset of this wave's next item in its block's range of n items, or -1:
-// lane 0 takes a ticket from the block's LDS counter.  Written as one asm
-// block so that the compiler adds no wait for the loads still in flight into
-// the LDS ring.
-__device__ inline int claim_item(uint32_t ctr_addr, int n, int lane) {
-  int off = 0;
-  if (lane == 0) {
-    __asm__ volatile("ds_add_rtn_u32 %0, %1, %2\n\ts_waitcnt lgkmcnt(0)"
-                     : "=v"(off)
-                     : "v"(ctr_addr), "v"(1)
-                     : "memory");
-  }
-  off = uniform(off);
-  return off < n ? off : -1;
-}
-
-// Move a cursor to `item` (>= its current item) of the layer table.
-template <int T>
-__device__ inline void load_goto(LoadCursor<T>& c, int64_t item, const DecLayer* tab, const DecHeader& h,
-                                 int lane) {
-  while (item >= c.G.lend) {
-    ++c.lidx;
-    load_enter_layer(c, load_layer(tab + c.lidx), h);
-  }
-  c.item = item;
-  split_item(item, c.G, c.rb, c.kc);
-  load_item(c, h, lane);
-}
-
-// Returns whether the cursor entered another layer.
-__device__ inline bool out_goto(OutCursor& c, int64_t item, const DecLayer* tab, int li) {
-  bool moved = false;
-  while (item >= c.G.lend) {
-    ++c.lidx;
-    out_enter_layer(c, load_layer(tab + c.lidx));
-    moved = true;
-  }
-  c.item = item;
-  split_item(item, c.G, c.rb, c.kc);
-  out_item(c, li);
-  return moved;
-}
 
 template <int T, int XW>
-using F4Cfg = StreamCfg<T, XW, f4_ring_slots(T), f4_waves(T)>;
+using F4Cfg = StreamCfg<T, XW, f4_ring_slots(T), block_waves(T)>;
 
 // NT activation tiles (2 tokens each); a ring slot holds XW KiB per tile.
 template <int T, int XW, int NT>
