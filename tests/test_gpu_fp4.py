@@ -208,3 +208,31 @@ def test_group_fp4_edge_tokens(gpu):
             assert err <= 1e-3
         else:
             assert err <= TOL_FP4
+
+
+def test_group_many_one_step_layers(gpu):
+    """Many consecutive one-step work items (K = 64 layers): at T = 1 the load
+    side of the streaming kernels runs three items ahead of the output side,
+    the deepest their item queue gets.  Both the fp4 and the int8 streaming
+    kernel against the oracle, and a repeated call bitwise identical."""
+    import torch
+    import paper_2512_02901_amd as f2
+    T, B = 1, 1
+    shapes = [(16 * (1 + i % 3), 64) for i in range(48)] + [(37, 320), (5, 64)]
+    layers = [(N, K, *quantized_layer(N, K, T, (47, i, N))) for i, (N, K) in enumerate(shapes)]
+    xs = [synth.bf16_round_complex(synth.activations(B, K, (48, i))) for i, (N, K) in enumerate(shapes)]
+    ys, refs, grp = run_fp4_group(layers, T, B, gpu, lambda i, N, K: xs[i])
+    first = [host(y).copy() for y in ys]
+    for y, yo in zip(ys, refs):
+        assert rel_l2(host(y), yo) <= TOL_FP4
+    grp.run()
+    for y, y1 in zip(ys, first):
+        np.testing.assert_array_equal(host(y).view(np.uint32), y1.view(np.uint32))
+    args = []
+    for i, (N, K, cu, su, cw, sw) in enumerate(layers):
+        y = torch.empty((B, N), dtype=torch.complex64, device=gpu)
+        args.append((f2.repack_tiled(dev(oracle.pack(cu), gpu)), dev(su, gpu),
+                     f2.repack_tiled(dev(oracle.pack(cw), gpu)), dev(sw, gpu), bf16_dev(xs[i], gpu), None, y))
+    f2.WlGroup(args, T=T, B=B, tiled=True).run()
+    for a, yo in zip(args, refs):
+        assert rel_l2(host(a[6]), yo) <= 1e-5
