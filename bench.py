@@ -5,8 +5,8 @@ Workload (one "step"): the full LLaMA-2-7B linear stack for one decode token
 -- 32 layers x {q, k, v, o: 4096x4096; gate, up: 11008x4096; down: 4096x11008}
 as widely-linear T = 2 layers (complex U, W of half size, 2-bit codes, about
 1.62 GB packed) -- each projection with its own bf16 activation token, all
-decoded by one grouped call (activation-operand kernel, int8-MFMA product
-kernel, split-K reduction) on one stream.  Weights are seeded synthetic
+decoded by one grouped call (activation-operand kernel, fp8 x fp4 MFMA
+product kernel, split-K reduction) on one stream.  Weights are seeded synthetic
 Student-t(4) draws with LLaMA-like outliers, quantised on the GPU by the
 library itself during setup (not timed).
 
@@ -14,7 +14,8 @@ Printed: ONE JSON line.  `value` is packed-weight GB/s of the whole step
 (packed code bytes / step time, inputs already resident in HBM).  Extra
 objects: `roofline` (the product kernel, timed live with HIP events on its
 stream), `cpu_baseline` (the CPU oracle on a bounded sample), `prefill`
-(2048-token int8 GEMMs, effective dense int8 TOPS), `stack_T3`.
+(2048-token int8 GEMMs, effective dense int8 TOPS), `stack_T3`, `stack_B*`
+(more tokens per layer), `per_layer` (one layer per call over rotated copies).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
 """
@@ -55,30 +56,31 @@ def batch_stack(f2, torch, dev, T, B, steps, warmup, seed=3000):
         y = torch.empty(B, N, dtype=torch.complex64, device=dev)
         layers.append((cu, su, cw, sw, x, None, y))
     grp = f2.WlGroup(layers, T=T, B=B, tiled=True)
-    return time_group(grp, torch, steps, warmup)
+    return time_group(grp, torch, steps, warmup, label=f"stack_B{B}_int8")
 
 
-def batch_stack_fp4(f2, torch, dev, T, layers, B, steps, warmup, seed=4000):
-    """The stack's fp4 tiled codes decoding B <= 2 bf16 tokens per layer."""
+def batch_stack_fp4(f2, torch, dev, T, fp4_layers, B, steps, warmup, seed=4000):
+    """The stack's fp4 tiled codes decoding B <= 4 bf16 tokens per layer."""
     g = torch.Generator(device=dev)
     g.manual_seed(seed + B)
     grp_layers = []
-    for (cu, su, cw, sw, x1, _, y1) in layers:
+    for (cu4, su, cw4, sw, x1, _, y1) in fp4_layers:
         N, K = y1.shape[1], x1.shape[1]
         x = torch.randn(B, K, 2, generator=g, device=dev).to(torch.bfloat16)
         y = torch.empty(B, N, dtype=torch.complex64, device=dev)
-        grp_layers.append((f2.repack_tiled_fp4(cu), su, f2.repack_tiled_fp4(cw), sw, x, None, y))
+        grp_layers.append((cu4, su, cw4, sw, x, None, y))
     grp = f2.WlGroup(grp_layers, T=T, B=B, layout=f2.LAYOUT_TILED_FP4)
-    return time_group(grp, torch, steps, warmup)
+    return time_group(grp, torch, steps, warmup, label=f"stack_B{B}")
 
 
 def build_stack(f2, synth, torch, dev, T, B=1, seed_base=1000, random_codes=False, with_tiled=False):
     """32 x 7 widely-linear layers with T-stage codes, each with its own
     bf16 activation token.  Returns (group, packed_bytes, algorithmic_bytes,
-    layers, tiled_group): the group decodes the fp4 tiled copies of the codes
-    (made once by fairy2i_repack_tiled_fp4, like the quantisation, outside
-    any timing); with_tiled also makes the tiled copies and a group over them
-    (the int8 matrix-core path); `layers` holds the D3 codes."""
+    layers, tiled_group, fp4_layers): the group decodes the fp4 tiled copies
+    of the codes (made once by fairy2i_repack_tiled_fp4, like the
+    quantisation, outside any timing); with_tiled also makes the tiled copies
+    and a group over them (the int8 matrix-core path); `layers` holds the D3
+    codes, `fp4_layers` the fp4 tiled copies."""
     layers, fp4_layers, tiled_layers, packed, algo = [], [], [], 0, 0
     stack_codes.clear()
     for layer in range(32):
@@ -115,16 +117,34 @@ def build_stack(f2, synth, torch, dev, T, B=1, seed_base=1000, random_codes=Fals
     torch.cuda.synchronize()
     grp = f2.WlGroup(fp4_layers, T=T, B=B, layout=f2.LAYOUT_TILED_FP4)
     grp_tiled = f2.WlGroup(tiled_layers, T=T, B=B, tiled=True) if with_tiled else None
-    return grp, packed, algo, layers, grp_tiled
+    return grp, packed, algo, layers, grp_tiled, fp4_layers
 
 
-def time_group(grp, torch, steps, warmup):
+WARMUP_MIN_S = 0.5   # the GPU clocks take about 0.3 s of back-to-back launches to settle
+
+
+def warm_up(fn, torch, count, min_s=WARMUP_MIN_S):
+    """At least `count` calls and at least `min_s` seconds of calls, in
+    batches of 10; returns (calls, seconds)."""
+    n, t0 = 0, time.time()
+    while n < count or time.time() - t0 < min_s:
+        for _ in range(10):
+            fn()
+        n += 10
+        torch.cuda.synchronize()
+    return n, time.time() - t0
+
+
+warmup_log = []      # (label, calls, seconds) of every warm-up phase
+
+
+def time_group(grp, torch, steps, warmup, label="group"):
     """(ms per step, prep ms, product ms, reduce ms): the step time from a
     loop of plain calls; the per-kernel split from a second loop in which
-    the library records events around its three launches."""
-    for _ in range(warmup):
-        grp.run()
-    torch.cuda.synchronize()
+    the library records events around its three launches.  Warm-up: at least
+    `warmup` calls and WARMUP_MIN_S seconds."""
+    n, sec = warm_up(grp.run, torch, warmup)
+    warmup_log.append((label, n, round(sec, 3)))
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     t0.record()
@@ -239,33 +259,119 @@ def prefill_bench(f2, synth, torch, dev, T=2, tokens=2048, reps=20):
 
 
 def cpu_baseline(f2, synth, torch, dev, layers, T, budget_s=12.0):
-    """The CPU oracle (unpack + dequantise + complex128 product) on a bounded
-    sample: the stack's first q-projection, repeated until ~budget_s."""
+    """The CPU oracle on a bounded sample: the stack's first q-projection,
+    from packed codes to y (unpack + dequantise + complex128 product),
+    repeated until ~budget_s; next to it the dense float64 product alone
+    (the dequantised matrices applied to the token), all with the BLAS
+    thread count set to the cores this process may run on."""
     import numpy as np
     import oracle
+    cores = len(os.sched_getaffinity(0))
+    blas = "unknown"
+    limiter = None
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
+        info = [d for d in threadpool_info() if d.get("user_api") == "blas"]
+        if info:
+            blas = f"{info[0].get('internal_api')} {info[0].get('version')}"
+        limiter = threadpool_limits(limits=cores, user_api="blas")
+    except Exception:
+        pass
     cu, su, cw, sw, x, _, _ = layers[0]
-    cu_h = oracle.unpack(cu.cpu().numpy(), 4 * cu.shape[2])
-    cw_h = oracle.unpack(cw.cpu().numpy(), 4 * cw.shape[2])
+    cu_p, cw_p = cu.cpu().numpy(), cw.cpu().numpy()
+    K = 4 * cu.shape[2]
     su_h, sw_h = su.cpu().numpy(), sw.cpu().numpy()
     xb = x.float().cpu().numpy()
     xh = xb[..., 0].astype(np.complex128) + 1j * xb[..., 1]
     packed = 2 * T * cu.shape[1] * cu.shape[2]
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
-    except Exception:
-        threads = 1
     reps, t0 = 0, time.perf_counter()
     while True:
-        oracle.wl_matmul(cu_h, su_h, cw_h, sw_h, xh)
+        oracle.wl_matmul(oracle.unpack(cu_p, K), su_h, oracle.unpack(cw_p, K), sw_h, xh)
         reps += 1
         el = time.perf_counter() - t0
         if el >= budget_s or reps >= 400:
             break
+    Uh = oracle.dequantize(oracle.unpack(cu_p, K), su_h)
+    Wh = oracle.dequantize(oracle.unpack(cw_p, K), sw_h)
+    dreps, t1 = 0, time.perf_counter()
+    while True:
+        xv = xh.reshape(-1)
+        _ = Uh @ xv + Wh @ np.conj(xv)
+        dreps += 1
+        del_ = time.perf_counter() - t1
+        if del_ >= 2.0 or dreps >= 2000:
+            break
+    if limiter is not None:
+        limiter.restore_original_limits()
     gbs = packed * reps / el / 1e9
-    return {"value": round(gbs, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "sample": f"{reps} oracle products of one 4096x4096 q-projection (complex 2048x2048, "
-                      f"T={T}, {packed} packed bytes, bf16 token) in {el:.1f} s; unit as the metric"}
+    return {"value": round(gbs, 4), "unit": "GB/s", "cores": cores, "kind": "oracle",
+            "blas": blas,
+            "sample": f"{reps} oracle products (unpack + dequantise + complex128 product) of one 4096x4096 "
+                      f"q-projection (complex 2048x2048, T={T}, {packed} packed bytes, bf16 token) in "
+                      f"{el:.1f} s; unit as the metric",
+            "oracle_us_per_layer": round(el / reps * 1e6, 1),
+            "dense_f64_matvec_us": round(del_ / dreps * 1e6, 1)}
+
+
+def per_layer_bench(f2, synth, torch, dev, T=2, min_bytes=512e6, reps=5):
+    """One layer per call at bs = 1: q (4096x4096), gate (11008x4096) and down
+    (4096x11008), each call on a different copy of the codes (at least
+    min_bytes of copies, so no call finds its codes in the 256 MB
+    last-level cache), launched from a HIP graph so host launch overhead does
+    not count.  Two routes: a one-layer grouped call over fp4 tiled codes, and
+    fairy2i_wl_matmul on the canonical codes."""
+    out = {}
+    for name in ("q", "gate", "down"):
+        rows, cols = synth.LLAMA2_7B_PROJ[name]
+        N, K = rows // 2, cols // 2
+        A = synth.torch_llama_weight(rows, cols, 6000 + len(out), dev)
+        U, W = f2.to_widely_linear(A)
+        del A
+        cu, su = f2.quantize(U, T)
+        cw, sw = f2.quantize(W, T)
+        del U, W
+        nbytes = 2 * T * N * K // 4
+        R = max(2, int(-(-min_bytes // nbytes)))
+        g = torch.Generator(device=dev)
+        g.manual_seed(6100 + len(out))
+        x = torch.randn(1, K, 2, generator=g, device=dev).to(torch.bfloat16)
+        y = torch.empty(1, N, dtype=torch.complex64, device=dev)
+        res = {"N": N, "K": K, "T": T, "packed_bytes": nbytes, "copies": R,
+               "rotated_MB": round(R * nbytes / 1e6, 1)}
+        cu4, cw4 = f2.repack_tiled_fp4(cu), f2.repack_tiled_fp4(cw)
+        groups = [f2.WlGroup([(cu4.clone(), su, cw4.clone(), sw, x, None, y)], T=T, B=1,
+                             layout=f2.LAYOUT_TILED_FP4) for _ in range(R)]
+        del cu4, cw4
+        d3 = [(cu.clone(), cw.clone()) for _ in range(R)]
+        ws = torch.empty(max(1, f2.wl_matmul_workspace_bytes(N, K, T, 1, f2.ACT_BF16)), dtype=torch.uint8,
+                         device=dev)
+        for label, calls in (("fp4_group", [grp.run for grp in groups]),
+                             ("d3_wl_matmul", [(lambda c=c: f2.wl_matmul(c[0], su, c[1], sw, x, out=y, workspace=ws))
+                                               for c in d3])):
+            for c in calls:
+                c()
+            torch.cuda.synchronize()
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                for c in calls:
+                    c()
+            warm_up(graph.replay, torch, 3, min_s=0.3)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                graph.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / (reps * R)
+            res[f"{label}_us"] = round(us, 2)
+            res[f"{label}_GBs"] = round(nbytes / (us * 1e-6) / 1e9, 1)
+            del graph
+        res["us_at_hbm_peak"] = round(nbytes / (HBM_PEAK_GBS * 1e9) * 1e6, 2)
+        out[name] = res
+        del groups, d3, cu, cw
+        torch.cuda.empty_cache()
+    return out
 
 
 def main():
@@ -303,11 +409,12 @@ def main():
     f2.load()
     T = 2
     t0 = time.time()
-    grp, packed, algo, layers, grp_tiled = build_stack(f2, synth, torch, dev, T, random_codes=args.random_codes,
-                                                       with_tiled=not args.no_extras)
+    grp, packed, algo, layers, grp_tiled, fp4_layers = build_stack(f2, synth, torch, dev, T,
+                                                                   random_codes=args.random_codes,
+                                                                   with_tiled=not args.no_extras)
     log(f"stack T={T}: {len(layers)} layers, {packed / 1e9:.3f} GB packed, setup {time.time() - t0:.1f} s")
 
-    ms, prep_ms, prod_ms, red_ms = time_group(grp, torch, args.steps, args.warmup)
+    ms, prep_ms, prod_ms, red_ms = time_group(grp, torch, args.steps, args.warmup, label="headline")
     gbs = packed / (ms * 1e-3) / 1e9
     log(f"step {ms * 1e3:.1f} us: prep {prep_ms * 1e3:.1f} us, product {prod_ms * 1e3:.1f} us, "
         f"reduce {red_ms * 1e3:.1f} us -> {gbs:.1f} GB/s packed")
@@ -335,7 +442,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16 activations as 15-bit fixed point, fp8 x fp4 MFMA with exact integer accumulation",
+        "dtype": "bf16 activations as two e4m3 digits per value, fp8 x fp4 MFMA, float32 accumulation",
         "data": ("synthetic: seeded uniform random 2-bit codes (counter run), N(0,1) bf16 tokens"
                  if args.random_codes else
                  "synthetic: seeded Student-t(4) weights with 1% outlier input channels, N(0,1) bf16 tokens"),
@@ -349,46 +456,55 @@ def main():
     }
     if not args.no_extras:
         # the same stack on the int8 matrix cores over the tiled copies
-        ms_t, _, prod_t, _ = time_group(grp_tiled, torch, args.steps, args.warmup)
+        ms_t, _, prod_t, _ = time_group(grp_tiled, torch, args.steps, args.warmup, label="stack_tiled_int8")
         result["stack_tiled_int8"] = {"ms_per_step": round(ms_t, 4), "GBs": round(packed / (ms_t * 1e-3) / 1e9, 1),
                                       "product_us": round(prod_t * 1e3, 1)}
         del grp_tiled
-        # two and four tokens per layer on the fp4 path (one and two activation tiles)
+        # 2 and 4 tokens per layer on the fp4 path (one activation tile of 2 tokens, or two)
         for Bb in (2, 4):
-            msb, _, prodb, _ = batch_stack_fp4(f2, torch, dev, T, layers, Bb, args.steps, args.warmup)
+            msb, _, prodb, _ = batch_stack_fp4(f2, torch, dev, T, fp4_layers, Bb, args.steps, args.warmup)
             result[f"stack_B{Bb}"] = {"ms_per_step": round(msb, 4), "GBs": round(packed / (msb * 1e-3) / 1e9, 1),
                                       "product_us": round(prodb * 1e3, 1)}
-        # 4 and 16 tokens per layer on the int8 matrix cores (tiled copies)
-        for Bb in (4, 16):
+        # 4, 8 and 16 tokens per layer on the int8 matrix cores (tiled copies)
+        for Bb in (4, 8, 16):
             msb, _, prodb, _ = batch_stack(f2, torch, dev, T, Bb, max(10, args.steps // 2), args.warmup)
             result[f"stack_B{Bb}_int8"] = {"ms_per_step": round(msb, 4),
                                            "GBs": round(packed / (msb * 1e-3) / 1e9, 1),
                                            "product_us": round(prodb * 1e3, 1)}
         # the same stack decoded straight from the canonical D3 codes
         grp_d3 = f2.WlGroup(layers, T=T, B=1)
-        ms_d3, _, prod_d3, _ = time_group(grp_d3, torch, args.steps, args.warmup)
+        ms_d3, _, prod_d3, _ = time_group(grp_d3, torch, args.steps, args.warmup, label="stack_d3_layout")
         result["stack_d3_layout"] = {"ms_per_step": round(ms_d3, 4), "GBs": round(packed / (ms_d3 * 1e-3) / 1e9, 1),
                                      "product_us": round(prod_d3 * 1e3, 1)}
         del grp_d3
-    del grp, layers
+    del grp, layers, fp4_layers
     stack_codes.clear()
     torch.cuda.empty_cache()
 
     if not args.no_extras:
-        grp3, packed3, _, layers3, _ = build_stack(f2, synth, torch, dev, 3, seed_base=2000)
-        ms3, _, _, _ = time_group(grp3, torch, max(5, args.steps // 2), args.warmup)
+        grp3, packed3, _, layers3, _, f3 = build_stack(f2, synth, torch, dev, 3, seed_base=2000)
+        ms3, _, _, _ = time_group(grp3, torch, max(5, args.steps // 2), args.warmup, label="stack_T3")
         result["stack_T3"] = {"ms_per_step": round(ms3, 4), "packed_bytes": packed3,
                               "GBs": round(packed3 / (ms3 * 1e-3) / 1e9, 1),
                               "time_ratio_T3_over_T2": round(ms3 / ms, 3)}
-        del grp3, layers3
+        del grp3, layers3, f3
         torch.cuda.empty_cache()
-        result["prefill"] = prefill_bench(f2, synth, torch, dev)
+        result["per_layer"] = per_layer_bench(f2, synth, torch, dev, T)
+        pf = prefill_bench(f2, synth, torch, dev)
+        g = pf["gate"]
+        # headline: the 11008x4096 (gate/up) shape; half of the dense MACs multiply structural zeros
+        result["prefill"] = {"tops": g["tops"], "frac_int8_peak": g["frac_int8_peak"], "useful_frac": 0.5,
+                             "useful_tops": round(g["tops"] * 0.5, 1), "us": g["us"],
+                             "workload": "2048 tokens x gate/up shape (real 11008x4096, complex 5504x2048), "
+                                         "T=2, int8 activations",
+                             "q": pf["q"], "gate": pf["gate"]}
         result["quantizer"] = quantizer_bench(f2, synth, torch, dev)
 
     if not args.no_cpu_baseline:
         # a fresh single-layer copy of the stack's first projection
         g1, _, _, l1 = build_stack_first(f2, synth, torch, dev, T)
         result["cpu_baseline"] = cpu_baseline(f2, synth, torch, dev, l1, T)
+    result["warmup_phases"] = [{"label": lab, "calls": n, "s": sec} for (lab, n, sec) in warmup_log]
     print(json.dumps(result), flush=True)
 
 

@@ -235,11 +235,16 @@ typedef struct fairy2i_wl_layer {
  * every K a multiple of 64, reserved == 0.  Each layer's codes are in the
  * layout its `layout` field names (same layout for U and W).  With
  * FAIRY2I_LAYOUT_TILED_FP4 every layer of the group must use it, with dtype
- * FAIRY2I_ACT_BF16 and B <= 2 (B <= 4 for T <= 3); the product then runs on the fp8 x fp4
- * matrix cores, each token taken as a 15-bit block fixed point
- * X = rint(x * 2^E) with 2^14 <= max |X| < 2^15 (every bf16 value within a
- * factor 2^7 of the token's largest magnitude exactly, smaller ones rounded
- * to the 2^-E grid), and the integer products are exact.
+ * FAIRY2I_ACT_BF16 and B <= 4 (B <= 2 for T = 4); the product then runs on the
+ * fp8 x fp4 matrix cores.  Each token is scaled by a power of two 2^S so that
+ * its largest magnitude m lies in [2^7, 2^8); a scaled value v is split by
+ * magnitude into two bands (|v| >= 1, and |v| < 1 taken times 2^8), and each
+ * band value u is written as two e4m3 digits, hi = e4m3(u) and
+ * lo = e4m3((u - hi) * 2^5) (round to nearest even), u = hi + 2^-5 lo.  Every
+ * value down to 2^-22 m is represented exactly, smaller ones to within
+ * 2^-30 m.  The digit products are exact and are summed in float32 on the
+ * matrix cores; y matches the exact product of the bf16 inputs to float32
+ * rounding (relative L2 about 1e-7).
  *
  * Use: size the workspace with fairy2i_wl_group_workspace_bytes and the
  * table with fairy2i_wl_group_table_bytes; fairy2i_wl_group_build_table

@@ -200,19 +200,37 @@ def wl_matmul(codes_U, scales_U, codes_W, scales_W, x, x_scale=None, out=None, w
     B, K = _act_shape(x)
     if K != 4 * KB:
         raise ValueError(f"activations have K={K}, codes have K={4 * KB}")
+    dev_ = x.device
+    for t, n in ((codes_U, "codes_U"), (codes_W, "codes_W"), (scales_U, "scales_U"), (scales_W, "scales_W")):
+        _require(t, None, n, dev_)
     if x_scale is not None:
-        _require(x_scale, torch.float32, "x_scale")
+        _require(x_scale, torch.float32, "x_scale", dev_)
+        if tuple(x_scale.shape) != (B,):
+            raise ValueError(f"x_scale must have shape ({B},), got {tuple(x_scale.shape)}")
     if out is None:
-        out = torch.empty((B, N), dtype=torch.complex64, device=x.device)
+        out = torch.empty((B, N), dtype=torch.complex64, device=dev_)
     else:
-        _require(out, torch.complex64, "out")
-    wsb = lib.fairy2i_wl_matmul_workspace_bytes(N, K, T, B, dt)
-    if wsb and workspace is None:
-        workspace = torch.empty(int(wsb), dtype=torch.uint8, device=x.device)
+        _require(out, torch.complex64, "out", dev_)
+        if tuple(out.shape) != (B, N):
+            raise ValueError(f"out must have shape ({B}, {N}), got {tuple(out.shape)}")
+    workspace, wsb = _workspace(lib.fairy2i_wl_matmul_workspace_bytes(N, K, T, B, dt), workspace, dev_)
     _check(lib.fairy2i_wl_matmul(_ptr(codes_U), _ptr(scales_U), _ptr(codes_W), _ptr(scales_W), T, N, K,
                                  _ptr(x), _ptr(x_scale), dt, B, _ptr(out), _ptr(workspace), wsb,
                                  _stream_ptr(x)), "fairy2i_wl_matmul")
     return out
+
+
+def _workspace(need, workspace, device):
+    """(workspace tensor or None, its size in bytes): a fresh uint8 device
+    buffer of `need` bytes when none is given, else the caller's, checked."""
+    torch = _torch()
+    need = int(need)
+    if workspace is None:
+        if need == 0:
+            return None, 0
+        workspace = torch.empty(need, dtype=torch.uint8, device=device)
+    _require(workspace, torch.uint8, "workspace", device)
+    return workspace, workspace.numel()
 
 
 def repack_tiled_bytes(N, K, T) -> int:
@@ -256,10 +274,12 @@ def int8_accumulators(codes_U, codes_W, q, workspace=None):
     B, K = _act_shape(q)
     if K != 4 * KB:
         raise ValueError("K mismatch")
+    _require(codes_W, None, "codes_W", q.device)
+    _require(codes_U, None, "codes_U", q.device)
+    if codes_W.shape != codes_U.shape:
+        raise ValueError("codes_U and codes_W shapes disagree")
     acc = torch.empty((2, T, 2, B, N, 2), dtype=torch.int32, device=q.device)
-    wsb = lib.fairy2i_wl_matmul_workspace_bytes(N, K, T, B, ACT_I8)
-    if wsb and workspace is None:
-        workspace = torch.empty(int(wsb), dtype=torch.uint8, device=q.device)
+    workspace, wsb = _workspace(lib.fairy2i_wl_matmul_workspace_bytes(N, K, T, B, ACT_I8), workspace, q.device)
     _check(lib.fairy2i_wl_int8_accumulators(_ptr(codes_U), _ptr(codes_W), T, N, K, _ptr(q), B,
                                             _ptr(acc), _ptr(workspace), wsb, _stream_ptr(q)),
            "fairy2i_wl_int8_accumulators")
@@ -294,22 +314,38 @@ class WlGroup:
         if not layers:
             raise ValueError("empty group")
         dt = _act_dtype(layers[0][4])
+        dev = layers[0][4].device
         self._keep = [t for layer in layers for t in layer if t is not None]
         arr = (WlLayer * len(layers))()
         for i, (cu, su, cw, sw, x, xs, y) in enumerate(layers):
+            _require(x, None, f"layers[{i}].x", dev)
             Bx, K = _act_shape(x)
             if Bx != B or _act_dtype(x) != dt:
                 raise ValueError("all layers of a group share B and the activation dtype")
-            N = y.shape[1] if tiled else cu.shape[1]
+            for t, n in ((cu, "codes_U"), (cw, "codes_W")):
+                _require(t, torch.uint8, f"layers[{i}].{n}", dev)
+            for t, n in ((su, "scales_U"), (sw, "scales_W")):
+                _require(t, torch.float32, f"layers[{i}].{n}", dev)
+                if tuple(t.shape) != (T, 2):
+                    raise ValueError(f"layers[{i}].{n} must have shape ({T}, 2)")
+            _require(y, torch.complex64, f"layers[{i}].y", dev)
+            if y.dim() != 2 or y.shape[0] != B:
+                raise ValueError(f"layers[{i}].y must have shape ({B}, N)")
+            N = y.shape[1]
+            if xs is not None:
+                _require(xs, torch.float32, f"layers[{i}].x_scale", dev)
+                if tuple(xs.shape) != (B,):
+                    raise ValueError(f"layers[{i}].x_scale must have shape ({B},)")
             if tiled:
                 need = repack_tiled_bytes(N, K, T)
                 if cu.numel() < need or cw.numel() < need:
                     raise ValueError("tiled codes smaller than fairy2i_repack_tiled_bytes")
+            elif tuple(cu.shape) != (T, N, K // 4) or tuple(cw.shape) != (T, N, K // 4):
+                raise ValueError(f"layers[{i}] codes must have shape ({T}, {N}, {K // 4})")
             arr[i] = WlLayer(cu.data_ptr(), su.data_ptr(), cw.data_ptr(), sw.data_ptr(), x.data_ptr(),
                              None if xs is None else xs.data_ptr(), y.data_ptr(), N, K,
                              layout, 0)
         self.n = len(layers)
-        dev = layers[0][4].device
         wsb = int(lib.fairy2i_wl_group_workspace_bytes(ctypes.byref(arr), self.n, T, dt, B))
         self.workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
         tb = int(lib.fairy2i_wl_group_table_bytes(self.n))

@@ -35,6 +35,7 @@ EXTRA = {
     # keep MFMA accumulators in VGPRs: the decode kernels accumulate across
     # steps and items, and AGPR accumulators cost copies on every step
     "decode.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+    "decode_f4.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
 }
 
 

@@ -272,7 +272,7 @@ static fairy2i_status check_group(const fairy2i_wl_layer* layers, int32_t n_laye
     // the decode kernels address a matrix with 32-bit offsets
     if (L.layout != FAIRY2I_LAYOUT_D3 && repack_tiled_bytes(L.N, L.K, T) >= ((size_t)1 << 31))
       return FAIRY2I_ERR_UNSUPPORTED;
-    // fp4 tiled codes: every layer, bf16 activations, one or two activation tiles
+    // fp4 tiled codes: every layer, bf16 activations, one or two activation tiles of 2 tokens
     if ((L.layout == FAIRY2I_LAYOUT_TILED_FP4) != (layers[0].layout == FAIRY2I_LAYOUT_TILED_FP4))
       return FAIRY2I_ERR_UNSUPPORTED;
     if (L.layout == FAIRY2I_LAYOUT_TILED_FP4 && (dtype != FAIRY2I_ACT_BF16 || B > 4 || (B > 2 && T > 3)))

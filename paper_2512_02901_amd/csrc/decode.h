@@ -9,7 +9,7 @@ namespace fairy2i {
 
 constexpr int kModeBf16 = 0;  // bf16 activations as 3 base-256 digits of a 23-bit fixed point
 constexpr int kModeI8 = 1;    // int8 activations with a per-token factor
-constexpr int kModeBf16F4 = 2;  // bf16 activations as 4 base-16 digits of a 15-bit fixed point,
+constexpr int kModeBf16F4 = 2;  // bf16 activations as e4m3 digit pairs in two magnitude bands,
                                 // codes in the fp4 tiled layout (fp8 x fp4 matrix cores)
 
 constexpr int kKernelReg = 0;     // codes staged in registers; any batch, accumulator export
@@ -56,6 +56,11 @@ DecHeader dec_header(int T, int mode, int64_t B, bool export_acc);
 // workspace bytes; with `ws` non-null also carve xf, xs, part out of it.
 // `single`: a one-layer call (slices chosen to give the GPU enough items).
 size_t dec_layer_setup(DecLayer& l, const DecHeader& h, bool single, char* ws);
+
+// The fp8 x fp4 path (decode_f4.hip): activation operand and product
+// launches of a kModeBf16F4 call (errors are left for hipGetLastError).
+void launch_f4_prep(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s);
+void launch_f4_product(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s);
 
 hipError_t launch_decode(const DecHeader& h, const DecLayer& inl, const DecLayer* tab,
                          int any_split, int64_t max_BN, bool export_acc, int64_t acc_elems,

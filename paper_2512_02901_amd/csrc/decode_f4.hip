@@ -1,0 +1,449 @@
+// Decode product (1..8 tokens) on the fp8 x fp4 matrix cores, for bf16
+// activations and codes in the fp4 tiled layout.  Sec. 3.4 / Algorithm 1 with
+// the dequantisation of Eq. (ifairy-dequant) and the W conj(x) term of
+// Eq. (widely-linear); the codes enter the matrix cores as e2m1 values masked
+// straight out of their packed words, the activations as e4m3 digits.
+#include "common.h"
+#include "decode_dev.h"
+
+namespace fairy2i {
+
+namespace {
+
+// ------------------------------------------------- prep, fp4 code path ---
+// Activation operand of the fp8 x fp4 product.  Each bf16 token b is scaled
+// by 2^S_b, S_b chosen so that its largest magnitude m lands in [2^7, 2^8).
+// A scaled value v (|v| < 2^8) is written as a pair of e4m3 digits
+//     hi = e4m3(v),   lo = e4m3((v - hi) * 2^5)      (round to nearest even),
+// v = hi + 2^-5 lo: hi holds the leading 4 significant bits, lo the next 4,
+// so the pair is exact whenever lo lands on the e4m3 grid (|v| >= 2^-7).
+//
+// The matrix cores multiply the digits exactly but add the products of an
+// MFMA in small groups with a narrow adder: a product more than about 2^13
+// below the largest product of its group loses the bits below that window
+// (measured with an in-bounds probe of v_mfma_f32_16x16x128_f8f6f4; groups of
+// values within 2^10 of each other are summed exactly).  So the values are
+// split into two bands by magnitude: |v| >= 1 goes to the first pair, whose
+// hi digits then span at most 2^8 .. 2^-3 and are summed exactly; smaller
+// values go, times 2^8, to a second pair.  Every value down to 2^-15 (2^-22 m)
+// is represented exactly, smaller ones to within 2^-23; the narrow adder can
+// only shave the lo digits and the second band, by at most about 2^-17 m per
+// group of products.  (One pair for all values would need half the columns,
+// but there a value near m drops the low bits of its small neighbours: 1.5e-4
+// relative L2 on tokens with a 300-sigma channel.)
+// A token owns 8 operand columns, 8 t' .. 8 t' + 7 for token t' of its tile
+// (two tokens per 16-column tile): column 4 band + j holds, for that band,
+// j = 0: hi of Re x, 1: hi of Im x, 2: lo of Re x, 3: lo of Im x.  The
+// output factor of token b is 2^-S_b (0 for an all-zero token).
+constexpr int kPrepF4Threads = 512;
+constexpr float kLoScale = 32.0f;     // lo digit = residual of hi times 2^5
+constexpr float kBand2Scale = 256.0f;  // second band: values below 1, times 2^8
+constexpr int kTokensPerTile = 2;      // 8 operand columns per token
+
+// e4m3 (OCP fp8: 1 sign, 4 exponent bits with bias 7, 3 mantissa bits, no
+// infinities, largest finite 448) code of v rounded to nearest, ties to even,
+// for |v| < 2^8 + 2^4 (the largest result is 2^8).  q receives the rounded
+// value as a float.
+__device__ inline uint32_t e4m3_rne(float v, float& q) {
+  const uint32_t u = __float_as_uint(v);
+  const uint32_t a = u & 0x7FFFFFFFu;
+  uint32_t c;
+  if (a < 0x3C800000u) {  // |v| < 2^-6: subnormal grid 2^-9, code = |v| / 2^-9 (8 is the smallest normal)
+    const float m = rintf(__uint_as_float(a) * 512.0f);
+    c = (uint32_t)m;
+    q = __uint_as_float(__float_as_uint(m * 0x1p-9f) | (u & 0x80000000u));
+  } else {                // keep 3 mantissa bits, ties to even; a carry moves into the exponent
+    const uint32_t r = a + 0x7FFFFu + ((a >> 20) & 1u);
+    c = (r >> 20) - (120u << 3);  // float32 exponent bias 127 -> e4m3 bias 7
+    q = __uint_as_float((r & 0xFFF00000u) | (u & 0x80000000u));
+  }
+  return c ? (c | ((u >> 24) & 0x80u)) : 0u;
+}
+
+// The (hi, lo) digit codes of v, |v| < 2^8.
+__device__ inline void digit_pair(float v, uint32_t& hi, uint32_t& lo) {
+  float qh, ql;
+  hi = e4m3_rne(v, qh);
+  lo = e4m3_rne((v - qh) * kLoScale, ql);  // v - qh is exact
+}
+
+// One block per (activation tile, layer): the largest magnitude of each of
+// the tile's tokens, then one thread per (16-code run, token): the run's
+// eight 16-byte chunks in operand order.
+__global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_kernel(DecHeader h, DecLayer inl,
+                                                                     const DecLayer* __restrict__ tab) {
+  const DecLayer L = tab ? load_layer(tab + blockIdx.y) : inl;
+  const int tile = blockIdx.x;
+  const int K = L.K;
+  constexpr int tpt = kTokensPerTile;
+  const int ntok = h.nc / 8;  // token slots written per tile
+  const bool vec = (reinterpret_cast<uintptr_t>(L.x) & 15) == 0;
+  __shared__ float red[kPrepF4Threads / 64][tpt];
+  __shared__ int sh_S[tpt];
+  const int wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int tk = 0; tk < tpt; ++tk) {
+    const int b = tpt * tile + tk;
+    float m = 0.0f;
+    if (tk < ntok && b < h.B) {
+      const uint16_t* xb = static_cast<const uint16_t*>(L.x) + (int64_t)b * K * 2;
+      if (vec) {
+        const uint4* xv = reinterpret_cast<const uint4*>(xb);
+        for (int i = threadIdx.x; i < K / 4; i += blockDim.x) {  // 8 bf16 (4 complex) per vector
+          const uint4 w = xv[i];
+          const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            m = fmaxf(m, fmaxf(fabsf(__uint_as_float(wd[j] << 16)), fabsf(__uint_as_float(wd[j] & 0xFFFF0000u))));
+        }
+      } else {
+        for (int i = threadIdx.x; i < 2 * K; i += blockDim.x) m = fmaxf(m, fabsf(__uint_as_float((uint32_t)xb[i] << 16)));
+      }
+    }
+    for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+    if ((threadIdx.x & 63) == 0) red[wave][tk] = m;
+  }
+  __syncthreads();
+  if (threadIdx.x < tpt) {
+    const int tk = threadIdx.x, b = tpt * tile + tk;
+    float g = 0.0f;
+    for (int w = 0; w < kPrepF4Threads / 64; ++w) g = fmaxf(g, red[w][tk]);
+    int S = 0;
+    if (g > 0.0f) {
+      int ex;
+      frexpf(g, &ex);  // g in [2^(ex-1), 2^ex), so g * 2^(8 - ex) in [2^7, 2^8)
+      S = 8 - ex;
+    }
+    sh_S[tk] = S;
+    if (tk < ntok && b < h.B) L.xs[b] = g > 0.0f ? ldexpf(1.0f, -S) : 0.0f;
+  }
+  __syncthreads();
+  const int nrun = L.nk4 * 16;  // runs of 16 codes: run r holds codes 16 r .. 16 r + 15
+  uint4* dst = reinterpret_cast<uint4*>(L.xf) + (int64_t)tile * nrun * h.nc;
+  for (int idx = threadIdx.x; idx < nrun * ntok; idx += blockDim.x) {
+    const int tk = idx % ntok, r = idx / ntok;
+    const int b = tpt * tile + tk;
+    const int k0 = 16 * r;  // = 256 step + 64 d + 16 g for r = 16 step + 4 d + g
+    uint32_t out[2][4][4] = {};  // [band][hi re, hi im, lo re, lo im][word]
+    if (b < h.B && k0 < K) {  // K % 64 == 0: the whole run is in range
+      int v[2][16];
+      load_run16<kModeBf16>(L.x, vec, ((int64_t)b * K + k0) * 2, 0, v[0]);
+      load_run16<kModeBf16>(L.x, vec, ((int64_t)b * K + k0) * 2, 1, v[1]);
+      const int S = sh_S[tk];
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float x = ldexpf(__uint_as_float((uint32_t)v[c][e] << 16), S);  // exact: |x| < 2^8
+          const int band = fabsf(x) < 1.0f ? 1 : 0;
+          uint32_t hi, lo;
+          digit_pair(band ? x * kBand2Scale : x, hi, lo);
+          const int sh = 8 * (e & 3);
+          if (band) {
+            out[1][c][e >> 2] |= hi << sh;
+            out[1][2 + c][e >> 2] |= lo << sh;
+          } else {
+            out[0][c][e >> 2] |= hi << sh;
+            out[0][2 + c][e >> 2] |= lo << sh;
+          }
+        }
+    }
+#pragma unroll
+    for (int bd = 0; bd < 2; ++bd)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        dst[(int64_t)r * h.nc + 8 * tk + 4 * bd + j] =
+            make_uint4(out[bd][j][0], out[bd][j][1], out[bd][j][2], out[bd][j][3]);
+  }
+}
+
+// ------------------------------------------- streaming kernel, fp4 codes ---
+// The same ring, cursors and work items as above, for codes in the fp4 tiled
+// layout and bf16 activations as two e4m3 digits per value (hi, lo; see the
+// fp4 prep kernel above), four tokens per 16-column tile.  With the
+// code bits (p, q) = (bit 0, bit 1) of code k, i^k = (1 - 2q)(1 - p) +
+// i (1 - 2q) p (Eq. realify-ops: b_re = (1 - 2q)(1 - p), b_im = (1 - 2q) p),
+// the kernel contracts two e2m1 operands with v_mfma_f32_16x16x128_f8f6f4:
+//     S = 1 - 2q  (every code: +-1)     and     I = (1 - 2q) p  (0 or +-1),
+// and forms b_re = S - I in the epilogue.  In the fp4 layout a nibble holds
+// the bits of two codes at (q_A, q_B, p_A, p_B) = bits (3, 2, 1, 0), so per
+// 32-bit word of 16 codes
+//     I_A = w & 0xAAAAAAAA,          S_A = I_A | 0x22222222,
+//     I_B = (w << 1) & 0xAAAAAAAA,   S_B = I_B | 0x22222222
+// (e2m1 0b0010 = 1, 0b1010 = -1, 0b0000 / 0b1000 = +-0): five VALU
+// instructions per 16 codes.  Every product is an e4m3 digit times 0 or +-1,
+// so the products are exact; the matrix core adds them into the float32
+// accumulators.
+
+// S and I operands of one 128-code MFMA from the lane's two code words
+// (S = I | 0x22222222: I keeps only bits 3 and 1 of each nibble).
+__device__ inline void expand_f4(uint32_t w0, uint32_t w1, v8i& bs, v8i& bi) {
+  const uint32_t ia0 = w0 & 0xAAAAAAAAu, ib0 = (w0 << 1) & 0xAAAAAAAAu;
+  const uint32_t ia1 = w1 & 0xAAAAAAAAu, ib1 = (w1 << 1) & 0xAAAAAAAAu;
+  bi = v8i{(int)ia0, (int)ib0, (int)ia1, (int)ib1, 0, 0, 0, 0};
+  bs = v8i{(int)(ia0 | 0x22222222u), (int)(ib0 | 0x22222222u), (int)(ia1 | 0x22222222u),
+           (int)(ib1 | 0x22222222u), 0, 0, 0, 0};
+}
+
+constexpr int kFmtFp8 = 0;  // MFMA operand format codes: e4m3
+constexpr int kFmtFp4 = 4;  // e2m1
+
+// Epilogue of a work item: lane (g, li) holds activation columns 4g..4g+3
+// of weight row li, i.e. (hi re, hi im, lo re, lo im) of band g % 2 of token
+// g / 2 of the tile, for every (plane, S or I) accumulator.  Each lane joins
+// its band's digits (hi + 2^-5 lo); the odd lane group passes its second band
+// down to the even group, which adds it times 2^-8, forms b_re = S - I and
+// b_im = I and applies the axis scales and the token factor, all in float32
+// with explicit fused multiply-adds in a fixed order: every inlined copy
+// rounds alike, so y does not depend on which wave or ring slot finishes the
+// item.  The layer's axis scales sc[m][t][axis] and the tile's token factors
+// xf[2] are the caller's (loaded once per layer).
+template <int T>
+__device__ inline void write_outputs_f4(const DecLayer& L, const DecHeader& h, int kc, int row, bool row_ok,
+                                        int lane, int tile, const v4f (&aS)[2 * T], const v4f (&aI)[2 * T],
+                                        const float (&sc)[2][T][2], const float (&xf)[2]) {
+  constexpr int P = 2 * T;
+  const int g = lane >> 4;
+  float vS[P][2], vI[P][2];
+#pragma unroll
+  for (int p = 0; p < P; ++p)
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      vS[p][c] = fmaf(aS[p][2 + c], 1.0f / kLoScale, aS[p][c]);
+      vI[p][c] = fmaf(aI[p][2 + c], 1.0f / kLoScale, aI[p][c]);
+      const float hS = __shfl_down(vS[p][c], 16), hI = __shfl_down(vI[p][c], 16);
+      vS[p][c] = fmaf(hS, 1.0f / kBand2Scale, vS[p][c]);
+      vI[p][c] = fmaf(hI, 1.0f / kBand2Scale, vI[p][c]);
+    }
+  const int tt = g >> 1;  // token slot within the tile
+  const int b = kTokensPerTile * tile + tt;
+  if ((g & 1) || !row_ok || b >= h.B) return;
+  float yr = 0.0f, yi = 0.0f;
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    float Pre[2][2], Pim[2][2];  // [matrix][component]: products with b_re = S - I and b_im = I
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {
+      const int p = m * T + t;
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        Pre[m][c] = vS[p][c] - vI[p][c];
+        Pim[m][c] = vI[p][c];
+      }
+    }
+    const float su_re = sc[0][t][0], su_im = sc[0][t][1];
+    const float sw_re = sc[1][t][0], sw_im = sc[1][t][1];
+    yr = fmaf(su_re, Pre[0][0], yr);
+    yr = fmaf(-su_im, Pim[0][1], yr);
+    yr = fmaf(sw_re, Pre[1][0], yr);
+    yr = fmaf(sw_im, Pim[1][1], yr);
+    yi = fmaf(su_re, Pre[0][1], yi);
+    yi = fmaf(su_im, Pim[0][0], yi);
+    yi = fmaf(-sw_re, Pre[1][1], yi);
+    yi = fmaf(sw_im, Pim[1][0], yi);
+  }
+  const float f = tt ? xf[1] : xf[0];
+  const float2 v = make_float2(__fmul_rn(yr, f), __fmul_rn(yi, f));
+  if (L.nkc == 1)
+    buf_store8(L.y, (uint32_t)h.B * L.N * 8, (uint32_t)((b * L.N + row) * 8), v);
+  else
+    buf_store8(L.part, (uint32_t)L.nkc * h.B * L.N * 8, (uint32_t)(((kc * h.B + b) * L.N + row) * 8), v);
+}
+
+constexpr int f4_ring_slots(int T) { return ring_slots(T); }
+
+
+template <int T, int XW>
+using F4Cfg = StreamCfg<T, XW, f4_ring_slots(T), block_waves(T)>;
+
+// NT activation tiles (two tokens each); a ring slot holds XW KiB per tile.
+template <int T, int XW, int NT>
+__global__ __launch_bounds__((64 * F4Cfg<T, NT * XW>::WAVES)) void dec_stream_f4_kernel(DecHeader h, DecLayer inl,
+                                                                                       const DecLayer* __restrict__ tab) {
+#if defined(__HIP_DEVICE_COMPILE__)  // LDS-DMA and buffer-descriptor code: device pass only
+  using C = F4Cfg<T, NT * XW>;
+  constexpr int P = C::P, NS = C::NS, XSLOT = C::XSLOT;
+  constexpr int WAVES = C::WAVES;
+  static_assert(NS <= 4, "the item queue holds the items of up to NS - 1 steps ahead");
+  __shared__ __attribute__((aligned(16))) uint8_t ring[WAVES][NS][XSLOT];
+  __shared__ __attribute__((aligned(16))) uint8_t zero16[16];
+  __shared__ uint32_t claim_ctr;
+  const int lane = threadIdx.x & 63;
+  const int g = lane >> 4, li = lane & 15;
+  const int wave = uniform(threadIdx.x >> 6);
+  if (threadIdx.x < 4) reinterpret_cast<uint32_t*>(zero16)[threadIdx.x] = 0u;
+  if (threadIdx.x == 0) claim_ctr = (uint32_t)WAVES;  // wave w starts with item b0 + w
+  __syncthreads();
+  // the block's items: an equal share of the call's
+  const int64_t b0 = uniform64((int64_t)blockIdx.x * h.total_items / gridDim.x);
+  const int nb = uniform((int)(uniform64(((int64_t)blockIdx.x + 1) * h.total_items / gridDim.x) - b0));
+  if (wave >= nb) return;
+  const int64_t i0 = b0 + wave;
+  const uint32_t ctr_addr = lds_addr(&claim_ctr);
+
+  // operand column li of tile t belongs to token 2 t + li / 8
+  bool xvalid[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) xvalid[t] = kTokensPerTile * t + li / 8 < h.B;
+
+  LoadCursor<T> lc;
+  OutCursor oc;
+  ItemQueue iq;
+  iq.n = 0;
+  {
+    const int lidx = tab ? find_layer(tab, h.n_layers, i0) : 0;
+    const DecLayer L0 = tab ? load_layer(tab + lidx) : inl;
+    lc.lidx = oc.lidx = lidx;
+    lc.item = oc.item = i0;
+    load_enter_layer(lc, L0, h);
+    out_enter_layer(oc, L0);
+    split_item(i0, lc.G, lc.rb, lc.kc);
+    oc.rb = lc.rb;
+    oc.kc = lc.kc;
+  }
+  load_item(lc, h, lane);
+  out_item(oc, li);
+  // the epilogue's per-layer constants, reloaded when the output side changes layer
+  float esc[2][T][2], exf[NT][2];
+  auto load_epilogue_consts = [&]() {
+    sload_scales<T>(uniform_ptr(oc.scales[0]), uniform_ptr(oc.scales[1]), esc);
+    // the factor array is padded to 256 bytes: both floats of every tile are inside it
+#pragma unroll
+    for (int t = 0; t < NT; ++t) sload_run<2>(uniform_ptr(oc.xs) + kTokensPerTile * t, exf[t]);
+  };
+  load_epilogue_consts();
+
+  // next step of the load side: the next step of its item, else a claimed
+  // item (queued for the output side); false once the block's items are gone
+  auto load_advance = [&]() -> bool {
+    if (++lc.j < lc.nsteps) {
+      ++lc.k4;
+      lc.voff += lc.vstep;
+      lc.xoff += 256 * h.nc;
+      return true;
+    }
+    const int off = claim_item(ctr_addr, nb, lane);
+    if (off < 0) return false;
+    load_goto(lc, b0 + off, tab, h, lane);
+    iq.push(off);
+    return true;
+  };
+  auto out_advance = [&]() -> bool {
+    if (++oc.j < oc.nsteps) return true;
+    if (iq.n == 0) return false;
+    if (out_goto(oc, b0 + iq.pop(), tab, li)) load_epilogue_consts();
+    return true;
+  };
+
+  v4i cq[NS][P];
+  bool live = true;
+#pragma unroll
+  for (int k = 0; k < NS - 1; ++k) {
+    stream_issue<XW, T, 32, NT>(lc, live, lane, cq[k], &ring[wave][k][0]);
+    if (live) live = load_advance();
+  }
+
+  v4f aS[NT][P], aI[NT][P];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int p = 0; p < P; ++p) aS[t][p] = aI[t][p] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  auto step = [&](auto kconst) -> bool {
+    constexpr int K = decltype(kconst)::value;
+    constexpr int KN = (K + NS - 1) % NS;
+    stream_issue<XW, T, 32, NT>(lc, live, lane, cq[KN], &ring[wave][KN][0]);
+    if (live) live = load_advance();
+    __builtin_amdgcn_s_waitcnt(C::WAITCNT);
+    v4i xr[NT][4];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const uint32_t xa = xvalid[t] ? lds_addr(&ring[wave][K][t * XW * 1024]) + (uint32_t)((g * h.nc + li) * 16)
+                                    : lds_addr(zero16);
+      const uint32_t xs = xvalid[t] ? (uint32_t)(4 * h.nc * 16) : 0u;
+      lds_read4(xa, xa + xs, xa + 2 * xs, xa + 3 * xs, xr[t]);
+    }
+    const v4i* cr = cq[K];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int p = 0; p < P; ++p) {
+        v8i bs, bi;
+        expand_f4((uint32_t)cr[p][2 * kb], (uint32_t)cr[p][2 * kb + 1], bs, bi);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          const v4i x0 = xr[t][2 * kb], x1 = xr[t][2 * kb + 1];
+          const v8i a = v8i{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+          aS[t][p] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bs, aS[t][p], kFmtFp8, kFmtFp4, 0, 0, 0, 0);
+          aI[t][p] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bi, aI[t][p], kFmtFp8, kFmtFp4, 0, 0, 0, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x002, 10, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2 * NT, 0);
+      }
+    }
+    if (oc.j == oc.nsteps - 1) {
+      const DecLayer Lo = out_layer(oc);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        write_outputs_f4<T>(Lo, h, oc.kc, oc.row, oc.row_ok, lane, t, aS[t], aI[t], esc, exf[t]);
+#pragma unroll
+        for (int p = 0; p < P; ++p) aS[t][p] = aI[t][p] = v4f{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+    return !out_advance();
+  };
+
+  static_assert(NS >= 2 && NS <= 6, "the ring loop below is unrolled for 2..6 slots");
+  while (true) {
+    if (step(std::integral_constant<int, 0>{})) break;
+    if (step(std::integral_constant<int, 1>{})) break;
+    if constexpr (NS > 2) if (step(std::integral_constant<int, 2 % NS>{})) break;
+    if constexpr (NS > 3) if (step(std::integral_constant<int, 3 % NS>{})) break;
+    if constexpr (NS > 4) if (step(std::integral_constant<int, 4 % NS>{})) break;
+    if constexpr (NS > 5) if (step(std::integral_constant<int, 5 % NS>{})) break;
+  }
+  __builtin_amdgcn_s_waitcnt(0);  // no load may still be writing LDS when the wave ends
+#endif
+}
+
+template <int T, int XW, int NT>
+void launch_stream_f4(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
+  auto k = dec_stream_f4_kernel<T, XW, NT>;
+  constexpr int waves = F4Cfg<T, NT * XW>::WAVES;
+  constexpr int threads = 64 * waves;
+  static const int resident = resident_blocks(reinterpret_cast<const void*>(k), threads);
+  const int64_t want = (h.total_items + waves - 1) / waves;
+  const int64_t blocks = want < resident ? want : resident;
+  hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(threads), 0, s, h, inl, tab);
+}
+
+// XW = KiB of activation operand per 256-code step and tile (nc / 4), NT =
+// activation tiles of two tokens (three or four tokens: two tiles, T <= 3).
+template <int T>
+void launch_stream_f4_t(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
+  if constexpr (T <= 3) {
+    if (h.ntile >= 2) {
+      launch_stream_f4<T, 4, 2>(h, inl, tab, s);
+      return;
+    }
+  }
+  if (h.nc <= 8) launch_stream_f4<T, 2, 1>(h, inl, tab, s);
+  else launch_stream_f4<T, 4, 1>(h, inl, tab, s);
+}
+
+}  // namespace
+
+void launch_f4_prep(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
+  hipLaunchKernelGGL(dec_prep_f4_kernel, dim3(h.ntile, h.n_layers), dim3(kPrepF4Threads), 0, s, h, inl, tab);
+}
+
+void launch_f4_product(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
+  switch (h.T) {
+    case 1: launch_stream_f4_t<1>(h, inl, tab, s); break;
+    case 2: launch_stream_f4_t<2>(h, inl, tab, s); break;
+    case 3: launch_stream_f4_t<3>(h, inl, tab, s); break;
+    default: launch_stream_f4_t<4>(h, inl, tab, s); break;
+  }
+}
+
+}  // namespace fairy2i
