@@ -188,6 +188,30 @@ fairy2i_status fairy2i_wl_matmul(const uint8_t* codes_U, const float* scales_U,
                                  void* stream);
 
 /*
+ * fairy2i_wl_matmul for callers that cannot allocate device memory (code
+ * under HIP graph capture, serving loops, harnesses that forbid hipMalloc):
+ * the same arguments without the workspace, which is taken from a device
+ * array of FAIRY2I_NOALLOC_SCRATCH_BYTES that the library holds on every GPU
+ * it runs on until the process ends (the array of the current device is used;
+ * `stream` must belong to that device).  Nothing is allocated or freed.
+ * Results are bitwise those of fairy2i_wl_matmul.  All calls on one GPU share
+ * that GPU's array: calls that overlap on one GPU (other streams, other host
+ * threads) race and must be serialised by the caller.  The workspace's
+ * contents are never read before being written, so no clearing is needed.
+ * Errors: as fairy2i_wl_matmul; FAIRY2I_ERR_WORKSPACE when the call would
+ * need more than FAIRY2I_NOALLOC_SCRATCH_BYTES of workspace
+ * (fairy2i_wl_matmul_workspace_bytes; for example more than about 2900
+ * int8 tokens at K = 5504); FAIRY2I_ERR_HIP if the array's address cannot be
+ * obtained.
+ */
+#define FAIRY2I_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+fairy2i_status fairy2i_wl_matmul_noalloc(const uint8_t* codes_U, const float* scales_U,
+                                         const uint8_t* codes_W, const float* scales_W,
+                                         int32_t T, int64_t N, int64_t K,
+                                         const void* x, const float* x_scale, int32_t dtype, int64_t B,
+                                         float* y, void* stream);
+
+/*
  * The exact integer products behind the int8 path of fairy2i_wl_matmul,
  * exported so they can be compared bit for bit:
  *   acc[M][t][p][b][i][c] = sum_j B^{M,t}_p[i][j] * q[b][j][c]

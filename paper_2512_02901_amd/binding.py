@@ -35,6 +35,8 @@ _SIGNATURES = {
     "fairy2i_wl_matmul_workspace_bytes": (_c_size, [_c_i64, _c_i64, _c_i32, _c_i64, _c_i32]),
     "fairy2i_wl_matmul": (_c_i32, [_c_p, _c_p, _c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_p,
                                    _c_i32, _c_i64, _c_p, _c_p, _c_size, _c_p]),
+    "fairy2i_wl_matmul_noalloc": (_c_i32, [_c_p, _c_p, _c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_p,
+                                           _c_i32, _c_i64, _c_p, _c_p]),
     "fairy2i_wl_int8_accumulators": (_c_i32, [_c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_i64,
                                               _c_p, _c_p, _c_size, _c_p]),
     "fairy2i_host_exact_mean_f32": (_c_i32, [_c_p, _c_i64, _c_p]),
@@ -217,6 +219,43 @@ def wl_matmul(codes_U, scales_U, codes_W, scales_W, x, x_scale=None, out=None, w
     _check(lib.fairy2i_wl_matmul(_ptr(codes_U), _ptr(scales_U), _ptr(codes_W), _ptr(scales_W), T, N, K,
                                  _ptr(x), _ptr(x_scale), dt, B, _ptr(out), _ptr(workspace), wsb,
                                  _stream_ptr(x)), "fairy2i_wl_matmul")
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 32 << 20
+
+
+def wl_matmul_noalloc(codes_U, scales_U, codes_W, scales_W, x, x_scale=None, out=None):
+    """wl_matmul without a workspace: the library's fixed device array
+    (NOALLOC_SCRATCH_BYTES per GPU) serves as one; allocates nothing when
+    ``out`` is given.  Calls that overlap on one GPU race."""
+    torch = _torch()
+    lib = load()
+    for t, n in ((codes_U, "codes_U"), (codes_W, "codes_W")):
+        _require(t, torch.uint8, n, x.device)
+    for t, n in ((scales_U, "scales_U"), (scales_W, "scales_W")):
+        _require(t, torch.float32, n, x.device)
+    _require(x, None, "x")
+    T, N, KB = codes_U.shape
+    if codes_W.shape != codes_U.shape or scales_U.shape != (T, 2) or scales_W.shape != (T, 2):
+        raise ValueError("codes/scales shapes disagree")
+    dt = _act_dtype(x)
+    B, K = _act_shape(x)
+    if K != 4 * KB:
+        raise ValueError(f"activations have K={K}, codes have K={4 * KB}")
+    if x_scale is not None:
+        _require(x_scale, torch.float32, "x_scale", x.device)
+        if tuple(x_scale.shape) != (B,):
+            raise ValueError(f"x_scale must have shape ({B},), got {tuple(x_scale.shape)}")
+    if out is None:
+        out = torch.empty((B, N), dtype=torch.complex64, device=x.device)
+    else:
+        _require(out, torch.complex64, "out", x.device)
+        if tuple(out.shape) != (B, N):
+            raise ValueError(f"out must have shape ({B}, {N}), got {tuple(out.shape)}")
+    _check(lib.fairy2i_wl_matmul_noalloc(_ptr(codes_U), _ptr(scales_U), _ptr(codes_W), _ptr(scales_W), T, N, K,
+                                         _ptr(x), _ptr(x_scale), dt, B, _ptr(out), _stream_ptr(x)),
+           "fairy2i_wl_matmul_noalloc")
     return out
 
 

@@ -2,6 +2,7 @@
 // caller's stream.  Nothing here allocates, frees or synchronises.
 #include <stddef.h>
 
+#include <mutex>
 #include <vector>
 
 #include "common.h"
@@ -90,6 +91,35 @@ struct GroupTableHeader {
   int64_t max_BN;
 };
 static_assert(sizeof(GroupTableHeader) % 16 == 0, "table header alignment");
+
+// ------------------------------------------------ allocation-free call ---
+// fairy2i_wl_matmul_noalloc runs fairy2i_wl_matmul with this array as its
+// workspace.  Every GPU the library runs on holds its own copy until the
+// process ends.  In host code `scratch` names a host-side stand-in, not the
+// device memory: the device address of the current device's copy is taken
+// once per device with hipGetSymbolAddress and only that address is used.
+constexpr size_t kNoAllocScratchBytes = FAIRY2I_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};  // device address of `scratch` per device, once looked up
+
+// Device address of the current device's scratch array (looked up on the
+// first call for that device).
+fairy2i_status current_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return FAIRY2I_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return FAIRY2I_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return FAIRY2I_ERR_HIP;
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return FAIRY2I_OK;
+}
 
 }  // namespace
 
@@ -214,6 +244,24 @@ fairy2i_status fairy2i_wl_matmul(const uint8_t* codes_U, const float* scales_U,
   const hipError_t e = (B <= FAIRY2I_MAX_DECODE_BATCH) ? launch_gemv(a, as_stream(stream))
                                                        : launch_gemm_i8(a, workspace, as_stream(stream));
   return hip_status(e);
+}
+
+fairy2i_status fairy2i_wl_matmul_noalloc(const uint8_t* codes_U, const float* scales_U,
+                                         const uint8_t* codes_W, const float* scales_W, int32_t T,
+                                         int64_t N, int64_t K, const void* x, const float* x_scale,
+                                         int32_t dtype, int64_t B, float* y, void* stream) {
+  // argument errors first, exactly as fairy2i_wl_matmul reports them
+  fairy2i_status st = check_wl_common(codes_U, codes_W, T, N, K, x, B, y);
+  if (st != FAIRY2I_OK) return st;
+  if (!scales_U || !scales_W) return FAIRY2I_ERR_NULL;
+  if (dtype != FAIRY2I_ACT_F32 && dtype != FAIRY2I_ACT_BF16 && dtype != FAIRY2I_ACT_I8)
+    return FAIRY2I_ERR_DTYPE;
+  const size_t need = fairy2i_wl_matmul_workspace_bytes(N, K, T, B, dtype);
+  if (need > kNoAllocScratchBytes) return FAIRY2I_ERR_WORKSPACE;
+  void* ws = nullptr;
+  if (need > 0 && (st = current_scratch(&ws)) != FAIRY2I_OK) return st;
+  return fairy2i_wl_matmul(codes_U, scales_U, codes_W, scales_W, T, N, K, x, x_scale, dtype, B, y, ws,
+                           need > 0 ? kNoAllocScratchBytes : 0, stream);
 }
 
 fairy2i_status fairy2i_wl_int8_accumulators(const uint8_t* codes_U, const uint8_t* codes_W, int32_t T,
