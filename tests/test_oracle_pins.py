@@ -393,6 +393,55 @@ def test_activation_quantizer_properties():
         assert abs(float(f[b]) - g / 127) <= 1e-7 * g
 
 
+def test_act_quant_ties_to_even():
+    """Reading S10, worked by hand: a token whose largest magnitude is 127
+    has inv = 127/127 = 1 exactly, so every x * inv is x itself and the
+    half-integers are exact ties; round-half-to-even gives 2.5 -> 2,
+    3.5 -> 4, -2.5 -> -2, 0.5 -> 0, -0.5 -> 0, 1.5 -> 2, 126.5 -> 126
+    (round-half-away would give 3, 4, -3, 1, -1, 2, 127)."""
+    re = np.array([127.0, 2.5, 3.5, -2.5, 0.5, -0.5, 1.5, 126.5], np.float32)
+    x = (re + 0j).astype(np.complex64).reshape(1, -1)
+    q, f = oracle.quantize_act_int8(x)
+    assert q[0, :, 0].tolist() == [127, 2, 4, -2, 0, 0, 2, 126]
+    assert not np.any(q[0, :, 1])
+    assert f[0] == np.float32(1.0)
+
+
+def test_act_quant_product_rounded_to_float32():
+    """Reading S10, worked by hand: gamma = 2.614424 (float32 0x402752B9)
+    gives inv = fl32(127 / gamma) = 48.576664 (0x42424E81).  For
+    x = 1.6983464 (0x3FD9636A) the exact product inv * x is 82.5000012..., and
+    its float32 rounding is 82.5 (float32 spacing there is 2^-17), an exact
+    tie that rounds to the even 82.  Rounding the exact product instead would
+    give 83, and so would the other order of operations,
+    fl32(fl32(x / gamma) * 127) = 82.50001."""
+    g = np.uint32(0x402752B9).view(np.float32)
+    xv = np.uint32(0x3FD9636A).view(np.float32)
+    inv = np.float32(np.float32(127.0) / g)
+    assert inv.view(np.uint32) == 0x42424E81
+    assert Fraction(float(inv)) * Fraction(float(xv)) - Fraction(165, 2) < Fraction(1, 2 ** 19)
+    x = np.array([[complex(g, 0.0), complex(xv, 0.0)]], np.complex64)
+    q, f = oracle.quantize_act_int8(x)
+    assert q[0, 0, 0] == 127 and q[0, 1, 0] == 82
+
+
+def test_residual_subtracts_stored_float32_scale():
+    """Reading S5, worked by hand: one row (1, 1, 1, (1 + 2^-23) + i 7 2^-26).
+    Stage 0 codes every entry +1 (real axis); the exact mean of |Re| is
+    1 + 2^-25, whose float32 rounding is 1 (half an ulp of 1 is 2^-24), so
+    s_re = 1 and s_im = 0 (empty group).  The last entry's stage-1 residual is
+    then 2^-23 + i 7 2^-26 with |Re| > |Im|: code 0 (+1).  Subtracting the
+    exact mean instead would leave 3 2^-25 + i 7 2^-26 with |Im| > |Re|:
+    code 1 (+i).  Stage 1's scales: s_re = mean(0, 0, 0, 2^-23) = 2^-25."""
+    M = np.array([[1.0, 1.0, 1.0, complex(1.0 + 2.0 ** -23, 7 * 2.0 ** -26)]], np.complex64)
+    assert M[0, 3].real == np.float32(1.0 + 2.0 ** -23) and M[0, 3].imag == np.float32(7 * 2.0 ** -26)
+    codes, scales = oracle.quantize(M, 2)
+    assert codes[0].tolist() == [[0, 0, 0, 0]]
+    assert scales[0].tolist() == [1.0, 0.0]
+    assert codes[1].tolist() == [[0, 0, 0, 0]]
+    assert scales[1].tolist() == [2.0 ** -25, 0.0]
+
+
 def test_small_layer_end_to_end_error():
     """The 256x256 case end to end: with T = 2 the codes path stays close to
     the real layer it approximates (sanity on the whole chain)."""
