@@ -35,7 +35,7 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 INT8_PEAK_TOPS = 5000.0        # MI355X dense int8 MFMA, TOPS
 PROFILES = os.path.join(ROOT, "profiles")
-PRODUCT_KERNEL_SRC = os.path.join(ROOT, "paper_2512_02901_amd", "csrc", "decode.hip")
+PRODUCT_KERNEL_SRC = os.path.join(ROOT, "paper_2512_02901_amd", "csrc", "decode_f4.hip")
 
 
 def log(msg):

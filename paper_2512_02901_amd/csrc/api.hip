@@ -2,6 +2,7 @@
 // caller's stream.  Nothing here allocates, frees or synchronises.
 #include <stddef.h>
 
+#include <algorithm>
 #include <mutex>
 #include <vector>
 
@@ -74,8 +75,10 @@ fairy2i_status run_single_decode(DecLayer l, int32_t T, int32_t dtype, int64_t B
   dec_layer_setup(l, h, true, static_cast<char*>(ws));
   l.acc = acc;
   l.item0 = 0;
+  l.step0 = 0;
   h.n_layers = 1;
   h.total_items = (int64_t)l.nrb * l.nkc;
+  h.total_steps = (int64_t)l.nrb * l.nk4;
   const int64_t acc_elems = acc ? (int64_t)2 * T * 2 * B * l.N * 2 : 0;
   return hip_status(launch_decode(h, l, nullptr, l.nkc > 1, B * (int64_t)l.N, acc != nullptr, acc_elems,
                                   acc, stream));
@@ -89,6 +92,7 @@ struct GroupTableHeader {
   DecHeader h;
   int32_t any_split, pad0_;
   int64_t max_BN;
+  int64_t pad1_;
 };
 static_assert(sizeof(GroupTableHeader) % 16 == 0, "table header alignment");
 
@@ -139,7 +143,7 @@ const char* fairy2i_status_string(fairy2i_status s) {
   }
 }
 
-int32_t fairy2i_abi_version(void) { return 3; }
+int32_t fairy2i_abi_version(void) { return 4; }
 
 fairy2i_status fairy2i_to_widely_linear(const float* A, int64_t rows, int64_t cols, float* U,
                                         float* W, void* stream) {
@@ -334,16 +338,27 @@ static int group_mode(const fairy2i_wl_layer* layers, int32_t dtype) {
   return layers[0].layout == FAIRY2I_LAYOUT_TILED_FP4 ? kModeBf16F4 : dec_mode(dtype);
 }
 
+// Whether a checked group runs every layer of at most kMaxFullKSteps steps
+// as one work item per row block: on the fp4 path, when the group has
+// enough row blocks to keep every wave busy without K slices.
+static bool group_full_k(const fairy2i_wl_layer* layers, int32_t n_layers, const DecHeader& h) {
+  if (h.mode != kModeBf16F4) return false;
+  int64_t rbs = 0;
+  for (int32_t i = 0; i < n_layers; ++i) rbs += (layers[i].N + 15) / 16;
+  return rbs >= kFullKMinItems;
+}
+
 size_t fairy2i_wl_group_workspace_bytes(const fairy2i_wl_layer* layers, int32_t n_layers, int32_t T,
                                         int32_t dtype, int64_t B) {
   if (check_group(layers, n_layers, T, dtype, B) != FAIRY2I_OK) return 0;
   const DecHeader h = dec_header(T, group_mode(layers, dtype), B, false);
+  const bool full_k = group_full_k(layers, n_layers, h);
   size_t total = 0;
   for (int32_t i = 0; i < n_layers; ++i) {
     DecLayer l{};
     l.N = (int32_t)layers[i].N;
     l.K = (int32_t)layers[i].K;
-    total += dec_layer_setup(l, h, false, nullptr);
+    total += dec_layer_setup(l, h, false, nullptr, full_k);
   }
   return total;
 }
@@ -360,18 +375,31 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
   auto* hdr = static_cast<GroupTableHeader*>(table);
   auto* tab = reinterpret_cast<DecLayer*>(hdr + 1);
   DecHeader h = dec_header(T, group_mode(layers, dtype), B, false);
+  const bool full_k = group_full_k(layers, n_layers, h);
   char* ws = static_cast<char*>(workspace);
-  int64_t items = 0;
+  // descriptors in table order; on the fp4 path the table lists the layers by
+  // decreasing work-item length (stable), so that the blocks of the product
+  // kernel claim their long items first and end on short ones
+  std::vector<DecLayer> ls((size_t)n_layers);
+  for (int32_t i = 0; i < n_layers; ++i) {
+    const fairy2i_wl_layer& L = layers[i];
+    DecLayer& l = ls[(size_t)i];
+    l = dec_layer(L.codes_U, L.scales_U, L.codes_W, L.scales_W, L.N, L.K, L.x, L.x_scale, L.y);
+    l.tiled = L.layout != FAIRY2I_LAYOUT_D3 ? 1 : 0;
+    ws += dec_layer_setup(l, h, false, ws, full_k);
+    l.acc = nullptr;
+  }
+  if (h.mode == kModeBf16F4)
+    std::stable_sort(ls.begin(), ls.end(), [](const DecLayer& a, const DecLayer& b) { return a.kc4 > b.kc4; });
+  int64_t items = 0, steps = 0;
   int any_split = 0;
   int64_t max_BN = 0;
   for (int32_t i = 0; i < n_layers; ++i) {
-    const fairy2i_wl_layer& L = layers[i];
-    DecLayer l = dec_layer(L.codes_U, L.scales_U, L.codes_W, L.scales_W, L.N, L.K, L.x, L.x_scale, L.y);
-    l.tiled = L.layout != FAIRY2I_LAYOUT_D3 ? 1 : 0;
-    ws += dec_layer_setup(l, h, false, ws);
-    l.acc = nullptr;
+    DecLayer l = ls[(size_t)i];
     l.item0 = items;
+    l.step0 = steps;
     items += (int64_t)l.nrb * l.nkc;
+    steps += (int64_t)l.nrb * l.nk4;
     if (l.nkc > 1) any_split = 1;
     if (B * (int64_t)l.N > max_BN) max_BN = B * (int64_t)l.N;
     tab[i] = l;
@@ -383,6 +411,7 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
   hdr->abi = (uint32_t)fairy2i_abi_version();
   h.n_layers = n_layers;
   h.total_items = items;
+  h.total_steps = steps;
   hdr->h = h;
   hdr->any_split = any_split;
   hdr->max_BN = max_BN;

@@ -33,6 +33,7 @@ struct DecLayer {
   int32_t tiled;             // codes in a tiled layout (tiled or fp4 tiled; else D3)
   int32_t pad_;
   int64_t item0;             // index of this layer's first work item
+  int64_t step0;             // 256-code steps of all work items before item0
 };
 
 struct DecHeader {
@@ -42,6 +43,7 @@ struct DecHeader {
   int32_t kernel;  // kKernelReg or kKernelStream
   int32_t pad_;
   int64_t total_items;
+  int64_t total_steps;  // 256-code steps of all work items
 };
 
 int dec_ntile(int mode, int64_t B);
@@ -55,7 +57,11 @@ DecHeader dec_header(int T, int mode, int64_t B, bool export_acc);
 // Fill the geometry fields of `l` (N, K set) for header h and return its
 // workspace bytes; with `ws` non-null also carve xf, xs, part out of it.
 // `single`: a one-layer call (slices chosen to give the GPU enough items).
-size_t dec_layer_setup(DecLayer& l, const DecHeader& h, bool single, char* ws);
+// `full_k`: a group with enough row blocks that a layer of at most
+// kMaxFullKSteps steps is not split along K (no partials, no reduction).
+constexpr int kMaxFullKSteps = 32;
+constexpr int64_t kFullKMinItems = 12288;
+size_t dec_layer_setup(DecLayer& l, const DecHeader& h, bool single, char* ws, bool full_k = false);
 
 // The fp8 x fp4 path (decode_f4.hip): activation operand and product
 // launches of a kModeBf16F4 call (errors are left for hipGetLastError).

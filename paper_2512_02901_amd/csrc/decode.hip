@@ -705,11 +705,13 @@ DecHeader dec_header(int T, int mode, int64_t B, bool export_acc) {
   return h;
 }
 
-size_t dec_layer_setup(DecLayer& l, const DecHeader& h, bool single, char* ws) {
+size_t dec_layer_setup(DecLayer& l, const DecHeader& h, bool single, char* ws, bool full_k) {
   l.nrb = (int32_t)((l.N + 15) / 16);
   l.nk4 = (int32_t)((l.K + 255) / 256);
   if (h.kernel == kKernelReg) {
     l.kc4 = kRegKc4;
+  } else if (full_k && l.nk4 <= kMaxFullKSteps) {
+    l.kc4 = l.nk4;  // one work item per row block
   } else {
     // slices of up to 8 steps (2048 codes); a single layer gets smaller
     // slices while that is needed to give the GPU ~2048 work items

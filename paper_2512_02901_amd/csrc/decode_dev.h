@@ -107,6 +107,31 @@ __device__ inline int find_layer(const DecLayer* tab, int n, int64_t item) {
   return lo;
 }
 
+// First work item whose first 256-code step is at or after step s (items
+// cover steps in table order; an item of row block rb and K slice kc of a
+// layer starts at step0 + rb nk4 + kc kc4).  total_items when s is past the
+// last step.  L is the layer from the table holding step s, or the only
+// layer of a single-layer call.
+__device__ inline int64_t item_at_step(const DecLayer& L, int64_t s, const DecHeader& h) {
+  if (s >= h.total_steps) return h.total_items;
+  const int64_t local = s - L.step0;
+  const int64_t rb = local / L.nk4;
+  const int rem = (int)(local - rb * L.nk4);
+  const int kc = (rem + L.kc4 - 1) / L.kc4;  // kc == nkc rolls over into the next row block (or layer)
+  return L.item0 + rb * L.nkc + kc;
+}
+
+// Layer holding step s (wave-uniform): the last layer whose step0 <= s.
+__device__ inline int find_layer_by_step(const DecLayer* tab, int n, int64_t s) {
+  int lo = 0, hi = n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (uniform64(tab[mid].step0) <= s) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
 // A descriptor from the table, with every field forced wave-uniform so that
 // pointers and buffer descriptors live in scalar registers.  Field by field,
 // so the copy never goes through memory.
@@ -137,6 +162,7 @@ __device__ inline DecLayer load_layer(const DecLayer* p) {
   o.tiled = uniform(p->tiled);
   o.pad_ = 0;
   o.item0 = uniform64(p->item0);
+  o.step0 = uniform64(p->step0);
   return o;
 }
 

@@ -43,21 +43,24 @@ constexpr int kTokensPerTile = 2;      // 8 operand columns per token
 // e4m3 (OCP fp8: 1 sign, 4 exponent bits with bias 7, 3 mantissa bits, no
 // infinities, largest finite 448) code of v rounded to nearest, ties to even,
 // for |v| < 2^8 + 2^4 (the largest result is 2^8).  q receives the rounded
-// value as a float.
+// value as a float.  Both roundings are computed and one is selected, so the
+// conversion has no branches.
 __device__ inline uint32_t e4m3_rne(float v, float& q) {
   const uint32_t u = __float_as_uint(v);
   const uint32_t a = u & 0x7FFFFFFFu;
-  uint32_t c;
-  if (a < 0x3C800000u) {  // |v| < 2^-6: subnormal grid 2^-9, code = |v| / 2^-9 (8 is the smallest normal)
-    const float m = rintf(__uint_as_float(a) * 512.0f);
-    c = (uint32_t)m;
-    q = __uint_as_float(__float_as_uint(m * 0x1p-9f) | (u & 0x80000000u));
-  } else {                // keep 3 mantissa bits, ties to even; a carry moves into the exponent
-    const uint32_t r = a + 0x7FFFFu + ((a >> 20) & 1u);
-    c = (r >> 20) - (120u << 3);  // float32 exponent bias 127 -> e4m3 bias 7
-    q = __uint_as_float((r & 0xFFF00000u) | (u & 0x80000000u));
-  }
-  return c ? (c | ((u >> 24) & 0x80u)) : 0u;
+  const uint32_t sgn = u & 0x80000000u;
+  // |v| >= 2^-6: keep 3 mantissa bits, ties to even; a carry moves into the exponent
+  const uint32_t r = a + 0x7FFFFu + ((a >> 20) & 1u);
+  const uint32_t cn = (r >> 20) - (120u << 3);  // float32 exponent bias 127 -> e4m3 bias 7
+  const float qn = __uint_as_float((r & 0xFFF00000u) | sgn);
+  // |v| < 2^-6: the subnormal grid 2^-9, code = |v| / 2^-9 (8 is the smallest normal)
+  const float m = rintf(__uint_as_float(a) * 512.0f);
+  const uint32_t cs = (uint32_t)m;
+  const float qs = __uint_as_float(__float_as_uint(m * 0x1p-9f) | sgn);
+  const bool sub = a < 0x3C800000u;
+  const uint32_t c = sub ? cs : cn;
+  q = sub ? qs : qn;
+  return c ? (c | (sgn >> 24)) : 0u;
 }
 
 // The (hi, lo) digit codes of v, |v| < 2^8.
@@ -68,8 +71,7 @@ __device__ inline void digit_pair(float v, uint32_t& hi, uint32_t& lo) {
 }
 
 // One block per (activation tile, layer): the largest magnitude of each of
-// the tile's tokens, then one thread per (16-code run, token): the run's
-// eight 16-byte chunks in operand order.
+// the tile's tokens, then the digits of every value.
 __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_kernel(DecHeader h, DecLayer inl,
                                                                      const DecLayer* __restrict__ tab) {
   const DecLayer L = tab ? load_layer(tab + blockIdx.y) : inl;
@@ -118,49 +120,56 @@ __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_kernel(DecHeader h
     if (tk < ntok && b < h.B) L.xs[b] = g > 0.0f ? ldexpf(1.0f, -S) : 0.0f;
   }
   __syncthreads();
-  const int nrun = L.nk4 * 16;  // runs of 16 codes: run r holds codes 16 r .. 16 r + 15
-  uint4* dst = reinterpret_cast<uint4*>(L.xf) + (int64_t)tile * nrun * h.nc;
-  for (int idx = threadIdx.x; idx < nrun * ntok; idx += blockDim.x) {
-    const int tk = idx % ntok, r = idx / ntok;
+  // one thread per (16-code run, token, component, half run): 8 values, whose
+  // four digit bytes per band go to the halves of the run's 16-byte chunks
+  const int nrun = L.nk4 * 16;  // run r holds codes 16 r .. 16 r + 15 (= 256 step + 64 d + 16 g for r = 16 step + 4 d + g)
+  uint8_t* dst = reinterpret_cast<uint8_t*>(L.xf) + (int64_t)tile * nrun * h.nc * 16;
+  for (int idx = threadIdx.x; idx < nrun * ntok * 4; idx += blockDim.x) {
+    const int hf = idx & 1, c = (idx >> 1) & 1, tk = (idx >> 2) % ntok, r = (idx >> 2) / ntok;
     const int b = tpt * tile + tk;
-    const int k0 = 16 * r;  // = 256 step + 64 d + 16 g for r = 16 step + 4 d + g
-    uint32_t out[2][4][4] = {};  // [band][hi re, hi im, lo re, lo im][word]
-    if (b < h.B && k0 < K) {  // K % 64 == 0: the whole run is in range
-      int v[2][16];
-      load_run16<kModeBf16>(L.x, vec, ((int64_t)b * K + k0) * 2, 0, v[0]);
-      load_run16<kModeBf16>(L.x, vec, ((int64_t)b * K + k0) * 2, 1, v[1]);
+    const int k0 = 16 * r + 8 * hf;
+    uint32_t out[2][2][2] = {};  // [band][hi, lo][word]: bytes e = 0..7 of the half chunk
+    if (b < h.B && k0 < K) {  // K % 64 == 0: the whole half run is in range
+      const uint16_t* p = static_cast<const uint16_t*>(L.x) + ((int64_t)b * K + k0) * 2;
+      uint32_t w[8];  // (re, im) bf16 pairs of the 8 complex values
+      if (vec) {
+        const uint4 v0 = reinterpret_cast<const uint4*>(p)[0], v1 = reinterpret_cast<const uint4*>(p)[1];
+        w[0] = v0.x; w[1] = v0.y; w[2] = v0.z; w[3] = v0.w;
+        w[4] = v1.x; w[5] = v1.y; w[6] = v1.z; w[7] = v1.w;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) w[e] = (uint32_t)p[2 * e] | ((uint32_t)p[2 * e + 1] << 16);
+      }
       const int S = sh_S[tk];
 #pragma unroll
-      for (int c = 0; c < 2; ++c)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const float x = ldexpf(__uint_as_float((uint32_t)v[c][e] << 16), S);  // exact: |x| < 2^8
-          const int band = fabsf(x) < 1.0f ? 1 : 0;
-          uint32_t hi, lo;
-          digit_pair(band ? x * kBand2Scale : x, hi, lo);
-          const int sh = 8 * (e & 3);
-          if (band) {
-            out[1][c][e >> 2] |= hi << sh;
-            out[1][2 + c][e >> 2] |= lo << sh;
-          } else {
-            out[0][c][e >> 2] |= hi << sh;
-            out[0][2 + c][e >> 2] |= lo << sh;
-          }
-        }
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t bits = c ? (w[e] & 0xFFFF0000u) : (w[e] << 16);
+        const float x = ldexpf(__uint_as_float(bits), S);  // exact: |x| < 2^8
+        const bool small = fabsf(x) < 1.0f;
+        uint32_t hi, lo;
+        digit_pair(small ? x * kBand2Scale : x, hi, lo);
+        const int sh = 8 * (e & 3);
+        const uint32_t hs = hi << sh, ls = lo << sh;
+        out[0][0][e >> 2] |= small ? 0u : hs;
+        out[0][1][e >> 2] |= small ? 0u : ls;
+        out[1][0][e >> 2] |= small ? hs : 0u;
+        out[1][1][e >> 2] |= small ? ls : 0u;
+      }
     }
+    // column 8 tk + 4 band + 2 digit + c of run r; this half is bytes 8 hf .. 8 hf + 7 of its chunk
 #pragma unroll
     for (int bd = 0; bd < 2; ++bd)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        dst[(int64_t)r * h.nc + 8 * tk + 4 * bd + j] =
-            make_uint4(out[bd][j][0], out[bd][j][1], out[bd][j][2], out[bd][j][3]);
+      for (int dg = 0; dg < 2; ++dg)
+        *reinterpret_cast<uint2*>(dst + ((int64_t)r * h.nc + 8 * tk + 4 * bd + 2 * dg + c) * 16 + 8 * hf) =
+            make_uint2(out[bd][dg][0], out[bd][dg][1]);
   }
 }
 
 // ------------------------------------------- streaming kernel, fp4 codes ---
 // The same ring, cursors and work items as above, for codes in the fp4 tiled
 // layout and bf16 activations as two e4m3 digits per value (hi, lo; see the
-// fp4 prep kernel above), four tokens per 16-column tile.  With the
+// fp4 prep kernel above), two tokens per 16-column tile.  With the
 // code bits (p, q) = (bit 0, bit 1) of code k, i^k = (1 - 2q)(1 - p) +
 // i (1 - 2q) p (Eq. realify-ops: b_re = (1 - 2q)(1 - p), b_im = (1 - 2q) p),
 // the kernel contracts two e2m1 operands with v_mfma_f32_16x16x128_f8f6f4:
@@ -274,9 +283,23 @@ __global__ __launch_bounds__((64 * F4Cfg<T, NT * XW>::WAVES)) void dec_stream_f4
   if (threadIdx.x < 4) reinterpret_cast<uint32_t*>(zero16)[threadIdx.x] = 0u;
   if (threadIdx.x == 0) claim_ctr = (uint32_t)WAVES;  // wave w starts with item b0 + w
   __syncthreads();
-  // the block's items: an equal share of the call's
-  const int64_t b0 = uniform64((int64_t)blockIdx.x * h.total_items / gridDim.x);
-  const int nb = uniform((int)(uniform64(((int64_t)blockIdx.x + 1) * h.total_items / gridDim.x) - b0));
+  // the block's items: those starting in an equal share of the call's steps
+  // (the table lists layers by decreasing item length, so a block claims its
+  // longest items first and its range ends with short ones)
+  int64_t b0, b1;
+  {
+    const int64_t s0 = (int64_t)blockIdx.x * h.total_steps / gridDim.x;
+    const int64_t s1 = ((int64_t)blockIdx.x + 1) * h.total_steps / gridDim.x;
+    if (tab) {
+      b0 = item_at_step(load_layer(tab + find_layer_by_step(tab, h.n_layers, s0)), s0, h);
+      b1 = item_at_step(load_layer(tab + find_layer_by_step(tab, h.n_layers, s1 < h.total_steps ? s1 : s0)), s1, h);
+    } else {
+      b0 = item_at_step(inl, s0, h);
+      b1 = item_at_step(inl, s1, h);
+    }
+  }
+  b0 = uniform64(b0);
+  const int nb = uniform((int)(uniform64(b1) - b0));
   if (wave >= nb) return;
   const int64_t i0 = b0 + wave;
   const uint32_t ctr_addr = lds_addr(&claim_ctr);

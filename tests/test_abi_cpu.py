@@ -42,7 +42,7 @@ def test_status_strings(lib):
     for s in range(8):
         assert lib.fairy2i_status_string(s)
     assert lib.fairy2i_status_string(99) == b"unknown status"
-    assert lib.fairy2i_abi_version() == 3
+    assert lib.fairy2i_abi_version() == 4
 
 
 def test_to_widely_linear_validation(lib):
