@@ -36,6 +36,7 @@ namespace {
 // j = 0: hi of Re x, 1: hi of Im x, 2: lo of Re x, 3: lo of Im x.  The
 // output factor of token b is 2^-S_b (0 for an all-zero token).
 constexpr int kPrepF4Threads = 512;
+constexpr int kPrepUnroll = 4;     // loads a prep thread issues before using them
 constexpr float kLoScale = 32.0f;     // lo digit = residual of hi times 2^5
 constexpr float kBand2Scale = 256.0f;  // second band: values below 1, times 2^8
 constexpr int kTokensPerTile = 2;      // 8 operand columns per token
@@ -83,6 +84,8 @@ __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_kernel(DecHeader h
   __shared__ float red[kPrepF4Threads / 64][tpt];
   __shared__ int sh_S[tpt];
   const int wave = threadIdx.x >> 6;
+  // every thread issues all its loads of a round before reducing them
+  constexpr int U = kPrepUnroll;
 #pragma unroll
   for (int tk = 0; tk < tpt; ++tk) {
     const int b = tpt * tile + tk;
@@ -91,12 +94,20 @@ __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_kernel(DecHeader h
       const uint16_t* xb = static_cast<const uint16_t*>(L.x) + (int64_t)b * K * 2;
       if (vec) {
         const uint4* xv = reinterpret_cast<const uint4*>(xb);
-        for (int i = threadIdx.x; i < K / 4; i += blockDim.x) {  // 8 bf16 (4 complex) per vector
-          const uint4 w = xv[i];
-          const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
+        for (int i0 = 0; i0 < K / 4; i0 += U * kPrepF4Threads) {  // 8 bf16 (4 complex) per vector
+          uint4 w[U];
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
-            m = fmaxf(m, fmaxf(fabsf(__uint_as_float(wd[j] << 16)), fabsf(__uint_as_float(wd[j] & 0xFFFF0000u))));
+          for (int u = 0; u < U; ++u) {
+            const int i = i0 + u * kPrepF4Threads + threadIdx.x;
+            w[u] = i < K / 4 ? xv[i] : make_uint4(0u, 0u, 0u, 0u);
+          }
+#pragma unroll
+          for (int u = 0; u < U; ++u) {
+            const uint32_t wd[4] = {w[u].x, w[u].y, w[u].z, w[u].w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+              m = fmaxf(m, fmaxf(fabsf(__uint_as_float(wd[j] << 16)), fabsf(__uint_as_float(wd[j] & 0xFFFF0000u))));
+          }
         }
       } else {
         for (int i = threadIdx.x; i < 2 * K; i += blockDim.x) m = fmaxf(m, fabsf(__uint_as_float((uint32_t)xb[i] << 16)));
@@ -124,45 +135,59 @@ __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_kernel(DecHeader h
   // four digit bytes per band go to the halves of the run's 16-byte chunks
   const int nrun = L.nk4 * 16;  // run r holds codes 16 r .. 16 r + 15 (= 256 step + 64 d + 16 g for r = 16 step + 4 d + g)
   uint8_t* dst = reinterpret_cast<uint8_t*>(L.xf) + (int64_t)tile * nrun * h.nc * 16;
-  for (int idx = threadIdx.x; idx < nrun * ntok * 4; idx += blockDim.x) {
-    const int hf = idx & 1, c = (idx >> 1) & 1, tk = (idx >> 2) % ntok, r = (idx >> 2) / ntok;
-    const int b = tpt * tile + tk;
-    const int k0 = 16 * r + 8 * hf;
-    uint32_t out[2][2][2] = {};  // [band][hi, lo][word]: bytes e = 0..7 of the half chunk
-    if (b < h.B && k0 < K) {  // K % 64 == 0: the whole half run is in range
-      const uint16_t* p = static_cast<const uint16_t*>(L.x) + ((int64_t)b * K + k0) * 2;
-      uint32_t w[8];  // (re, im) bf16 pairs of the 8 complex values
-      if (vec) {
-        const uint4 v0 = reinterpret_cast<const uint4*>(p)[0], v1 = reinterpret_cast<const uint4*>(p)[1];
-        w[0] = v0.x; w[1] = v0.y; w[2] = v0.z; w[3] = v0.w;
-        w[4] = v1.x; w[5] = v1.y; w[6] = v1.z; w[7] = v1.w;
-      } else {
+  for (int idx0 = 0; idx0 < nrun * ntok * 4; idx0 += U * kPrepF4Threads) {
+    // the loads of all U units of this thread first, then their digits
+    uint32_t wu[U][8];  // (re, im) bf16 pairs of each unit's 8 complex values
 #pragma unroll
-        for (int e = 0; e < 8; ++e) w[e] = (uint32_t)p[2 * e] | ((uint32_t)p[2 * e + 1] << 16);
-      }
-      const int S = sh_S[tk];
+    for (int u = 0; u < U; ++u) {
+      const int idx = idx0 + u * kPrepF4Threads + threadIdx.x;
+      const int hf = idx & 1, tk = (idx >> 2) % ntok, r = (idx >> 2) / ntok;
+      const int b = tpt * tile + tk, k0 = 16 * r + 8 * hf;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const uint32_t bits = c ? (w[e] & 0xFFFF0000u) : (w[e] << 16);
-        const float x = ldexpf(__uint_as_float(bits), S);  // exact: |x| < 2^8
-        const bool small = fabsf(x) < 1.0f;
-        uint32_t hi, lo;
-        digit_pair(small ? x * kBand2Scale : x, hi, lo);
-        const int sh = 8 * (e & 3);
-        const uint32_t hs = hi << sh, ls = lo << sh;
-        out[0][0][e >> 2] |= small ? 0u : hs;
-        out[0][1][e >> 2] |= small ? 0u : ls;
-        out[1][0][e >> 2] |= small ? hs : 0u;
-        out[1][1][e >> 2] |= small ? ls : 0u;
+      for (int e = 0; e < 8; ++e) wu[u][e] = 0u;
+      if (idx < nrun * ntok * 4 && b < h.B && k0 < K) {  // K % 64 == 0: the whole half run is in range
+        const uint16_t* p = static_cast<const uint16_t*>(L.x) + ((int64_t)b * K + k0) * 2;
+        if (vec) {
+          const uint4 v0 = reinterpret_cast<const uint4*>(p)[0], v1 = reinterpret_cast<const uint4*>(p)[1];
+          wu[u][0] = v0.x; wu[u][1] = v0.y; wu[u][2] = v0.z; wu[u][3] = v0.w;
+          wu[u][4] = v1.x; wu[u][5] = v1.y; wu[u][6] = v1.z; wu[u][7] = v1.w;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) wu[u][e] = (uint32_t)p[2 * e] | ((uint32_t)p[2 * e + 1] << 16);
+        }
       }
     }
-    // column 8 tk + 4 band + 2 digit + c of run r; this half is bytes 8 hf .. 8 hf + 7 of its chunk
 #pragma unroll
-    for (int bd = 0; bd < 2; ++bd)
+    for (int u = 0; u < U; ++u) {
+      const int idx = idx0 + u * kPrepF4Threads + threadIdx.x;
+      if (idx >= nrun * ntok * 4) break;
+      const int hf = idx & 1, c = (idx >> 1) & 1, tk = (idx >> 2) % ntok, r = (idx >> 2) / ntok;
+      uint32_t out[2][2][2] = {};  // [band][hi, lo][word]: bytes e = 0..7 of the half chunk
+      {
+        const int S = sh_S[tk];
 #pragma unroll
-      for (int dg = 0; dg < 2; ++dg)
-        *reinterpret_cast<uint2*>(dst + ((int64_t)r * h.nc + 8 * tk + 4 * bd + 2 * dg + c) * 16 + 8 * hf) =
-            make_uint2(out[bd][dg][0], out[bd][dg][1]);
+        for (int e = 0; e < 8; ++e) {
+          const uint32_t bits = c ? (wu[u][e] & 0xFFFF0000u) : (wu[u][e] << 16);
+          const float x = ldexpf(__uint_as_float(bits), S);  // exact: |x| < 2^8
+          const bool small = fabsf(x) < 1.0f;
+          uint32_t hi, lo;
+          digit_pair(small ? x * kBand2Scale : x, hi, lo);
+          const int sh = 8 * (e & 3);
+          const uint32_t hs = hi << sh, ls = lo << sh;
+          out[0][0][e >> 2] |= small ? 0u : hs;
+          out[0][1][e >> 2] |= small ? 0u : ls;
+          out[1][0][e >> 2] |= small ? hs : 0u;
+          out[1][1][e >> 2] |= small ? ls : 0u;
+        }
+      }
+      // column 8 tk + 4 band + 2 digit + c of run r; this half is bytes 8 hf .. 8 hf + 7 of its chunk
+#pragma unroll
+      for (int bd = 0; bd < 2; ++bd)
+#pragma unroll
+        for (int dg = 0; dg < 2; ++dg)
+          *reinterpret_cast<uint2*>(dst + ((int64_t)r * h.nc + 8 * tk + 4 * bd + 2 * dg + c) * 16 + 8 * hf) =
+              make_uint2(out[bd][dg][0], out[bd][dg][1]);
+    }
   }
 }
 
