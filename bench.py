@@ -374,6 +374,65 @@ def per_layer_bench(f2, synth, torch, dev, T=2, min_bytes=512e6, reps=5):
     return out
 
 
+def block_bench(f2, synth, torch, dev, T=2, ctx=2048, reps=50):
+    """One decode token through one widely-linear LLaMA-2-7B decoder block
+    (fairy2i_block_decode: n = 2048 complex, 32 heads, FFN 5504 complex,
+    T = 2 seeded synthetic weights) attending over `ctx` cached positions:
+    time per token from plain calls and from a HIP graph of the calls, and
+    the bytes a token reads (packed codes of the seven projections and the
+    key/value caches)."""
+    n, f, H = 2048, 5504, 32
+    shapes = {"q": (n, n), "k": (n, n), "v": (n, n), "o": (n, n), "gate": (f, n), "up": (f, n), "down": (n, f)}
+    layers, code_bytes = {}, 0
+    for i, (name, (N, K)) in enumerate(shapes.items()):
+        A = synth.torch_llama_weight(2 * N, 2 * K, 9000 + i, dev)
+        U, W = f2.to_widely_linear(A)
+        del A
+        cu, su = f2.quantize(U, T)
+        cw, sw = f2.quantize(W, T)
+        del U, W
+        layers[name] = (f2.repack_tiled_fp4(cu), su, f2.repack_tiled_fp4(cw), sw)
+        code_bytes += 2 * T * N * K // 4
+    g = torch.Generator(device=dev)
+    g.manual_seed(9100)
+    norm_a = 1.0 + 0.1 * torch.randn(2 * n, generator=g, device=dev)
+    norm_m = 1.0 + 0.1 * torch.randn(2 * n, generator=g, device=dev)
+    blk = f2.WlBlock(layers, norm_a, norm_m, n=n, n_ff=f, n_heads=H, T=T, max_ctx=ctx)
+    kc = torch.randn(H, ctx, n // H, generator=g, device=dev, dtype=torch.complex64)
+    vc = torch.randn(H, ctx, n // H, generator=g, device=dev, dtype=torch.complex64)
+    x = torch.randn(1, n, generator=g, device=dev, dtype=torch.complex64)
+    y = torch.empty(1, n, dtype=torch.complex64, device=dev)
+    pos = ctx - 1
+
+    def call():
+        blk.decode(x, kc, vc, pos, out=y)
+    warm_up(call, torch, 10, min_s=0.3)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(10):
+            call()
+    warm_up(graph.replay, torch, 3, min_s=0.3)
+    e0.record()
+    for _ in range(reps // 10):
+        graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    us_graph = e0.elapsed_time(e1) * 1e3 / (10 * (reps // 10))
+    kv_bytes = 2 * H * ctx * (n // H) * 8
+    return {"workload": f"one decode token, LLaMA-2-7B block shape (4096 hidden, 32 heads, 11008 FFN), T={T}, "
+                        f"context {ctx}", "us_per_token": round(us, 2), "us_per_token_graph": round(us_graph, 2),
+            "code_bytes": code_bytes, "kv_cache_bytes": kv_bytes,
+            "GBs_graph": round((code_bytes + kv_bytes) / (us_graph * 1e-6) / 1e9, 1)}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -490,6 +549,7 @@ def main():
         del grp3, layers3, f3
         torch.cuda.empty_cache()
         result["per_layer"] = per_layer_bench(f2, synth, torch, dev, T)
+        result["decoder_block"] = block_bench(f2, synth, torch, dev, T)
         pf = prefill_bench(f2, synth, torch, dev)
         g = pf["gate"]
         # headline: the 11008x4096 (gate/up) shape; half of the dense MACs multiply structural zeros

@@ -349,6 +349,83 @@ fairy2i_status fairy2i_wl_matmul_group_timed(const void* table, const void* tabl
                                              void* stream, void* const* events);
 
 /*
+ * One widely-linear decoder block for one decode token (Sec. 1: every linear
+ * layer of the LLaMA-style block converted; Sec. 3.1, self-attention
+ * paragraph, Eq. hermitian-score).  With x the complex residual stream
+ * (n entries standing for the 2n real components [Re x ; Im x]):
+ *   z   = bf16(RMSNorm(x; norm_attn))            over the 2n real components
+ *   q, k, v = the q, k, v widely-linear layers of z (grouped fp4 decode)
+ *   q, k turned by the rotary embedding: entry j of a head times
+ *        e^{i pos theta_j}, theta_j = rope_base^(-2 j / dh)
+ *   k, v stored at position pos of the caches
+ *   per head: s_m = Re(q^H k_m) / sqrt(dh) for m = 0 .. pos, p = softmax(s),
+ *        o = sum_m p_m v_m;  o rounded to bf16
+ *   h1  = x + o-layer(o)
+ *   z2  = bf16(RMSNorm(h1; norm_mlp)); g, u = gate/up layers of z2
+ *   act = bf16(silu(Re g) Re u + i silu(Im g) Im u)
+ *   out = h1 + down-layer(act)
+ * A head owns dc = n / n_heads consecutive complex entries; entry j holds the
+ * head's real dims j and j + dc (dh = 2 dc), which makes the Hermitian score
+ * the head's real dot-product score and the rotary embedding the half-split
+ * rotation of those dims.  Caches: complex64 [n_heads][max_ctx][dc] each,
+ * positions 0 .. pos - 1 filled by earlier calls.  All pointers are device
+ * memory except where noted.  Reductions run in a fixed order: results are
+ * bitwise reproducible.
+ *
+ * Use: fill fairy2i_block_desc (codes in the fp4 tiled layout of
+ * fairy2i_repack_tiled_fp4, B = 1); size the workspace with
+ * fairy2i_block_workspace_bytes and the plan with fairy2i_block_plan_bytes;
+ * fairy2i_block_build_plan (host only, enqueues nothing) writes the plan into
+ * HOST memory; copy those bytes unchanged to device memory; then each
+ * fairy2i_block_decode(plan, plan_device, x, k_cache, v_cache, pos, out,
+ * stream) runs the block for one token.  The workspace, the weights and both
+ * plan copies must stay alive and unchanged while calls that use them run;
+ * calls sharing a workspace must not overlap.
+ * Errors: FAIRY2I_ERR_NULL; FAIRY2I_ERR_SHAPE for sizes that are not
+ * positive, n % n_heads != 0, dc > 256, n or n_ff not a multiple of 64, T
+ * out of range, or pos outside [0, max_ctx); FAIRY2I_ERR_WORKSPACE;
+ * FAIRY2I_ERR_UNSUPPORTED for a plan not built by this library version;
+ * FAIRY2I_ERR_HIP.
+ */
+typedef struct fairy2i_block_desc {
+  int64_t n;          /* complex width of the residual stream (2n real)        */
+  int64_t n_ff;       /* complex width of the gate/up outputs and down input   */
+  int32_t n_heads;    /* attention heads                                       */
+  int32_t T;          /* stages of every projection                            */
+  int64_t max_ctx;    /* positions each cache holds                            */
+  float eps;          /* RMSNorm epsilon                                       */
+  int32_t reserved;   /* 0                                                     */
+  double rope_base;   /* rotary base                                           */
+  /* per projection, in the order q, k, v, o, gate, up, down: fp4 tiled codes
+     and float32 [T][2] scales of U and W */
+  const uint8_t* codes_U[7];
+  const float* scales_U[7];
+  const uint8_t* codes_W[7];
+  const float* scales_W[7];
+  const float* norm_attn;  /* float32 [2n]: gains of Re parts, then of Im parts */
+  const float* norm_mlp;   /* float32 [2n] */
+} fairy2i_block_desc;
+
+size_t fairy2i_block_workspace_bytes(const fairy2i_block_desc* desc);
+size_t fairy2i_block_plan_bytes(const fairy2i_block_desc* desc);
+fairy2i_status fairy2i_block_build_plan(const fairy2i_block_desc* desc, void* workspace, size_t workspace_bytes,
+                                        void* plan, size_t plan_bytes);
+fairy2i_status fairy2i_block_decode(const void* plan, const void* plan_device, const float* x /* [n] complex64 */,
+                                    float* k_cache, float* v_cache, int64_t pos, float* out /* [n] complex64 */,
+                                    void* stream);
+/*
+ * Test export: the device addresses of the block's intermediate vectors in
+ * its workspace, as the last fairy2i_block_decode on that workspace left
+ * them: ptrs[0..11] = z (bf16 pairs [n]), q after the rotary embedding
+ * (complex64 [n]), v (complex64 [n]), o (bf16 pairs [n]), o-layer output a,
+ * h1, z2 (bf16 pairs [n]), g, u (complex64 [n_ff]), act (bf16 pairs [n_ff]),
+ * down-layer output d (complex64 [n]), k before the rotary embedding
+ * (complex64 [n]).  Host-only; enqueues nothing.
+ * Errors: FAIRY2I_ERR_NULL; FAIRY2I_ERR_UNSUPPORTED for a foreign plan.
+ */
+fairy2i_status fairy2i_block_intermediates(const void* plan, void** ptrs);
+
+/*
  * Host-side self-check of the exact-mean rounding used by fairy2i_quantize
  * for the axis scales: *out = float32 nearest (ties to even) to
  * (sum of |values[i]|) / n_values, with the sum taken exactly; 0 when

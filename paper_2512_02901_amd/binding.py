@@ -46,6 +46,11 @@ _SIGNATURES = {
                                               _c_p, _c_size]),
     "fairy2i_wl_matmul_group": (_c_i32, [_c_p, _c_p, _c_p]),
     "fairy2i_wl_matmul_group_timed": (_c_i32, [_c_p, _c_p, _c_p, _c_p]),
+    "fairy2i_block_workspace_bytes": (_c_size, [_c_p]),
+    "fairy2i_block_plan_bytes": (_c_size, [_c_p]),
+    "fairy2i_block_build_plan": (_c_i32, [_c_p, _c_p, _c_size, _c_p, _c_size]),
+    "fairy2i_block_decode": (_c_i32, [_c_p, _c_p, _c_p, _c_p, _c_p, _c_i64, _c_p, _c_p]),
+    "fairy2i_block_intermediates": (_c_i32, [_c_p, _c_p]),
 }
 
 
@@ -54,6 +59,14 @@ class WlLayer(ctypes.Structure):
     _fields_ = [("codes_U", _c_p), ("scales_U", _c_p), ("codes_W", _c_p), ("scales_W", _c_p),
                 ("x", _c_p), ("x_scale", _c_p), ("y", _c_p), ("N", _c_i64), ("K", _c_i64),
                 ("layout", _c_i32), ("reserved", _c_i32)]
+
+
+class BlockDesc(ctypes.Structure):
+    """fairy2i_block_desc of include/fairy2i.h."""
+    _fields_ = [("n", _c_i64), ("n_ff", _c_i64), ("n_heads", _c_i32), ("T", _c_i32), ("max_ctx", _c_i64),
+                ("eps", ctypes.c_float), ("reserved", _c_i32), ("rope_base", ctypes.c_double),
+                ("codes_U", _c_p * 7), ("scales_U", _c_p * 7), ("codes_W", _c_p * 7), ("scales_W", _c_p * 7),
+                ("norm_attn", _c_p), ("norm_mlp", _c_p)]
 
 
 class Fairy2iError(RuntimeError):
@@ -410,3 +423,101 @@ class WlGroup:
         handles = (_c_p * 4)(*[e.cuda_event for e in events])
         _check(lib.fairy2i_wl_matmul_group_timed(ctypes.byref(self._table), _ptr(self.table_device), stream,
                                                  handles), "fairy2i_wl_matmul_group_timed")
+
+
+BLOCK_PROJ = ("q", "k", "v", "o", "gate", "up", "down")
+
+
+class WlBlock:
+    """One widely-linear decoder block for one decode token
+    (fairy2i_block_decode).  ``layers``: {name: (codes_U, scales_U, codes_W,
+    scales_W)} for q, k, v, o, gate, up, down, codes in the fp4 tiled layout
+    (repack_tiled_fp4); ``norm_attn``, ``norm_mlp``: float32 [2n] device
+    tensors.  Keeps the weights, the workspace and both plan copies alive."""
+
+    def __init__(self, layers, norm_attn, norm_mlp, n, n_ff, n_heads, T, max_ctx, eps=1e-5, rope_base=10000.0):
+        torch = _torch()
+        lib = load()
+        dev = norm_attn.device
+        d = BlockDesc()
+        d.n, d.n_ff, d.n_heads, d.T, d.max_ctx = n, n_ff, n_heads, T, max_ctx
+        d.eps, d.reserved, d.rope_base = eps, 0, rope_base
+        self._keep = []
+        for i, name in enumerate(BLOCK_PROJ):
+            cu, su, cw, sw = layers[name]
+            for t, nm, dt in ((cu, "codes_U", torch.uint8), (cw, "codes_W", torch.uint8),
+                              (su, "scales_U", torch.float32), (sw, "scales_W", torch.float32)):
+                _require(t, dt, f"{name}.{nm}", dev)
+            N = n_ff if name in ("gate", "up") else n
+            K = n_ff if name == "down" else n
+            need = repack_tiled_bytes(N, K, T)
+            if cu.numel() < need or cw.numel() < need or tuple(su.shape) != (T, 2) or tuple(sw.shape) != (T, 2):
+                raise ValueError(f"{name}: codes or scales do not match a {N}x{K} layer with T={T}")
+            d.codes_U[i], d.scales_U[i] = cu.data_ptr(), su.data_ptr()
+            d.codes_W[i], d.scales_W[i] = cw.data_ptr(), sw.data_ptr()
+            self._keep += [cu, su, cw, sw]
+        for t, nm in ((norm_attn, "norm_attn"), (norm_mlp, "norm_mlp")):
+            _require(t, torch.float32, nm, dev)
+            if t.numel() != 2 * n:
+                raise ValueError(f"{nm} must hold 2n = {2 * n} gains")
+        d.norm_attn, d.norm_mlp = norm_attn.data_ptr(), norm_mlp.data_ptr()
+        self._keep += [norm_attn, norm_mlp]
+        self.n, self.n_ff, self.n_heads, self.max_ctx = n, n_ff, n_heads, max_ctx
+        self._desc = d
+        wsb = int(lib.fairy2i_block_workspace_bytes(ctypes.byref(d)))
+        pb = int(lib.fairy2i_block_plan_bytes(ctypes.byref(d)))
+        if wsb == 0 or pb == 0:
+            raise Fairy2iError(ERR_SHAPE, "fairy2i_block_workspace_bytes")
+        self.workspace = torch.empty(wsb, dtype=torch.uint8, device=dev)
+        self._plan = (ctypes.c_uint8 * pb)()
+        _check(lib.fairy2i_block_build_plan(ctypes.byref(d), _ptr(self.workspace), wsb, ctypes.byref(self._plan), pb),
+               "fairy2i_block_build_plan")
+        self.plan_device = torch.frombuffer(bytearray(bytes(self._plan)), dtype=torch.uint8).to(dev)
+        torch.cuda.synchronize(dev)
+
+    BLOCK_INTERMEDIATES = (("z", "bf16", "n"), ("q_rot", "c64", "n"), ("v", "c64", "n"), ("o", "bf16", "n"),
+                           ("a", "c64", "n"), ("h1", "c64", "n"), ("z2", "bf16", "n"), ("g", "c64", "f"),
+                           ("u", "c64", "f"), ("act", "bf16", "f"), ("d", "c64", "n"), ("k", "c64", "n"))
+
+    def intermediates(self):
+        """Views of the workspace buffers that the last decode left
+        (fairy2i_block_intermediates): {name: tensor}, complex64 [len] or
+        bf16 [len, 2]."""
+        torch = _torch()
+        lib = load()
+        ptrs = (_c_p * 12)()
+        _check(lib.fairy2i_block_intermediates(ctypes.byref(self._plan), ptrs), "fairy2i_block_intermediates")
+        base = self.workspace.data_ptr()
+        out = {}
+        for (name, kind, ln), p in zip(self.BLOCK_INTERMEDIATES, ptrs):
+            count = self.n if ln == "n" else self.n_ff
+            off = int(p) - base
+            if kind == "c64":
+                out[name] = self.workspace[off:off + 8 * count].view(torch.complex64)
+            else:
+                out[name] = self.workspace[off:off + 4 * count].view(torch.bfloat16).view(count, 2)
+        return out
+
+    def decode(self, x, k_cache, v_cache, pos, out=None):
+        """x: complex64 [1, n]; caches complex64 [n_heads, max_ctx, n / n_heads];
+        returns out complex64 [1, n]."""
+        torch = _torch()
+        lib = load()
+        dev = self.plan_device.device
+        dc = self.n // self.n_heads
+        _require(x, torch.complex64, "x", dev)
+        if x.numel() != self.n:
+            raise ValueError(f"x must hold {self.n} complex entries")
+        for t, nm in ((k_cache, "k_cache"), (v_cache, "v_cache")):
+            _require(t, torch.complex64, nm, dev)
+            if tuple(t.shape) != (self.n_heads, self.max_ctx, dc):
+                raise ValueError(f"{nm} must have shape ({self.n_heads}, {self.max_ctx}, {dc})")
+        if out is None:
+            out = torch.empty((1, self.n), dtype=torch.complex64, device=dev)
+        else:
+            _require(out, torch.complex64, "out", dev)
+            if out.numel() != self.n:
+                raise ValueError(f"out must hold {self.n} complex entries")
+        _check(lib.fairy2i_block_decode(ctypes.byref(self._plan), _ptr(self.plan_device), _ptr(x), _ptr(k_cache),
+                                        _ptr(v_cache), int(pos), _ptr(out), _stream_ptr(x)), "fairy2i_block_decode")
+        return out
