@@ -382,8 +382,9 @@ fairy2i_status fairy2i_wl_matmul_group_timed(const void* table, const void* tabl
  * plan copies must stay alive and unchanged while calls that use them run;
  * calls sharing a workspace must not overlap.
  * Errors: FAIRY2I_ERR_NULL; FAIRY2I_ERR_SHAPE for sizes that are not
- * positive, n % n_heads != 0, dc > 256, n or n_ff not a multiple of 64, T
- * out of range, or pos outside [0, max_ctx); FAIRY2I_ERR_WORKSPACE;
+ * positive, n % n_heads != 0, dc odd or above 256, n or n_ff not a multiple
+ * of 64, T out of range, max_ctx above 262144, or pos outside [0, max_ctx);
+ * FAIRY2I_ERR_WORKSPACE;
  * FAIRY2I_ERR_UNSUPPORTED for a plan not built by this library version;
  * FAIRY2I_ERR_HIP.
  */

@@ -338,27 +338,38 @@ static int group_mode(const fairy2i_wl_layer* layers, int32_t dtype) {
   return layers[0].layout == FAIRY2I_LAYOUT_TILED_FP4 ? kModeBf16F4 : dec_mode(dtype);
 }
 
-// Whether a checked group runs every layer of at most kMaxFullKSteps steps
-// as one work item per row block: on the fp4 path, when the group has
-// enough row blocks to keep every wave busy without K slices.
-static bool group_full_k(const fairy2i_wl_layer* layers, int32_t n_layers, const DecHeader& h) {
-  if (h.mode != kModeBf16F4) return false;
+// Steps per K slice for a checked group: kSliceFullK (every layer of at most
+// kMaxFullKSteps steps as one work item per row block) on the fp4 path when
+// the group has enough row blocks to keep every wave busy without K slices;
+// otherwise 8, halved while the group has fewer than kMinGroupItems items.
+static int group_slice(const fairy2i_wl_layer* layers, int32_t n_layers, const DecHeader& h) {
   int64_t rbs = 0;
   for (int32_t i = 0; i < n_layers; ++i) rbs += (layers[i].N + 15) / 16;
-  return rbs >= kFullKMinItems;
+  if (h.mode == kModeBf16F4 && rbs >= kFullKMinItems) return kSliceFullK;
+  int slice = 8;
+  while (slice > 1) {
+    int64_t items = 0;
+    for (int32_t i = 0; i < n_layers; ++i) {
+      const int64_t nk4 = (layers[i].K + 255) / 256;
+      items += (layers[i].N + 15) / 16 * ((nk4 + slice - 1) / slice);
+    }
+    if (items >= kMinGroupItems) break;
+    slice /= 2;
+  }
+  return slice;
 }
 
 size_t fairy2i_wl_group_workspace_bytes(const fairy2i_wl_layer* layers, int32_t n_layers, int32_t T,
                                         int32_t dtype, int64_t B) {
   if (check_group(layers, n_layers, T, dtype, B) != FAIRY2I_OK) return 0;
   const DecHeader h = dec_header(T, group_mode(layers, dtype), B, false);
-  const bool full_k = group_full_k(layers, n_layers, h);
+  const int slice = group_slice(layers, n_layers, h);
   size_t total = 0;
   for (int32_t i = 0; i < n_layers; ++i) {
     DecLayer l{};
     l.N = (int32_t)layers[i].N;
     l.K = (int32_t)layers[i].K;
-    total += dec_layer_setup(l, h, false, nullptr, full_k);
+    total += dec_layer_setup(l, h, false, nullptr, slice);
   }
   return total;
 }
@@ -375,7 +386,7 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
   auto* hdr = static_cast<GroupTableHeader*>(table);
   auto* tab = reinterpret_cast<DecLayer*>(hdr + 1);
   DecHeader h = dec_header(T, group_mode(layers, dtype), B, false);
-  const bool full_k = group_full_k(layers, n_layers, h);
+  const int slice = group_slice(layers, n_layers, h);
   char* ws = static_cast<char*>(workspace);
   // descriptors in table order; on the fp4 path the table lists the layers by
   // decreasing work-item length (stable), so that the blocks of the product
@@ -386,7 +397,7 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
     DecLayer& l = ls[(size_t)i];
     l = dec_layer(L.codes_U, L.scales_U, L.codes_W, L.scales_W, L.N, L.K, L.x, L.x_scale, L.y);
     l.tiled = L.layout != FAIRY2I_LAYOUT_D3 ? 1 : 0;
-    ws += dec_layer_setup(l, h, false, ws, full_k);
+    ws += dec_layer_setup(l, h, false, ws, slice);
     l.acc = nullptr;
   }
   if (h.mode == kModeBf16F4)

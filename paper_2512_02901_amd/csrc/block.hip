@@ -27,6 +27,7 @@ namespace fairy2i {
 namespace {
 
 constexpr int kAttnSlice = 64;   // positions per attention slice (one per lane)
+constexpr int kMaxAttnSlices = 4096;  // slices per head the combine keeps in LDS
 constexpr int kNormThreads = 256;
 
 __device__ inline uint16_t bf16_rne(float f) {
@@ -105,59 +106,69 @@ __global__ void rope_append_kernel(const float2* __restrict__ q, const float2* _
   v_cache[at] = v[i];
 }
 
-// One wave per (64-position slice, head): lane l scores position
-// n0 + l as Re(q^H k) * scale (the wave's butterfly sum over the head's dc
-// entries, lane j holding entries j, j + 64, ...), then the slice's maximum m,
-// e_l = exp(s_l - m), l = sum e_l and o_j = sum e_l v_{n0+l, j}.
-// Partial record per (head, slice): [m, l, o (2 dc floats)].
-template <int R>  // complex entries per lane: dc <= 64 R
+// One wave per (64-position slice, head).  Lane t scores position n0 + t as
+// Re(q^H k) * scale, reading its key with 16-byte loads and the query from
+// LDS (every lane reads the same address: a broadcast); then the slice's
+// maximum m, e_t = exp(s_t - m), l = sum e_t; then lane j forms
+// o_j = sum_t e_t v_{n0+t, j} over the slice (t wave-uniform, eight value loads
+// in flight).  Partial record per (head, slice): [m, l, o (2 dc floats)].
+template <int R>  // complex entries per lane in the value pass: dc <= 64 R
 __global__ __launch_bounds__(64) void attn_partial_kernel(const float2* __restrict__ q_rot,
                                                           const float2* __restrict__ k_cache,
                                                           const float2* __restrict__ v_cache, int dc, int64_t n_ctx,
                                                           int64_t max_ctx, float scale, float* __restrict__ part) {
+  __shared__ float4 qs[64 * R / 2];
   const int h = blockIdx.y, sl = blockIdx.x, lane = threadIdx.x;
   const int64_t n0 = (int64_t)sl * kAttnSlice;
   const int cnt = (int)min((int64_t)kAttnSlice, n_ctx - n0);
-  float2 qv[R];
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const int j = lane + 64 * r;
-    qv[r] = j < dc ? q_rot[h * dc + j] : make_float2(0.f, 0.f);
-  }
+  for (int j = lane; j < dc / 2; j += 64) qs[j] = reinterpret_cast<const float4*>(q_rot + h * dc)[j];
+  __syncthreads();
   const float2* kh = k_cache + (int64_t)h * max_ctx * dc;
   const float2* vh = v_cache + (int64_t)h * max_ctx * dc;
-  float my_s = -INFINITY;
-  for (int t = 0; t < cnt; ++t) {
-    const float2* kp = kh + (n0 + t) * dc;
-    float p = 0.0f;
+  float s = -INFINITY;
+  if (lane < cnt) {
+    const float4* kp = reinterpret_cast<const float4*>(kh + (n0 + lane) * dc);
+    float acc = 0.0f;
+    for (int j0 = 0; j0 < dc / 2; j0 += 8) {
+      float4 kv[8];
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const int j = lane + 64 * r;
-      if (j < dc) {
-        const float2 kv = kp[j];
-        p = fmaf(qv[r].x, kv.x, p);
-        p = fmaf(qv[r].y, kv.y, p);
+      for (int u = 0; u < 8; ++u) kv[u] = j0 + u < dc / 2 ? kp[j0 + u] : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (j0 + u < dc / 2) {
+          const float4 qv = qs[j0 + u];
+          acc = fmaf(qv.x, kv[u].x, acc);
+          acc = fmaf(qv.y, kv[u].y, acc);
+          acc = fmaf(qv.z, kv[u].z, acc);
+          acc = fmaf(qv.w, kv[u].w, acc);
+        }
       }
     }
-    const float s = wave_sum(p) * scale;
-    if (lane == t) my_s = s;
+    s = acc * scale;
   }
-  const float m = wave_max(my_s);
-  const float e = lane < cnt ? expf(my_s - m) : 0.0f;
+  const float m = wave_max(s);
+  const float e = lane < cnt ? expf(s - m) : 0.0f;
   const float l = wave_sum(e);
   float2 o[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) o[r] = make_float2(0.f, 0.f);
-  for (int t = 0; t < cnt; ++t) {
-    const float w = __shfl(e, t);
-    const float2* vp = vh + (n0 + t) * dc;
+  for (int t0 = 0; t0 < cnt; t0 += 8) {
+    float2 vv[8][R];
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const int j = lane + 64 * r;
-      if (j < dc) {
-        const float2 vv = vp[j];
-        o[r].x = fmaf(w, vv.x, o[r].x);
-        o[r].y = fmaf(w, vv.y, o[r].y);
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        const int j = lane + 64 * r;
+        vv[u][r] = (t0 + u < cnt && j < dc) ? vh[(n0 + t0 + u) * dc + j] : make_float2(0.f, 0.f);
+      }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      // lanes t >= cnt hold e = 0, and t0 + u < 64
+      const float w = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(e), t0 + u));
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        o[r].x = fmaf(w, vv[u][r].x, o[r].x);
+        o[r].y = fmaf(w, vv[u][r].y, o[r].y);
       }
     }
   }
@@ -176,27 +187,45 @@ __global__ __launch_bounds__(64) void attn_partial_kernel(const float2* __restri
   }
 }
 
-// Per head: M = max m_s, L = sum_s l_s e^(m_s - M), o = sum_s o_s e^(m_s - M)
-// / L over the slices in order; written as bf16 pairs at the head's entries.
+// Per head: M = max_s m_s, f_s = e^(m_s - M) (kept in LDS), L = sum_s l_s f_s,
+// o_j = sum_s o_{s,j} f_s / L over the slices in order; written as bf16 pairs
+// at the head's entries.
 __global__ __launch_bounds__(64) void attn_combine_kernel(const float* __restrict__ part, int n_slices, int dc,
                                                           uint16_t* __restrict__ o_out) {
-  const int h = blockIdx.x;
-  const float* ph = part + (int64_t)h * n_slices * (2 + 2 * dc);
+  __shared__ float fs[kMaxAttnSlices];
+  const int h = blockIdx.x, lane = threadIdx.x;
+  const int rl = 2 + 2 * dc;
+  const float* ph = part + (int64_t)h * n_slices * rl;
   float M = -INFINITY;
-  for (int s = 0; s < n_slices; ++s) M = fmaxf(M, ph[(int64_t)s * (2 + 2 * dc)]);
+  for (int sl = lane; sl < n_slices; sl += 64) M = fmaxf(M, ph[(int64_t)sl * rl]);
+  M = wave_max(M);
   float L = 0.0f;
-  for (int s = 0; s < n_slices; ++s) {
-    const float* rec = ph + (int64_t)s * (2 + 2 * dc);
-    L = fmaf(rec[1], expf(rec[0] - M), L);
+  for (int s0 = 0; s0 < n_slices; s0 += 64) {
+    const int sl = s0 + lane;
+    float f = 0.0f, t = 0.0f;
+    if (sl < n_slices) {
+      f = expf(ph[(int64_t)sl * rl] - M);
+      t = ph[(int64_t)sl * rl + 1] * f;
+      fs[sl] = f;
+    }
+    L += wave_sum(t);
   }
+  __syncthreads();
   const float invL = 1.0f / L;
-  for (int j = threadIdx.x; j < dc; j += blockDim.x) {
+  for (int j = lane; j < dc; j += 64) {
     float ore = 0.0f, oim = 0.0f;
-    for (int s = 0; s < n_slices; ++s) {
-      const float* rec = ph + (int64_t)s * (2 + 2 * dc);
-      const float f = expf(rec[0] - M);
-      ore = fmaf(rec[2 + 2 * j], f, ore);
-      oim = fmaf(rec[3 + 2 * j], f, oim);
+    for (int s0 = 0; s0 < n_slices; s0 += 8) {
+      float2 ov[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        ov[u] = s0 + u < n_slices ? *reinterpret_cast<const float2*>(ph + (int64_t)(s0 + u) * rl + 2 + 2 * j)
+                                  : make_float2(0.f, 0.f);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float f = s0 + u < n_slices ? fs[s0 + u] : 0.0f;
+        ore = fmaf(ov[u].x, f, ore);
+        oim = fmaf(ov[u].y, f, oim);
+      }
     }
     o_out[2 * (h * dc + j)] = bf16_rne(ore * invL);
     o_out[2 * (h * dc + j) + 1] = bf16_rne(oim * invL);
@@ -259,9 +288,9 @@ const int kGroupLayers[kGroups][3] = {{0, 1, 2}, {3, -1, -1}, {4, 5, -1}, {6, -1
 
 bool block_desc_ok(const fairy2i_block_desc* d) {
   if (!d || d->n <= 0 || d->n_ff <= 0 || d->n_heads <= 0 || d->max_ctx <= 0) return false;
-  if (d->n % d->n_heads != 0 || d->n / d->n_heads > 256) return false;
+  if (d->n % d->n_heads != 0 || d->n / d->n_heads > 256 || (d->n / d->n_heads) % 2 != 0) return false;
   if (d->n % 64 != 0 || d->n_ff % 64 != 0) return false;
-  if (d->n > (1 << 24) || d->n_ff > (1 << 24) || d->max_ctx > (1 << 24)) return false;
+  if (d->n > (1 << 24) || d->n_ff > (1 << 24) || d->max_ctx > (int64_t)kAttnSlice * kMaxAttnSlices) return false;
   if (d->T < 1 || d->T > FAIRY2I_MAX_STAGES || !(d->eps >= 0.0f) || !(d->rope_base > 0.0)) return false;
   return true;
 }

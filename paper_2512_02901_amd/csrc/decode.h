@@ -57,11 +57,14 @@ DecHeader dec_header(int T, int mode, int64_t B, bool export_acc);
 // Fill the geometry fields of `l` (N, K set) for header h and return its
 // workspace bytes; with `ws` non-null also carve xf, xs, part out of it.
 // `single`: a one-layer call (slices chosen to give the GPU enough items).
-// `full_k`: a group with enough row blocks that a layer of at most
+// `slice`: steps per K slice chosen for a whole group: 0 for the default
+// (8), kSliceFullK for a group with enough row blocks that a layer of at most
 // kMaxFullKSteps steps is not split along K (no partials, no reduction).
+constexpr int kSliceFullK = -1;
 constexpr int kMaxFullKSteps = 32;
 constexpr int64_t kFullKMinItems = 12288;
-size_t dec_layer_setup(DecLayer& l, const DecHeader& h, bool single, char* ws, bool full_k = false);
+constexpr int64_t kMinGroupItems = 2048;  // a small group gets shorter slices until it has this many items
+size_t dec_layer_setup(DecLayer& l, const DecHeader& h, bool single, char* ws, int slice = 0);
 
 // The fp8 x fp4 path (decode_f4.hip): activation operand and product
 // launches of a kModeBf16F4 call (errors are left for hipGetLastError).

@@ -705,17 +705,18 @@ DecHeader dec_header(int T, int mode, int64_t B, bool export_acc) {
   return h;
 }
 
-size_t dec_layer_setup(DecLayer& l, const DecHeader& h, bool single, char* ws, bool full_k) {
+size_t dec_layer_setup(DecLayer& l, const DecHeader& h, bool single, char* ws, int slice) {
   l.nrb = (int32_t)((l.N + 15) / 16);
   l.nk4 = (int32_t)((l.K + 255) / 256);
   if (h.kernel == kKernelReg) {
     l.kc4 = kRegKc4;
-  } else if (full_k && l.nk4 <= kMaxFullKSteps) {
+  } else if (slice == kSliceFullK && l.nk4 <= kMaxFullKSteps) {
     l.kc4 = l.nk4;  // one work item per row block
   } else {
-    // slices of up to 8 steps (2048 codes); a single layer gets smaller
-    // slices while that is needed to give the GPU ~2048 work items
-    l.kc4 = 8;
+    // slices of up to 8 steps (2048 codes), or the group's choice; a single
+    // layer gets smaller slices while that is needed to give the GPU ~2048
+    // work items
+    l.kc4 = slice > 0 ? slice : 8;
     if (single)
       while (l.kc4 > 1 && (int64_t)l.nrb * ((l.nk4 + l.kc4 - 1) / l.kc4) < 2048) l.kc4 /= 2;
   }
