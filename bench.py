@@ -197,6 +197,37 @@ def quantizer_bench(f2, synth, torch, dev, T=2, reps=5):
     return out
 
 
+def cpu_lut_bench(f2, torch, layers, T, passes=3):
+    """The CPU table-lookup kernel over the whole stack on the host cores:
+    the stack's canonical codes and scales copied to host memory, each
+    layer's bf16 token quantised to int8 (fairy2i_quantize_act_int8), then
+    whole passes over the 224 layers, one library call per layer."""
+    import numpy as np
+    host = []
+    for (cu, su, cw, sw, x, _, y) in layers:
+        q, f = f2.quantize_act_int8(x)
+        host.append((cu.cpu().numpy(), su.cpu().numpy(), cw.cpu().numpy(), sw.cpu().numpy(),
+                     q.cpu().numpy(), f.cpu().numpy()))
+    kmax = max(h[0].shape[2] * 4 for h in host)
+    ws = np.empty(f2.cpu_lut_workspace_bytes(T, kmax, 1), dtype=np.uint8)
+    packed = sum(h[0].nbytes + h[2].nbytes for h in host)
+
+    def one_pass():
+        for (cu, su, cw, sw, q, f) in host:
+            f2.cpu_lut_wl_matmul(cu, su, cw, sw, q, f, workspace=ws)
+
+    one_pass()
+    t0 = time.perf_counter()
+    for _ in range(passes):
+        one_pass()
+    sec = (time.perf_counter() - t0) / passes
+    del host
+    return {"workload": f"LLaMA-2-7B linear stack, {len(layers)} layers, T={T}, one int8 token per layer, "
+                        "host cores", "ms_per_step": round(sec * 1e3, 2), "GBs": round(packed / sec / 1e9, 2),
+            "threads": len(os.sched_getaffinity(0)), "passes": passes,
+            "kernel": "fairy2i_cpu_lut_wl_matmul (8-bit index of four codes, int16 tables, SSE2)"}
+
+
 def traffic_record():
     """HBM bytes per launch of the product kernel from committed rocprofv3
     --pmc summaries, or None when absent or when the kernel source changed
@@ -536,6 +567,7 @@ def main():
         result["stack_d3_layout"] = {"ms_per_step": round(ms_d3, 4), "GBs": round(packed / (ms_d3 * 1e-3) / 1e9, 1),
                                      "product_us": round(prod_d3 * 1e3, 1)}
         del grp_d3
+        result["cpu_lut"] = cpu_lut_bench(f2, torch, layers, T)
     del grp, layers, fp4_layers
     stack_codes.clear()
     torch.cuda.empty_cache()

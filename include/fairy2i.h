@@ -437,6 +437,41 @@ fairy2i_status fairy2i_block_intermediates(const void* plan, void** ptrs);
  */
 fairy2i_status fairy2i_host_exact_mean_f32(const double* values, int64_t n_values, float* out);
 
+/*
+ * CPU table-lookup product for int8 activations (Sec. 3.4, the paragraph on
+ * lookup tables for CPU inference): every four consecutive codes of a row
+ * (one byte of the canonical packed layout) index a 256-entry table of their
+ * partial sums with the token's int8 activations, built once per token and
+ * column group, so the row loop is table fetches and integer adds.  Host
+ * code; every pointer is HOST memory and nothing runs on the GPU.
+ *
+ *   codes_U, codes_W: canonical packed codes, uint8 [T][N][K/4] each;
+ *   scales_U, scales_W: float32 [T][2] (s_re, s_im); q: int8 [B][K][2]
+ *   (re, im) as written by fairy2i_quantize_act_int8; x_scale: float32 [B]
+ *   per-token dequantisation factors; y: complex64 [B][N] output, or NULL;
+ *   acc: int32 [2][T][2][B][N][2] output (the layout of
+ *   fairy2i_wl_int8_accumulators), or NULL.  At least one of y and acc.
+ *   y is Eq. (ifairy-dequant) applied to the exact integer sums in double,
+ *   stages in increasing order, U with q and W with conj(q), times x_scale,
+ *   rounded once to float32.
+ *   workspace: host scratch of at least fairy2i_cpu_lut_workspace_bytes(T,
+ *   K, B, n_threads) bytes (the table plus per-thread accumulators), 16-byte
+ *   aligned; n_threads <= 0 uses every CPU in the calling thread's affinity
+ *   mask (at most 256).
+ * The threads are a persistent pool owned by the library; concurrent calls
+ * are serialised.
+ * Errors: FAIRY2I_ERR_NULL; FAIRY2I_ERR_STAGES; FAIRY2I_ERR_SHAPE if N, K <=
+ * 0, K % 4 != 0 or B outside [1, FAIRY2I_MAX_DECODE_BATCH];
+ * FAIRY2I_ERR_WORKSPACE if the workspace is too small.
+ */
+size_t fairy2i_cpu_lut_workspace_bytes(int32_t T, int64_t K, int64_t B, int32_t n_threads);
+fairy2i_status fairy2i_cpu_lut_wl_matmul(const uint8_t* codes_U, const float* scales_U,
+                                         const uint8_t* codes_W, const float* scales_W,
+                                         int32_t T, int64_t N, int64_t K,
+                                         const int8_t* q, const float* x_scale, int64_t B,
+                                         float* y, int32_t* acc,
+                                         void* workspace, size_t workspace_bytes, int32_t n_threads);
+
 #ifdef __cplusplus
 }
 #endif

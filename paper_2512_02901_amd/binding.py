@@ -51,6 +51,9 @@ _SIGNATURES = {
     "fairy2i_block_build_plan": (_c_i32, [_c_p, _c_p, _c_size, _c_p, _c_size]),
     "fairy2i_block_decode": (_c_i32, [_c_p, _c_p, _c_p, _c_p, _c_p, _c_i64, _c_p, _c_p]),
     "fairy2i_block_intermediates": (_c_i32, [_c_p, _c_p]),
+    "fairy2i_cpu_lut_workspace_bytes": (_c_size, [_c_i32, _c_i64, _c_i64, _c_i32]),
+    "fairy2i_cpu_lut_wl_matmul": (_c_i32, [_c_p, _c_p, _c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_p, _c_i64,
+                                           _c_p, _c_p, _c_p, _c_size, _c_i32]),
 }
 
 
@@ -346,6 +349,65 @@ def host_exact_mean_f32(values) -> np.float32:
     _check(lib.fairy2i_host_exact_mean_f32(v.ctypes.data_as(ctypes.c_void_p), v.size,
                                            ctypes.byref(out)), "fairy2i_host_exact_mean_f32")
     return np.float32(out.value)
+
+
+def _host(a, dtype, name, shape=None):
+    """A C-contiguous numpy view of a host array or CPU tensor, checked."""
+    if hasattr(a, "is_cuda"):
+        if a.is_cuda:
+            raise ValueError(f"{name} must be host memory")
+        a = a.numpy()
+    if not isinstance(a, np.ndarray) or a.dtype != dtype or not a.flags.c_contiguous:
+        raise TypeError(f"{name} must be a C-contiguous {np.dtype(dtype).name} array")
+    if shape is not None and a.shape != tuple(shape):
+        raise ValueError(f"{name} has shape {a.shape}, expected {tuple(shape)}")
+    return a
+
+
+def _hp(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def cpu_lut_workspace_bytes(T: int, K: int, B: int, threads: int = 0) -> int:
+    return int(load().fairy2i_cpu_lut_workspace_bytes(T, K, B, threads))
+
+
+def cpu_lut_wl_matmul(codes_U, scales_U, codes_W, scales_W, q, x_scale, want_y=True, want_acc=False,
+                      threads: int = 0, workspace=None):
+    """The CPU table-lookup product (host arrays only): codes uint8 [T, N,
+    K/4], scales float32 [T, 2], q int8 [B, K, 2], x_scale float32 [B].
+    Returns (y complex64 [B, N] or None, acc int32 [2, T, 2, B, N, 2] or
+    None).  ``workspace``: optional uint8 host array to reuse across calls."""
+    lib = load()
+    codes_U = _host(codes_U, np.uint8, "codes_U")
+    if codes_U.ndim != 3:
+        raise ValueError("codes_U must be [T, N, K/4]")
+    T, N, K4 = codes_U.shape
+    K = 4 * K4
+    codes_W = _host(codes_W, np.uint8, "codes_W", (T, N, K4))
+    q = _host(q, np.int8, "q")
+    if q.ndim != 3 or q.shape[1:] != (K, 2):
+        raise ValueError(f"q must be [B, {K}, 2], got {q.shape}")
+    B = q.shape[0]
+    su = sw = xs = None
+    y = acc = None
+    if want_y:
+        su = _host(scales_U, np.float32, "scales_U", (T, 2))
+        sw = _host(scales_W, np.float32, "scales_W", (T, 2))
+        xs = _host(x_scale, np.float32, "x_scale", (B,))
+        y = np.empty((B, N), dtype=np.complex64)
+    if want_acc:
+        acc = np.empty((2, T, 2, B, N, 2), dtype=np.int32)
+    need = cpu_lut_workspace_bytes(T, K, B, threads)
+    if need == 0:
+        raise ValueError(f"unsupported shape T={T} K={K} B={B}")
+    if workspace is None or workspace.nbytes < need:
+        workspace = np.empty(need, dtype=np.uint8)
+    _host(workspace, np.uint8, "workspace")
+    _check(lib.fairy2i_cpu_lut_wl_matmul(_hp(codes_U), _hp(su), _hp(codes_W), _hp(sw), T, N, K, _hp(q), _hp(xs), B,
+                                         _hp(y), _hp(acc), _hp(workspace), workspace.nbytes, threads),
+           "fairy2i_cpu_lut_wl_matmul")
+    return y, acc
 
 
 class WlGroup:
