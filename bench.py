@@ -474,6 +474,8 @@ def main():
     ap.add_argument("--random-codes", action="store_true",
                     help="random codes instead of quantised weights (for hardware-counter runs only; "
                          "the JSON line then says so in `data`)")
+    ap.add_argument("--prefill-only", action="store_true",
+                    help="only run the two 2048-token prefill GEMMs (for hardware-counter runs)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run 5 plain 256 MiB device copies (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -497,6 +499,9 @@ def main():
 
     dev = torch.device("cuda:0")
     f2.load()
+    if args.prefill_only:
+        print(json.dumps({"prefill": prefill_bench(f2, synth, torch, dev)}), flush=True)
+        return
     T = 2
     t0 = time.time()
     grp, packed, algo, layers, grp_tiled, fp4_layers = build_stack(f2, synth, torch, dev, T,
