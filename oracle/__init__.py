@@ -12,3 +12,4 @@ from .fairy2i import (CODEWORDS, axis_scales, code_planes, combine_accumulators,
                       realify_lin, round_to_f32, stack_real, to_widely_linear,
                       to_widely_linear_f64, unpack, wl_matmul, wl_matmul_int8)
 from . import block  # noqa: F401,E402
+from . import groups  # noqa: F401,E402
