@@ -197,6 +197,41 @@ def quantizer_bench(f2, synth, torch, dev, T=2, reps=5):
     return out
 
 
+def grouped_stack_bench(f2, synth, torch, dev, T, G, steps, warmup, seed_base=1000):
+    """The decode stack with per-group axis scales (groups of G input columns
+    per row, fairy2i_quantize_grouped) on the fp4 path: the same weights as
+    the headline stack, the scale arrays read alongside the codes."""
+    layers, packed, scale_bytes = [], 0, 0
+    for layer in range(32):
+        for p in synth.PROJ_ORDER:
+            rows, cols = synth.LLAMA2_7B_PROJ[p]
+            N, K = rows // 2, cols // 2
+            g = torch.Generator(device=dev)
+            g.manual_seed(seed_base * 31 + len(layers))
+            A = synth.torch_llama_weight(rows, cols, seed_base + 7 * layer + synth.PROJ_ORDER.index(p), dev)
+            U, W = f2.to_widely_linear(A)
+            del A
+            cu, su = f2.quantize_grouped(U, T, G)
+            cw, sw = f2.quantize_grouped(W, T, G)
+            del U, W
+            x = torch.randn(1, K, 2, generator=g, device=dev).to(torch.bfloat16)
+            y = torch.empty(1, N, dtype=torch.complex64, device=dev)
+            layers.append((f2.repack_tiled_fp4(cu), su, f2.repack_tiled_fp4(cw), sw, x, None, y))
+            del cu, cw
+            packed += 2 * T * N * K // 4
+            scale_bytes += su.numel() * 4 + sw.numel() * 4
+    torch.cuda.synchronize()
+    grp = f2.WlGroup(layers, T=T, B=1, layout=f2.LAYOUT_TILED_FP4, group_size=G)
+    ms, _, prod, _ = time_group(grp, torch, steps, warmup, label=f"stack_group{G}")
+    out = {"group_size": G, "ms_per_step": round(ms, 4), "product_us": round(prod * 1e3, 1),
+           "packed_bytes": packed, "scale_bytes": scale_bytes,
+           "GBs": round(packed / (ms * 1e-3) / 1e9, 1),
+           "GBs_codes_and_scales": round((packed + scale_bytes) / (ms * 1e-3) / 1e9, 1)}
+    del grp, layers
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_lut_bench(f2, torch, layers, T, passes=3):
     """The CPU table-lookup kernel over the whole stack on the host cores:
     the stack's canonical codes and scales copied to host memory, each
@@ -585,6 +620,8 @@ def main():
                               "time_ratio_T3_over_T2": round(ms3 / ms, 3)}
         del grp3, layers3, f3
         torch.cuda.empty_cache()
+        result["stack_group256"] = grouped_stack_bench(f2, synth, torch, dev, T, 256, args.steps, args.warmup)
+        result["stack_group256"]["time_ratio_over_per_tensor"] = round(result["stack_group256"]["ms_per_step"] / ms, 3)
         result["per_layer"] = per_layer_bench(f2, synth, torch, dev, T)
         result["decoder_block"] = block_bench(f2, synth, torch, dev, T)
         pf = prefill_bench(f2, synth, torch, dev)

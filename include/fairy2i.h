@@ -130,6 +130,25 @@ fairy2i_status fairy2i_quantize(const float* M, int64_t N, int64_t K, int32_t T,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * fairy2i_quantize with per-group axis scales (Sec. 1 and the footnote to
+ * Eq. ifairy-scale name per-group scale sharing; the paper itself uses one
+ * pair per tensor).  A group is G consecutive input columns of one output
+ * row, j in [g G, min((g+1) G, K)), so a row has ngroups = ceil(K / G)
+ * groups and the last may be shorter.  Each stage projects every entry as
+ * above; each group gets its own (s_re, s_im), the exact mean over the
+ * group's entries rounded once to float32 (0 for an empty axis group); the
+ * residual subtracts the stored scales of the entry's own group.
+ * M: complex64 [N][K].  codes: uint8 [T][N][K/4] output (packed layout
+ * above).  scales: float32 [T][N][ngroups][2] output.  No workspace.
+ * Results are bitwise deterministic.
+ * Errors: FAIRY2I_ERR_NULL; FAIRY2I_ERR_SHAPE if N, K <= 0, K % 4 != 0,
+ * N*K > FAIRY2I_MAX_QUANTIZE_ENTRIES, G < 4 or G % 4 != 0;
+ * FAIRY2I_ERR_STAGES.
+ */
+fairy2i_status fairy2i_quantize_grouped(const float* M, int64_t N, int64_t K, int32_t T, int64_t G,
+                                        uint8_t* codes, float* scales, void* stream);
+
+/*
  * Per-token int8 activations (the paper names INT8 activations for its
  * look-up-table inference paragraph in Sec. 3.4 without defining the
  * quantiser; this is the library's definition).  For token b, in float32:
@@ -247,7 +266,11 @@ typedef struct fairy2i_wl_layer {
   int64_t K;
   int32_t layout;    /* FAIRY2I_LAYOUT_D3, _TILED or _TILED_FP4, for both
                         codes_U and codes_W (same T as the call)           */
-  int32_t reserved;  /* 0 */
+  int32_t group_size; /* 0: scales_U, scales_W are float32 [T][2] (one pair
+                        per stage).  G > 0: per-group scales as written by
+                        fairy2i_quantize_grouped, float32
+                        [T][N][ceil(K / G)][2]; G a multiple of 256 and
+                        layout FAIRY2I_LAYOUT_TILED_FP4 (see below)          */
 } fairy2i_wl_layer;
 
 /*
@@ -256,7 +279,7 @@ typedef struct fairy2i_wl_layer {
  * input) in a fixed number of kernel launches, so the weight stream of all
  * layers runs back to back instead of paying a launch per layer.
  * Restrictions: dtype FAIRY2I_ACT_BF16 or FAIRY2I_ACT_I8, 1 <= B <= 16,
- * every K a multiple of 64, reserved == 0.  Each layer's codes are in the
+ * every K a multiple of 64.  Each layer's codes are in the
  * layout its `layout` field names (same layout for U and W).  With
  * FAIRY2I_LAYOUT_TILED_FP4 every layer of the group must use it, with dtype
  * FAIRY2I_ACT_BF16 and B <= 4 (B <= 2 for T = 4); the product then runs on the
@@ -269,6 +292,12 @@ typedef struct fairy2i_wl_layer {
  * 2^-30 m.  The digit products are exact and are summed in float32 on the
  * matrix cores; y matches the exact product of the bf16 inputs to float32
  * rounding (relative L2 about 1e-7).
+ * Per-group scales (group_size G > 0) are supported on this fp4 path only,
+ * for every layer of the group or for none (G may differ between layers).
+ * The products of each 256-code step then start from zero and are folded,
+ * in float32, into sums scaled by the step's group scales (Eq. ifairy-dequant
+ * per group); the scale arrays are read alongside the codes (8 bytes per
+ * row, group, stage and matrix).
  *
  * Use: size the workspace with fairy2i_wl_group_workspace_bytes and the
  * table with fairy2i_wl_group_table_bytes; fairy2i_wl_group_build_table

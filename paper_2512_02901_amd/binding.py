@@ -28,6 +28,7 @@ _SIGNATURES = {
     "fairy2i_to_widely_linear": (_c_i32, [_c_p, _c_i64, _c_i64, _c_p, _c_p, _c_p]),
     "fairy2i_quantize_workspace_bytes": (_c_size, [_c_i64, _c_i64, _c_i32]),
     "fairy2i_quantize": (_c_i32, [_c_p, _c_i64, _c_i64, _c_i32, _c_p, _c_p, _c_p, _c_size, _c_p]),
+    "fairy2i_quantize_grouped": (_c_i32, [_c_p, _c_i64, _c_i64, _c_i32, _c_i64, _c_p, _c_p, _c_p]),
     "fairy2i_repack_tiled_bytes": (_c_size, [_c_i64, _c_i64, _c_i32]),
     "fairy2i_repack_tiled": (_c_i32, [_c_p, _c_i64, _c_i64, _c_i32, _c_p, _c_size, _c_p]),
     "fairy2i_repack_tiled_fp4": (_c_i32, [_c_p, _c_i64, _c_i64, _c_i32, _c_p, _c_size, _c_p]),
@@ -61,7 +62,7 @@ class WlLayer(ctypes.Structure):
     """fairy2i_wl_layer of include/fairy2i.h."""
     _fields_ = [("codes_U", _c_p), ("scales_U", _c_p), ("codes_W", _c_p), ("scales_W", _c_p),
                 ("x", _c_p), ("x_scale", _c_p), ("y", _c_p), ("N", _c_i64), ("K", _c_i64),
-                ("layout", _c_i32), ("reserved", _c_i32)]
+                ("layout", _c_i32), ("group_size", _c_i32)]
 
 
 class BlockDesc(ctypes.Structure):
@@ -161,6 +162,22 @@ def quantize(M, T: int):
     ws = torch.empty(max(int(wsb), 1), dtype=torch.uint8, device=M.device)
     _check(lib.fairy2i_quantize(_ptr(M), N, K, T, _ptr(codes), _ptr(scales), _ptr(ws), wsb,
                                 _stream_ptr(M)), "fairy2i_quantize")
+    return codes, scales
+
+
+def quantize_grouped(M, T: int, G: int):
+    """M: complex64 [N, K] -> (codes uint8 [T, N, K/4], scales float32
+    [T, N, ceil(K/G), 2]): one pair of axis scales per group of G input
+    columns of a row."""
+    torch = _torch()
+    lib = load()
+    _require(M, torch.complex64, "M")
+    N, K = M.shape
+    ng = -(-K // G) if G > 0 else 0
+    codes = torch.empty((T, N, K // 4), dtype=torch.uint8, device=M.device)
+    scales = torch.empty((T, N, max(ng, 1), 2), dtype=torch.float32, device=M.device)
+    _check(lib.fairy2i_quantize_grouped(_ptr(M), N, K, T, G, _ptr(codes), _ptr(scales), _stream_ptr(M)),
+           "fairy2i_quantize_grouped")
     return codes, scales
 
 
@@ -417,9 +434,10 @@ class WlGroup:
     the workspace and both copies of the table alive.  ``layout``: LAYOUT_D3
     (codes [T, N, K/4]), LAYOUT_TILED or LAYOUT_TILED_FP4 (repacked copies,
     a 1-D uint8 tensor per matrix; N is then taken from y); ``tiled=True``
-    is LAYOUT_TILED."""
+    is LAYOUT_TILED.  ``group_size`` G > 0: every layer has per-group scales
+    [T, N, ceil(K/G), 2] (fairy2i_quantize_grouped; LAYOUT_TILED_FP4 only)."""
 
-    def __init__(self, layers, T: int, B: int, tiled: bool = False, layout=None):
+    def __init__(self, layers, T: int, B: int, tiled: bool = False, layout=None, group_size: int = 0):
         if layout is None:
             layout = LAYOUT_TILED if tiled else LAYOUT_D3
         tiled = layout != LAYOUT_D3
@@ -438,14 +456,15 @@ class WlGroup:
                 raise ValueError("all layers of a group share B and the activation dtype")
             for t, n in ((cu, "codes_U"), (cw, "codes_W")):
                 _require(t, torch.uint8, f"layers[{i}].{n}", dev)
-            for t, n in ((su, "scales_U"), (sw, "scales_W")):
-                _require(t, torch.float32, f"layers[{i}].{n}", dev)
-                if tuple(t.shape) != (T, 2):
-                    raise ValueError(f"layers[{i}].{n} must have shape ({T}, 2)")
             _require(y, torch.complex64, f"layers[{i}].y", dev)
             if y.dim() != 2 or y.shape[0] != B:
                 raise ValueError(f"layers[{i}].y must have shape ({B}, N)")
             N = y.shape[1]
+            sshape = (T, 2) if group_size == 0 else (T, N, -(-K // group_size) if group_size > 0 else 0, 2)
+            for t, n in ((su, "scales_U"), (sw, "scales_W")):
+                _require(t, torch.float32, f"layers[{i}].{n}", dev)
+                if tuple(t.shape) != sshape:
+                    raise ValueError(f"layers[{i}].{n} must have shape {sshape}")
             if xs is not None:
                 _require(xs, torch.float32, f"layers[{i}].x_scale", dev)
                 if tuple(xs.shape) != (B,):
@@ -458,7 +477,7 @@ class WlGroup:
                 raise ValueError(f"layers[{i}] codes must have shape ({T}, {N}, {K // 4})")
             arr[i] = WlLayer(cu.data_ptr(), su.data_ptr(), cw.data_ptr(), sw.data_ptr(), x.data_ptr(),
                              None if xs is None else xs.data_ptr(), y.data_ptr(), N, K,
-                             layout, 0)
+                             layout, group_size)
         self.n = len(layers)
         wsb = int(lib.fairy2i_wl_group_workspace_bytes(ctypes.byref(arr), self.n, T, dt, B))
         self.workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)

@@ -50,9 +50,14 @@ def sources():
     return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith((".hip", ".cpp")))
 
 
-def _compile(src):
+def object_path(src):
     stem, ext = os.path.splitext(os.path.basename(src))
-    obj = os.path.join(BUILD, stem + (".host.o" if ext == ".cpp" else ".o"))
+    return os.path.join(BUILD, stem + (".host.o" if ext == ".cpp" else ".o"))
+
+
+def _compile(src):
+    ext = os.path.splitext(src)[1]
+    obj = object_path(src)
     if ext == ".cpp":
         cmd = [HOST_CXX, *HOST_FLAGS, "-c", src, "-o", obj]
     else:
@@ -63,17 +68,21 @@ def _compile(src):
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
-    srcs = sources()
-    with ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
-        objs = list(ex.map(_compile, srcs))
+def link(objs):
     tmp = LIB + ".tmp"
     cmd = [HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-pthread", "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
     os.replace(tmp, LIB)
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    srcs = sources()
+    with ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+        objs = list(ex.map(_compile, srcs))
+    link(objs)
     if verbose:
         print("built", LIB)
     return LIB

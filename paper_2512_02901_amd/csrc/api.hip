@@ -143,7 +143,7 @@ const char* fairy2i_status_string(fairy2i_status s) {
   }
 }
 
-int32_t fairy2i_abi_version(void) { return 4; }
+int32_t fairy2i_abi_version(void) { return 5; }
 
 fairy2i_status fairy2i_to_widely_linear(const float* A, int64_t rows, int64_t cols, float* U,
                                         float* W, void* stream) {
@@ -168,6 +168,16 @@ fairy2i_status fairy2i_quantize(const float* M, int64_t N, int64_t K, int32_t T,
   if (!workspace || workspace_bytes < quantize_workspace_bytes(N, K)) return FAIRY2I_ERR_WORKSPACE;
   return hip_status(launch_quantize(reinterpret_cast<const float2*>(M), N, K, T, codes, scales,
                                     workspace, as_stream(stream)));
+}
+
+fairy2i_status fairy2i_quantize_grouped(const float* M, int64_t N, int64_t K, int32_t T, int64_t G,
+                                        uint8_t* codes, float* scales, void* stream) {
+  if (!M || !codes || !scales) return FAIRY2I_ERR_NULL;
+  if (N <= 0 || K <= 0 || (K % 4) != 0 || N > FAIRY2I_MAX_QUANTIZE_ENTRIES / K || G < 4 || (G % 4) != 0)
+    return FAIRY2I_ERR_SHAPE;
+  if (T < 1 || T > FAIRY2I_MAX_STAGES) return FAIRY2I_ERR_STAGES;
+  return hip_status(launch_quantize_grouped(reinterpret_cast<const float2*>(M), N, K, T, G < K ? G : K, codes,
+                                            scales, as_stream(stream)));
 }
 
 static bool repack_shape_ok(int64_t N, int64_t K) {
@@ -318,7 +328,13 @@ static fairy2i_status check_group(const fairy2i_wl_layer* layers, int32_t n_laye
     if (dtype != FAIRY2I_ACT_I8 && L.x_scale) return FAIRY2I_ERR_UNSUPPORTED;
     if (!use_mfma_decode(dtype, L.N, L.K, B) || L.N > ((int64_t)1 << 30) || L.K > ((int64_t)1 << 24))
       return FAIRY2I_ERR_UNSUPPORTED;
-    if (L.reserved != 0) return FAIRY2I_ERR_UNSUPPORTED;
+    // per-group scales: fp4 path, every layer or none, groups of whole 256-code steps
+    if (L.group_size < 0 || L.group_size % 256 != 0) return FAIRY2I_ERR_UNSUPPORTED;
+    if ((L.group_size != 0) != (layers[0].group_size != 0)) return FAIRY2I_ERR_UNSUPPORTED;
+    if (L.group_size != 0 && L.layout != FAIRY2I_LAYOUT_TILED_FP4) return FAIRY2I_ERR_UNSUPPORTED;
+    // the kernel addresses a scale array with 32-bit offsets
+    if (L.group_size != 0 && (int64_t)T * L.N * ((L.K + L.group_size - 1) / L.group_size) * 8 >= ((int64_t)1 << 31))
+      return FAIRY2I_ERR_UNSUPPORTED;
     if (L.layout != FAIRY2I_LAYOUT_D3 && L.layout != FAIRY2I_LAYOUT_TILED && L.layout != FAIRY2I_LAYOUT_TILED_FP4)
       return FAIRY2I_ERR_UNSUPPORTED;
     // the decode kernels address a matrix with 32-bit offsets
@@ -397,6 +413,7 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
     DecLayer& l = ls[(size_t)i];
     l = dec_layer(L.codes_U, L.scales_U, L.codes_W, L.scales_W, L.N, L.K, L.x, L.x_scale, L.y);
     l.tiled = L.layout != FAIRY2I_LAYOUT_D3 ? 1 : 0;
+    l.gsteps = L.group_size / 256;
     ws += dec_layer_setup(l, h, false, ws, slice);
     l.acc = nullptr;
   }
@@ -423,6 +440,7 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
   h.n_layers = n_layers;
   h.total_items = items;
   h.total_steps = steps;
+  h.grouped = layers[0].group_size != 0 ? 1 : 0;
   hdr->h = h;
   hdr->any_split = any_split;
   hdr->max_BN = max_BN;

@@ -17,6 +17,8 @@ hipError_t launch_to_widely_linear(const float* A, int64_t N, int64_t K, float2*
 constexpr int kQzThreads = 256;
 constexpr int kQzMaxBlocks = 1024;
 size_t quantize_workspace_bytes(int64_t N, int64_t K);
+hipError_t launch_quantize_grouped(const float2* M, int64_t N, int64_t K, int T, int64_t G, uint8_t* codes,
+                                   float* scales, hipStream_t stream);
 hipError_t launch_quantize(const float2* M, int64_t N, int64_t K, int T, uint8_t* codes,
                            float* scales, void* workspace, hipStream_t stream);
 

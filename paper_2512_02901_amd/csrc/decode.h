@@ -31,7 +31,8 @@ struct DecLayer {
   int32_t N, K;
   int32_t nrb, nk4, nkc, kc4;  // 16-row blocks, 256-code steps, K slices, steps per slice
   int32_t tiled;             // codes in a tiled layout (tiled or fp4 tiled; else D3)
-  int32_t pad_;
+  int32_t gsteps;            // per-group scales: 256-code steps per group (scales [T][N][groups][2]);
+                             // 0: one pair per stage (scales [T][2])
   int64_t item0;             // index of this layer's first work item
   int64_t step0;             // 256-code steps of all work items before item0
 };
@@ -41,7 +42,7 @@ struct DecHeader {
   int32_t ntile;   // 16-column activation tiles
   int32_t nc;      // stored columns per tile (the first tile's valid columns)
   int32_t kernel;  // kKernelReg or kKernelStream
-  int32_t pad_;
+  int32_t grouped;  // every layer has per-group scales (fp4 path only)
   int64_t total_items;
   int64_t total_steps;  // 256-code steps of all work items
 };

@@ -160,7 +160,7 @@ __device__ inline DecLayer load_layer(const DecLayer* p) {
   o.nkc = uniform(p->nkc);
   o.kc4 = uniform(p->kc4);
   o.tiled = uniform(p->tiled);
-  o.pad_ = 0;
+  o.gsteps = uniform(p->gsteps);
   o.item0 = uniform64(p->item0);
   o.step0 = uniform64(p->step0);
   return o;
@@ -521,9 +521,9 @@ constexpr int block_waves(int T) { return T <= 2 ? 12 : 8; }
 // waves per block of the streaming kernel (fewer when the ring would not
 // fit the LDS)
 constexpr int kStreamWaves = 4;
-constexpr int stream_waves(int NS, int XW, int base = kStreamWaves) {
+constexpr int stream_waves(int NS, int XW, int base = kStreamWaves, int unit = 1024) {
   int w = base;
-  while (w > 1 && w * NS * XW * 1024 > 150 * 1024) w /= 2;
+  while (w > 1 && w * NS * XW * unit > 150 * 1024) w /= 2;
   return w;
 }
 

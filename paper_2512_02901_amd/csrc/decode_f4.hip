@@ -284,22 +284,219 @@ __device__ inline void write_outputs_f4(const DecLayer& L, const DecHeader& h, i
     buf_store8(L.part, (uint32_t)L.nkc * h.B * L.N * 8, (uint32_t)(((kc * h.B + b) * L.N + row) * 8), v);
 }
 
+// ------------------------------------------------ per-group axis scales ---
+// With per-group scales (a pair (s_re, s_im) per stage, row and group of
+// 256 gsteps consecutive codes; scales [T][N][groups][2]) the MFMAs of a
+// step start from zero, and the step's products, digits joined, are folded
+// into float32 sums with the scales of the step's group:
+//     Are += s_re (S - I),   Aim += s_im I        (per plane and component),
+// so the epilogue needs no scales.  Every step's scales of both matrices
+// arrive in the ring slot with the step's codes: per matrix ceil(T/2)
+// direct-to-LDS dword loads, lane l of load i carrying component l % 2 of
+// row (l % 32) / 2 of stage 2 i + l / 32, so the slot holds
+// [matrix][stage][16 rows][s_re, s_im] with 256 bytes per load.
+
+template <int T>
+struct GroupCursor {
+  const float* base[2];  // U, W scale arrays of the current layer
+  uint32_t bytes;        // bytes of each array
+  uint32_t tstride;      // bytes from stage t to stage t + 2
+  uint32_t off;          // this lane's offset for the current step's group
+  int gsteps, gpos, ngroups, N;
+  bool ok;               // this lane's row and stage exist
+};
+
+template <int T>
+__device__ inline void group_enter_layer(GroupCursor<T>& c, const DecLayer& L) {
+  c.base[0] = L.scales[0];
+  c.base[1] = L.scales[1];
+  c.gsteps = L.gsteps;
+  c.N = L.N;
+  c.ngroups = (L.nk4 + L.gsteps - 1) / L.gsteps;
+  c.bytes = (uint32_t)T * (uint32_t)L.N * (uint32_t)c.ngroups * 8u;
+  c.tstride = 2u * (uint32_t)L.N * (uint32_t)c.ngroups * 8u;
+}
+
+// Position the cursor at step k4 of row block rb.
+template <int T>
+__device__ inline void group_item(GroupCursor<T>& c, int rb, int k4, int lane) {
+  const int gi = k4 / c.gsteps;
+  c.gpos = k4 - gi * c.gsteps;
+  const int row = rb * 16 + ((lane & 31) >> 1);
+  const int t = lane >> 5;
+  c.ok = row < c.N && t < T;
+  c.off = ((uint32_t)(t * c.N + row) * (uint32_t)c.ngroups + (uint32_t)gi) * 8u + 4u * (uint32_t)(lane & 1);
+}
+
+template <int T>
+__device__ inline void group_step(GroupCursor<T>& c) {
+  if (++c.gpos == c.gsteps) {
+    c.gpos = 0;
+    c.off += 8u;
+  }
+}
+
+constexpr int group_loads(int T) { return (T + 1) / 2; }  // direct-to-LDS loads per matrix and step
+constexpr int group_slot_bytes(int T) { return 2 * group_loads(T) * 256; }
+
+// Issue the step's scale loads into the slot's scale area (a dead cursor
+// issues them out of range, so every step issues the same number of loads).
+template <int T>
+__device__ inline void group_issue(const GroupCursor<T>& c, bool live, int lane, uint8_t* gslot) {
+  constexpr int NI = group_loads(T);
+  const int bytes = __builtin_amdgcn_readfirstlane((int)c.bytes);
+#pragma unroll
+  for (int m = 0; m < 2; ++m) {
+    const auto r = make_rsrc(uniform_ptr(c.base[m]), (uint32_t)bytes);
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const bool v = live && c.ok && 2 * i + (lane >> 5) < T;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(gslot + (m * NI + i) * 256), 4,
+                                               v ? c.off + (uint32_t)i * c.tstride : kOob, 0, 0, 0);
+    }
+  }
+}
+
+// Scales (s_re, s_im) of plane p = m T + t for weight row li from a slot:
+// 2T LDS reads and their wait as one asm block, so that the compiler adds no
+// wait of its own for the loads still in flight into the ring's other slots
+// (the caller's vmcnt wait has already covered this slot).
+template <int T>
+__device__ inline void group_read(const uint8_t* gslot, int li, float (&gs)[2 * T][2]) {
+  constexpr int NI = group_loads(T);
+  const uint32_t a = lds_addr(gslot) + (uint32_t)li * 8u;
+  v2f r[2 * T];
+  // plane p = m T + t sits at (m NI + t / 2) * 256 + (t % 2) * 128
+#define F4_GOFF(m, t) (((m) * NI + (t) / 2) * 256 + ((t) % 2) * 128)
+  if constexpr (T == 1) {
+    __asm__ volatile("ds_read_b64 %0, %2 offset:%3\n\tds_read_b64 %1, %2 offset:%4\n\ts_waitcnt lgkmcnt(0)"
+                     : "=&v"(r[0]), "=&v"(r[1])
+                     : "v"(a), "i"(F4_GOFF(0, 0)), "i"(F4_GOFF(1, 0))
+                     : "memory");
+  } else if constexpr (T == 2) {
+    __asm__ volatile(
+        "ds_read_b64 %0, %4 offset:%5\n\tds_read_b64 %1, %4 offset:%6\n\t"
+        "ds_read_b64 %2, %4 offset:%7\n\tds_read_b64 %3, %4 offset:%8\n\ts_waitcnt lgkmcnt(0)"
+        : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3])
+        : "v"(a), "i"(F4_GOFF(0, 0)), "i"(F4_GOFF(0, 1)), "i"(F4_GOFF(1, 0)), "i"(F4_GOFF(1, 1))
+        : "memory");
+  } else if constexpr (T == 3) {
+    __asm__ volatile(
+        "ds_read_b64 %0, %6 offset:%7\n\tds_read_b64 %1, %6 offset:%8\n\tds_read_b64 %2, %6 offset:%9\n\t"
+        "ds_read_b64 %3, %6 offset:%10\n\tds_read_b64 %4, %6 offset:%11\n\tds_read_b64 %5, %6 offset:%12\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5])
+        : "v"(a), "i"(F4_GOFF(0, 0)), "i"(F4_GOFF(0, 1)), "i"(F4_GOFF(0, 2)), "i"(F4_GOFF(1, 0)),
+          "i"(F4_GOFF(1, 1)), "i"(F4_GOFF(1, 2))
+        : "memory");
+  } else {
+    static_assert(T == 4, "1 <= T <= 4");
+    __asm__ volatile(
+        "ds_read_b64 %0, %8 offset:%9\n\tds_read_b64 %1, %8 offset:%10\n\tds_read_b64 %2, %8 offset:%11\n\t"
+        "ds_read_b64 %3, %8 offset:%12\n\tds_read_b64 %4, %8 offset:%13\n\tds_read_b64 %5, %8 offset:%14\n\t"
+        "ds_read_b64 %6, %8 offset:%15\n\tds_read_b64 %7, %8 offset:%16\n\ts_waitcnt lgkmcnt(0)"
+        : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]), "=&v"(r[7])
+        : "v"(a), "i"(F4_GOFF(0, 0)), "i"(F4_GOFF(0, 1)), "i"(F4_GOFF(0, 2)), "i"(F4_GOFF(0, 3)),
+          "i"(F4_GOFF(1, 0)), "i"(F4_GOFF(1, 1)), "i"(F4_GOFF(1, 2)), "i"(F4_GOFF(1, 3))
+        : "memory");
+  }
+#undef F4_GOFF
+#pragma unroll
+  for (int p = 0; p < 2 * T; ++p) {
+    gs[p][0] = r[p][0];
+    gs[p][1] = r[p][1];
+  }
+}
+
+// Fold one step's products into the scaled sums (see above).
+template <int P>
+__device__ inline void fold_group(const v4f (&aS)[P], const v4f (&aI)[P], const float (&gs)[P][2],
+                                  float (&Are)[P][2], float (&Aim)[P][2]) {
+#pragma unroll
+  for (int p = 0; p < P; ++p)
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const float vS = fmaf(aS[p][2 + c], 1.0f / kLoScale, aS[p][c]);
+      const float vI = fmaf(aI[p][2 + c], 1.0f / kLoScale, aI[p][c]);
+      Are[p][c] = fmaf(gs[p][0], vS - vI, Are[p][c]);
+      Aim[p][c] = fmaf(gs[p][1], vI, Aim[p][c]);
+    }
+}
+
+// Epilogue of a work item with per-group scales: the lane's scaled sums,
+// second band passed down from the odd lane group (times 2^-8), then
+// Eq. (ifairy-dequant)'s combination with the scales already applied, U
+// with x and W with conj(x), stages in order, times the token factor.
+template <int T>
+__device__ inline void write_outputs_f4_gs(const DecLayer& L, const DecHeader& h, int kc, int row, bool row_ok,
+                                           int lane, int tile, const float (&Are)[2 * T][2],
+                                           const float (&Aim)[2 * T][2], const float (&xf)[2]) {
+  constexpr int P = 2 * T;
+  const int g = lane >> 4;
+  float vr[P][2], vi[P][2];
+#pragma unroll
+  for (int p = 0; p < P; ++p)
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const float hr = __shfl_down(Are[p][c], 16), hi = __shfl_down(Aim[p][c], 16);
+      vr[p][c] = fmaf(hr, 1.0f / kBand2Scale, Are[p][c]);
+      vi[p][c] = fmaf(hi, 1.0f / kBand2Scale, Aim[p][c]);
+    }
+  const int tt = g >> 1;
+  const int b = kTokensPerTile * tile + tt;
+  if ((g & 1) || !row_ok || b >= h.B) return;
+  float yr = 0.0f, yi = 0.0f;
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const int u = t, w = T + t;
+    yr = __fadd_rn(yr, vr[u][0]);
+    yr = __fsub_rn(yr, vi[u][1]);
+    yr = __fadd_rn(yr, vr[w][0]);
+    yr = __fadd_rn(yr, vi[w][1]);
+    yi = __fadd_rn(yi, vr[u][1]);
+    yi = __fadd_rn(yi, vi[u][0]);
+    yi = __fsub_rn(yi, vr[w][1]);
+    yi = __fadd_rn(yi, vi[w][0]);
+  }
+  const float f = tt ? xf[1] : xf[0];
+  const float2 v = make_float2(__fmul_rn(yr, f), __fmul_rn(yi, f));
+  if (L.nkc == 1)
+    buf_store8(L.y, (uint32_t)h.B * L.N * 8, (uint32_t)((b * L.N + row) * 8), v);
+  else
+    buf_store8(L.part, (uint32_t)L.nkc * h.B * L.N * 8, (uint32_t)(((kc * h.B + b) * L.N + row) * 8), v);
+}
+
 constexpr int f4_ring_slots(int T) { return ring_slots(T); }
 
 
 template <int T, int XW>
 using F4Cfg = StreamCfg<T, XW, f4_ring_slots(T), block_waves(T)>;
 
+// The streaming configuration with the per-group scale area in every slot.
+template <int T, int XW, bool GS>
+struct F4Ring {
+  using Base = F4Cfg<T, XW>;
+  static constexpr int P = Base::P, NS = Base::NS;
+  static constexpr int XSLOT = Base::XSLOT;                    // activation operand bytes
+  static constexpr int SLOT = XSLOT + (GS ? group_slot_bytes(T) : 0);
+  static constexpr int WAVES = stream_waves(NS, SLOT, block_waves(T), 1);  // fewer when the ring would not fit
+  static constexpr int LOADS = Base::LOADS + (GS ? 2 * group_loads(T) : 0);
+  static constexpr int WAIT = (NS - 1) * LOADS;
+  static constexpr int WAITCNT = (WAIT & 0xF) | (0x7 << 4) | (0xF << 8) | (((WAIT >> 4) & 3) << 14);
+  static_assert(WAIT < 64, "vmcnt holds at most 63");
+};
+
 // NT activation tiles (two tokens each); a ring slot holds XW KiB per tile.
-template <int T, int XW, int NT>
-__global__ __launch_bounds__((64 * F4Cfg<T, NT * XW>::WAVES)) void dec_stream_f4_kernel(DecHeader h, DecLayer inl,
-                                                                                       const DecLayer* __restrict__ tab) {
+// GS: per-group scales (every layer of the call).
+template <int T, int XW, int NT, bool GS>
+__global__ __launch_bounds__((64 * F4Ring<T, NT * XW, GS>::WAVES)) void dec_stream_f4_kernel(
+    DecHeader h, DecLayer inl, const DecLayer* __restrict__ tab) {
 #if defined(__HIP_DEVICE_COMPILE__)  // LDS-DMA and buffer-descriptor code: device pass only
-  using C = F4Cfg<T, NT * XW>;
-  constexpr int P = C::P, NS = C::NS, XSLOT = C::XSLOT;
+  using C = F4Ring<T, NT * XW, GS>;
+  constexpr int P = C::P, NS = C::NS, XSLOT = C::XSLOT, SLOT = C::SLOT;
   constexpr int WAVES = C::WAVES;
   static_assert(NS <= 4, "the item queue holds the items of up to NS - 1 steps ahead");
-  __shared__ __attribute__((aligned(16))) uint8_t ring[WAVES][NS][XSLOT];
+  __shared__ __attribute__((aligned(16))) uint8_t ring[WAVES][NS][SLOT];
   __shared__ __attribute__((aligned(16))) uint8_t zero16[16];
   __shared__ uint32_t claim_ctr;
   const int lane = threadIdx.x & 63;
@@ -336,6 +533,7 @@ __global__ __launch_bounds__((64 * F4Cfg<T, NT * XW>::WAVES)) void dec_stream_f4
 
   LoadCursor<T> lc;
   OutCursor oc;
+  GroupCursor<T> gc;
   ItemQueue iq;
   iq.n = 0;
   {
@@ -345,16 +543,18 @@ __global__ __launch_bounds__((64 * F4Cfg<T, NT * XW>::WAVES)) void dec_stream_f4
     lc.item = oc.item = i0;
     load_enter_layer(lc, L0, h);
     out_enter_layer(oc, L0);
+    if constexpr (GS) group_enter_layer(gc, L0);
     split_item(i0, lc.G, lc.rb, lc.kc);
     oc.rb = lc.rb;
     oc.kc = lc.kc;
   }
   load_item(lc, h, lane);
+  if constexpr (GS) group_item(gc, lc.rb, lc.k4, lane);
   out_item(oc, li);
   // the epilogue's per-layer constants, reloaded when the output side changes layer
   float esc[2][T][2], exf[NT][2];
   auto load_epilogue_consts = [&]() {
-    sload_scales<T>(uniform_ptr(oc.scales[0]), uniform_ptr(oc.scales[1]), esc);
+    if constexpr (!GS) sload_scales<T>(uniform_ptr(oc.scales[0]), uniform_ptr(oc.scales[1]), esc);
     // the factor array is padded to 256 bytes: both floats of every tile are inside it
 #pragma unroll
     for (int t = 0; t < NT; ++t) sload_run<2>(uniform_ptr(oc.xs) + kTokensPerTile * t, exf[t]);
@@ -368,11 +568,17 @@ __global__ __launch_bounds__((64 * F4Cfg<T, NT * XW>::WAVES)) void dec_stream_f4
       ++lc.k4;
       lc.voff += lc.vstep;
       lc.xoff += 256 * h.nc;
+      if constexpr (GS) group_step(gc);
       return true;
     }
     const int off = claim_item(ctr_addr, nb, lane);
     if (off < 0) return false;
+    const int lidx_before = lc.lidx;
     load_goto(lc, b0 + off, tab, h, lane);
+    if constexpr (GS) {
+      if (lc.lidx != lidx_before) group_enter_layer(gc, load_layer(tab + lc.lidx));
+      group_item(gc, lc.rb, lc.k4, lane);
+    }
     iq.push(off);
     return true;
   };
@@ -385,9 +591,13 @@ __global__ __launch_bounds__((64 * F4Cfg<T, NT * XW>::WAVES)) void dec_stream_f4
 
   v4i cq[NS][P];
   bool live = true;
+  auto issue = [&](int k, v4i (&q)[P]) {
+    stream_issue<XW, T, 32, NT>(lc, live, lane, q, &ring[wave][k][0]);
+    if constexpr (GS) group_issue<T>(gc, live, lane, &ring[wave][k][XSLOT]);
+  };
 #pragma unroll
   for (int k = 0; k < NS - 1; ++k) {
-    stream_issue<XW, T, 32, NT>(lc, live, lane, cq[k], &ring[wave][k][0]);
+    issue(k, cq[k]);
     if (live) live = load_advance();
   }
 
@@ -396,11 +606,19 @@ __global__ __launch_bounds__((64 * F4Cfg<T, NT * XW>::WAVES)) void dec_stream_f4
   for (int t = 0; t < NT; ++t)
 #pragma unroll
     for (int p = 0; p < P; ++p) aS[t][p] = aI[t][p] = v4f{0.f, 0.f, 0.f, 0.f};
+  // per-group scales: the scaled sums of the current item
+  float Are[NT][P][2], Aim[NT][P][2];
+  if constexpr (GS) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int p = 0; p < P; ++p) Are[t][p][0] = Are[t][p][1] = Aim[t][p][0] = Aim[t][p][1] = 0.0f;
+  }
 
   auto step = [&](auto kconst) -> bool {
     constexpr int K = decltype(kconst)::value;
     constexpr int KN = (K + NS - 1) % NS;
-    stream_issue<XW, T, 32, NT>(lc, live, lane, cq[KN], &ring[wave][KN][0]);
+    issue(KN, cq[KN]);
     if (live) live = load_advance();
     __builtin_amdgcn_s_waitcnt(C::WAITCNT);
     v4i xr[NT][4];
@@ -422,20 +640,35 @@ __global__ __launch_bounds__((64 * F4Cfg<T, NT * XW>::WAVES)) void dec_stream_f4
         for (int t = 0; t < NT; ++t) {
           const v4i x0 = xr[t][2 * kb], x1 = xr[t][2 * kb + 1];
           const v8i a = v8i{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
-          aS[t][p] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bs, aS[t][p], kFmtFp8, kFmtFp4, 0, 0, 0, 0);
-          aI[t][p] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bi, aI[t][p], kFmtFp8, kFmtFp4, 0, 0, 0, 0);
+          // per-group scales: every step starts from zero
+          const v4f cS = (GS && kb == 0) ? v4f{0.f, 0.f, 0.f, 0.f} : aS[t][p];
+          const v4f cI = (GS && kb == 0) ? v4f{0.f, 0.f, 0.f, 0.f} : aI[t][p];
+          aS[t][p] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bs, cS, kFmtFp8, kFmtFp4, 0, 0, 0, 0);
+          aI[t][p] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bi, cI, kFmtFp8, kFmtFp4, 0, 0, 0, 0);
         }
         __builtin_amdgcn_sched_group_barrier(0x002, 10, 0);
         __builtin_amdgcn_sched_group_barrier(0x008, 2 * NT, 0);
       }
     }
+    if constexpr (GS) {
+      float gs[P][2];
+      group_read<T>(&ring[wave][K][XSLOT], li, gs);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) fold_group<P>(aS[t], aI[t], gs, Are[t], Aim[t]);
+    }
     if (oc.j == oc.nsteps - 1) {
       const DecLayer Lo = out_layer(oc);
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        write_outputs_f4<T>(Lo, h, oc.kc, oc.row, oc.row_ok, lane, t, aS[t], aI[t], esc, exf[t]);
+        if constexpr (GS) {
+          write_outputs_f4_gs<T>(Lo, h, oc.kc, oc.row, oc.row_ok, lane, t, Are[t], Aim[t], exf[t]);
 #pragma unroll
-        for (int p = 0; p < P; ++p) aS[t][p] = aI[t][p] = v4f{0.f, 0.f, 0.f, 0.f};
+          for (int p = 0; p < P; ++p) Are[t][p][0] = Are[t][p][1] = Aim[t][p][0] = Aim[t][p][1] = 0.0f;
+        } else {
+          write_outputs_f4<T>(Lo, h, oc.kc, oc.row, oc.row_ok, lane, t, aS[t], aI[t], esc, exf[t]);
+#pragma unroll
+          for (int p = 0; p < P; ++p) aS[t][p] = aI[t][p] = v4f{0.f, 0.f, 0.f, 0.f};
+        }
       }
     }
     return !out_advance();
@@ -454,10 +687,10 @@ __global__ __launch_bounds__((64 * F4Cfg<T, NT * XW>::WAVES)) void dec_stream_f4
 #endif
 }
 
-template <int T, int XW, int NT>
+template <int T, int XW, int NT, bool GS>
 void launch_stream_f4(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
-  auto k = dec_stream_f4_kernel<T, XW, NT>;
-  constexpr int waves = F4Cfg<T, NT * XW>::WAVES;
+  auto k = dec_stream_f4_kernel<T, XW, NT, GS>;
+  constexpr int waves = F4Ring<T, NT * XW, GS>::WAVES;
   constexpr int threads = 64 * waves;
   static const int resident = resident_blocks(reinterpret_cast<const void*>(k), threads);
   const int64_t want = (h.total_items + waves - 1) / waves;
@@ -467,16 +700,22 @@ void launch_stream_f4(const DecHeader& h, const DecLayer& inl, const DecLayer* t
 
 // XW = KiB of activation operand per 256-code step and tile (nc / 4), NT =
 // activation tiles of two tokens (three or four tokens: two tiles, T <= 3).
-template <int T>
-void launch_stream_f4_t(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
+template <int T, bool GS>
+void launch_stream_f4_g(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
   if constexpr (T <= 3) {
     if (h.ntile >= 2) {
-      launch_stream_f4<T, 4, 2>(h, inl, tab, s);
+      launch_stream_f4<T, 4, 2, GS>(h, inl, tab, s);
       return;
     }
   }
-  if (h.nc <= 8) launch_stream_f4<T, 2, 1>(h, inl, tab, s);
-  else launch_stream_f4<T, 4, 1>(h, inl, tab, s);
+  if (h.nc <= 8) launch_stream_f4<T, 2, 1, GS>(h, inl, tab, s);
+  else launch_stream_f4<T, 4, 1, GS>(h, inl, tab, s);
+}
+
+template <int T>
+void launch_stream_f4_t(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
+  if (h.grouped) launch_stream_f4_g<T, true>(h, inl, tab, s);
+  else launch_stream_f4_g<T, false>(h, inl, tab, s);
 }
 
 }  // namespace

@@ -41,6 +41,31 @@ __device__ inline void sa_add_lds(unsigned long long* acc, double v) {
   if (hi) atomicAdd(&acc[limb + 2], (unsigned long long)hi);
 }
 
+// Rebuild the float64 residual of one entry from M and the codes/scales of
+// stages < t (R(tp+1) = R(tp) - W^(tp)), project it, and add its magnitude
+// on the chosen axis to the block's exact accumulator.  Returns the code.
+__device__ inline uint32_t qz_entry(float2 m, const uint32_t* prev, int e, int t, const double* s_re,
+                                    const double* s_im, unsigned long long (*acc)[SA_LIMBS],
+                                    unsigned long long& n_re, unsigned long long& n_im) {
+  double re = (double)m.x, im = (double)m.y;
+  for (int tp = 0; tp < t; ++tp) {
+    const uint32_t k = (prev[tp] >> (2 * e)) & 3u;
+    if (k == 0u) re = re - s_re[tp];
+    else if (k == 2u) re = re + s_re[tp];
+    else if (k == 1u) im = im - s_im[tp];
+    else im = im + s_im[tp];
+  }
+  const uint32_t k = project_code(re, im);
+  if (k & 1u) {
+    sa_add_lds(acc[1], fabs(im));
+    ++n_im;
+  } else {
+    sa_add_lds(acc[0], fabs(re));
+    ++n_re;
+  }
+  return k;
+}
+
 __global__ __launch_bounds__(kQzThreads) void qz_stage_kernel(
     const float2* __restrict__ M, int64_t nbytes, uint8_t* __restrict__ codes,
     const float* __restrict__ scales, int t, unsigned long long* __restrict__ tot) {
@@ -62,26 +87,7 @@ __global__ __launch_bounds__(kQzThreads) void qz_stage_kernel(
     for (int tp = 0; tp < t; ++tp) prev[tp] = codes[(int64_t)tp * nbytes + bi];
     uint32_t out = 0;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float2 m = M[4 * bi + e];
-      double re = (double)m.x, im = (double)m.y;
-      for (int tp = 0; tp < t; ++tp) {  // R(tp+1) = R(tp) - W^(tp)
-        const uint32_t k = (prev[tp] >> (2 * e)) & 3u;
-        if (k == 0u) re = re - s_re[tp];
-        else if (k == 2u) re = re + s_re[tp];
-        else if (k == 1u) im = im - s_im[tp];
-        else im = im + s_im[tp];
-      }
-      const uint32_t k = project_code(re, im);
-      out |= k << (2 * e);
-      if (k & 1u) {
-        sa_add_lds(acc[1], fabs(im));
-        ++n_im;
-      } else {
-        sa_add_lds(acc[0], fabs(re));
-        ++n_re;
-      }
-    }
+    for (int e = 0; e < 4; ++e) out |= qz_entry(M[4 * bi + e], prev, e, t, s_re, s_im, acc, n_re, n_im) << (2 * e);
     codes[(int64_t)t * nbytes + bi] = (uint8_t)out;
   }
   if (n_re) atomicAdd(&cnt[0], n_re);
@@ -104,6 +110,51 @@ __global__ __launch_bounds__(64) void qz_finalize_kernel(const unsigned long lon
   }
 }
 
+// Per-group scales: one block per (row, group of G columns).  The block
+// quantises the group's entries at stage t exactly as qz_stage_kernel does,
+// with the residual rebuilt from the group's own scales of earlier stages,
+// and rounds the group's two exact means once to float32 into
+// scales[t][row][g][axis].  No cross-block reduction is needed.
+constexpr int kQzgThreads = 64;
+
+__global__ __launch_bounds__(kQzgThreads) void qzg_stage_kernel(const float2* __restrict__ M, int64_t N, int64_t K,
+                                                                 int64_t G, int64_t ngroups,
+                                                                 uint8_t* __restrict__ codes,
+                                                                 float* __restrict__ scales, int t) {
+  __shared__ unsigned long long acc[2][SA_LIMBS];
+  __shared__ unsigned long long cnt[2];
+  for (int i = threadIdx.x; i < 2 * SA_LIMBS; i += blockDim.x) (&acc[0][0])[i] = 0ull;
+  if (threadIdx.x < 2) cnt[threadIdx.x] = 0ull;
+  __syncthreads();
+  const int64_t row = (int64_t)blockIdx.x / ngroups;
+  const int64_t g = (int64_t)blockIdx.x - row * ngroups;
+  const int64_t j0 = g * G, j1 = j0 + G < K ? j0 + G : K;  // columns of the group (multiples of 4)
+  const int64_t nbytes = N * K / 4;
+  double s_re[FAIRY2I_MAX_STAGES], s_im[FAIRY2I_MAX_STAGES];
+  for (int tp = 0; tp < t; ++tp) {
+    const float* sp = scales + ((tp * N + row) * ngroups + g) * 2;
+    s_re[tp] = (double)sp[0];
+    s_im[tp] = (double)sp[1];
+  }
+  unsigned long long n_re = 0, n_im = 0;
+  for (int64_t bi = row * (K / 4) + j0 / 4 + threadIdx.x; bi < row * (K / 4) + j1 / 4; bi += blockDim.x) {
+    uint32_t prev[FAIRY2I_MAX_STAGES];
+    for (int tp = 0; tp < t; ++tp) prev[tp] = codes[(int64_t)tp * nbytes + bi];
+    uint32_t out = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) out |= qz_entry(M[4 * bi + e], prev, e, t, s_re, s_im, acc, n_re, n_im) << (2 * e);
+    codes[(int64_t)t * nbytes + bi] = (uint8_t)out;
+  }
+  if (n_re) atomicAdd(&cnt[0], n_re);
+  if (n_im) atomicAdd(&cnt[1], n_im);
+  __syncthreads();
+  if (threadIdx.x < 2) {
+    const unsigned long long n = cnt[threadIdx.x];
+    scales[((t * N + row) * ngroups + g) * 2 + threadIdx.x] =
+        n ? sa_mean_to_f32(reinterpret_cast<const uint64_t*>(acc[threadIdx.x]), n) : 0.0f;
+  }
+}
+
 __global__ __launch_bounds__(256) void qz_zero_kernel(unsigned long long* __restrict__ p, int n) {
   for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = 0ull;
 }
@@ -117,6 +168,18 @@ int quantize_blocks(int64_t N, int64_t K) {
 }
 
 }  // namespace
+
+hipError_t launch_quantize_grouped(const float2* M, int64_t N, int64_t K, int T, int64_t G, uint8_t* codes,
+                                   float* scales, hipStream_t stream) {
+  const int64_t ngroups = (K + G - 1) / G;
+  for (int t = 0; t < T; ++t) {
+    hipLaunchKernelGGL(qzg_stage_kernel, dim3((unsigned)(N * ngroups)), dim3(kQzgThreads), 0, stream, M, N, K, G,
+                       ngroups, codes, scales, t);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
 
 size_t quantize_workspace_bytes(int64_t N, int64_t K) {
   (void)N;

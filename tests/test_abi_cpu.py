@@ -42,7 +42,7 @@ def test_status_strings(lib):
     for s in range(8):
         assert lib.fairy2i_status_string(s)
     assert lib.fairy2i_status_string(99) == b"unknown status"
-    assert lib.fairy2i_abi_version() == 4
+    assert lib.fairy2i_abi_version() == 5
 
 
 def test_to_widely_linear_validation(lib):
@@ -158,10 +158,10 @@ def test_scale_rounding_random_ties(lib):
 
 def _layer(**kw):
     d = dict(codes_U=0x1000, scales_U=0x1000, codes_W=0x1000, scales_W=0x1000, x=0x1000, x_scale=None,
-             y=0x1000, N=64, K=128, layout=binding.LAYOUT_D3, reserved=0)
+             y=0x1000, N=64, K=128, layout=binding.LAYOUT_D3, group_size=0)
     d.update(kw)
     return binding.WlLayer(d["codes_U"], d["scales_U"], d["codes_W"], d["scales_W"], d["x"], d["x_scale"],
-                           d["y"], d["N"], d["K"], d["layout"], d["reserved"])
+                           d["y"], d["N"], d["K"], d["layout"], d["group_size"])
 
 
 def test_group_build_validation(lib):
@@ -199,7 +199,9 @@ def test_group_build_validation(lib):
     assert build([_layer(layout=fp4), _layer()]) == binding.ERR_UNSUPPORTED  # fp4 for every layer or none
     assert build([_layer(), _layer(layout=fp4)]) == binding.ERR_UNSUPPORTED
     assert build([_layer(layout=3)]) == binding.ERR_UNSUPPORTED
-    assert build([_layer(reserved=1)]) == binding.ERR_UNSUPPORTED
+    assert build([_layer(group_size=1)]) == binding.ERR_UNSUPPORTED       # not whole 256-code steps
+    assert build([_layer(group_size=256)]) == binding.ERR_UNSUPPORTED     # per-group scales need fp4 codes
+    assert build([_layer(group_size=-256)]) == binding.ERR_UNSUPPORTED
 
 
 def test_repack_validation_and_size(lib):

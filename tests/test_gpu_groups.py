@@ -1,0 +1,205 @@
+"""GPU parity of per-group axis scales against the CPU oracle
+(oracle/groups.py: groups of G input columns of one output row).
+
+Bars: the grouped quantiser's codes and scales bit-exact (each scale is an
+exact group mean rounded once, so it does not depend on the order of the
+GPU's additions); the grouped decode (fp4 path, bf16 tokens) within relative
+L2 TOL_FP4 = 1e-6 of the oracle's product with the same codes and scales.
+Every step's products are folded into float32 sums with its group's scales,
+so the float32 rounding grows with the number of groups, not with K; the
+measured error is about 1e-7."""
+import numpy as np
+import pytest
+
+import oracle
+from oracle import groups as og
+import synth
+
+pytestmark = pytest.mark.gpu
+
+TOL_FP4 = 1e-6
+
+
+def rel_l2(got, want):
+    got = np.asarray(got, dtype=np.complex128)
+    want = np.asarray(want, dtype=np.complex128)
+    den = np.linalg.norm(want)
+    return np.linalg.norm(got - want) / (den if den > 0 else 1.0)
+
+
+def dev(a, gpu):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).to(gpu)
+
+
+def host(t):
+    return t.detach().cpu().numpy()
+
+
+def bf16_dev(x, gpu):
+    import torch
+    bits = np.stack([synth.bf16_bits(x.real.astype(np.float32)),
+                     synth.bf16_bits(x.imag.astype(np.float32))], axis=-1)
+    return dev(bits.view(np.int16), gpu).view(torch.bfloat16)
+
+
+def bf16_tokens(rng, B, K):
+    x = rng.standard_normal((B, K)) + 1j * rng.standard_normal((B, K))
+    return synth.bf16_round_complex(x)
+
+
+@pytest.mark.parametrize("N,K,G,T", [(64, 1024, 256, 2), (37, 520, 100, 2), (16, 5504, 256, 3),
+                                     (9, 64, 4, 4), (20, 96, 1000, 1), (33, 2048, 512, 2)])
+def test_quantize_grouped_bit_exact(gpu, N, K, G, T):
+    import paper_2512_02901_amd as f2
+    A = synth.llama_weight(2 * N, 2 * K, (N, K, G))
+    U, _ = oracle.to_widely_linear(A)
+    codes, scales = og.quantize_grouped(U, T, G)
+    d_codes, d_scales = f2.quantize_grouped(dev(U, gpu), T, G)
+    np.testing.assert_array_equal(host(d_codes), oracle.pack(codes))
+    np.testing.assert_array_equal(host(d_scales), scales)
+
+
+def test_quantize_grouped_degenerate(gpu):
+    """Rows of zeros (every entry codes +1, empty im-axis groups), a pure
+    imaginary row, and ties on the diagonals."""
+    import paper_2512_02901_amd as f2
+    N, K, G, T = 4, 64, 16, 2
+    M = np.zeros((N, K), dtype=np.complex64)
+    M[1] = 1j * np.arange(1, K + 1, dtype=np.float32)
+    M[2] = (1 + 1j) * np.linspace(-2, 2, K).astype(np.float32)
+    M[3, ::2] = -3.0
+    codes, scales = og.quantize_grouped(M, T, G)
+    d_codes, d_scales = f2.quantize_grouped(dev(M, gpu), T, G)
+    np.testing.assert_array_equal(host(d_codes), oracle.pack(codes))
+    np.testing.assert_array_equal(host(d_scales), scales)
+
+
+def grouped_layers(shapes, T, G, gpu, seed):
+    """[(N, K, G)] -> device args and oracle inputs, quantised on the GPU
+    (the oracle product takes the downloaded codes and scales)."""
+    import paper_2512_02901_amd as f2
+    out = []
+    for i, (N, K, g) in enumerate(shapes):
+        gg = g or G
+        A = synth.llama_weight(2 * N, 2 * K, (seed, i))
+        U, W = oracle.to_widely_linear(A)
+        cu, su = f2.quantize_grouped(dev(U, gpu), T, gg)
+        cw, sw = f2.quantize_grouped(dev(W, gpu), T, gg)
+        out.append((N, K, gg, cu, su, cw, sw))
+    return out
+
+
+def run_grouped(layers, T, B, gpu, rng, check_layers=None):
+    import torch
+    import paper_2512_02901_amd as f2
+    G = layers[0][2]
+    args, xs = [], []
+    for (N, K, g, cu, su, cw, sw) in layers:
+        assert g == G
+        x = bf16_tokens(rng, B, K)
+        y = torch.empty((B, N), dtype=torch.complex64, device=gpu)
+        args.append((f2.repack_tiled_fp4(cu), su, f2.repack_tiled_fp4(cw), sw, bf16_dev(x, gpu), None, y))
+        xs.append(x)
+    grp = f2.WlGroup(args, T=T, B=B, layout=f2.LAYOUT_TILED_FP4, group_size=G)
+    grp.run()
+    torch.cuda.synchronize()
+    errs = []
+    for i in (check_layers if check_layers is not None else range(len(layers))):
+        N, K, g, cu, su, cw, sw = layers[i]
+        Kc = cu.shape[2] * 4
+        want = og.wl_matmul_grouped(oracle.unpack(host(cu), Kc), host(su), oracle.unpack(host(cw), Kc), host(sw),
+                                    xs[i], g)
+        errs.append(rel_l2(host(args[i][6]), want))
+    return errs, grp, args
+
+
+@pytest.mark.parametrize("B", [1, 2, 3, 4])
+@pytest.mark.parametrize("T,G", [(1, 256), (2, 256), (2, 512), (3, 1024)])
+def test_grouped_decode_matches_oracle(gpu, B, T, G):
+    rng = np.random.default_rng(100 * B + 10 * T + G)
+    shapes = [(128, 1024, None), (37, 5504, None), (200, 256, None), (16, 2048, None)]
+    layers = grouped_layers(shapes, T, G, gpu, seed=B * 7 + T)
+    errs, _, _ = run_grouped(layers, T, B, gpu, rng)
+    assert max(errs) <= TOL_FP4, errs
+
+
+def test_grouped_decode_t4(gpu):
+    rng = np.random.default_rng(44)
+    layers = grouped_layers([(48, 1280, None), (16, 512, None)], 4, 256, gpu, seed=44)
+    for B in (1, 2):
+        errs, _, _ = run_grouped(layers, 4, B, gpu, rng)
+        assert max(errs) <= TOL_FP4, errs
+
+
+def test_grouped_decode_repeatable_and_mixed_group_sizes(gpu):
+    """Layers with different group sizes in one call; repeated calls give
+    bitwise equal results."""
+    import torch
+    import paper_2512_02901_amd as f2
+    rng = np.random.default_rng(45)
+    T, B = 2, 1
+    layers = grouped_layers([(64, 1024, 256), (40, 2048, 768), (16, 5504, 2048)], T, 0, gpu, seed=45)
+    args, xs = [], []
+    for (N, K, g, cu, su, cw, sw) in layers:
+        x = bf16_tokens(rng, B, K)
+        y = torch.empty((B, N), dtype=torch.complex64, device=gpu)
+        args.append((f2.repack_tiled_fp4(cu), su, f2.repack_tiled_fp4(cw), sw, bf16_dev(x, gpu), None, y))
+        xs.append(x)
+    # the binding takes one group size per call: build the table through the C ABI directly
+    from paper_2512_02901_amd import binding
+    import ctypes
+    lib = binding.load()
+    arr = (binding.WlLayer * len(args))()
+    for i, (a, L) in enumerate(zip(args, layers)):
+        cu4, su, cw4, sw, x, _, y = a
+        arr[i] = binding.WlLayer(cu4.data_ptr(), su.data_ptr(), cw4.data_ptr(), sw.data_ptr(), x.data_ptr(), None,
+                                 y.data_ptr(), L[0], L[1], binding.LAYOUT_TILED_FP4, L[2])
+    wsb = int(lib.fairy2i_wl_group_workspace_bytes(ctypes.byref(arr), len(args), T, binding.ACT_BF16, B))
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=gpu)
+    tb = int(lib.fairy2i_wl_group_table_bytes(len(args)))
+    table = (ctypes.c_uint8 * tb)()
+    assert lib.fairy2i_wl_group_build_table(ctypes.byref(arr), len(args), T, binding.ACT_BF16, B,
+                                            ctypes.c_void_p(ws.data_ptr()), wsb, ctypes.byref(table), tb) == 0
+    table_dev = torch.frombuffer(bytearray(bytes(table)), dtype=torch.uint8).to(gpu)
+    stream = torch.cuda.current_stream(gpu).cuda_stream
+    outs = []
+    for _ in range(3):
+        assert lib.fairy2i_wl_matmul_group(ctypes.byref(table), ctypes.c_void_p(table_dev.data_ptr()), stream) == 0
+        torch.cuda.synchronize()
+        outs.append([host(a[6]).copy() for a in args])
+    for o in outs[1:]:
+        for a, b in zip(outs[0], o):
+            np.testing.assert_array_equal(a, b)
+    for i, (N, K, g, cu, su, cw, sw) in enumerate(layers):
+        want = og.wl_matmul_grouped(oracle.unpack(host(cu), K), host(su), oracle.unpack(host(cw), K), host(sw),
+                                    xs[i], g)
+        assert rel_l2(outs[0][i], want) <= TOL_FP4
+
+
+def test_grouped_stack_full_k_items(gpu):
+    """A group large enough for full-K work items (every row block one item,
+    no partials): 70 LLaMA-2-7B-shaped layers (ten layers of each
+    projection, 13,280 row blocks), G = 256, checked on four of them."""
+    import synth as s
+    rng = np.random.default_rng(46)
+    T, G, B = 2, 256, 1
+    shapes = []
+    for layer in range(10):
+        for p in s.PROJ_ORDER:
+            rows, cols = s.LLAMA2_7B_PROJ[p]
+            shapes.append((rows // 2, cols // 2, None))
+    # quantise on the GPU from torch-generated LLaMA-like weights (fast at this size)
+    import torch
+    import paper_2512_02901_amd as f2
+    layers = []
+    for i, (N, K, _) in enumerate(shapes):
+        A = s.torch_llama_weight(2 * N, 2 * K, 7000 + i, gpu)
+        U, W = f2.to_widely_linear(A)
+        cu, su = f2.quantize_grouped(U, T, G)
+        cw, sw = f2.quantize_grouped(W, T, G)
+        layers.append((N, K, G, cu, su, cw, sw))
+        del A, U, W
+    assert sum((N + 15) // 16 for N, _, _ in shapes) >= 12288   # full-K work items
+    errs, _, _ = run_grouped(layers, T, B, gpu, rng, check_layers=[0, 4, 6, 69])
+    assert max(errs) <= TOL_FP4, errs
