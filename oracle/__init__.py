@@ -13,3 +13,4 @@ from .fairy2i import (CODEWORDS, axis_scales, code_planes, combine_accumulators,
                       to_widely_linear_f64, unpack, wl_matmul, wl_matmul_int8)
 from . import block  # noqa: F401,E402
 from . import groups  # noqa: F401,E402
+from . import qat  # noqa: F401,E402
