@@ -467,6 +467,86 @@ fairy2i_status fairy2i_block_intermediates(const void* plan, void** ptrs);
 fairy2i_status fairy2i_host_exact_mean_f32(const double* values, int64_t n_values, float* out);
 
 /*
+ * Quantisation-aware training of one widely-linear layer (Sec. 3.2, QAT
+ * paragraph and remark (iii); Sec. 3.3, the QAT remarks after the formal
+ * definition): full-precision masters, a fake-quantised forward pass, a
+ * straight-through backward pass, and complex GEMMs with Gauss's three real
+ * products.
+ *
+ * fairy2i_qat_fake_quant: the quantiser of fairy2i_quantize (same codes,
+ * scales, workspace and errors) followed by the dequantised sum
+ * W^ = sum_t (s_re b_re + i s_im b_im) of every entry (Eq. res-sum), summed
+ * in double and rounded once to out_dtype: FAIRY2I_ACT_F32 (complex64
+ * [N][K]) or FAIRY2I_ACT_BF16 (bf16 pairs [N][K][2]).  The codes and scales
+ * are what fairy2i_qat_ste_backward takes.
+ * Errors: as fairy2i_quantize; FAIRY2I_ERR_DTYPE for another out_dtype.
+ */
+fairy2i_status fairy2i_qat_fake_quant(const float* M, int64_t N, int64_t K, int32_t T, uint8_t* codes,
+                                      float* scales, void* w_hat, int32_t out_dtype, void* workspace,
+                                      size_t workspace_bytes, void* stream);
+
+/*
+ * Straight-through backward of the fake quantiser: from g_hat = dL/dW^
+ * (complex64 [N][K], g = dL/dRe + i dL/dIm) to g_master = dL/dM (complex64
+ * [N][K] output), through W^ = sum_t Q_t, Q_t = s_t b(R_t), R_{t+1} = R_t -
+ * Q_t, R_0 = M, taking b(.) as the identity map of the complex entry (no
+ * clipping radius) and each scale as the masked mean of Eq. (ifairy-scale)
+ * with its mask fixed (d s_re / d Re r_j = b_re_j / n_re on the entries
+ * coded +-1, likewise s_im).  Stage t, in reverse order, with H = dL/dR_{t+1}
+ * (0 for t = T-1) and G_Q = g_hat - H:
+ *   H += (s_re Re G_Q + b_re d_re) + i (s_im Im G_Q + b_im d_im),
+ *   d_re = sum_j Re(G_Q_j) b_re_j / n_re,  d_im likewise (0 when empty).
+ * The sums are taken in double in a fixed order (bitwise reproducible); H is
+ * kept in g_master as complex64.  codes, scales: as written by
+ * fairy2i_qat_fake_quant.  workspace: fairy2i_qat_ste_workspace_bytes(N, K).
+ * Errors: FAIRY2I_ERR_NULL; FAIRY2I_ERR_SHAPE (as fairy2i_quantize);
+ * FAIRY2I_ERR_STAGES; FAIRY2I_ERR_WORKSPACE.
+ */
+size_t fairy2i_qat_ste_workspace_bytes(int64_t N, int64_t K);
+fairy2i_status fairy2i_qat_ste_backward(const uint8_t* codes, const float* scales, int32_t T, int64_t N, int64_t K,
+                                        const float* g_hat, float* g_master, void* workspace,
+                                        size_t workspace_bytes, void* stream);
+
+/*
+ * One operand of fairy2i_cgemm_gauss: `rows` x K complex values (rows = M
+ * for A, N for B), either with K contiguous (trans = 0: element (r, k) at
+ * index r * ld + k, ld >= K) or with the rows contiguous (trans = 1: element
+ * (r, k) at index k * ld + r, ld >= rows).  dtype FAIRY2I_ACT_F32 (complex64
+ * values) or FAIRY2I_ACT_BF16 (bf16 pairs); conj = 1 takes the conjugate.
+ */
+typedef struct fairy2i_cgemm_operand {
+  const void* data;
+  int64_t ld;
+  int32_t dtype;
+  int32_t trans;
+  int32_t conj;
+  int32_t reserved; /* 0 */
+} fairy2i_cgemm_operand;
+
+/*
+ * Complex GEMM with Gauss's three real products (Sec. 3.2, remark (iii)):
+ *   C[m][n] (+)= sum over segments s < nseg, k < K[s] of A[s](m, k) B[s](n, k)
+ * with each complex product formed as P1 = Ar Br, P2 = Ai Bi,
+ * P3 = (Ar + Ai)(Br + Bi), C = (P1 - P2) + i (P3 - P1 - P2): three real
+ * products instead of four.  The operands are rounded to bf16 (the sums
+ * Ar + Ai and Br + Bi formed in float32 from the inputs and rounded once)
+ * and multiplied on the bf16 matrix cores with float32 accumulation.  Two
+ * segments cover the widely-linear layer in one call: Y = X U^T + conj(X)
+ * W^T (forward), G_X = G_Y conj(U) + conj(G_Y) W and [G_U | G_W] =
+ * G_Y^T [conj(X) | X] (backward).  C: complex64 [M][ldc]; accumulate = 1
+ * adds to C.  Error: the real part as exact as float32 accumulation of the
+ * bf16 operands; the imaginary part carries the bf16 rounding of the two
+ * sums, at most about 2^-8 sum_k |Ar + Ai| |Br + Bi| per element.
+ * Errors: FAIRY2I_ERR_NULL; FAIRY2I_ERR_SHAPE for nseg outside [1, 2],
+ * M, N, K[s] <= 0, ldc < N, an ld below its minimum, or a bad dtype / trans
+ * / conj / reserved field; FAIRY2I_ERR_UNSUPPORTED for M above 4,194,240
+ * (65,535 tiles of 64 rows) or N above 2^31.
+ */
+fairy2i_status fairy2i_cgemm_gauss(const fairy2i_cgemm_operand* A, const fairy2i_cgemm_operand* B, const int64_t* K,
+                                   int32_t nseg, int64_t M, int64_t N, float* C, int64_t ldc, int32_t accumulate,
+                                   void* stream);
+
+/*
  * CPU table-lookup product for int8 activations (Sec. 3.4, the paragraph on
  * lookup tables for CPU inference): every four consecutive codes of a row
  * (one byte of the canonical packed layout) index a 256-entry table of their

@@ -52,6 +52,11 @@ _SIGNATURES = {
     "fairy2i_block_build_plan": (_c_i32, [_c_p, _c_p, _c_size, _c_p, _c_size]),
     "fairy2i_block_decode": (_c_i32, [_c_p, _c_p, _c_p, _c_p, _c_p, _c_i64, _c_p, _c_p]),
     "fairy2i_block_intermediates": (_c_i32, [_c_p, _c_p]),
+    "fairy2i_qat_fake_quant": (_c_i32, [_c_p, _c_i64, _c_i64, _c_i32, _c_p, _c_p, _c_p, _c_i32, _c_p, _c_size,
+                                        _c_p]),
+    "fairy2i_qat_ste_workspace_bytes": (_c_size, [_c_i64, _c_i64]),
+    "fairy2i_qat_ste_backward": (_c_i32, [_c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_size, _c_p]),
+    "fairy2i_cgemm_gauss": (_c_i32, [_c_p, _c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_i64, _c_i32, _c_p]),
     "fairy2i_cpu_lut_workspace_bytes": (_c_size, [_c_i32, _c_i64, _c_i64, _c_i32]),
     "fairy2i_cpu_lut_wl_matmul": (_c_i32, [_c_p, _c_p, _c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_p, _c_i64,
                                            _c_p, _c_p, _c_p, _c_size, _c_i32]),
@@ -63,6 +68,12 @@ class WlLayer(ctypes.Structure):
     _fields_ = [("codes_U", _c_p), ("scales_U", _c_p), ("codes_W", _c_p), ("scales_W", _c_p),
                 ("x", _c_p), ("x_scale", _c_p), ("y", _c_p), ("N", _c_i64), ("K", _c_i64),
                 ("layout", _c_i32), ("group_size", _c_i32)]
+
+
+class CgemmOperand(ctypes.Structure):
+    """fairy2i_cgemm_operand of include/fairy2i.h."""
+    _fields_ = [("data", _c_p), ("ld", _c_i64), ("dtype", _c_i32), ("trans", _c_i32), ("conj", _c_i32),
+                ("reserved", _c_i32)]
 
 
 class BlockDesc(ctypes.Structure):
@@ -366,6 +377,89 @@ def host_exact_mean_f32(values) -> np.float32:
     _check(lib.fairy2i_host_exact_mean_f32(v.ctypes.data_as(ctypes.c_void_p), v.size,
                                            ctypes.byref(out)), "fairy2i_host_exact_mean_f32")
     return np.float32(out.value)
+
+
+def qat_fake_quant(M, T: int, out_dtype: int = ACT_BF16):
+    """Fake-quant forward of a complex64 master [N, K]: (W^, codes, scales);
+    W^ is bf16 pairs [N, K, 2] (ACT_BF16) or complex64 [N, K] (ACT_F32)."""
+    torch = _torch()
+    lib = load()
+    _require(M, torch.complex64, "M")
+    N, K = M.shape
+    codes = torch.empty((T, N, K // 4), dtype=torch.uint8, device=M.device)
+    scales = torch.empty((T, 2), dtype=torch.float32, device=M.device)
+    if out_dtype == ACT_BF16:
+        w_hat = torch.empty((N, K, 2), dtype=torch.bfloat16, device=M.device)
+    else:
+        w_hat = torch.empty((N, K), dtype=torch.complex64, device=M.device)
+    wsb = lib.fairy2i_quantize_workspace_bytes(N, K, T)
+    ws = torch.empty(max(int(wsb), 1), dtype=torch.uint8, device=M.device)
+    _check(lib.fairy2i_qat_fake_quant(_ptr(M), N, K, T, _ptr(codes), _ptr(scales), _ptr(w_hat), out_dtype, _ptr(ws),
+                                      wsb, _stream_ptr(M)), "fairy2i_qat_fake_quant")
+    return w_hat, codes, scales
+
+
+def qat_ste_backward(codes, scales, g_hat):
+    """dL/dM from dL/dW^ (complex64 [N, K]) through the fake quantiser."""
+    torch = _torch()
+    lib = load()
+    _require(g_hat, torch.complex64, "g_hat")
+    N, K = g_hat.shape
+    T = codes.shape[0]
+    _require(codes, torch.uint8, "codes", g_hat.device)
+    _require(scales, torch.float32, "scales", g_hat.device)
+    if tuple(codes.shape) != (T, N, K // 4) or tuple(scales.shape) != (T, 2):
+        raise ValueError("codes [T, N, K/4] and scales [T, 2] must match g_hat")
+    out = torch.empty_like(g_hat)
+    wsb = lib.fairy2i_qat_ste_workspace_bytes(N, K)
+    ws = torch.empty(max(int(wsb), 1), dtype=torch.uint8, device=g_hat.device)
+    _check(lib.fairy2i_qat_ste_backward(_ptr(codes), _ptr(scales), T, N, K, _ptr(g_hat), _ptr(out), _ptr(ws), wsb,
+                                        _stream_ptr(g_hat)), "fairy2i_qat_ste_backward")
+    return out
+
+
+def _cgemm_operand(t, trans, conj, rows, K, name):
+    """A complex operand tensor: complex64 [a, b] or bf16 pairs [a, b, 2],
+    contiguous; [rows, K] when trans == 0, [K, rows] when trans == 1."""
+    torch = _torch()
+    _require(t, None, name)
+    if t.dtype == torch.complex64 and t.dim() == 2:
+        dt = ACT_F32
+    elif t.dtype == torch.bfloat16 and t.dim() == 3 and t.shape[2] == 2:
+        dt = ACT_BF16
+    else:
+        raise TypeError(f"{name} must be complex64 [a, b] or bf16 [a, b, 2]")
+    want = (K, rows) if trans else (rows, K)
+    if tuple(t.shape[:2]) != want:
+        raise ValueError(f"{name} has shape {tuple(t.shape[:2])}, expected {want}")
+    return CgemmOperand(t.data_ptr(), t.shape[1], dt, int(trans), int(conj), 0)
+
+
+def cgemm_gauss(segments, M: int, N: int, out=None, accumulate: bool = False):
+    """C [M, N] complex64 (+)= sum over segments of op(A) op(B)^T with
+    Gauss's three real products.  segments: up to two tuples
+    (A, a_trans, a_conj, B, b_trans, b_conj, K); see _cgemm_operand."""
+    torch = _torch()
+    lib = load()
+    if not 1 <= len(segments) <= 2:
+        raise ValueError("one or two segments")
+    dev = segments[0][0].device
+    A = (CgemmOperand * 2)()
+    Bo = (CgemmOperand * 2)()
+    Ks = (ctypes.c_int64 * 2)()
+    for i, (a, at, ac, b, bt, bc, K) in enumerate(segments):
+        A[i] = _cgemm_operand(a, at, ac, M, K, f"segments[{i}].A")
+        Bo[i] = _cgemm_operand(b, bt, bc, N, K, f"segments[{i}].B")
+        Ks[i] = K
+    if out is None:
+        out = torch.zeros((M, N), dtype=torch.complex64, device=dev) if accumulate else \
+            torch.empty((M, N), dtype=torch.complex64, device=dev)
+    _require(out, torch.complex64, "out", dev)
+    if tuple(out.shape) != (M, N):
+        raise ValueError(f"out must have shape ({M}, {N})")
+    _check(lib.fairy2i_cgemm_gauss(ctypes.byref(A), ctypes.byref(Bo), ctypes.byref(Ks), len(segments), M, N,
+                                   _ptr(out), N, int(accumulate), _stream_ptr(out)), "fairy2i_cgemm_gauss")
+    return out
 
 
 def _host(a, dtype, name, shape=None):
