@@ -232,6 +232,78 @@ def grouped_stack_bench(f2, synth, torch, dev, T, G, steps, warmup, seed_base=10
     return out
 
 
+def qat_bench(f2, synth, torch, dev, T=2, tokens=4096, reps=10):
+    """One quantisation-aware training step of a q-shaped widely-linear layer
+    (masters U, W complex 2048 x 2048, T stages) on `tokens` bf16 tokens:
+    fake-quant forward of both masters, Y = X U^T + conj(X) W^T, the input
+    gradient and both weight gradients (Gauss GEMMs), and the
+    straight-through gradients of the masters.  Synthetic LLaMA-shaped
+    masters, N(0,1) tokens and output gradients."""
+    rows, cols = synth.LLAMA2_7B_PROJ["q"]
+    N, K = rows // 2, cols // 2
+    A = synth.torch_llama_weight(rows, cols, 6000, dev)
+    U, W = f2.to_widely_linear(A)
+    del A
+    g = torch.Generator(device=dev)
+    g.manual_seed(6001)
+    X = torch.randn(tokens, K, 2, generator=g, device=dev).to(torch.bfloat16)
+    GY = torch.randn(tokens, N, 2, generator=g, device=dev).to(torch.bfloat16)
+    Y = torch.empty(tokens, N, dtype=torch.complex64, device=dev)
+    GX = torch.empty(tokens, K, dtype=torch.complex64, device=dev)
+    GU = torch.empty(N, K, dtype=torch.complex64, device=dev)
+    GW = torch.empty(N, K, dtype=torch.complex64, device=dev)
+    state = {}
+
+    def fq():
+        state["u"] = f2.qat_fake_quant(U, T)
+        state["w"] = f2.qat_fake_quant(W, T)
+
+    def fwd():
+        f2.cgemm_gauss([(X, 0, 0, state["u"][0], 0, 0, K), (X, 0, 1, state["w"][0], 0, 0, K)], tokens, N, out=Y)
+
+    def bwd_x():
+        f2.cgemm_gauss([(GY, 0, 0, state["u"][0], 1, 1, N), (GY, 0, 1, state["w"][0], 1, 0, N)], tokens, K, out=GX)
+
+    def bwd_w():
+        f2.cgemm_gauss([(GY, 1, 0, X, 1, 1, tokens)], N, K, out=GU)
+        f2.cgemm_gauss([(GY, 1, 0, X, 1, 0, tokens)], N, K, out=GW)
+
+    def ste():
+        f2.qat_ste_backward(state["u"][1], state["u"][2], GU)
+        f2.qat_ste_backward(state["w"][1], state["w"][2], GW)
+
+    phases = [("fake_quant", fq), ("forward_gemm", fwd), ("input_grad_gemm", bwd_x), ("weight_grad_gemms", bwd_w),
+              ("ste_backward", ste)]
+    fq()
+    for _, fn in phases:
+        fn()
+    warm_up(lambda: [fn() for _, fn in phases], torch, 3)
+    out = {"workload": f"one QAT step of a q-shaped layer (complex {N}x{K}, T={T}), {tokens} bf16 tokens"}
+    total = 0.0
+    for name, fn in phases:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / reps * 1e3
+        out[name + "_us"] = round(us, 1)
+        total += us
+    out["step_us"] = round(total, 1)
+    # each GEMM phase: 3 real products of 2 M N K flops per complex MAC; "effective" counts the 8 flops of a
+    # complex MAC done with four products
+    macs = {"forward_gemm": 2 * tokens * N * K, "input_grad_gemm": 2 * tokens * N * K,
+            "weight_grad_gemms": 2 * N * K * tokens}
+    gemm_us = sum(out[k + "_us"] for k in macs)
+    out["gemm_exec_TFLOPs"] = round(6 * sum(macs.values()) / gemm_us / 1e6, 1)
+    out["gemm_effective_TFLOPs"] = round(8 * sum(macs.values()) / gemm_us / 1e6, 1)
+    out["gemm_frac_bf16_peak"] = round(out["gemm_exec_TFLOPs"] / 2500.0, 4)
+    del U, W, X, GY, Y, GX, GU, GW, state
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_lut_bench(f2, torch, layers, T, passes=3):
     """The CPU table-lookup kernel over the whole stack on the host cores:
     the stack's canonical codes and scales copied to host memory, each
@@ -624,6 +696,7 @@ def main():
         result["stack_group256"]["time_ratio_over_per_tensor"] = round(result["stack_group256"]["ms_per_step"] / ms, 3)
         result["per_layer"] = per_layer_bench(f2, synth, torch, dev, T)
         result["decoder_block"] = block_bench(f2, synth, torch, dev, T)
+        result["qat_step"] = qat_bench(f2, synth, torch, dev, T)
         pf = prefill_bench(f2, synth, torch, dev)
         g = pf["gate"]
         # headline: the 11008x4096 (gate/up) shape; half of the dense MACs multiply structural zeros
