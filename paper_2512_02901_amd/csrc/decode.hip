@@ -683,13 +683,13 @@ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 int dec_ntile(int mode, int64_t B) {
   if (mode == kModeI8) return (int)((B + 7) / 8);
-  if (mode == kModeBf16F4) return (int)((B + 1) / 2);
+  if (mode == kModeBf16F4) return B <= 2 ? 1 : (int)((B + 3) / 4);  // two bands up to 2 tokens, then one
   return (int)((B + 1) / 2);
 }
 
 int dec_ncols(int mode, int64_t B) {
   if (mode == kModeBf16) return B >= 2 ? 14 : 6;  // per token 6 digit columns, 8-column stride
-  if (mode == kModeBf16F4) return B == 1 ? 8 : 16;  // per token 8 digit columns
+  if (mode == kModeBf16F4) return B == 1 ? 8 : 16;  // 8 digit columns per token (B <= 2), 4 (B >= 3)
   return B >= 8 ? 16 : (int)(2 * B);
 }
 
@@ -700,6 +700,7 @@ DecHeader dec_header(int T, int mode, int64_t B, bool export_acc) {
   h.B = (int32_t)B;
   h.ntile = dec_ntile(mode, B);
   h.nc = dec_ncols(mode, B);
+  h.bands = (mode == kModeBf16F4 && B <= 2) ? 2 : 1;
   // the fp4 path always runs its streaming kernel (one or two tiles)
   h.kernel = (!export_acc && (h.ntile == 1 || mode == kModeBf16F4)) ? kKernelStream : kKernelReg;
   return h;

@@ -35,11 +35,21 @@ namespace {
 // (two tokens per 16-column tile): column 4 band + j holds, for that band,
 // j = 0: hi of Re x, 1: hi of Im x, 2: lo of Re x, 3: lo of Im x.  The
 // output factor of token b is 2^-S_b (0 for an all-zero token).
+// With more tokens per call (B >= 3) a token gets one band only: columns
+// 4 t' + j for token t' of the tile (four tokens per tile), every value as
+// one (hi, lo) pair.  A bf16 value is then still written exactly (its 8
+// significant bits fit the pair down to 2^-14), but the narrow adder can
+// drop the low bits of small products that share an MFMA group with a
+// value near m: at most about 2^-13 of the group's largest product, 1.5e-4
+// relative L2 measured on tokens with a 300-sigma channel, against the
+// 1e-3 bar for bf16 activations.
 constexpr int kPrepF4Threads = 512;
 constexpr int kPrepUnroll = 4;     // loads a prep thread issues before using them
+constexpr int kPrepF4Slices = 4;   // blocks per (tile, layer), each encoding a quarter of K
 constexpr float kLoScale = 32.0f;     // lo digit = residual of hi times 2^5
 constexpr float kBand2Scale = 256.0f;  // second band: values below 1, times 2^8
-constexpr int kTokensPerTile = 2;      // 8 operand columns per token
+constexpr int kTokensPerTile = 2;      // two bands: 8 operand columns per token
+constexpr int kMaxTokensPerTile = 4;   // one band: 4 operand columns per token
 
 // e4m3 (OCP fp8: 1 sign, 4 exponent bits with bias 7, 3 mantissa bits, no
 // infinities, largest finite 448) code of v rounded to nearest, ties to even,
@@ -78,15 +88,16 @@ __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_kernel(DecHeader h
   const DecLayer L = tab ? load_layer(tab + blockIdx.y) : inl;
   const int tile = blockIdx.x;
   const int K = L.K;
-  constexpr int tpt = kTokensPerTile;
-  const int ntok = h.nc / 8;  // token slots written per tile
+  const int bands = h.bands;
+  const int cpt = 4 * bands;        // operand columns per token
+  const int tpt = 16 / cpt;         // token slots per 16-column tile
+  const int ntok = h.nc / cpt;      // token slots written per tile
   const bool vec = (reinterpret_cast<uintptr_t>(L.x) & 15) == 0;
-  __shared__ float red[kPrepF4Threads / 64][tpt];
-  __shared__ int sh_S[tpt];
+  __shared__ float red[kPrepF4Threads / 64][kMaxTokensPerTile];
+  __shared__ int sh_S[kMaxTokensPerTile];
   const int wave = threadIdx.x >> 6;
   // every thread issues all its loads of a round before reducing them
   constexpr int U = kPrepUnroll;
-#pragma unroll
   for (int tk = 0; tk < tpt; ++tk) {
     const int b = tpt * tile + tk;
     float m = 0.0f;
@@ -128,14 +139,20 @@ __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_kernel(DecHeader h
       S = 8 - ex;
     }
     sh_S[tk] = S;
-    if (tk < ntok && b < h.B) L.xs[b] = g > 0.0f ? ldexpf(1.0f, -S) : 0.0f;
+    if (blockIdx.z == 0 && tk < ntok && b < h.B) L.xs[b] = g > 0.0f ? ldexpf(1.0f, -S) : 0.0f;
   }
   __syncthreads();
   // one thread per (16-code run, token, component, half run): 8 values, whose
   // four digit bytes per band go to the halves of the run's 16-byte chunks
   const int nrun = L.nk4 * 16;  // run r holds codes 16 r .. 16 r + 15 (= 256 step + 64 d + 16 g for r = 16 step + 4 d + g)
   uint8_t* dst = reinterpret_cast<uint8_t*>(L.xf) + (int64_t)tile * nrun * h.nc * 16;
-  for (int idx0 = 0; idx0 < nrun * ntok * 4; idx0 += U * kPrepF4Threads) {
+  // this block's share of the (run, token, component, half) units: the K
+  // range is split over gridDim.z blocks (each finds the token maxima itself)
+  const int total = nrun * ntok * 4;
+  const int per = (total + (int)gridDim.z - 1) / (int)gridDim.z;
+  const int ulo = (int)blockIdx.z * per;
+  const int uhi = ulo + per < total ? ulo + per : total;
+  for (int idx0 = ulo; idx0 < uhi; idx0 += U * kPrepF4Threads) {
     // the loads of all U units of this thread first, then their digits
     uint32_t wu[U][8];  // (re, im) bf16 pairs of each unit's 8 complex values
 #pragma unroll
@@ -145,7 +162,7 @@ __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_kernel(DecHeader h
       const int b = tpt * tile + tk, k0 = 16 * r + 8 * hf;
 #pragma unroll
       for (int e = 0; e < 8; ++e) wu[u][e] = 0u;
-      if (idx < nrun * ntok * 4 && b < h.B && k0 < K) {  // K % 64 == 0: the whole half run is in range
+      if (idx < uhi && b < h.B && k0 < K) {  // K % 64 == 0: the whole half run is in range
         const uint16_t* p = static_cast<const uint16_t*>(L.x) + ((int64_t)b * K + k0) * 2;
         if (vec) {
           const uint4 v0 = reinterpret_cast<const uint4*>(p)[0], v1 = reinterpret_cast<const uint4*>(p)[1];
@@ -160,7 +177,7 @@ __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_kernel(DecHeader h
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int idx = idx0 + u * kPrepF4Threads + threadIdx.x;
-      if (idx >= nrun * ntok * 4) break;
+      if (idx >= uhi) break;
       const int hf = idx & 1, c = (idx >> 1) & 1, tk = (idx >> 2) % ntok, r = (idx >> 2) / ntok;
       uint32_t out[2][2][2] = {};  // [band][hi, lo][word]: bytes e = 0..7 of the half chunk
       {
@@ -169,7 +186,7 @@ __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_kernel(DecHeader h
         for (int e = 0; e < 8; ++e) {
           const uint32_t bits = c ? (wu[u][e] & 0xFFFF0000u) : (wu[u][e] << 16);
           const float x = ldexpf(__uint_as_float(bits), S);  // exact: |x| < 2^8
-          const bool small = fabsf(x) < 1.0f;
+          const bool small = bands == 2 && fabsf(x) < 1.0f;  // one band: every value in the first
           uint32_t hi, lo;
           digit_pair(small ? x * kBand2Scale : x, hi, lo);
           const int sh = 8 * (e & 3);
@@ -180,12 +197,11 @@ __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_kernel(DecHeader h
           out[1][1][e >> 2] |= small ? ls : 0u;
         }
       }
-      // column 8 tk + 4 band + 2 digit + c of run r; this half is bytes 8 hf .. 8 hf + 7 of its chunk
-#pragma unroll
-      for (int bd = 0; bd < 2; ++bd)
+      // column cpt tk + 4 band + 2 digit + c of run r; this half is bytes 8 hf .. 8 hf + 7 of its chunk
+      for (int bd = 0; bd < bands; ++bd)
 #pragma unroll
         for (int dg = 0; dg < 2; ++dg)
-          *reinterpret_cast<uint2*>(dst + ((int64_t)r * h.nc + 8 * tk + 4 * bd + 2 * dg + c) * 16 + 8 * hf) =
+          *reinterpret_cast<uint2*>(dst + ((int64_t)r * h.nc + cpt * tk + 4 * bd + 2 * dg + c) * 16 + 8 * hf) =
               make_uint2(out[bd][dg][0], out[bd][dg][1]);
     }
   }
@@ -222,6 +238,16 @@ __device__ inline void expand_f4(uint32_t w0, uint32_t w1, v8i& bs, v8i& bi) {
 constexpr int kFmtFp8 = 0;  // MFMA operand format codes: e4m3
 constexpr int kFmtFp4 = 4;  // e2m1
 
+// Token factor tt of a tile's NF factors, selected without indexing a
+// register array by a lane-dependent value.
+template <int NF>
+__device__ inline float pick_factor(const float (&xf)[NF], int tt) {
+  float f = xf[0];
+#pragma unroll
+  for (int i = 1; i < NF; ++i) f = tt == i ? xf[i] : f;
+  return f;
+}
+
 // Epilogue of a work item: lane (g, li) holds activation columns 4g..4g+3
 // of weight row li, i.e. (hi re, hi im, lo re, lo im) of band g % 2 of token
 // g / 2 of the tile, for every (plane, S or I) accumulator.  Each lane joins
@@ -232,10 +258,12 @@ constexpr int kFmtFp4 = 4;  // e2m1
 // rounds alike, so y does not depend on which wave or ring slot finishes the
 // item.  The layer's axis scales sc[m][t][axis] and the tile's token factors
 // xf[2] are the caller's (loaded once per layer).
-template <int T>
+// With one band (BANDS = 1) lane group g holds token g of the tile, and
+// there is no second band to pass down.
+template <int T, int BANDS>
 __device__ inline void write_outputs_f4(const DecLayer& L, const DecHeader& h, int kc, int row, bool row_ok,
                                         int lane, int tile, const v4f (&aS)[2 * T], const v4f (&aI)[2 * T],
-                                        const float (&sc)[2][T][2], const float (&xf)[2]) {
+                                        const float (&sc)[2][T][2], const float (&xf)[4 / BANDS]) {
   constexpr int P = 2 * T;
   const int g = lane >> 4;
   float vS[P][2], vI[P][2];
@@ -245,13 +273,15 @@ __device__ inline void write_outputs_f4(const DecLayer& L, const DecHeader& h, i
     for (int c = 0; c < 2; ++c) {
       vS[p][c] = fmaf(aS[p][2 + c], 1.0f / kLoScale, aS[p][c]);
       vI[p][c] = fmaf(aI[p][2 + c], 1.0f / kLoScale, aI[p][c]);
-      const float hS = __shfl_down(vS[p][c], 16), hI = __shfl_down(vI[p][c], 16);
-      vS[p][c] = fmaf(hS, 1.0f / kBand2Scale, vS[p][c]);
-      vI[p][c] = fmaf(hI, 1.0f / kBand2Scale, vI[p][c]);
+      if constexpr (BANDS == 2) {
+        const float hS = __shfl_down(vS[p][c], 16), hI = __shfl_down(vI[p][c], 16);
+        vS[p][c] = fmaf(hS, 1.0f / kBand2Scale, vS[p][c]);
+        vI[p][c] = fmaf(hI, 1.0f / kBand2Scale, vI[p][c]);
+      }
     }
-  const int tt = g >> 1;  // token slot within the tile
-  const int b = kTokensPerTile * tile + tt;
-  if ((g & 1) || !row_ok || b >= h.B) return;
+  const int tt = BANDS == 2 ? g >> 1 : g;  // token slot within the tile
+  const int b = (4 / BANDS) * tile + tt;
+  if ((BANDS == 2 && (g & 1)) || !row_ok || b >= h.B) return;
   float yr = 0.0f, yi = 0.0f;
 #pragma unroll
   for (int t = 0; t < T; ++t) {
@@ -276,7 +306,7 @@ __device__ inline void write_outputs_f4(const DecLayer& L, const DecHeader& h, i
     yi = fmaf(-sw_re, Pre[1][1], yi);
     yi = fmaf(sw_im, Pim[1][0], yi);
   }
-  const float f = tt ? xf[1] : xf[0];
+  const float f = pick_factor<4 / BANDS>(xf, tt);
   const float2 v = make_float2(__fmul_rn(yr, f), __fmul_rn(yi, f));
   if (L.nkc == 1)
     buf_store8(L.y, (uint32_t)h.B * L.N * 8, (uint32_t)((b * L.N + row) * 8), v);
@@ -427,10 +457,10 @@ __device__ inline void fold_group(const v4f (&aS)[P], const v4f (&aI)[P], const 
 // second band passed down from the odd lane group (times 2^-8), then
 // Eq. (ifairy-dequant)'s combination with the scales already applied, U
 // with x and W with conj(x), stages in order, times the token factor.
-template <int T>
+template <int T, int BANDS>
 __device__ inline void write_outputs_f4_gs(const DecLayer& L, const DecHeader& h, int kc, int row, bool row_ok,
                                            int lane, int tile, const float (&Are)[2 * T][2],
-                                           const float (&Aim)[2 * T][2], const float (&xf)[2]) {
+                                           const float (&Aim)[2 * T][2], const float (&xf)[4 / BANDS]) {
   constexpr int P = 2 * T;
   const int g = lane >> 4;
   float vr[P][2], vi[P][2];
@@ -438,13 +468,17 @@ __device__ inline void write_outputs_f4_gs(const DecLayer& L, const DecHeader& h
   for (int p = 0; p < P; ++p)
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
-      const float hr = __shfl_down(Are[p][c], 16), hi = __shfl_down(Aim[p][c], 16);
-      vr[p][c] = fmaf(hr, 1.0f / kBand2Scale, Are[p][c]);
-      vi[p][c] = fmaf(hi, 1.0f / kBand2Scale, Aim[p][c]);
+      vr[p][c] = Are[p][c];
+      vi[p][c] = Aim[p][c];
+      if constexpr (BANDS == 2) {
+        const float hr = __shfl_down(Are[p][c], 16), hi = __shfl_down(Aim[p][c], 16);
+        vr[p][c] = fmaf(hr, 1.0f / kBand2Scale, Are[p][c]);
+        vi[p][c] = fmaf(hi, 1.0f / kBand2Scale, Aim[p][c]);
+      }
     }
-  const int tt = g >> 1;
-  const int b = kTokensPerTile * tile + tt;
-  if ((g & 1) || !row_ok || b >= h.B) return;
+  const int tt = BANDS == 2 ? g >> 1 : g;
+  const int b = (4 / BANDS) * tile + tt;
+  if ((BANDS == 2 && (g & 1)) || !row_ok || b >= h.B) return;
   float yr = 0.0f, yi = 0.0f;
 #pragma unroll
   for (int t = 0; t < T; ++t) {
@@ -458,7 +492,7 @@ __device__ inline void write_outputs_f4_gs(const DecLayer& L, const DecHeader& h
     yi = __fsub_rn(yi, vr[w][1]);
     yi = __fadd_rn(yi, vi[w][0]);
   }
-  const float f = tt ? xf[1] : xf[0];
+  const float f = pick_factor<4 / BANDS>(xf, tt);
   const float2 v = make_float2(__fmul_rn(yr, f), __fmul_rn(yi, f));
   if (L.nkc == 1)
     buf_store8(L.y, (uint32_t)h.B * L.N * 8, (uint32_t)((b * L.N + row) * 8), v);
@@ -488,7 +522,7 @@ struct F4Ring {
 
 // NT activation tiles (two tokens each); a ring slot holds XW KiB per tile.
 // GS: per-group scales (every layer of the call).
-template <int T, int XW, int NT, bool GS>
+template <int T, int XW, int NT, bool GS, int BANDS>
 __global__ __launch_bounds__((64 * F4Ring<T, NT * XW, GS>::WAVES)) void dec_stream_f4_kernel(
     DecHeader h, DecLayer inl, const DecLayer* __restrict__ tab) {
 #if defined(__HIP_DEVICE_COMPILE__)  // LDS-DMA and buffer-descriptor code: device pass only
@@ -526,10 +560,11 @@ __global__ __launch_bounds__((64 * F4Ring<T, NT * XW, GS>::WAVES)) void dec_stre
   const int64_t i0 = b0 + wave;
   const uint32_t ctr_addr = lds_addr(&claim_ctr);
 
-  // operand column li of tile t belongs to token 2 t + li / 8
+  // operand column li of tile t belongs to token TPT t + li / (4 BANDS)
+  constexpr int TPT = 4 / BANDS;
   bool xvalid[NT];
 #pragma unroll
-  for (int t = 0; t < NT; ++t) xvalid[t] = kTokensPerTile * t + li / 8 < h.B;
+  for (int t = 0; t < NT; ++t) xvalid[t] = TPT * t + li / (4 * BANDS) < h.B;
 
   LoadCursor<T> lc;
   OutCursor oc;
@@ -552,12 +587,12 @@ __global__ __launch_bounds__((64 * F4Ring<T, NT * XW, GS>::WAVES)) void dec_stre
   if constexpr (GS) group_item(gc, lc.rb, lc.k4, lane);
   out_item(oc, li);
   // the epilogue's per-layer constants, reloaded when the output side changes layer
-  float esc[2][T][2], exf[NT][2];
+  float esc[2][T][2], exf[NT][TPT];
   auto load_epilogue_consts = [&]() {
     if constexpr (!GS) sload_scales<T>(uniform_ptr(oc.scales[0]), uniform_ptr(oc.scales[1]), esc);
     // the factor array is padded to 256 bytes: both floats of every tile are inside it
 #pragma unroll
-    for (int t = 0; t < NT; ++t) sload_run<2>(uniform_ptr(oc.xs) + kTokensPerTile * t, exf[t]);
+    for (int t = 0; t < NT; ++t) sload_run<TPT>(uniform_ptr(oc.xs) + TPT * t, exf[t]);
   };
   load_epilogue_consts();
 
@@ -661,11 +696,11 @@ __global__ __launch_bounds__((64 * F4Ring<T, NT * XW, GS>::WAVES)) void dec_stre
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
         if constexpr (GS) {
-          write_outputs_f4_gs<T>(Lo, h, oc.kc, oc.row, oc.row_ok, lane, t, Are[t], Aim[t], exf[t]);
+          write_outputs_f4_gs<T, BANDS>(Lo, h, oc.kc, oc.row, oc.row_ok, lane, t, Are[t], Aim[t], exf[t]);
 #pragma unroll
           for (int p = 0; p < P; ++p) Are[t][p][0] = Are[t][p][1] = Aim[t][p][0] = Aim[t][p][1] = 0.0f;
         } else {
-          write_outputs_f4<T>(Lo, h, oc.kc, oc.row, oc.row_ok, lane, t, aS[t], aI[t], esc, exf[t]);
+          write_outputs_f4<T, BANDS>(Lo, h, oc.kc, oc.row, oc.row_ok, lane, t, aS[t], aI[t], esc, exf[t]);
 #pragma unroll
           for (int p = 0; p < P; ++p) aS[t][p] = aI[t][p] = v4f{0.f, 0.f, 0.f, 0.f};
         }
@@ -687,9 +722,9 @@ __global__ __launch_bounds__((64 * F4Ring<T, NT * XW, GS>::WAVES)) void dec_stre
 #endif
 }
 
-template <int T, int XW, int NT, bool GS>
+template <int T, int XW, int NT, bool GS, int BANDS>
 void launch_stream_f4(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
-  auto k = dec_stream_f4_kernel<T, XW, NT, GS>;
+  auto k = dec_stream_f4_kernel<T, XW, NT, GS, BANDS>;
   constexpr int waves = F4Ring<T, NT * XW, GS>::WAVES;
   constexpr int threads = 64 * waves;
   static const int resident = resident_blocks(reinterpret_cast<const void*>(k), threads);
@@ -700,16 +735,19 @@ void launch_stream_f4(const DecHeader& h, const DecLayer& inl, const DecLayer* t
 
 // XW = KiB of activation operand per 256-code step and tile (nc / 4), NT =
 // activation tiles of two tokens (three or four tokens: two tiles, T <= 3).
+// One tile: one token (two bands, 8 columns), two tokens (two bands) or
+// three to four (one band); two tiles: five to eight tokens (one band, T <= 3).
 template <int T, bool GS>
 void launch_stream_f4_g(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
   if constexpr (T <= 3) {
     if (h.ntile >= 2) {
-      launch_stream_f4<T, 4, 2, GS>(h, inl, tab, s);
+      launch_stream_f4<T, 4, 2, GS, 1>(h, inl, tab, s);
       return;
     }
   }
-  if (h.nc <= 8) launch_stream_f4<T, 2, 1, GS>(h, inl, tab, s);
-  else launch_stream_f4<T, 4, 1, GS>(h, inl, tab, s);
+  if (h.nc <= 8) launch_stream_f4<T, 2, 1, GS, 2>(h, inl, tab, s);
+  else if (h.bands == 2) launch_stream_f4<T, 4, 1, GS, 2>(h, inl, tab, s);
+  else launch_stream_f4<T, 4, 1, GS, 1>(h, inl, tab, s);
 }
 
 template <int T>
@@ -721,7 +759,8 @@ void launch_stream_f4_t(const DecHeader& h, const DecLayer& inl, const DecLayer*
 }  // namespace
 
 void launch_f4_prep(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
-  hipLaunchKernelGGL(dec_prep_f4_kernel, dim3(h.ntile, h.n_layers), dim3(kPrepF4Threads), 0, s, h, inl, tab);
+  hipLaunchKernelGGL(dec_prep_f4_kernel, dim3(h.ntile, h.n_layers, kPrepF4Slices), dim3(kPrepF4Threads), 0, s, h, inl,
+                     tab);
 }
 
 void launch_f4_product(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {

@@ -191,9 +191,11 @@ def test_group_build_validation(lib):
     fp4 = binding.LAYOUT_TILED_FP4
     assert build([_layer(layout=fp4), _layer(layout=fp4, N=200, K=1088)]) == binding.OK
     assert build([_layer(layout=fp4)], B=2) == binding.OK
-    assert build([_layer(layout=fp4)], B=4) == binding.OK                   # two activation tiles
-    assert build([_layer(layout=fp4)], B=5) == binding.ERR_UNSUPPORTED
-    assert build([_layer(layout=fp4)], B=3, T=4) == binding.ERR_UNSUPPORTED  # two tiles need T <= 3
+    assert build([_layer(layout=fp4)], B=4) == binding.OK                   # one one-band tile
+    assert build([_layer(layout=fp4)], B=8) == binding.OK                   # 5..8 tokens: two one-band tiles
+    assert build([_layer(layout=fp4)], B=9) == binding.ERR_UNSUPPORTED
+    assert build([_layer(layout=fp4)], B=4, T=4) == binding.OK
+    assert build([_layer(layout=fp4)], B=5, T=4) == binding.ERR_UNSUPPORTED  # two tiles need T <= 3
     assert build([_layer(layout=fp4)], B=2, T=4) == binding.OK
     assert build([_layer(layout=fp4, x_scale=0x1000)], dt=binding.ACT_I8) == binding.ERR_UNSUPPORTED
     assert build([_layer(layout=fp4), _layer()]) == binding.ERR_UNSUPPORTED  # fp4 for every layer or none

@@ -24,6 +24,21 @@ import synth
 pytestmark = pytest.mark.gpu
 
 TOL_FP4 = 1e-6
+# Three or more tokens per call: one band of (hi, lo) digits per value, four
+# columns per token.  Every bf16 value is still held exactly, but the matrix
+# core's narrow adder may drop the low bits of a small product that shares
+# an MFMA group with one near the token's largest magnitude (at most about
+# 2^-13 of that product).  Measured about 4e-6 for N(0,1) tokens and up to
+# 1.5e-4 with a 300-sigma channel; TOL_ONE_BAND keeps a factor 2 to the 1e-3
+# bar for bf16 activations, TOL_ONE_BAND_TYPICAL applies to N(0,1) tokens.
+TOL_ONE_BAND = 5e-4
+TOL_ONE_BAND_TYPICAL = 2e-5
+
+
+def tol_for(B, typical=False):
+    if B <= 2:
+        return TOL_FP4
+    return TOL_ONE_BAND_TYPICAL if typical else TOL_ONE_BAND
 
 
 def rel_l2(got, want):
@@ -125,17 +140,17 @@ def run_fp4_group(layers, T, B, gpu, x_of):
 @pytest.mark.parametrize("T", [1, 2, 3, 4])
 def test_group_fp4_matches_oracle(gpu, T):
     """One grouped fp4 call over layers of several shapes (ragged row blocks,
-    K with a partial 256-code step, one row), 1 to 4 tokens (one or two
-    activation tiles of 2 tokens), against the oracle; a repeated call is
-    bitwise identical."""
+    K with a partial 256-code step, one row), 1 to 8 tokens (two-band tiles
+    of 1 or 2 tokens, one-band tiles of 4), against the oracle; a repeated
+    call is bitwise identical."""
     layers = [(N, K, *quantized_layer(N, K, T, (40, i, N))) for i, (N, K) in enumerate(SHAPES)]
-    for B in ((1, 2, 3, 4) if T <= 3 else (1, 2)):   # B > 2: two activation tiles (T <= 3)
+    for B in ((1, 2, 3, 4, 5, 7, 8) if T <= 3 else (1, 2, 3, 4)):   # B > 4: two tiles (T <= 3)
         ys, refs, grp = run_fp4_group(layers, T, B, gpu,
                                       lambda i, N, K: synth.bf16_round_complex(synth.activations(B, K, (41, i, B))))
         first = [host(y).copy() for y in ys]
         errs = [rel_l2(host(y), yo) for y, yo in zip(ys, refs)]
         print(f"T={T} B={B} rel-L2 per layer:", " ".join(f"{e:.2e}" for e in errs))
-        assert max(errs) <= TOL_FP4
+        assert max(errs) <= tol_for(B, typical=True)
         grp.run()
         for y, y1 in zip(ys, first):
             np.testing.assert_array_equal(host(y).view(np.uint32), y1.view(np.uint32))
@@ -159,7 +174,7 @@ def test_group_fp4_exact_for_representable_tokens(gpu):
     import paper_2512_02901_amd as f2
     T = 2
     layers = [(N, K, *quantized_layer(N, K, T, (42, i, N))) for i, (N, K) in enumerate(SHAPES)]
-    for B in (1, 2, 3, 4):
+    for B in (1, 2):
         xs = {}
 
         def x_of(i, N, K):
@@ -185,12 +200,14 @@ def test_group_fp4_exact_for_representable_tokens(gpu):
 def test_group_fp4_outlier_channels(gpu, T):
     """Tokens of N(0,1) values with one complex channel multiplied by 30, 300
     or 3000 (the crest factors of LLaMA-style activation outliers), at
-    K = 2048 and K = 5504, 1 to 4 tokens per call: every value keeps its own 8
-    significant bits and y matches to float32 rounding."""
+    K = 2048 and K = 5504, 1 to 8 tokens per call: with two bands (1 or 2
+    tokens) every value keeps its own 8 significant bits and y matches to
+    float32 rounding; with one band (3 to 8 tokens) y stays inside the bf16
+    bar with a factor 2 to spare."""
     shapes = [(64, 2048), (48, 5504)]
     layers = [(N, K, *quantized_layer(N, K, T, (49, i, N))) for i, (N, K) in enumerate(shapes)]
     for mult in (30.0, 300.0, 3000.0):
-        for B in (1, 2, 3, 4):
+        for B in (1, 2, 3, 4, 6, 8):
             def x_of(i, N, K):
                 x = synth.activations(B, K, (50, i, B, int(mult)))
                 rng = np.random.default_rng((51, i, B, int(mult)))
@@ -200,7 +217,7 @@ def test_group_fp4_outlier_channels(gpu, T):
             ys, refs, _ = run_fp4_group(layers, T, B, gpu, x_of)
             errs = [rel_l2(host(y), yo) for y, yo in zip(ys, refs)]
             print(f"T={T} x{mult:g} B={B} rel-L2:", " ".join(f"{e:.2e}" for e in errs))
-            assert max(errs) <= TOL_FP4
+            assert max(errs) <= tol_for(B)
 
 
 def test_group_fp4_edge_tokens(gpu):
@@ -220,6 +237,7 @@ def test_group_fp4_edge_tokens(gpu):
         "huge": synth.bf16_round_complex((normal * np.float32(2.0 ** 100)).astype(np.complex64)),
         "tiny": synth.bf16_round_complex((normal * np.float32(2.0 ** -100)).astype(np.complex64)),
     }
+    cases["zero+normal x3"] = np.concatenate([cases["zero+normal"], normal])  # a one-band tile
     for name, x in cases.items():
         B = x.shape[0]
         ys, refs, _ = run_fp4_group(layer, T, B, gpu, lambda i, N_, K_: x)
@@ -227,9 +245,9 @@ def test_group_fp4_edge_tokens(gpu):
         err = rel_l2(y, yo)
         print(f"{name}: rel-L2 {err:.2e}")
         assert np.all(np.isfinite(y.view(np.float32)))
-        if name == "zero+normal":
+        if name.startswith("zero+normal"):
             assert np.all(y[0] == 0)
-            assert rel_l2(y[1], yo[1]) <= TOL_FP4
+            assert rel_l2(y[1], yo[1]) <= tol_for(B, typical=True)
         else:
             assert err <= TOL_FP4
 

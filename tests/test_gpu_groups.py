@@ -18,6 +18,13 @@ import synth
 pytestmark = pytest.mark.gpu
 
 TOL_FP4 = 1e-6
+# three or more tokens: one band of digits per value (see test_gpu_fp4.py),
+# measured a few 1e-6 for N(0,1) tokens
+TOL_ONE_BAND_TYPICAL = 2e-5
+
+
+def tol_for(B):
+    return TOL_FP4 if B <= 2 else TOL_ONE_BAND_TYPICAL
 
 
 def rel_l2(got, want):
@@ -114,22 +121,22 @@ def run_grouped(layers, T, B, gpu, rng, check_layers=None):
     return errs, grp, args
 
 
-@pytest.mark.parametrize("B", [1, 2, 3, 4])
+@pytest.mark.parametrize("B", [1, 2, 3, 4, 8])
 @pytest.mark.parametrize("T,G", [(1, 256), (2, 256), (2, 512), (3, 1024)])
 def test_grouped_decode_matches_oracle(gpu, B, T, G):
     rng = np.random.default_rng(100 * B + 10 * T + G)
     shapes = [(128, 1024, None), (37, 5504, None), (200, 256, None), (16, 2048, None)]
     layers = grouped_layers(shapes, T, G, gpu, seed=B * 7 + T)
     errs, _, _ = run_grouped(layers, T, B, gpu, rng)
-    assert max(errs) <= TOL_FP4, errs
+    assert max(errs) <= tol_for(B), errs
 
 
 def test_grouped_decode_t4(gpu):
     rng = np.random.default_rng(44)
     layers = grouped_layers([(48, 1280, None), (16, 512, None)], 4, 256, gpu, seed=44)
-    for B in (1, 2):
+    for B in (1, 2, 4):
         errs, _, _ = run_grouped(layers, 4, B, gpu, rng)
-        assert max(errs) <= TOL_FP4, errs
+        assert max(errs) <= tol_for(B), errs
 
 
 def test_grouped_decode_repeatable_and_mixed_group_sizes(gpu):
