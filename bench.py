@@ -662,9 +662,9 @@ def main():
         result["stack_tiled_int8"] = {"ms_per_step": round(ms_t, 4), "GBs": round(packed / (ms_t * 1e-3) / 1e9, 1),
                                       "product_us": round(prod_t * 1e3, 1)}
         del grp_tiled
-        # 2, 4 and 8 tokens per layer on the fp4 path (one two-band tile of 2 tokens, one one-band
-        # tile of 4, two one-band tiles)
-        for Bb in (2, 4, 8):
+        # 2, 4, 8 and 16 tokens per layer on the fp4 path (one two-band tile of 2 tokens, one, two or
+        # four one-band tiles of 4)
+        for Bb in (2, 4, 8, 16):
             msb, _, prodb, _ = batch_stack_fp4(f2, torch, dev, T, fp4_layers, Bb, args.steps, args.warmup)
             result[f"stack_B{Bb}"] = {"ms_per_step": round(msb, 4), "GBs": round(packed / (msb * 1e-3) / 1e9, 1),
                                       "product_us": round(prodb * 1e3, 1)}

@@ -282,7 +282,8 @@ typedef struct fairy2i_wl_layer {
  * every K a multiple of 64.  Each layer's codes are in the
  * layout its `layout` field names (same layout for U and W).  With
  * FAIRY2I_LAYOUT_TILED_FP4 every layer of the group must use it, with dtype
- * FAIRY2I_ACT_BF16 and B <= 8 (B <= 4 for T = 4); the product then runs on the
+ * FAIRY2I_ACT_BF16 and B <= 16 (B <= 8 for T = 3, B <= 4 for T = 4); the
+ * product then runs on the
  * fp8 x fp4 matrix cores.  Each token is scaled by a power of two 2^S so that
  * its largest magnitude m lies in [2^7, 2^8).  For B <= 2 a scaled value v is
  * split by magnitude into two bands (|v| >= 1, and |v| < 1 taken times 2^8),
@@ -291,7 +292,7 @@ typedef struct fairy2i_wl_layer {
  * value down to 2^-22 m is represented exactly, smaller ones to within
  * 2^-30 m.  The digit products are exact and are summed in float32 on the
  * matrix cores; y matches the exact product of the bf16 inputs to float32
- * rounding (relative L2 about 1e-7).  For 3 <= B <= 8 each value gets one
+ * rounding (relative L2 about 1e-7).  For 3 <= B <= 16 each value gets one
  * (hi, lo) pair (four tokens per 16-column tile): still exact per value, but
  * the matrix core's narrow adder may drop the low bits of a small product
  * next to one near m in the same group of products, at most about 2^-13 of

@@ -342,7 +342,8 @@ static fairy2i_status check_group(const fairy2i_wl_layer* layers, int32_t n_laye
     // fp4 tiled codes: every layer, bf16 activations, one or two activation tiles of 2 tokens
     if ((L.layout == FAIRY2I_LAYOUT_TILED_FP4) != (layers[0].layout == FAIRY2I_LAYOUT_TILED_FP4))
       return FAIRY2I_ERR_UNSUPPORTED;
-    if (L.layout == FAIRY2I_LAYOUT_TILED_FP4 && (dtype != FAIRY2I_ACT_BF16 || B > 8 || (B > 4 && T > 3)))
+    if (L.layout == FAIRY2I_LAYOUT_TILED_FP4 &&
+        (dtype != FAIRY2I_ACT_BF16 || B > 16 || (B > 8 && T > 2) || (B > 4 && T > 3)))
       return FAIRY2I_ERR_UNSUPPORTED;
   }
   return FAIRY2I_OK;

@@ -736,9 +736,16 @@ void launch_stream_f4(const DecHeader& h, const DecLayer& inl, const DecLayer* t
 // XW = KiB of activation operand per 256-code step and tile (nc / 4), NT =
 // activation tiles of two tokens (three or four tokens: two tiles, T <= 3).
 // One tile: one token (two bands, 8 columns), two tokens (two bands) or
-// three to four (one band); two tiles: five to eight tokens (one band, T <= 3).
+// three to four (one band); two tiles: five to eight tokens (one band,
+// T <= 3); four tiles: nine to sixteen tokens (one band, T <= 2).
 template <int T, bool GS>
 void launch_stream_f4_g(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
+  if constexpr (T <= 2) {
+    if (h.ntile >= 3) {
+      launch_stream_f4<T, 4, 4, GS, 1>(h, inl, tab, s);
+      return;
+    }
+  }
   if constexpr (T <= 3) {
     if (h.ntile >= 2) {
       launch_stream_f4<T, 4, 2, GS, 1>(h, inl, tab, s);

@@ -193,7 +193,9 @@ def test_group_build_validation(lib):
     assert build([_layer(layout=fp4)], B=2) == binding.OK
     assert build([_layer(layout=fp4)], B=4) == binding.OK                   # one one-band tile
     assert build([_layer(layout=fp4)], B=8) == binding.OK                   # 5..8 tokens: two one-band tiles
-    assert build([_layer(layout=fp4)], B=9) == binding.ERR_UNSUPPORTED
+    assert build([_layer(layout=fp4)], B=16) == binding.OK                  # 9..16 tokens: four (T <= 2)
+    assert build([_layer(layout=fp4)], B=9, T=3) == binding.ERR_UNSUPPORTED
+    assert build([_layer(layout=fp4)], B=17) == binding.ERR_UNSUPPORTED
     assert build([_layer(layout=fp4)], B=4, T=4) == binding.OK
     assert build([_layer(layout=fp4)], B=5, T=4) == binding.ERR_UNSUPPORTED  # two tiles need T <= 3
     assert build([_layer(layout=fp4)], B=2, T=4) == binding.OK

@@ -144,7 +144,8 @@ def test_group_fp4_matches_oracle(gpu, T):
     of 1 or 2 tokens, one-band tiles of 4), against the oracle; a repeated
     call is bitwise identical."""
     layers = [(N, K, *quantized_layer(N, K, T, (40, i, N))) for i, (N, K) in enumerate(SHAPES)]
-    for B in ((1, 2, 3, 4, 5, 7, 8) if T <= 3 else (1, 2, 3, 4)):   # B > 4: two tiles (T <= 3)
+    Bs = {1: (1, 2, 3, 4, 5, 8, 9, 16), 2: (1, 2, 3, 4, 5, 7, 8, 12, 16), 3: (1, 2, 3, 4, 5, 8), 4: (1, 2, 3, 4)}[T]
+    for B in Bs:   # B > 4: two tiles (T <= 3); B > 8: four tiles (T <= 2)
         ys, refs, grp = run_fp4_group(layers, T, B, gpu,
                                       lambda i, N, K: synth.bf16_round_complex(synth.activations(B, K, (41, i, B))))
         first = [host(y).copy() for y in ys]
@@ -207,7 +208,7 @@ def test_group_fp4_outlier_channels(gpu, T):
     shapes = [(64, 2048), (48, 5504)]
     layers = [(N, K, *quantized_layer(N, K, T, (49, i, N))) for i, (N, K) in enumerate(shapes)]
     for mult in (30.0, 300.0, 3000.0):
-        for B in (1, 2, 3, 4, 6, 8):
+        for B in ((1, 2, 3, 4, 6, 8, 16) if T <= 2 else (1, 2, 3, 4, 6, 8)):
             def x_of(i, N, K):
                 x = synth.activations(B, K, (50, i, B, int(mult)))
                 rng = np.random.default_rng((51, i, B, int(mult)))

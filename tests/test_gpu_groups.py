@@ -121,9 +121,11 @@ def run_grouped(layers, T, B, gpu, rng, check_layers=None):
     return errs, grp, args
 
 
-@pytest.mark.parametrize("B", [1, 2, 3, 4, 8])
+@pytest.mark.parametrize("B", [1, 2, 3, 4, 8, 16])
 @pytest.mark.parametrize("T,G", [(1, 256), (2, 256), (2, 512), (3, 1024)])
 def test_grouped_decode_matches_oracle(gpu, B, T, G):
+    if B > 8 and T > 2:
+        pytest.skip("more than 8 tokens per call on the fp4 path needs T <= 2")
     rng = np.random.default_rng(100 * B + 10 * T + G)
     shapes = [(128, 1024, None), (37, 5504, None), (200, 256, None), (16, 2048, None)]
     layers = grouped_layers(shapes, T, G, gpu, seed=B * 7 + T)
