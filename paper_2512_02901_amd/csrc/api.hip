@@ -419,15 +419,21 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
   }
   if (h.mode == kModeBf16F4)
     std::stable_sort(ls.begin(), ls.end(), [](const DecLayer& a, const DecLayer& b) { return a.kc4 > b.kc4; });
-  int64_t items = 0, steps = 0;
+  int64_t items = 0, steps = 0, sitems = 0, ssteps = 0;
   int any_split = 0;
   int64_t max_BN = 0;
   for (int32_t i = 0; i < n_layers; ++i) {
     DecLayer l = ls[(size_t)i];
     l.item0 = items;
     l.step0 = steps;
+    l.sitem0 = sitems;
+    l.sstep0 = ssteps;
     items += (int64_t)l.nrb * l.nkc;
     steps += (int64_t)l.nrb * l.nk4;
+    const int rbg = coop_row_blocks(h.ntile);
+    const int64_t groups = ((int64_t)l.nrb + rbg - 1) / rbg;
+    sitems += groups;
+    ssteps += groups * l.nk4;
     if (l.nkc > 1) any_split = 1;
     if (B * (int64_t)l.N > max_BN) max_BN = B * (int64_t)l.N;
     tab[i] = l;
@@ -440,7 +446,10 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
   h.n_layers = n_layers;
   h.total_items = items;
   h.total_steps = steps;
+  h.total_ssteps = ssteps;
   h.grouped = layers[0].group_size != 0 ? 1 : 0;
+  h.coop = (h.mode == kModeBf16F4 && slice == kSliceFullK && !any_split) ? 1 : 0;
+  h.coop_rb = coop_row_blocks(h.ntile);
   hdr->h = h;
   hdr->any_split = any_split;
   hdr->max_BN = max_BN;

@@ -12,6 +12,10 @@ constexpr int kModeI8 = 1;    // int8 activations with a per-token factor
 constexpr int kModeBf16F4 = 2;  // bf16 activations as e4m3 digit pairs in two magnitude bands,
                                 // codes in the fp4 tiled layout (fp8 x fp4 matrix cores)
 
+constexpr int kCoopWaves = 4;     // waves of a block of the cooperative fp4 kernel
+// row blocks per block of the cooperative kernel: with four activation tiles
+// two waves share a row block (two tiles each), else each wave has its own
+inline int coop_row_blocks(int ntile) { return ntile >= 3 ? 2 : kCoopWaves; }
 constexpr int kKernelReg = 0;     // codes staged in registers; any batch, accumulator export
 constexpr int kKernelStream = 1;  // codes streamed through an LDS ring; one activation tile
 constexpr int kRegKc4 = 2;        // 256-code steps per work item of the register kernel
@@ -35,6 +39,8 @@ struct DecLayer {
                              // 0: one pair per stage (scales [T][2])
   int64_t item0;             // index of this layer's first work item
   int64_t step0;             // 256-code steps of all work items before item0
+  int64_t sitem0;            // block-cooperative kernel: first group of kCoopWaves row blocks
+  int64_t sstep0;            //   and the group steps (groups x nk4) of all layers before this one
 };
 
 struct DecHeader {
@@ -47,6 +53,9 @@ struct DecHeader {
   int32_t pad_;
   int64_t total_items;
   int64_t total_steps;  // 256-code steps of all work items
+  int64_t total_ssteps; // block-cooperative kernel: steps of all row-block groups
+  int32_t coop;         // every layer is one full-K item per row block: the cooperative kernel may run
+  int32_t coop_rb;      // row blocks per group of the cooperative kernel
 };
 
 int dec_ntile(int mode, int64_t B);

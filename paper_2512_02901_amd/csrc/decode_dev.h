@@ -163,6 +163,8 @@ __device__ inline DecLayer load_layer(const DecLayer* p) {
   o.gsteps = uniform(p->gsteps);
   o.item0 = uniform64(p->item0);
   o.step0 = uniform64(p->step0);
+  o.sitem0 = uniform64(p->sitem0);
+  o.sstep0 = uniform64(p->sstep0);
   return o;
 }
 
@@ -400,6 +402,14 @@ __device__ inline void lds_read4(uint32_t a0, uint32_t a1, uint32_t a2, uint32_t
       : "=&v"(x[0]), "=&v"(x[1]), "=&v"(x[2]), "=&v"(x[3])
       : "v"(a0), "v"(a1), "v"(a2), "v"(a3)
       : "memory");
+}
+
+// Two 16-byte LDS reads and the wait for them, as one unit (see lds_read4).
+__device__ inline void lds_read2(uint32_t a0, uint32_t a1, v4i (&x)[2]) {
+  __asm__ volatile("ds_read_b128 %0, %2\n\tds_read_b128 %1, %3\n\ts_waitcnt lgkmcnt(0)"
+                   : "=&v"(x[0]), "=&v"(x[1])
+                   : "v"(a0), "v"(a1)
+                   : "memory");
 }
 
 // Compute side: which item the current step belongs to, and what its

@@ -45,40 +45,30 @@ namespace {
 // 1e-3 bar for bf16 activations.
 constexpr int kPrepF4Threads = 512;
 constexpr int kPrepUnroll = 4;     // loads a prep thread issues before using them
-constexpr int kPrepF4Slices = 4;   // blocks per (tile, layer), each encoding a quarter of K
+constexpr int kPrepF4Blocks = 4;   // blocks per layer (tiles x K slices): each slice finds the token maxima itself
 constexpr float kLoScale = 32.0f;     // lo digit = residual of hi times 2^5
 constexpr float kBand2Scale = 256.0f;  // second band: values below 1, times 2^8
 constexpr int kTokensPerTile = 2;      // two bands: 8 operand columns per token
 constexpr int kMaxTokensPerTile = 4;   // one band: 4 operand columns per token
 
-// e4m3 (OCP fp8: 1 sign, 4 exponent bits with bias 7, 3 mantissa bits, no
-// infinities, largest finite 448) code of v rounded to nearest, ties to even,
-// for |v| < 2^8 + 2^4 (the largest result is 2^8).  q receives the rounded
-// value as a float.  Both roundings are computed and one is selected, so the
-// conversion has no branches.
-__device__ inline uint32_t e4m3_rne(float v, float& q) {
-  const uint32_t u = __float_as_uint(v);
-  const uint32_t a = u & 0x7FFFFFFFu;
-  const uint32_t sgn = u & 0x80000000u;
-  // |v| >= 2^-6: keep 3 mantissa bits, ties to even; a carry moves into the exponent
-  const uint32_t r = a + 0x7FFFFu + ((a >> 20) & 1u);
-  const uint32_t cn = (r >> 20) - (120u << 3);  // float32 exponent bias 127 -> e4m3 bias 7
-  const float qn = __uint_as_float((r & 0xFFF00000u) | sgn);
-  // |v| < 2^-6: the subnormal grid 2^-9, code = |v| / 2^-9 (8 is the smallest normal)
-  const float m = rintf(__uint_as_float(a) * 512.0f);
-  const uint32_t cs = (uint32_t)m;
-  const float qs = __uint_as_float(__float_as_uint(m * 0x1p-9f) | sgn);
-  const bool sub = a < 0x3C800000u;
-  const uint32_t c = sub ? cs : cn;
-  q = sub ? qs : qn;
-  return c ? (c | (sgn >> 24)) : 0u;
-}
-
-// The (hi, lo) digit codes of v, |v| < 2^8.
-__device__ inline void digit_pair(float v, uint32_t& hi, uint32_t& lo) {
-  float qh, ql;
-  hi = e4m3_rne(v, qh);
-  lo = e4m3_rne((v - qh) * kLoScale, ql);  // v - qh is exact
+// The (hi, lo) digit words of four values, |v| < 2^8 (byte i = value i):
+// hi = e4m3(v), lo = e4m3((v - hi) 2^5), e4m3 being OCP fp8 (1 sign bit, 4
+// exponent bits with bias 7, 3 mantissa bits, largest finite 448), rounded
+// to nearest with ties to even by the hardware conversion v_cvt_pk_fp8_f32;
+// its inverse gives hi back as a float, and v - hi is exact in float32.
+// The largest digit is 2^8 (hi of a value next to 2^8, or lo of a value
+// near 2^7), well inside e4m3's range.
+__device__ inline void digit_words(const float (&v)[4], uint32_t& hi, uint32_t& lo) {
+  int h = __builtin_amdgcn_cvt_pk_fp8_f32(v[0], v[1], 0, false);
+  h = __builtin_amdgcn_cvt_pk_fp8_f32(v[2], v[3], h, true);
+  const float r0 = (v[0] - __builtin_amdgcn_cvt_f32_fp8(h, 0)) * kLoScale;
+  const float r1 = (v[1] - __builtin_amdgcn_cvt_f32_fp8(h, 1)) * kLoScale;
+  const float r2 = (v[2] - __builtin_amdgcn_cvt_f32_fp8(h, 2)) * kLoScale;
+  const float r3 = (v[3] - __builtin_amdgcn_cvt_f32_fp8(h, 3)) * kLoScale;
+  int l = __builtin_amdgcn_cvt_pk_fp8_f32(r0, r1, 0, false);
+  l = __builtin_amdgcn_cvt_pk_fp8_f32(r2, r3, l, true);
+  hi = (uint32_t)h;
+  lo = (uint32_t)l;
 }
 
 // One block per (activation tile, layer): the largest magnitude of each of
@@ -182,19 +172,28 @@ __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_kernel(DecHeader h
       uint32_t out[2][2][2] = {};  // [band][hi, lo][word]: bytes e = 0..7 of the half chunk
       {
         const int S = sh_S[tk];
+        float x[8];
+        bool small[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const uint32_t bits = c ? (wu[u][e] & 0xFFFF0000u) : (wu[u][e] << 16);
-          const float x = ldexpf(__uint_as_float(bits), S);  // exact: |x| < 2^8
-          const bool small = bands == 2 && fabsf(x) < 1.0f;  // one band: every value in the first
-          uint32_t hi, lo;
-          digit_pair(small ? x * kBand2Scale : x, hi, lo);
-          const int sh = 8 * (e & 3);
-          const uint32_t hs = hi << sh, ls = lo << sh;
-          out[0][0][e >> 2] |= small ? 0u : hs;
-          out[0][1][e >> 2] |= small ? 0u : ls;
-          out[1][0][e >> 2] |= small ? hs : 0u;
-          out[1][1][e >> 2] |= small ? ls : 0u;
+          x[e] = ldexpf(__uint_as_float(bits), S);  // exact: |x| < 2^8
+          small[e] = bands == 2 && fabsf(x[e]) < 1.0f;  // one band: every value in the first
+        }
+        for (int bd = 0; bd < bands; ++bd) {
+#pragma unroll
+          for (int w = 0; w < 2; ++w) {
+            float v[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int e = 4 * w + i;
+              v[i] = bd == 0 ? (small[e] ? 0.0f : x[e]) : (small[e] ? x[e] * kBand2Scale : 0.0f);
+            }
+            uint32_t hi, lo;
+            digit_words(v, hi, lo);
+            out[bd][0][w] = hi;
+            out[bd][1][w] = lo;
+          }
         }
       }
       // column cpt tk + 4 band + 2 digit + c of run r; this half is bytes 8 hf .. 8 hf + 7 of its chunk
@@ -757,17 +756,286 @@ void launch_stream_f4_g(const DecHeader& h, const DecLayer& inl, const DecLayer*
   else launch_stream_f4<T, 4, 1, GS, 1>(h, inl, tab, s);
 }
 
+template <int T, int NT>
+void launch_coop_f4(const DecHeader& h, const DecLayer* tab, hipStream_t s);  // the block-cooperative kernel below
+
 template <int T>
 void launch_stream_f4_t(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
-  if (h.grouped) launch_stream_f4_g<T, true>(h, inl, tab, s);
-  else launch_stream_f4_g<T, false>(h, inl, tab, s);
+  if (h.grouped) {
+    launch_stream_f4_g<T, true>(h, inl, tab, s);
+    return;
+  }
+  if constexpr (T <= 2) {
+    if (tab && h.coop && h.ntile >= 3) {
+      launch_coop_f4<T, 4>(h, tab, s);
+      return;
+    }
+  }
+  if constexpr (T <= 2) {
+    if (tab && h.coop && h.ntile == 2) {
+      launch_coop_f4<T, 2>(h, tab, s);
+      return;
+    }
+  }
+  launch_stream_f4_g<T, false>(h, inl, tab, s);
+}
+
+// ------------------------------------------- block-cooperative kernel ---
+// With five or more tokens a step's activation operand (NT tiles of 4 KiB)
+// outweighs its codes (2T KiB), and a per-wave ring of it leaves room for
+// few waves per CU.  Here the kCoopWaves waves of a block decode kCoopWaves
+// consecutive row blocks of one layer (a group) together, stepping through
+// K in lockstep.  One ring of kCoopSlots slots in LDS holds each step's
+// activation operand once for the whole block (each wave loads its share),
+// the codes go to each wave's own registers as in the streaming kernel, and
+// one barrier per step both publishes the slot about to be read and retires
+// the slot read the step before (the one the step's new loads overwrite).
+// Blocks take the groups that start in an equal share of the call's group
+// steps; the table lists layers by decreasing length.  Used when every layer
+// is one full-K item per row block (no partials).
+constexpr int kCoopSlots = 3;
+
+// Global index of the first group (of rbg row blocks) whose first step is at
+// or after group step s.
+__device__ inline int64_t coop_group_at_step(const DecLayer* tab, int n, int64_t s, int64_t total, int rbg) {
+  if (s >= total) {
+    const int64_t g0 = uniform64(tab[n - 1].sitem0);
+    return g0 + (uniform(tab[n - 1].nrb) + rbg - 1) / rbg;
+  }
+  int lo = 0, hi = n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (uniform64(tab[mid].sstep0) <= s) lo = mid;
+    else hi = mid - 1;
+  }
+  const int nk4 = uniform(tab[lo].nk4);
+  return uniform64(tab[lo].sitem0) + (s - uniform64(tab[lo].sstep0) + nk4 - 1) / nk4;
+}
+
+// Layer holding global group q: the last layer whose sitem0 <= q.
+__device__ inline int coop_layer_of_group(const DecLayer* tab, int n, int64_t q) {
+  int lo = 0, hi = n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (uniform64(tab[mid].sitem0) <= q) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Wave-uniform position in the block's sequence of (group, step).
+struct CoopCursor {
+  int64_t q, qend;  // global group, one past the block's last
+  const uint8_t* codes[2];
+  const int8_t* xf;
+  int lidx;
+  int g, k4;        // group within the layer, step within the group
+  int ngroups, nk4, nrb, N, K, rbg;
+  bool live;
+};
+
+__device__ inline void coop_enter_layer(CoopCursor& c, const DecLayer& L) {
+  c.codes[0] = L.codes[0];
+  c.codes[1] = L.codes[1];
+  c.xf = L.xf;
+  c.nk4 = L.nk4;
+  c.nrb = L.nrb;
+  c.N = L.N;
+  c.K = L.K;
+  c.ngroups = (L.nrb + c.rbg - 1) / c.rbg;
+}
+
+// Next step; enters the next group / layer (reading its descriptor).
+__device__ inline void coop_advance(CoopCursor& c, const DecLayer* tab) {
+  if (++c.k4 < c.nk4) return;
+  c.k4 = 0;
+  ++c.q;
+  if (c.q >= c.qend) {
+    c.live = false;
+    return;
+  }
+  if (++c.g == c.ngroups) {
+    c.g = 0;
+    ++c.lidx;
+    coop_enter_layer(c, load_layer(tab + c.lidx));
+  }
+}
+
+// TS activation tiles per wave: with NT = 4 two waves share a row block,
+// two tiles each, so a wave's accumulators stay at 64 registers; two blocks
+// per CU (eight waves, at most 256 registers per lane).
+template <int T, int NT, int TS>
+__global__ __launch_bounds__(64 * kCoopWaves, 2) void dec_coop_f4_kernel(DecHeader h,
+                                                                      const DecLayer* __restrict__ tab) {
+#if defined(__HIP_DEVICE_COMPILE__)  // LDS-DMA and buffer-descriptor code: device pass only
+  constexpr int P = 2 * T;
+  constexpr int W = kCoopWaves;
+  constexpr int SH = NT / TS;           // waves sharing a row block
+  constexpr int RBG = W / SH;           // row blocks per group
+  static_assert(NT % TS == 0 && W % SH == 0, "tiles split evenly over the waves of a row block");
+  constexpr int NS = kCoopSlots;
+  constexpr int XS = NT * 4096;         // a step's activation operand: NT tiles x 16 columns x 256 codes
+  constexpr int DMA = NT * 4 / W;       // 1-KiB activation loads per wave and step
+  static_assert((NT * 4) % W == 0, "the activation loads split evenly over the waves");
+  constexpr int LOADS = P + DMA;        // vector memory ops per wave and step
+  constexpr int WAIT = (NS - 2) * LOADS;  // when step j is read, steps j+1 .. j+NS-2 may still load
+  constexpr int WAITCNT = (WAIT & 0xF) | (0x7 << 4) | (0xF << 8) | (((WAIT >> 4) & 3) << 14);
+  static_assert(WAIT < 64, "vmcnt holds at most 63");
+  __shared__ __attribute__((aligned(16))) uint8_t ring[NS][XS];
+  __shared__ __attribute__((aligned(16))) uint8_t zero16[16];
+  const int lane = threadIdx.x & 63;
+  const int g4 = lane >> 4, li = lane & 15;
+  const int wave = uniform(threadIdx.x >> 6);
+  if (threadIdx.x < 4) reinterpret_cast<uint32_t*>(zero16)[threadIdx.x] = 0u;
+  __syncthreads();
+
+  // the block's groups: those starting in an equal share of the group steps
+  const int64_t s0 = (int64_t)blockIdx.x * h.total_ssteps / gridDim.x;
+  const int64_t s1 = ((int64_t)blockIdx.x + 1) * h.total_ssteps / gridDim.x;
+  const int64_t q0 = uniform64(coop_group_at_step(tab, h.n_layers, s0, h.total_ssteps, RBG));
+  const int64_t q1 = uniform64(coop_group_at_step(tab, h.n_layers, s1, h.total_ssteps, RBG));
+  if (q0 >= q1) return;  // the whole block leaves before its first barrier
+  const int wrb = wave / SH;              // this wave's row block within a group
+  const int t0 = (wave % SH) * TS;        // and its first activation tile
+
+  CoopCursor lc;
+  {
+    lc.rbg = RBG;
+    lc.q = q0;
+    lc.qend = q1;
+    lc.lidx = coop_layer_of_group(tab, h.n_layers, q0);
+    const DecLayer L0 = load_layer(tab + lc.lidx);
+    coop_enter_layer(lc, L0);
+    lc.g = (int)(q0 - L0.sitem0);
+    lc.k4 = 0;
+    lc.live = true;
+  }
+  CoopCursor oc = lc;
+
+  // issue the loads of the load cursor's step into slot k: this wave's codes
+  // (registers cq) and its share of the activation operand (LDS)
+  auto issue = [&](int k, v4i (&cq)[P]) {
+    const int rb = lc.g * RBG + wrb;
+    const bool ok = lc.live && rb < lc.nrb && rb * 16 + li < lc.N && lc.k4 * 256 + 32 * g4 < lc.K;
+    const uint32_t pb = (uint32_t)(T * lc.nrb * lc.nk4 * 1024) - (uint32_t)(T - 1) * 1024u;
+    const uint32_t off = ok ? (uint32_t)((rb * lc.nk4 + lc.k4) * T) * 1024u + (uint32_t)lane * 16u : kOob;
+#pragma unroll
+    for (int p = 0; p < P; ++p)
+      cq[p] = __builtin_amdgcn_raw_buffer_load_b128(make_rsrc(uniform_ptr(lc.codes[p / T] + (p % T) * 1024), pb),
+                                                    off, 0, kNonTemporal);
+    const uint32_t xtile = (uint32_t)(lc.nk4 * 4096);
+    const auto xr = make_rsrc(uniform_ptr(lc.xf), (uint32_t)(h.ntile * xtile));
+#pragma unroll
+    for (int i = 0; i < DMA; ++i) {
+      const int d = wave * DMA + i, t = d >> 2, c = d & 3;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          xr, (lds_ptr_t)(&ring[k][t * 4096 + c * 1024]), 16,
+          lc.live ? (uint32_t)t * xtile + (uint32_t)(lc.k4 * 4096 + c * 1024 + lane * 16) : kOob, 0, 0, 0);
+    }
+  };
+
+  // the epilogue's per-layer constants of the output cursor's layer
+  float esc[2][T][2], exf[TS][4];
+  DecLayer Lo;
+  auto load_out_layer = [&]() {
+    Lo = load_layer(tab + oc.lidx);
+    sload_scales<T>(uniform_ptr(Lo.scales[0]), uniform_ptr(Lo.scales[1]), esc);
+#pragma unroll
+    for (int t = 0; t < TS; ++t) sload_run<4>(uniform_ptr(Lo.xs) + 4 * (t0 + t), exf[t]);
+  };
+  load_out_layer();
+
+  bool xvalid[TS];
+#pragma unroll
+  for (int t = 0; t < TS; ++t) xvalid[t] = 4 * (t0 + t) + li / 4 < h.B;
+
+  v4i cq[NS][P];
+#pragma unroll
+  for (int k = 0; k < NS - 1; ++k) {
+    issue(k, cq[k]);
+    if (lc.live) coop_advance(lc, tab);
+  }
+  v4f aS[TS][P], aI[TS][P];
+#pragma unroll
+  for (int t = 0; t < TS; ++t)
+#pragma unroll
+    for (int p = 0; p < P; ++p) aS[t][p] = aI[t][p] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  auto step = [&](auto kconst) -> bool {
+    constexpr int K = decltype(kconst)::value;
+    constexpr int KN = (K + NS - 1) % NS;  // the slot read the step before
+    __builtin_amdgcn_s_waitcnt(WAITCNT);   // this wave's loads of slot K are done
+    __builtin_amdgcn_s_barrier();           // every wave's loads of slot K are done; slot KN is free
+    issue(KN, cq[KN]);
+    if (lc.live) coop_advance(lc, tab);
+    const v4i* cr = cq[K];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      v4i xr[TS][2];
+#pragma unroll
+      for (int t = 0; t < TS; ++t) {
+        const uint32_t xa = xvalid[t]
+                                ? lds_addr(&ring[K][(t0 + t) * 4096]) + (uint32_t)((g4 * 16 + li) * 16) + kb * 2048u
+                                : lds_addr(zero16);
+        const uint32_t xs = xvalid[t] ? 1024u : 0u;
+        lds_read2(xa, xa + xs, xr[t]);
+      }
+#pragma unroll
+      for (int p = 0; p < P; ++p) {
+        v8i bs, bi;
+        expand_f4((uint32_t)cr[p][2 * kb], (uint32_t)cr[p][2 * kb + 1], bs, bi);
+#pragma unroll
+        for (int t = 0; t < TS; ++t) {
+          const v4i x0 = xr[t][0], x1 = xr[t][1];
+          const v8i a = v8i{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+          aS[t][p] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bs, aS[t][p], kFmtFp8, kFmtFp4, 0, 0, 0, 0);
+          aI[t][p] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bi, aI[t][p], kFmtFp8, kFmtFp4, 0, 0, 0, 0);
+        }
+        // one plane's expansion, then its MFMAs: bounds the registers the schedule keeps live
+        __builtin_amdgcn_sched_group_barrier(0x002, 10, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2 * TS, 0);
+      }
+    }
+    if (oc.k4 == oc.nk4 - 1) {
+      const int rb = oc.g * RBG + wrb;
+      const int row = rb * 16 + li;
+      const bool row_ok = rb < oc.nrb && row < oc.N;
+#pragma unroll
+      for (int t = 0; t < TS; ++t) {
+        write_outputs_f4<T, 1>(Lo, h, 0, row, row_ok, lane, t0 + t, aS[t], aI[t], esc, exf[t]);
+#pragma unroll
+        for (int p = 0; p < P; ++p) aS[t][p] = aI[t][p] = v4f{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+    const int lbefore = oc.lidx;
+    coop_advance(oc, tab);
+    if (!oc.live) return true;
+    if (oc.lidx != lbefore) load_out_layer();
+    return false;
+  };
+
+  static_assert(NS == 3, "the ring loop below is unrolled for 3 slots");
+  while (true) {
+    if (step(std::integral_constant<int, 0>{})) break;
+    if (step(std::integral_constant<int, 1>{})) break;
+    if (step(std::integral_constant<int, 2>{})) break;
+  }
+  __builtin_amdgcn_s_waitcnt(0);  // no load may still be writing LDS when the wave ends
+#endif
+}
+
+template <int T, int NT>
+void launch_coop_f4(const DecHeader& h, const DecLayer* tab, hipStream_t s) {
+  auto k = dec_coop_f4_kernel<T, NT, NT >= 4 ? 2 : NT>;
+  static const int resident = resident_blocks(reinterpret_cast<const void*>(k), 64 * kCoopWaves);
+  hipLaunchKernelGGL(k, dim3((unsigned)resident), dim3(64 * kCoopWaves), 0, s, h, tab);
 }
 
 }  // namespace
 
 void launch_f4_prep(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
-  hipLaunchKernelGGL(dec_prep_f4_kernel, dim3(h.ntile, h.n_layers, kPrepF4Slices), dim3(kPrepF4Threads), 0, s, h, inl,
-                     tab);
+  const int slices = h.ntile >= kPrepF4Blocks ? 1 : kPrepF4Blocks / h.ntile;
+  hipLaunchKernelGGL(dec_prep_f4_kernel, dim3(h.ntile, h.n_layers, slices), dim3(kPrepF4Threads), 0, s, h, inl, tab);
 }
 
 void launch_f4_product(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {

@@ -279,3 +279,54 @@ def test_group_many_one_step_layers(gpu):
     f2.WlGroup(args, T=T, B=B, tiled=True).run()
     for a, yo in zip(args, refs):
         assert rel_l2(host(a[6]), yo) <= 1e-5
+
+
+def test_coop_kernel_full_k_group(gpu):
+    """A group large enough for full-K work items (70 LLaMA-2-7B-shaped
+    layers, 13,280 row blocks) with 5 to 16 tokens: the block-cooperative
+    kernel (four waves on consecutive row blocks of one layer sharing one
+    activation ring) against the oracle on sampled layers, and a repeated
+    call bitwise identical."""
+    import torch
+    import paper_2512_02901_amd as f2
+    T = 2
+    shapes = []
+    for layer in range(10):
+        for p in synth.PROJ_ORDER:
+            rows, cols = synth.LLAMA2_7B_PROJ[p]
+            shapes.append((rows // 2, cols // 2))
+    assert sum((N + 15) // 16 for N, _ in shapes) >= 12288
+    mats = []
+    for i, (N, K) in enumerate(shapes):
+        A = synth.torch_llama_weight(2 * N, 2 * K, 8000 + i, gpu)
+        U, W = f2.to_widely_linear(A)
+        cu, su = f2.quantize(U, T)
+        cw, sw = f2.quantize(W, T)
+        mats.append((N, K, cu, su, cw, sw, f2.repack_tiled_fp4(cu), f2.repack_tiled_fp4(cw)))
+        del A, U, W
+    check = [0, 4, 6, 69]
+    for B in (5, 8, 16):
+        rng = np.random.default_rng(B)
+        args, xs = [], []
+        for (N, K, cu, su, cw, sw, cu4, cw4) in mats:
+            x = synth.bf16_round_complex((rng.standard_normal((B, K)) + 1j * rng.standard_normal((B, K)))
+                                         .astype(np.complex64))
+            y = torch.empty((B, N), dtype=torch.complex64, device=gpu)
+            args.append((cu4, su, cw4, sw, bf16_dev(x, gpu), None, y))
+            xs.append(x)
+        grp = f2.WlGroup(args, T=T, B=B, layout=f2.LAYOUT_TILED_FP4)
+        grp.run()
+        torch.cuda.synchronize()
+        first = [host(a[6]).copy() for a in args]
+        errs = []
+        for i in check:
+            N, K, cu, su, cw, sw, _, _ = mats[i]
+            want = oracle.wl_matmul(oracle.unpack(host(cu), K), host(su), oracle.unpack(host(cw), K), host(sw), xs[i])
+            errs.append(rel_l2(first[i], want))
+        print(f"B={B} coop rel-L2:", " ".join(f"{e:.2e}" for e in errs))
+        assert max(errs) <= tol_for(B, typical=True)
+        grp.run()
+        torch.cuda.synchronize()
+        for a, y1 in zip(args, first):
+            np.testing.assert_array_equal(host(a[6]).view(np.uint32), y1.view(np.uint32))
+        del grp, args
