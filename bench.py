@@ -629,8 +629,8 @@ def main():
                 # committed counters were taken for another kernel source)
                 "traffic": None if traffic is None else int(traffic),
                 "traffic_over_algorithmic": None if traffic is None else round(traffic / algo, 3),
-                "kernel": "dec_stream_f4_kernel<T=2> (fp8 x fp4 MFMA product over fp4-tiled codes, "
-                          "one launch per step)",
+                "kernel": "dec_coop_f4_kernel<T=2> (fp8 x fp4 MFMA product over fp4-tiled codes, four waves "
+                          "per block sharing one activation ring; one launch per step)",
                 "algorithmic_bytes_per_launch": algo, "avg_launch_us": round(prod_ms * 1e3, 2)}
 
     result = {

@@ -756,8 +756,9 @@ void launch_stream_f4_g(const DecHeader& h, const DecLayer& inl, const DecLayer*
   else launch_stream_f4<T, 4, 1, GS, 1>(h, inl, tab, s);
 }
 
-template <int T, int NT>
+template <int T, int NT, int NC, int BANDS>
 void launch_coop_f4(const DecHeader& h, const DecLayer* tab, hipStream_t s);  // the block-cooperative kernel below
+constexpr bool kCoopSmallB = true;  // one tile (1-4 tokens) on the cooperative kernel too
 
 template <int T>
 void launch_stream_f4_t(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
@@ -767,13 +768,17 @@ void launch_stream_f4_t(const DecHeader& h, const DecLayer& inl, const DecLayer*
   }
   if constexpr (T <= 2) {
     if (tab && h.coop && h.ntile >= 3) {
-      launch_coop_f4<T, 4>(h, tab, s);
+      launch_coop_f4<T, 4, 16, 1>(h, tab, s);
       return;
     }
-  }
-  if constexpr (T <= 2) {
     if (tab && h.coop && h.ntile == 2) {
-      launch_coop_f4<T, 2>(h, tab, s);
+      launch_coop_f4<T, 2, 16, 1>(h, tab, s);
+      return;
+    }
+    if (tab && h.coop && kCoopSmallB) {
+      if (h.nc <= 8) launch_coop_f4<T, 1, 8, 2>(h, tab, s);
+      else if (h.bands == 2) launch_coop_f4<T, 1, 16, 2>(h, tab, s);
+      else launch_coop_f4<T, 1, 16, 1>(h, tab, s);
       return;
     }
   }
@@ -864,7 +869,8 @@ __device__ inline void coop_advance(CoopCursor& c, const DecLayer* tab) {
 // TS activation tiles per wave: with NT = 4 two waves share a row block,
 // two tiles each, so a wave's accumulators stay at 64 registers; two blocks
 // per CU (eight waves, at most 256 registers per lane).
-template <int T, int NT, int TS>
+// NC columns per tile (8: one two-band token; 16), BANDS digit bands per token.
+template <int T, int NT, int TS, int NC, int BANDS>
 __global__ __launch_bounds__(64 * kCoopWaves, 2) void dec_coop_f4_kernel(DecHeader h,
                                                                       const DecLayer* __restrict__ tab) {
 #if defined(__HIP_DEVICE_COMPILE__)  // LDS-DMA and buffer-descriptor code: device pass only
@@ -874,15 +880,21 @@ __global__ __launch_bounds__(64 * kCoopWaves, 2) void dec_coop_f4_kernel(DecHead
   constexpr int RBG = W / SH;           // row blocks per group
   static_assert(NT % TS == 0 && W % SH == 0, "tiles split evenly over the waves of a row block");
   constexpr int NS = kCoopSlots;
-  constexpr int XS = NT * 4096;         // a step's activation operand: NT tiles x 16 columns x 256 codes
-  constexpr int DMA = NT * 4 / W;       // 1-KiB activation loads per wave and step
-  static_assert((NT * 4) % W == 0, "the activation loads split evenly over the waves");
+  constexpr int XT = NC * 256;          // a tile's operand per step: NC columns x 256 codes
+  constexpr int XS = NT * XT;           // a step's activation operand
+  constexpr int NDMA = XS / 1024;       // its 1-KiB loads
+  constexpr int DMA = (NDMA + W - 1) / W;  // per wave (waves past the last load issue an empty one)
+  constexpr int TPT = 4 / BANDS;        // tokens per 16 columns
+  constexpr int CPT = 4 * BANDS;        // columns per token
   constexpr int LOADS = P + DMA;        // vector memory ops per wave and step
   constexpr int WAIT = (NS - 2) * LOADS;  // when step j is read, steps j+1 .. j+NS-2 may still load
   constexpr int WAITCNT = (WAIT & 0xF) | (0x7 << 4) | (0xF << 8) | (((WAIT >> 4) & 3) << 14);
   static_assert(WAIT < 64, "vmcnt holds at most 63");
   __shared__ __attribute__((aligned(16))) uint8_t ring[NS][XS];
   __shared__ __attribute__((aligned(16))) uint8_t zero16[16];
+  // target of the empty loads of waves past the step's last activation load
+  // (an out-of-range load still writes its zeros to LDS)
+  __shared__ __attribute__((aligned(16))) uint8_t spare[NDMA % W ? 1024 : 16];
   const int lane = threadIdx.x & 63;
   const int g4 = lane >> 4, li = lane & 15;
   const int wave = uniform(threadIdx.x >> 6);
@@ -923,31 +935,33 @@ __global__ __launch_bounds__(64 * kCoopWaves, 2) void dec_coop_f4_kernel(DecHead
     for (int p = 0; p < P; ++p)
       cq[p] = __builtin_amdgcn_raw_buffer_load_b128(make_rsrc(uniform_ptr(lc.codes[p / T] + (p % T) * 1024), pb),
                                                     off, 0, kNonTemporal);
-    const uint32_t xtile = (uint32_t)(lc.nk4 * 4096);
+    const uint32_t xtile = (uint32_t)(lc.nk4 * XT);
     const auto xr = make_rsrc(uniform_ptr(lc.xf), (uint32_t)(h.ntile * xtile));
 #pragma unroll
     for (int i = 0; i < DMA; ++i) {
-      const int d = wave * DMA + i, t = d >> 2, c = d & 3;
+      const int d0 = wave * DMA + i;
+      const bool real = d0 < NDMA;
+      const int d = real ? d0 : 0, t = d / (XT / 1024), c = d % (XT / 1024);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          xr, (lds_ptr_t)(&ring[k][t * 4096 + c * 1024]), 16,
-          lc.live ? (uint32_t)t * xtile + (uint32_t)(lc.k4 * 4096 + c * 1024 + lane * 16) : kOob, 0, 0, 0);
+          xr, (lds_ptr_t)(real ? &ring[k][t * XT + c * 1024] : &spare[0]), 16,
+          lc.live && real ? (uint32_t)t * xtile + (uint32_t)(lc.k4 * XT + c * 1024 + lane * 16) : kOob, 0, 0, 0);
     }
   };
 
   // the epilogue's per-layer constants of the output cursor's layer
-  float esc[2][T][2], exf[TS][4];
+  float esc[2][T][2], exf[TS][TPT];
   DecLayer Lo;
   auto load_out_layer = [&]() {
     Lo = load_layer(tab + oc.lidx);
     sload_scales<T>(uniform_ptr(Lo.scales[0]), uniform_ptr(Lo.scales[1]), esc);
 #pragma unroll
-    for (int t = 0; t < TS; ++t) sload_run<4>(uniform_ptr(Lo.xs) + 4 * (t0 + t), exf[t]);
+    for (int t = 0; t < TS; ++t) sload_run<TPT>(uniform_ptr(Lo.xs) + TPT * (t0 + t), exf[t]);
   };
   load_out_layer();
 
   bool xvalid[TS];
 #pragma unroll
-  for (int t = 0; t < TS; ++t) xvalid[t] = 4 * (t0 + t) + li / 4 < h.B;
+  for (int t = 0; t < TS; ++t) xvalid[t] = li < NC && TPT * (t0 + t) + li / CPT < h.B;
 
   v4i cq[NS][P];
 #pragma unroll
@@ -974,10 +988,10 @@ __global__ __launch_bounds__(64 * kCoopWaves, 2) void dec_coop_f4_kernel(DecHead
       v4i xr[TS][2];
 #pragma unroll
       for (int t = 0; t < TS; ++t) {
-        const uint32_t xa = xvalid[t]
-                                ? lds_addr(&ring[K][(t0 + t) * 4096]) + (uint32_t)((g4 * 16 + li) * 16) + kb * 2048u
-                                : lds_addr(zero16);
-        const uint32_t xs = xvalid[t] ? 1024u : 0u;
+        const uint32_t xa = xvalid[t] ? lds_addr(&ring[K][(t0 + t) * XT]) + (uint32_t)((g4 * NC + li) * 16) +
+                                            kb * (uint32_t)(2 * 64 * NC)
+                                      : lds_addr(zero16);
+        const uint32_t xs = xvalid[t] ? (uint32_t)(64 * NC) : 0u;
         lds_read2(xa, xa + xs, xr[t]);
       }
 #pragma unroll
@@ -1002,7 +1016,7 @@ __global__ __launch_bounds__(64 * kCoopWaves, 2) void dec_coop_f4_kernel(DecHead
       const bool row_ok = rb < oc.nrb && row < oc.N;
 #pragma unroll
       for (int t = 0; t < TS; ++t) {
-        write_outputs_f4<T, 1>(Lo, h, 0, row, row_ok, lane, t0 + t, aS[t], aI[t], esc, exf[t]);
+        write_outputs_f4<T, BANDS>(Lo, h, 0, row, row_ok, lane, t0 + t, aS[t], aI[t], esc, exf[t]);
 #pragma unroll
         for (int p = 0; p < P; ++p) aS[t][p] = aI[t][p] = v4f{0.f, 0.f, 0.f, 0.f};
       }
@@ -1024,9 +1038,9 @@ __global__ __launch_bounds__(64 * kCoopWaves, 2) void dec_coop_f4_kernel(DecHead
 #endif
 }
 
-template <int T, int NT>
+template <int T, int NT, int NC, int BANDS>
 void launch_coop_f4(const DecHeader& h, const DecLayer* tab, hipStream_t s) {
-  auto k = dec_coop_f4_kernel<T, NT, NT >= 4 ? 2 : NT>;
+  auto k = dec_coop_f4_kernel<T, NT, NT >= 4 ? 2 : NT, NC, BANDS>;
   static const int resident = resident_blocks(reinterpret_cast<const void*>(k), 64 * kCoopWaves);
   hipLaunchKernelGGL(k, dim3((unsigned)resident), dim3(64 * kCoopWaves), 0, s, h, tab);
 }

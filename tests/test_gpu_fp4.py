@@ -283,7 +283,7 @@ def test_group_many_one_step_layers(gpu):
 
 def test_coop_kernel_full_k_group(gpu):
     """A group large enough for full-K work items (70 LLaMA-2-7B-shaped
-    layers, 13,280 row blocks) with 5 to 16 tokens: the block-cooperative
+    layers, 13,280 row blocks) with 1 to 16 tokens: the block-cooperative
     kernel (four waves on consecutive row blocks of one layer sharing one
     activation ring) against the oracle on sampled layers, and a repeated
     call bitwise identical."""
@@ -305,7 +305,7 @@ def test_coop_kernel_full_k_group(gpu):
         mats.append((N, K, cu, su, cw, sw, f2.repack_tiled_fp4(cu), f2.repack_tiled_fp4(cw)))
         del A, U, W
     check = [0, 4, 6, 69]
-    for B in (5, 8, 16):
+    for B in (1, 2, 3, 4, 5, 8, 16):
         rng = np.random.default_rng(B)
         args, xs = [], []
         for (N, K, cu, su, cw, sw, cu4, cw4) in mats:
