@@ -798,7 +798,7 @@ void launch_stream_f4_t(const DecHeader& h, const DecLayer& inl, const DecLayer*
 // Blocks take the groups that start in an equal share of the call's group
 // steps; the table lists layers by decreasing length.  Used when every layer
 // is one full-K item per row block (no partials).
-constexpr int kCoopSlots = 3;
+constexpr int kCoopSlots = 4;
 
 // Global index of the first group (of rbg row blocks) whose first step is at
 // or after group step s.
@@ -1028,11 +1028,12 @@ __global__ __launch_bounds__(64 * kCoopWaves, 2) void dec_coop_f4_kernel(DecHead
     return false;
   };
 
-  static_assert(NS == 3, "the ring loop below is unrolled for 3 slots");
+  static_assert(NS == 3 || NS == 4, "the ring loop below is unrolled for 3 or 4 slots");
   while (true) {
     if (step(std::integral_constant<int, 0>{})) break;
     if (step(std::integral_constant<int, 1>{})) break;
     if (step(std::integral_constant<int, 2>{})) break;
+    if constexpr (NS == 4) if (step(std::integral_constant<int, 3 % NS>{})) break;
   }
   __builtin_amdgcn_s_waitcnt(0);  // no load may still be writing LDS when the wave ends
 #endif
