@@ -1049,7 +1049,8 @@ void launch_coop_f4(const DecHeader& h, const DecLayer* tab, hipStream_t s) {
 }  // namespace
 
 void launch_f4_prep(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
-  const int slices = h.ntile >= kPrepF4Blocks ? 1 : kPrepF4Blocks / h.ntile;
+  // one token: one block per layer (its work is a latency chain, not throughput)
+  const int slices = (h.B == 1 || h.ntile >= kPrepF4Blocks) ? 1 : kPrepF4Blocks / h.ntile;
   hipLaunchKernelGGL(dec_prep_f4_kernel, dim3(h.ntile, h.n_layers, slices), dim3(kPrepF4Threads), 0, s, h, inl, tab);
 }
 
