@@ -5,8 +5,9 @@ Workload (one "step"): the full LLaMA-2-7B linear stack for one decode token
 -- 32 layers x {q, k, v, o: 4096x4096; gate, up: 11008x4096; down: 4096x11008}
 as widely-linear T = 2 layers (complex U, W of half size, 2-bit codes, about
 1.62 GB packed) -- each projection with its own bf16 activation token, all
-decoded by one grouped call (activation-operand kernel, fp8 x fp4 MFMA
-product kernel, split-K reduction) on one stream.  Weights are seeded synthetic
+decoded by one grouped call (activation-operand kernel and the
+block-cooperative fp8 x fp4 MFMA product kernel; every layer is one full-K
+work item per row block, so no split-K reduction runs) on one stream.  Weights are seeded synthetic
 Student-t(4) draws with LLaMA-like outliers, quantised on the GPU by the
 library itself during setup (not timed).
 
@@ -15,7 +16,10 @@ Printed: ONE JSON line.  `value` is packed-weight GB/s of the whole step
 objects: `roofline` (the product kernel, timed live with HIP events on its
 stream), `cpu_baseline` (the CPU oracle on a bounded sample), `prefill`
 (2048-token int8 GEMMs, effective dense int8 TOPS), `stack_T3`, `stack_B*`
-(more tokens per layer), `per_layer` (one layer per call over rotated copies).
+(more tokens per layer), `stack_group256` (per-group scales), `per_layer`
+(one layer per call over rotated copies), `decoder_block`, `qat_step`
+(one training step of a q-shaped layer), `cpu_lut` (the host table-lookup
+kernel over the whole stack), `quantizer`.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
 """
@@ -335,11 +339,22 @@ def cpu_lut_bench(f2, torch, layers, T, passes=3):
             "kernel": "fairy2i_cpu_lut_wl_matmul (8-bit index of four codes, int16 tables, SSE2)"}
 
 
+def code_hash(path):
+    """First 16 hex digits of the sha256 of a C++/HIP source with its
+    comments and white space removed: edits to comments leave it unchanged,
+    edits to code do not."""
+    import re
+    text = open(path).read()
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return hashlib.sha256("".join(text.split()).encode()).hexdigest()[:16]
+
+
 def traffic_record():
     """HBM bytes per launch of the product kernel from committed rocprofv3
-    --pmc summaries, or None when absent or when the kernel source changed
+    --pmc summaries, or None when absent or when the kernel's code changed
     since the counters were taken."""
-    path = os.path.join(PROFILES, "dec_stream_f4_stack_T2_bf16_traffic.txt")
+    path = os.path.join(PROFILES, "dec_coop_f4_stack_T2_bf16_traffic.txt")
     if not os.path.exists(path):
         return None
     rec = {}
@@ -347,8 +362,7 @@ def traffic_record():
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             rec[k.strip()] = v.strip()
-    src_hash = hashlib.sha256(open(PRODUCT_KERNEL_SRC, "rb").read()).hexdigest()[:16]
-    if rec.get("kernel_source_sha256_16") != src_hash:
+    if rec.get("kernel_code_sha256_16") != code_hash(PRODUCT_KERNEL_SRC):
         return None
     try:
         return float(rec["hbm_bytes_per_launch"])

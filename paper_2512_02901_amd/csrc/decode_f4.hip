@@ -786,11 +786,13 @@ void launch_stream_f4_t(const DecHeader& h, const DecLayer& inl, const DecLayer*
 }
 
 // ------------------------------------------- block-cooperative kernel ---
-// With five or more tokens a step's activation operand (NT tiles of 4 KiB)
-// outweighs its codes (2T KiB), and a per-wave ring of it leaves room for
-// few waves per CU.  Here the kCoopWaves waves of a block decode kCoopWaves
-// consecutive row blocks of one layer (a group) together, stepping through
-// K in lockstep.  One ring of kCoopSlots slots in LDS holds each step's
+// A per-wave ring holds a copy of each step's activation operand per wave;
+// with five or more tokens that operand (NT tiles of 4 KiB) outweighs the
+// step's codes (2T KiB) and leaves room for few waves per CU, and even with
+// one token every wave fetches it from L2 again.  Here the waves of a block
+// decode consecutive row blocks of one layer (a group) together, stepping
+// through K in lockstep (with four tiles two waves share a row block, two
+// tiles each).  One ring of kCoopSlots slots in LDS holds each step's
 // activation operand once for the whole block (each wave loads its share),
 // the codes go to each wave's own registers as in the streaming kernel, and
 // one barrier per step both publishes the slot about to be read and retires
