@@ -35,7 +35,10 @@ EXTRA = {
     # keep MFMA accumulators in VGPRs: the decode kernels accumulate across
     # steps and items, and AGPR accumulators cost copies on every step
     "decode.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
-    "decode_f4.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+    # and leave the cooperative kernel's one-lane claim atomics as written (the
+    # atomic optimizer would read each result back at once, waiting for every
+    # load in flight)
+    "decode_f4.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"],
 }
 
 

@@ -380,7 +380,7 @@ size_t fairy2i_wl_group_workspace_bytes(const fairy2i_wl_layer* layers, int32_t 
   if (check_group(layers, n_layers, T, dtype, B) != FAIRY2I_OK) return 0;
   const DecHeader h = dec_header(T, group_mode(layers, dtype), B, false);
   const int slice = group_slice(layers, n_layers, h);
-  size_t total = 0;
+  size_t total = kGroupCallBytes;
   for (int32_t i = 0; i < n_layers; ++i) {
     DecLayer l{};
     l.N = (int32_t)layers[i].N;
@@ -404,6 +404,8 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
   DecHeader h = dec_header(T, group_mode(layers, dtype), B, false);
   const int slice = group_slice(layers, n_layers, h);
   char* ws = static_cast<char*>(workspace);
+  h.coop_ctr = reinterpret_cast<uint32_t*>(ws);
+  ws += kGroupCallBytes;
   // descriptors in table order; on the fp4 path the table lists the layers by
   // decreasing work-item length (stable), so that the blocks of the product
   // kernel claim their long items first and end on short ones
@@ -420,6 +422,7 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
   if (h.mode == kModeBf16F4)
     std::stable_sort(ls.begin(), ls.end(), [](const DecLayer& a, const DecLayer& b) { return a.kc4 > b.kc4; });
   int64_t items = 0, steps = 0, sitems = 0, ssteps = 0;
+  int32_t min_nk4 = INT32_MAX;
   int any_split = 0;
   int64_t max_BN = 0;
   for (int32_t i = 0; i < n_layers; ++i) {
@@ -434,6 +437,7 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
     const int64_t groups = ((int64_t)l.nrb + rbg - 1) / rbg;
     sitems += groups;
     ssteps += groups * l.nk4;
+    if (l.nk4 < min_nk4) min_nk4 = l.nk4;
     if (l.nkc > 1) any_split = 1;
     if (B * (int64_t)l.N > max_BN) max_BN = B * (int64_t)l.N;
     tab[i] = l;
@@ -450,6 +454,27 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
   h.grouped = layers[0].group_size != 0 ? 1 : 0;
   h.coop = (h.mode == kModeBf16F4 && slice == kSliceFullK && !any_split) ? 1 : 0;
   h.coop_rb = coop_row_blocks(h.ntile);
+  // Run-time claims need every group to last more steps than the kernel's
+  // ring holds (a claim is answered kCoopSlots steps after it is made); the
+  // claimed region starts at the first group at or after the static
+  // fraction of the group steps (the table is sorted by decreasing length,
+  // so it holds the shortest groups).
+  h.coop_groups = sitems;
+  h.coop_dyn0 = sitems;
+  h.coop_dyn_steps = ssteps;
+  if (h.coop && !h.grouped && min_nk4 > kCoopSlots) {
+    const int64_t target = (int64_t)(kCoopStaticFrac * (double)ssteps);
+    const int rbg = h.coop_rb;
+    for (int32_t i = 0; i < n_layers; ++i) {
+      const DecLayer& l = tab[i];
+      const int64_t groups = ((int64_t)l.nrb + rbg - 1) / rbg;
+      if (l.sstep0 + groups * l.nk4 <= target) continue;
+      const int64_t g = l.sstep0 >= target ? 0 : (target - l.sstep0 + l.nk4 - 1) / l.nk4;
+      h.coop_dyn0 = l.sitem0 + g;
+      h.coop_dyn_steps = l.sstep0 + g * l.nk4;
+      break;
+    }
+  }
   hdr->h = h;
   hdr->any_split = any_split;
   hdr->max_BN = max_BN;

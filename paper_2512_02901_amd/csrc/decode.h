@@ -13,6 +13,7 @@ constexpr int kModeBf16F4 = 2;  // bf16 activations as e4m3 digit pairs in two m
                                 // codes in the fp4 tiled layout (fp8 x fp4 matrix cores)
 
 constexpr int kCoopWaves = 4;     // waves of a block of the cooperative fp4 kernel
+constexpr int kCoopSlots = 4;     // steps in the cooperative kernel's ring
 // row blocks per block of the cooperative kernel: with four activation tiles
 // two waves share a row block (two tiles each), else each wave has its own
 inline int coop_row_blocks(int ntile) { return ntile >= 3 ? 2 : kCoopWaves; }
@@ -56,7 +57,22 @@ struct DecHeader {
   int64_t total_ssteps; // block-cooperative kernel: steps of all row-block groups
   int32_t coop;         // every layer is one full-K item per row block: the cooperative kernel may run
   int32_t coop_rb;      // row blocks per group of the cooperative kernel
+  // Cooperative kernel: groups [0, coop_dyn0) (coop_dyn_steps group steps) are
+  // split over the blocks in equal shares of steps; the rest are claimed one
+  // at a time at run time from *coop_ctr (zeroed by the activation
+  // preparation of the same call).  coop_dyn0 == coop_groups: no claims.
+  uint32_t* coop_ctr;
+  int64_t coop_groups;
+  int64_t coop_dyn0;
+  int64_t coop_dyn_steps;
 };
+
+// Bytes at the start of a group call's workspace that hold the cooperative
+// kernel's claim counter.
+constexpr size_t kGroupCallBytes = 256;
+// Fraction of a cooperative call's group steps split statically (the rest is
+// claimed at run time, where the shortest groups sit).
+constexpr double kCoopStaticFrac = 0.65;
 
 int dec_ntile(int mode, int64_t B);
 int dec_ncols(int mode, int64_t B);

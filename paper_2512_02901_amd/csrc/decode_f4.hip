@@ -76,6 +76,8 @@ __device__ inline void digit_words(const float (&v)[4], uint32_t& hi, uint32_t& 
 __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_kernel(DecHeader h, DecLayer inl,
                                                                      const DecLayer* __restrict__ tab) {
   const DecLayer L = tab ? load_layer(tab + blockIdx.y) : inl;
+  // the cooperative product kernel's claim counter starts every call at zero
+  if (h.coop_ctr && blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0 && threadIdx.x == 0) *h.coop_ctr = 0u;
   const int tile = blockIdx.x;
   const int K = L.K;
   const int bands = h.bands;
@@ -238,12 +240,17 @@ constexpr int kFmtFp8 = 0;  // MFMA operand format codes: e4m3
 constexpr int kFmtFp4 = 4;  // e2m1
 
 // Token factor tt of a tile's NF factors, selected without indexing a
-// register array by a lane-dependent value.
+// register array by a lane-dependent value (such an array lives in scratch
+// memory, whose loads share the vector-memory queue with the code loads in
+// flight, so a wait for one waits for all).  The factors pass through
+// readfirstlane so that the selects choose between values, not between
+// loads, which the compiler would otherwise fold back into one indexed load.
 template <int NF>
 __device__ inline float pick_factor(const float (&xf)[NF], int tt) {
-  float f = xf[0];
+  auto val = [](float x) { return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(x))); };
+  float f = val(xf[0]);
 #pragma unroll
-  for (int i = 1; i < NF; ++i) f = tt == i ? xf[i] : f;
+  for (int i = 1; i < NF; ++i) f = tt == i ? val(xf[i]) : f;
   return f;
 }
 
@@ -800,7 +807,18 @@ void launch_stream_f4_t(const DecHeader& h, const DecLayer& inl, const DecLayer*
 // Blocks take the groups that start in an equal share of the call's group
 // steps; the table lists layers by decreasing length.  Used when every layer
 // is one full-K item per row block (no partials).
-constexpr int kCoopSlots = 4;
+//
+// Blocks that share a CU do not progress at the same rate (the waves of the
+// block dispatched first are served first), so with static shares alone the
+// first blocks finish early and the last ones leave the chip half idle.  The
+// last groups (the shortest) are therefore claimed at run time: when a
+// block's load cursor starts its last known group, lane 0 of wave 0 takes a
+// ticket from a global counter; the ticket returns with that step's loads,
+// is read kCoopSlots - 1 steps later after the step's wait, translated to a
+// (group, layer) pair and posted in LDS, where every wave reads it after the
+// next barrier.  That needs groups longer than kCoopSlots steps (the host
+// enables claims only then).  A group's outputs do not depend on which block
+// decodes it.
 
 // Global index of the first group (of rbg row blocks) whose first step is at
 // or after group step s.
@@ -852,19 +870,91 @@ __device__ inline void coop_enter_layer(CoopCursor& c, const DecLayer& L) {
   c.ngroups = (L.nrb + c.rbg - 1) / c.rbg;
 }
 
-// Next step; enters the next group / layer (reading its descriptor).
-__device__ inline void coop_advance(CoopCursor& c, const DecLayer* tab) {
+// A claimed group as posted in LDS by wave 0: global group index (past the
+// last group: nothing left) and its layer.
+struct __attribute__((aligned(16))) CoopPost {
+  int64_t q;
+  int32_t lidx, pad_;
+};
+
+// Next step; enters the next group / layer (reading its descriptor).  Past
+// the block's known groups: the claimed group posted in LDS, if claims run.
+__device__ inline void coop_advance(CoopCursor& c, const DecLayer* tab, const DecHeader& h, const CoopPost* post) {
   if (++c.k4 < c.nk4) return;
   c.k4 = 0;
   ++c.q;
   if (c.q >= c.qend) {
-    c.live = false;
+    if (h.coop_dyn0 >= h.coop_groups) {
+      c.live = false;
+      return;
+    }
+    int64_t q;
+    int l;
+    asm volatile(
+        "ds_read_b64 %0, %2\n"
+        "ds_read_b32 %1, %2 offset:8\n"
+        "s_waitcnt lgkmcnt(0)"
+        : "=v"(q), "=v"(l)
+        : "v"(lds_addr(post))
+        : "memory");
+    q = uniform64(q);
+    if (q >= h.coop_groups) {
+      c.live = false;
+      return;
+    }
+    c.q = q;
+    c.qend = q + 1;
+    c.lidx = uniform(l);
+    const DecLayer L = load_layer(tab + c.lidx);
+    coop_enter_layer(c, L);
+    c.g = (int)(q - L.sitem0);
     return;
   }
   if (++c.g == c.ngroups) {
     c.g = 0;
     ++c.lidx;
     coop_enter_layer(c, load_layer(tab + c.lidx));
+  }
+}
+
+// A step's activation reads for one wave: both 128-code halves (kb) of TS
+// tiles, two 16-byte reads each, issued together; the asm waits only for the
+// first half's reads, and coop_wait_x for the rest, so the second half's LDS
+// latency hides behind the first half's MFMAs.  The second half's registers
+// pass through coop_wait_x as in/out operands, which keeps every use of them
+// after that wait.
+template <int TS>
+__device__ inline void coop_read_x(const uint32_t (&a)[2][TS][2], v4i (&x)[2][TS][2]) {
+  static_assert(TS == 1 || TS == 2, "one or two tiles per wave");
+  if constexpr (TS == 1) {
+    __asm__ volatile(
+        "ds_read_b128 %0, %4\n\tds_read_b128 %1, %5\n\tds_read_b128 %2, %6\n\tds_read_b128 %3, %7\n\t"
+        "s_waitcnt lgkmcnt(2)"
+        : "=&v"(x[0][0][0]), "=&v"(x[0][0][1]), "=&v"(x[1][0][0]), "=&v"(x[1][0][1])
+        : "v"(a[0][0][0]), "v"(a[0][0][1]), "v"(a[1][0][0]), "v"(a[1][0][1])
+        : "memory");
+  } else {
+    __asm__ volatile(
+        "ds_read_b128 %0, %8\n\tds_read_b128 %1, %9\n\tds_read_b128 %2, %10\n\tds_read_b128 %3, %11\n\t"
+        "ds_read_b128 %4, %12\n\tds_read_b128 %5, %13\n\tds_read_b128 %6, %14\n\tds_read_b128 %7, %15\n\t"
+        "s_waitcnt lgkmcnt(4)"
+        : "=&v"(x[0][0][0]), "=&v"(x[0][0][1]), "=&v"(x[0][1][0]), "=&v"(x[0][1][1]), "=&v"(x[1][0][0]),
+          "=&v"(x[1][0][1]), "=&v"(x[1][1][0]), "=&v"(x[1][1][1])
+        : "v"(a[0][0][0]), "v"(a[0][0][1]), "v"(a[0][1][0]), "v"(a[0][1][1]), "v"(a[1][0][0]), "v"(a[1][0][1]),
+          "v"(a[1][1][0]), "v"(a[1][1][1])
+        : "memory");
+  }
+}
+
+template <int TS>
+__device__ inline void coop_wait_x(v4i (&x)[2][TS][2]) {
+  if constexpr (TS == 1) {
+    __asm__ volatile("s_waitcnt lgkmcnt(0)" : "+v"(x[1][0][0]), "+v"(x[1][0][1]) : : "memory");
+  } else {
+    __asm__ volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(x[1][0][0]), "+v"(x[1][0][1]), "+v"(x[1][1][0]), "+v"(x[1][1][1])
+                     :
+                     : "memory");
   }
 }
 
@@ -897,18 +987,29 @@ __global__ __launch_bounds__(64 * kCoopWaves, 2) void dec_coop_f4_kernel(DecHead
   // target of the empty loads of waves past the step's last activation load
   // (an out-of-range load still writes its zeros to LDS)
   __shared__ __attribute__((aligned(16))) uint8_t spare[NDMA % W ? 1024 : 16];
+  __shared__ CoopPost post;
   const int lane = threadIdx.x & 63;
   const int g4 = lane >> 4, li = lane & 15;
   const int wave = uniform(threadIdx.x >> 6);
   if (threadIdx.x < 4) reinterpret_cast<uint32_t*>(zero16)[threadIdx.x] = 0u;
   __syncthreads();
 
-  // the block's groups: those starting in an equal share of the group steps
-  const int64_t s0 = (int64_t)blockIdx.x * h.total_ssteps / gridDim.x;
-  const int64_t s1 = ((int64_t)blockIdx.x + 1) * h.total_ssteps / gridDim.x;
-  const int64_t q0 = uniform64(coop_group_at_step(tab, h.n_layers, s0, h.total_ssteps, RBG));
-  const int64_t q1 = uniform64(coop_group_at_step(tab, h.n_layers, s1, h.total_ssteps, RBG));
-  if (q0 >= q1) return;  // the whole block leaves before its first barrier
+  // the block's groups: those starting in an equal share of the statically
+  // split group steps, then (with claims) groups claimed at run time
+  const bool dyn = h.coop_dyn0 < h.coop_groups;
+  const int64_t s0 = (int64_t)blockIdx.x * h.coop_dyn_steps / gridDim.x;
+  const int64_t s1 = ((int64_t)blockIdx.x + 1) * h.coop_dyn_steps / gridDim.x;
+  int64_t q0 = uniform64(coop_group_at_step(tab, h.n_layers, s0, h.total_ssteps, RBG));
+  int64_t q1 = uniform64(coop_group_at_step(tab, h.n_layers, s1, h.total_ssteps, RBG));
+  if (q0 >= q1) {
+    if (!dyn) return;  // the whole block leaves before its first barrier
+    // no static share: claim the first group now
+    if (threadIdx.x == 0) post.q = h.coop_dyn0 + (int64_t)atomicAdd(h.coop_ctr, 1u);
+    __syncthreads();
+    q0 = uniform64(post.q);
+    if (q0 >= h.coop_groups) return;  // nothing left: the whole block leaves
+    q1 = q0 + 1;
+  }
   const int wrb = wave / SH;              // this wave's row block within a group
   const int t0 = (wave % SH) * TS;        // and its first activation tile
 
@@ -926,9 +1027,26 @@ __global__ __launch_bounds__(64 * kCoopWaves, 2) void dec_coop_f4_kernel(DecHead
   }
   CoopCursor oc = lc;
 
+  // the claim in flight (wave 0; at most one, since claims are a group
+  // apart): the ring slot whose loads carried it, and a ticket register per
+  // slot (so that the compiler sees each ticket written a ring round before
+  // it is read or overwritten, and adds no wait of its own)
+  uint32_t cret[NS];
+  int cslot = -1;
+
   // issue the loads of the load cursor's step into slot k: this wave's codes
-  // (registers cq) and its share of the activation operand (LDS)
+  // (registers cq) and its share of the activation operand (LDS).  At the
+  // first step of the block's last known group wave 0 also claims the next
+  // group; the claim goes out before the slot's loads, so the wait for them
+  // covers it.
   auto issue = [&](int k, v4i (&cq)[P]) {
+    if (dyn && wave == 0 && lc.live && lc.k4 == 0 && lc.q + 1 >= lc.qend) {
+      // one lane's atomic without a divergent branch: the other lanes' offsets
+      // are out of range, so their adds are dropped
+      cret[k] = (uint32_t)__builtin_amdgcn_raw_ptr_buffer_atomic_add_i32(1, make_rsrc(h.coop_ctr, 4u),
+                                                                         lane == 0 ? 0u : kOob, 0, 0);
+      cslot = k;
+    }
     const int rb = lc.g * RBG + wrb;
     const bool ok = lc.live && rb < lc.nrb && rb * 16 + li < lc.N && lc.k4 * 256 + 32 * g4 < lc.K;
     const uint32_t pb = (uint32_t)(T * lc.nrb * lc.nk4 * 1024) - (uint32_t)(T - 1) * 1024u;
@@ -969,7 +1087,7 @@ __global__ __launch_bounds__(64 * kCoopWaves, 2) void dec_coop_f4_kernel(DecHead
 #pragma unroll
   for (int k = 0; k < NS - 1; ++k) {
     issue(k, cq[k]);
-    if (lc.live) coop_advance(lc, tab);
+    if (lc.live) coop_advance(lc, tab, h, &post);
   }
   v4f aS[TS][P], aI[TS][P];
 #pragma unroll
@@ -982,20 +1100,48 @@ __global__ __launch_bounds__(64 * kCoopWaves, 2) void dec_coop_f4_kernel(DecHead
     constexpr int KN = (K + NS - 1) % NS;  // the slot read the step before
     __builtin_amdgcn_s_waitcnt(WAITCNT);   // this wave's loads of slot K are done
     __builtin_amdgcn_s_barrier();           // every wave's loads of slot K are done; slot KN is free
+    if (uniform(cslot) == K) {
+      // wave 0: the claim sent with slot K's loads has returned (the wait
+      // above covers it); post it for every wave (read at the load cursor's
+      // next group change, which comes at least one barrier later).  The
+      // ticket is read here, in order, so that no earlier read of it forces
+      // a wait for every load in flight.
+      cslot = -1;
+      uint32_t t;
+      asm volatile("v_readfirstlane_b32 %0, %1" : "=s"(t) : "v"(cret[K]));
+      const int64_t q = h.coop_dyn0 + (int64_t)t;
+      const int l = q < h.coop_groups ? coop_layer_of_group(tab, h.n_layers, q) : 0;
+      if (lane == 0)
+        asm volatile(
+            "ds_write_b64 %0, %1\n"
+            "ds_write_b32 %0, %2 offset:8\n"
+            "s_waitcnt lgkmcnt(0)"
+            :
+            : "v"(lds_addr(&post)), "v"(q), "v"(l)
+            : "memory");
+    }
     issue(KN, cq[KN]);
-    if (lc.live) coop_advance(lc, tab);
+    if (lc.live) coop_advance(lc, tab, h, &post);
     const v4i* cr = cq[K];
+    v4i xq[2][TS][2];
+    {
+      uint32_t xa[2][TS][2];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int t = 0; t < TS; ++t) {
+          const uint32_t a = xvalid[t] ? lds_addr(&ring[K][(t0 + t) * XT]) + (uint32_t)((g4 * NC + li) * 16) +
+                                             kb * (uint32_t)(2 * 64 * NC)
+                                       : lds_addr(zero16);
+          xa[kb][t][0] = a;
+          xa[kb][t][1] = a + (xvalid[t] ? (uint32_t)(64 * NC) : 0u);
+        }
+      coop_read_x<TS>(xa, xq);
+    }
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
-      v4i xr[TS][2];
-#pragma unroll
-      for (int t = 0; t < TS; ++t) {
-        const uint32_t xa = xvalid[t] ? lds_addr(&ring[K][(t0 + t) * XT]) + (uint32_t)((g4 * NC + li) * 16) +
-                                            kb * (uint32_t)(2 * 64 * NC)
-                                      : lds_addr(zero16);
-        const uint32_t xs = xvalid[t] ? (uint32_t)(64 * NC) : 0u;
-        lds_read2(xa, xa + xs, xr[t]);
-      }
+      if (kb == 1) coop_wait_x<TS>(xq);
+      const v4i(&xr)[TS][2] = xq[kb];
 #pragma unroll
       for (int p = 0; p < P; ++p) {
         v8i bs, bi;
@@ -1024,7 +1170,16 @@ __global__ __launch_bounds__(64 * kCoopWaves, 2) void dec_coop_f4_kernel(DecHead
       }
     }
     const int lbefore = oc.lidx;
-    coop_advance(oc, tab);
+    if (dyn) {
+      // the load cursor runs kCoopSlots - 1 steps ahead through the same
+      // groups, each longer than that: at a group change it is in the next one
+      if (++oc.k4 == oc.nk4) {
+        oc = lc;
+        oc.k4 = 0;
+      }
+    } else {
+      coop_advance(oc, tab, h, &post);
+    }
     if (!oc.live) return true;
     if (oc.lidx != lbefore) load_out_layer();
     return false;

@@ -285,8 +285,9 @@ def test_coop_kernel_full_k_group(gpu):
     """A group large enough for full-K work items (70 LLaMA-2-7B-shaped
     layers, 13,280 row blocks) with 1 to 16 tokens: the block-cooperative
     kernel (four waves on consecutive row blocks of one layer sharing one
-    activation ring) against the oracle on sampled layers, and a repeated
-    call bitwise identical."""
+    activation ring; the last groups claimed at run time) against the oracle
+    on sampled layers, and a repeated call bitwise identical (which blocks
+    take the claimed groups changes from call to call)."""
     import torch
     import paper_2512_02901_amd as f2
     T = 2
@@ -304,7 +305,10 @@ def test_coop_kernel_full_k_group(gpu):
         cw, sw = f2.quantize(W, T)
         mats.append((N, K, cu, su, cw, sw, f2.repack_tiled_fp4(cu), f2.repack_tiled_fp4(cw)))
         del A, U, W
-    check = [0, 4, 6, 69]
+    # the table lists the 22-step down projections first; the last 35 % of the
+    # group steps (2048-wide layers of the last projections) are claimed at
+    # run time, so the sample covers both parts
+    check = [0, 4, 6, 60, 64, 66, 68, 69]
     for B in (1, 2, 3, 4, 5, 8, 16):
         rng = np.random.default_rng(B)
         args, xs = [], []
