@@ -12,11 +12,18 @@ constexpr int kModeI8 = 1;    // int8 activations with a per-token factor
 constexpr int kModeBf16F4 = 2;  // bf16 activations as e4m3 digit pairs in two magnitude bands,
                                 // codes in the fp4 tiled layout (fp8 x fp4 matrix cores)
 
-constexpr int kCoopWaves = 4;     // waves of a block of the cooperative fp4 kernel
 constexpr int kCoopSlots = 4;     // steps in the cooperative kernel's ring
-// row blocks per block of the cooperative kernel: with four activation tiles
-// two waves share a row block (two tiles each), else each wave has its own
-inline int coop_row_blocks(int ntile) { return ntile >= 3 ? 2 : kCoopWaves; }
+// Cooperative fp4 kernel geometry by its activation tiles per call (NT = 1,
+// 2 or 4; three tiles run as four): waves per block (four for one tile, three
+// blocks per CU; eight for more, one block per CU, so that more row blocks
+// share each step's activation operand), tiles per wave (with four tiles two
+// waves share a row block, two tiles each) and row blocks per group.
+constexpr int coop_nt(int ntile) { return ntile >= 3 ? 4 : ntile; }
+constexpr int coop_waves(int nt) { return nt >= 2 ? 8 : 4; }
+constexpr int coop_tiles_per_wave(int nt) { return nt >= 4 ? 2 : nt; }
+constexpr int coop_row_blocks(int ntile) {
+  return coop_waves(coop_nt(ntile)) / (coop_nt(ntile) / coop_tiles_per_wave(coop_nt(ntile)));
+}
 constexpr int kKernelReg = 0;     // codes staged in registers; any batch, accumulator export
 constexpr int kKernelStream = 1;  // codes streamed through an LDS ring; one activation tile
 constexpr int kRegKc4 = 2;        // 256-code steps per work item of the register kernel
@@ -40,7 +47,7 @@ struct DecLayer {
                              // 0: one pair per stage (scales [T][2])
   int64_t item0;             // index of this layer's first work item
   int64_t step0;             // 256-code steps of all work items before item0
-  int64_t sitem0;            // block-cooperative kernel: first group of kCoopWaves row blocks
+  int64_t sitem0;            // block-cooperative kernel: first group of coop_row_blocks row blocks
   int64_t sstep0;            //   and the group steps (groups x nk4) of all layers before this one
 };
 

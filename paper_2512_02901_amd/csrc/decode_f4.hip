@@ -963,11 +963,11 @@ __device__ inline void coop_wait_x(v4i (&x)[2][TS][2]) {
 // per CU (eight waves, at most 256 registers per lane).
 // NC columns per tile (8: one two-band token; 16), BANDS digit bands per token.
 template <int T, int NT, int TS, int NC, int BANDS>
-__global__ __launch_bounds__(64 * kCoopWaves, 2) void dec_coop_f4_kernel(DecHeader h,
+__global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) void dec_coop_f4_kernel(DecHeader h,
                                                                       const DecLayer* __restrict__ tab) {
 #if defined(__HIP_DEVICE_COMPILE__)  // LDS-DMA and buffer-descriptor code: device pass only
   constexpr int P = 2 * T;
-  constexpr int W = kCoopWaves;
+  constexpr int W = coop_waves(NT);
   constexpr int SH = NT / TS;           // waves sharing a row block
   constexpr int RBG = W / SH;           // row blocks per group
   static_assert(NT % TS == 0 && W % SH == 0, "tiles split evenly over the waves of a row block");
@@ -1198,9 +1198,9 @@ __global__ __launch_bounds__(64 * kCoopWaves, 2) void dec_coop_f4_kernel(DecHead
 
 template <int T, int NT, int NC, int BANDS>
 void launch_coop_f4(const DecHeader& h, const DecLayer* tab, hipStream_t s) {
-  auto k = dec_coop_f4_kernel<T, NT, NT >= 4 ? 2 : NT, NC, BANDS>;
-  static const int resident = resident_blocks(reinterpret_cast<const void*>(k), 64 * kCoopWaves);
-  hipLaunchKernelGGL(k, dim3((unsigned)resident), dim3(64 * kCoopWaves), 0, s, h, tab);
+  auto k = dec_coop_f4_kernel<T, NT, coop_tiles_per_wave(NT), NC, BANDS>;
+  static const int resident = resident_blocks(reinterpret_cast<const void*>(k), 64 * coop_waves(NT));
+  hipLaunchKernelGGL(k, dim3((unsigned)resident), dim3(64 * coop_waves(NT)), 0, s, h, tab);
 }
 
 }  // namespace
