@@ -257,20 +257,28 @@ def qat_bench(f2, synth, torch, dev, T=2, tokens=4096, reps=10):
     GU = torch.empty(N, K, dtype=torch.complex64, device=dev)
     GW = torch.empty(N, K, dtype=torch.complex64, device=dev)
     state = {}
+    # the GEMMs run on the planar path (bf16 planes, one batched library GEMM); one workspace for all
+    ws = torch.empty(max(f2.cgemm_gauss_planar_workspace_bytes(kk, m, n)
+                         for kk, m, n in (([K, K], tokens, N), ([N, N], tokens, K), ([tokens], N, K))),
+                     dtype=torch.uint8, device=dev)
+    mode = {"planar": True}
+
+    def gemm(segs, m, n, out):
+        f2.cgemm_gauss(segs, m, n, out=out, planar=mode["planar"], workspace=ws if mode["planar"] else None)
 
     def fq():
         state["u"] = f2.qat_fake_quant(U, T)
         state["w"] = f2.qat_fake_quant(W, T)
 
     def fwd():
-        f2.cgemm_gauss([(X, 0, 0, state["u"][0], 0, 0, K), (X, 0, 1, state["w"][0], 0, 0, K)], tokens, N, out=Y)
+        gemm([(X, 0, 0, state["u"][0], 0, 0, K), (X, 0, 1, state["w"][0], 0, 0, K)], tokens, N, Y)
 
     def bwd_x():
-        f2.cgemm_gauss([(GY, 0, 0, state["u"][0], 1, 1, N), (GY, 0, 1, state["w"][0], 1, 0, N)], tokens, K, out=GX)
+        gemm([(GY, 0, 0, state["u"][0], 1, 1, N), (GY, 0, 1, state["w"][0], 1, 0, N)], tokens, K, GX)
 
     def bwd_w():
-        f2.cgemm_gauss([(GY, 1, 0, X, 1, 1, tokens)], N, K, out=GU)
-        f2.cgemm_gauss([(GY, 1, 0, X, 1, 0, tokens)], N, K, out=GW)
+        gemm([(GY, 1, 0, X, 1, 1, tokens)], N, K, GU)
+        gemm([(GY, 1, 0, X, 1, 0, tokens)], N, K, GW)
 
     def ste():
         f2.qat_ste_backward(state["u"][1], state["u"][2], GU)
@@ -282,16 +290,22 @@ def qat_bench(f2, synth, torch, dev, T=2, tokens=4096, reps=10):
     for _, fn in phases:
         fn()
     warm_up(lambda: [fn() for _, fn in phases], torch, 3)
-    out = {"workload": f"one QAT step of a q-shaped layer (complex {N}x{K}, T={T}), {tokens} bf16 tokens"}
-    total = 0.0
-    for name, fn in phases:
+    out = {"workload": f"one QAT step of a q-shaped layer (complex {N}x{K}, T={T}), {tokens} bf16 tokens",
+           "gemm_path": "planar: bf16 planes (Re, Im, Re+Im) by this library's kernels, the three real products "
+                        "as one batched hipBLASLt GEMM, combine kernel"}
+
+    def timed(fn):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
         for _ in range(reps):
             fn()
         e1.record()
         torch.cuda.synchronize()
-        us = e0.elapsed_time(e1) / reps * 1e3
+        return e0.elapsed_time(e1) / reps * 1e3
+
+    total = 0.0
+    for name, fn in phases:
+        us = timed(fn)
         out[name + "_us"] = round(us, 1)
         total += us
     out["step_us"] = round(total, 1)
@@ -303,7 +317,11 @@ def qat_bench(f2, synth, torch, dev, T=2, tokens=4096, reps=10):
     out["gemm_exec_TFLOPs"] = round(6 * sum(macs.values()) / gemm_us / 1e6, 1)
     out["gemm_effective_TFLOPs"] = round(8 * sum(macs.values()) / gemm_us / 1e6, 1)
     out["gemm_frac_bf16_peak"] = round(out["gemm_exec_TFLOPs"] / 2500.0, 4)
-    del U, W, X, GY, Y, GX, GU, GW, state
+    # the same three GEMM phases on the single-kernel path, for comparison
+    mode["planar"] = False
+    warm_up(lambda: [fn() for name, fn in phases if name in macs], torch, 3)
+    out["single_kernel_gemms_us"] = round(sum(timed(fn) for name, fn in phases if name in macs), 1)
+    del U, W, X, GY, Y, GX, GU, GW, state, ws
     torch.cuda.empty_cache()
     return out
 
@@ -407,7 +425,39 @@ def prefill_bench(f2, synth, torch, dev, T=2, tokens=2048, reps=20):
         tops = ops / (ms * 1e-3) / 1e12
         out[name] = {"N": N, "K": K, "tokens": tokens, "us": round(ms * 1e3, 2), "tops": round(tops, 1),
                      "frac_int8_peak": round(tops / INT8_PEAK_TOPS, 4)}
+        del cu, cw, q, y, ws
+        # context, not the product: the same dense int8 op count as one plain library GEMM
+        # ((2 tokens) x K x (4TN), torch._int_mm), timed the same way
+        out[name]["library_int8_gemm"] = library_int8_gemm(torch, dev, 2 * tokens, K, 4 * T * N, reps)
     return out
+
+
+def library_int8_gemm(torch, dev, M, K, N, reps):
+    """A plain int8 x int8 -> int32 GEMM of the given shape through torch's
+    library path (hipBLASLt on ROCm): TOPS and fraction of the int8 peak."""
+    g = torch.Generator(device=dev)
+    g.manual_seed(4200 + M + N)
+    a = torch.randint(-127, 128, (M, K), dtype=torch.int8, device=dev, generator=g)
+    b = torch.randint(-127, 128, (K, N), dtype=torch.int8, device=dev, generator=g)
+    try:
+        t_w = time.time()
+        while time.time() - t_w < 0.3:
+            for _ in range(5):
+                torch._int_mm(a, b)
+            torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            torch._int_mm(a, b)
+        e1.record()
+        torch.cuda.synchronize()
+    except RuntimeError as ex:  # no int8 GEMM in this torch build
+        return {"error": str(ex)[:120]}
+    ms = e0.elapsed_time(e1) / reps
+    tops = 2 * M * K * N / (ms * 1e-3) / 1e12
+    return {"shape_MxKxN": [M, K, N], "us": round(ms * 1e3, 2), "tops": round(tops, 1),
+            "frac_int8_peak": round(tops / INT8_PEAK_TOPS, 4)}
 
 
 def cpu_baseline(f2, synth, torch, dev, layers, T, budget_s=12.0):

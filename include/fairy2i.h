@@ -553,6 +553,32 @@ fairy2i_status fairy2i_cgemm_gauss(const fairy2i_cgemm_operand* A, const fairy2i
                                    void* stream);
 
 /*
+ * The same product as fairy2i_cgemm_gauss (Sec. 3.2, remark (iii)), with
+ * the three real products run as plain GEMMs: a kernel writes each operand
+ * as three bf16 planes (Re, Im, Re + Im, rounded exactly as in
+ * fairy2i_cgemm_gauss, K padded to a multiple of 64 with zeros), one batched
+ * bf16 GEMM of the vendor library (hipBLASLt, float32 accumulation) forms
+ * P1, P2, P3, and a kernel writes C (+)= (P1 - P2) + i (P3 - P1 - P2).  The
+ * result differs from fairy2i_cgemm_gauss only in the order of the float32
+ * accumulation.  Arguments as fairy2i_cgemm_gauss, plus workspace: device
+ * memory of at least fairy2i_cgemm_gauss_planar_workspace_bytes(K, nseg,
+ * M, N) bytes, 256-byte aligned (the planes, the three float32 products and
+ * the library's own 32 MiB), caller-owned; its contents are scratch.
+ * fairy2i_cgemm_gauss_planar_workspace_bytes returns 0 for invalid sizes.
+ * The first call on a device creates the library's handle there, and the
+ * first call of a shape asks the library for its algorithm (kept for later
+ * calls of that shape); neither is allowed under stream capture.
+ * Errors: as fairy2i_cgemm_gauss; FAIRY2I_ERR_WORKSPACE for a missing or
+ * short workspace; FAIRY2I_ERR_UNSUPPORTED for M or N above 4,194,240 or no
+ * library algorithm for the shape; FAIRY2I_ERR_HIP for a library error.
+ */
+size_t fairy2i_cgemm_gauss_planar_workspace_bytes(const int64_t* K, int32_t nseg, int64_t M, int64_t N);
+fairy2i_status fairy2i_cgemm_gauss_planar(const fairy2i_cgemm_operand* A, const fairy2i_cgemm_operand* B,
+                                          const int64_t* K, int32_t nseg, int64_t M, int64_t N, float* C,
+                                          int64_t ldc, int32_t accumulate, void* workspace, size_t workspace_bytes,
+                                          void* stream);
+
+/*
  * CPU table-lookup product for int8 activations (Sec. 3.4, the paragraph on
  * lookup tables for CPU inference): every four consecutive codes of a row
  * (one byte of the canonical packed layout) index a 256-entry table of their

@@ -57,6 +57,9 @@ _SIGNATURES = {
     "fairy2i_qat_ste_workspace_bytes": (_c_size, [_c_i64, _c_i64]),
     "fairy2i_qat_ste_backward": (_c_i32, [_c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_size, _c_p]),
     "fairy2i_cgemm_gauss": (_c_i32, [_c_p, _c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_i64, _c_i32, _c_p]),
+    "fairy2i_cgemm_gauss_planar_workspace_bytes": (_c_size, [_c_p, _c_i32, _c_i64, _c_i64]),
+    "fairy2i_cgemm_gauss_planar": (_c_i32, [_c_p, _c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_i64, _c_i32, _c_p,
+                                            _c_size, _c_p]),
     "fairy2i_cpu_lut_workspace_bytes": (_c_size, [_c_i32, _c_i64, _c_i64, _c_i32]),
     "fairy2i_cpu_lut_wl_matmul": (_c_i32, [_c_p, _c_p, _c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_p, _c_i64,
                                            _c_p, _c_p, _c_p, _c_size, _c_i32]),
@@ -435,10 +438,20 @@ def _cgemm_operand(t, trans, conj, rows, K, name):
     return CgemmOperand(t.data_ptr(), t.shape[1], dt, int(trans), int(conj), 0)
 
 
-def cgemm_gauss(segments, M: int, N: int, out=None, accumulate: bool = False):
+def cgemm_gauss_planar_workspace_bytes(Ks, M: int, N: int) -> int:
+    k = (ctypes.c_int64 * 2)(*(list(Ks) + [0] * (2 - len(Ks))))
+    return int(load().fairy2i_cgemm_gauss_planar_workspace_bytes(ctypes.byref(k), len(Ks), M, N))
+
+
+def cgemm_gauss(segments, M: int, N: int, out=None, accumulate: bool = False, planar: bool = False,
+                workspace=None):
     """C [M, N] complex64 (+)= sum over segments of op(A) op(B)^T with
     Gauss's three real products.  segments: up to two tuples
-    (A, a_trans, a_conj, B, b_trans, b_conj, K); see _cgemm_operand."""
+    (A, a_trans, a_conj, B, b_trans, b_conj, K); see _cgemm_operand.
+    planar: bf16 planes and one batched library GEMM
+    (fairy2i_cgemm_gauss_planar, with a uint8 device workspace of
+    cgemm_gauss_planar_workspace_bytes, allocated here when not given);
+    else the single-kernel fairy2i_cgemm_gauss."""
     torch = _torch()
     lib = load()
     if not 1 <= len(segments) <= 2:
@@ -457,8 +470,17 @@ def cgemm_gauss(segments, M: int, N: int, out=None, accumulate: bool = False):
     _require(out, torch.complex64, "out", dev)
     if tuple(out.shape) != (M, N):
         raise ValueError(f"out must have shape ({M}, {N})")
-    _check(lib.fairy2i_cgemm_gauss(ctypes.byref(A), ctypes.byref(Bo), ctypes.byref(Ks), len(segments), M, N,
-                                   _ptr(out), N, int(accumulate), _stream_ptr(out)), "fairy2i_cgemm_gauss")
+    if not planar:
+        _check(lib.fairy2i_cgemm_gauss(ctypes.byref(A), ctypes.byref(Bo), ctypes.byref(Ks), len(segments), M, N,
+                                       _ptr(out), N, int(accumulate), _stream_ptr(out)), "fairy2i_cgemm_gauss")
+        return out
+    need = int(lib.fairy2i_cgemm_gauss_planar_workspace_bytes(ctypes.byref(Ks), len(segments), M, N))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    _require(workspace, torch.uint8, "workspace", dev)
+    _check(lib.fairy2i_cgemm_gauss_planar(ctypes.byref(A), ctypes.byref(Bo), ctypes.byref(Ks), len(segments), M, N,
+                                          _ptr(out), N, int(accumulate), _ptr(workspace),
+                                          workspace.numel(), _stream_ptr(out)), "fairy2i_cgemm_gauss_planar")
     return out
 
 

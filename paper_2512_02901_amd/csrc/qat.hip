@@ -83,11 +83,6 @@ __global__ __launch_bounds__(kQatThreads) void fq_dequant_kernel(const uint8_t* 
 //   G_Q = G - H;  d_re = sum_j Re G_Q_j b_re_j / n_re,  d_im likewise;
 //   H  += (s_re Re G_Q + b_re d_re) + i (s_im Im G_Q + b_im d_im).
 
-__global__ __launch_bounds__(256) void ste_zero_kernel(float* __restrict__ p, int64_t n) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = 0.0f;
-}
-
 struct StePart {
   double sum[2];
   unsigned long long n[2];
@@ -115,26 +110,80 @@ __device__ inline unsigned long long block_sum_u64(unsigned long long v, unsigne
   return s;
 }
 
+// Each thread takes units of 16 entries: 4 code bytes (entry e is code
+// (byte[e / 4] >> 2 (e % 4)) & 3) and 128 bytes of G and of H, as 16-byte
+// loads when G and H are 16-byte aligned (VEC) and the unit is whole; a last,
+// partial unit goes one entry at a time.  FIRST: the first stage of the
+// reverse recursion, where H is still zero (not read, only written).
+template <bool VEC>
+__device__ inline int ste_unit(const uint8_t* __restrict__ codes_t, const float2* __restrict__ p, int64_t u,
+                               int64_t nelem, uint32_t& c, float2 (&v)[16]) {
+  const int64_t e0 = 16 * u;
+  const int n = nelem - e0 < 16 ? (int)(nelem - e0) : 16;
+  c = 0u;
+  for (int b = 0; b < (n + 3) / 4; ++b) c |= (uint32_t)codes_t[4 * u + b] << (8 * b);
+  if (VEC && n == 16) {
+    const float4* q = reinterpret_cast<const float4*>(p + e0);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float4 f = q[i];
+      v[2 * i] = make_float2(f.x, f.y);
+      v[2 * i + 1] = make_float2(f.z, f.w);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v[i] = i < n ? p[e0 + i] : make_float2(0.0f, 0.0f);
+  }
+  return n;
+}
+
+template <bool VEC>
+__device__ inline void ste_h16(const float2* __restrict__ p, int64_t u, int n, float2 (&v)[16]) {
+  const int64_t e0 = 16 * u;
+  if (VEC && n == 16) {
+    const float4* q = reinterpret_cast<const float4*>(p + e0);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float4 f = q[i];
+      v[2 * i] = make_float2(f.x, f.y);
+      v[2 * i + 1] = make_float2(f.z, f.w);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v[i] = i < n ? p[e0 + i] : make_float2(0.0f, 0.0f);
+  }
+}
+
+template <bool VEC, bool FIRST>
 __global__ __launch_bounds__(kQatThreads) void ste_reduce_kernel(const uint8_t* __restrict__ codes_t,
                                                                  const float2* __restrict__ G,
-                                                                 const float2* __restrict__ H, int64_t nbytes,
+                                                                 const float2* __restrict__ H, int64_t nelem,
                                                                  StePart* __restrict__ part) {
   __shared__ double shd[kQatThreads / 64];
   __shared__ unsigned long long shn[kQatThreads / 64];
   double s_re = 0.0, s_im = 0.0;
   unsigned long long n_re = 0, n_im = 0;
+  const int64_t nunits = (nelem + 15) / 16;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t bi = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; bi < nbytes; bi += stride) {
-    const uint32_t c = codes_t[bi];
+  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < nunits; u += stride) {
+    uint32_t c;
+    float2 g[16], h[16];
+    const int n = ste_unit<VEC>(codes_t, G, u, nelem, c, g);
+    if constexpr (!FIRST) ste_h16<VEC>(H, u, n, h);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
+    for (int e = 0; e < 16; ++e) {
+      if (e >= n) break;
       const uint32_t k = (c >> (2 * e)) & 3u;
-      const float2 g = G[4 * bi + e], h = H[4 * bi + e];
-      const double gq_re = (double)g.x - (double)h.x, gq_im = (double)g.y - (double)h.y;
-      if (k == 0u) { s_re += gq_re; ++n_re; }
-      else if (k == 2u) { s_re -= gq_re; ++n_re; }
-      else if (k == 1u) { s_im += gq_im; ++n_im; }
-      else { s_im -= gq_im; ++n_im; }
+      const double gq_re = FIRST ? (double)g[e].x : (double)g[e].x - (double)h[e].x;
+      const double gq_im = FIRST ? (double)g[e].y : (double)g[e].y - (double)h[e].y;
+      const double sg = (k & 2u) ? -1.0 : 1.0;  // codes 2, 3 are -1, -i
+      if (k & 1u) {
+        s_im += sg * gq_im;
+        ++n_im;
+      } else {
+        s_re += sg * gq_re;
+        ++n_re;
+      }
     }
   }
   const double a = block_sum_double(s_re, shd);
@@ -149,40 +198,61 @@ __global__ __launch_bounds__(kQatThreads) void ste_reduce_kernel(const uint8_t* 
   }
 }
 
-// d[axis] = (sum of the blocks' partial sums, in block order) / n
-__global__ __launch_bounds__(64) void ste_finalize_kernel(const StePart* __restrict__ part, int nblk,
-                                                          double* __restrict__ d) {
-  if (threadIdx.x < 2) {
-    double s = 0.0;
-    unsigned long long n = 0;
-    for (int i = 0; i < nblk; ++i) {
-      s += part[i].sum[threadIdx.x];
-      n += part[i].n[threadIdx.x];
-    }
-    d[threadIdx.x] = n ? s / (double)n : 0.0;
-  }
-}
-
+template <bool VEC, bool FIRST>
 __global__ __launch_bounds__(kQatThreads) void ste_update_kernel(const uint8_t* __restrict__ codes_t,
                                                                  const float* __restrict__ scales_t,
                                                                  const float2* __restrict__ G,
-                                                                 float2* __restrict__ H, int64_t nbytes,
-                                                                 const double* __restrict__ d) {
+                                                                 float2* __restrict__ H, int64_t nelem,
+                                                                 const StePart* __restrict__ part, int nblk) {
+  // d[axis] = (sum of the reduction blocks' partial sums) / n, formed by every
+  // block alike: thread i sums partials i, i + 256, ... in order, then the
+  // block's fixed-order tree, so every block (and every run) gets the same d
+  __shared__ double shd[kQatThreads / 64];
+  __shared__ unsigned long long shn[kQatThreads / 64];
+  double a = 0.0, b = 0.0;
+  unsigned long long na = 0, nb = 0;
+  for (int i = threadIdx.x; i < nblk; i += blockDim.x) {
+    a += part[i].sum[0];
+    b += part[i].sum[1];
+    na += part[i].n[0];
+    nb += part[i].n[1];
+  }
+  a = block_sum_double(a, shd);
+  b = block_sum_double(b, shd);
+  na = block_sum_u64(na, shn);
+  nb = block_sum_u64(nb, shn);
   const double s_re = (double)scales_t[0], s_im = (double)scales_t[1];
-  const double d_re = d[0], d_im = d[1];
+  const double d_re = na ? a / (double)na : 0.0, d_im = nb ? b / (double)nb : 0.0;
+  const int64_t nunits = (nelem + 15) / 16;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t bi = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; bi < nbytes; bi += stride) {
-    const uint32_t c = codes_t[bi];
+  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < nunits; u += stride) {
+    uint32_t c;
+    float2 g[16], h[16];
+    const int n = ste_unit<VEC>(codes_t, G, u, nelem, c, g);
+    if constexpr (FIRST) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
+      for (int e = 0; e < 16; ++e) h[e] = make_float2(0.0f, 0.0f);
+    } else {
+      ste_h16<VEC>(H, u, n, h);
+    }
+    float2 o[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
       const uint32_t k = (c >> (2 * e)) & 3u;
-      const float2 g = G[4 * bi + e], h = H[4 * bi + e];
-      const double gq_re = (double)g.x - (double)h.x, gq_im = (double)g.y - (double)h.y;
-      const double b_re = k == 0u ? 1.0 : (k == 2u ? -1.0 : 0.0);
-      const double b_im = k == 1u ? 1.0 : (k == 3u ? -1.0 : 0.0);
-      const double nr = (double)h.x + (s_re * gq_re + b_re * d_re);
-      const double ni = (double)h.y + (s_im * gq_im + b_im * d_im);
-      H[4 * bi + e] = make_float2((float)nr, (float)ni);
+      const double gq_re = (double)g[e].x - (double)h[e].x, gq_im = (double)g[e].y - (double)h[e].y;
+      const double sg = (k & 2u) ? -1.0 : 1.0;
+      const double b_re = (k & 1u) ? 0.0 : sg;
+      const double b_im = (k & 1u) ? sg : 0.0;
+      const double nr = (double)h[e].x + (s_re * gq_re + b_re * d_re);
+      const double ni = (double)h[e].y + (s_im * gq_im + b_im * d_im);
+      o[e] = make_float2((float)nr, (float)ni);
+    }
+    if (VEC && n == 16) {
+      float4* q = reinterpret_cast<float4*>(H + 16 * u);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) q[i] = make_float4(o[2 * i].x, o[2 * i].y, o[2 * i + 1].x, o[2 * i + 1].y);
+    } else {
+      for (int e = 0; e < n; ++e) H[16 * u + e] = o[e];
     }
   }
 }
@@ -407,7 +477,7 @@ fairy2i_status fairy2i_qat_fake_quant(const float* M, int64_t N, int64_t K, int3
 
 size_t fairy2i_qat_ste_workspace_bytes(int64_t N, int64_t K) {
   if (N <= 0 || K <= 0 || (K % 4) != 0) return 0;
-  return (size_t)qat_blocks(N * K / 4) * sizeof(StePart) + 2 * sizeof(double);
+  return (size_t)qat_blocks((N * K + 15) / 16) * sizeof(StePart);
 }
 
 fairy2i_status fairy2i_qat_ste_backward(const uint8_t* codes, const float* scales, int32_t T, int64_t N, int64_t K,
@@ -418,21 +488,23 @@ fairy2i_status fairy2i_qat_ste_backward(const uint8_t* codes, const float* scale
   if (T < 1 || T > FAIRY2I_MAX_STAGES) return FAIRY2I_ERR_STAGES;
   if (!workspace || workspace_bytes < fairy2i_qat_ste_workspace_bytes(N, K)) return FAIRY2I_ERR_WORKSPACE;
   const hipStream_t s = qat_stream(stream);
-  const int64_t nbytes = N * K / 4;
-  const int nblk = qat_blocks(nbytes);
+  const int64_t nelem = N * K, nbytes = nelem / 4;
+  const int nblk = qat_blocks((nelem + 15) / 16);
   auto* part = static_cast<StePart*>(workspace);
-  auto* d = reinterpret_cast<double*>(part + nblk);
   const auto* G = reinterpret_cast<const float2*>(g_hat);
   auto* H = reinterpret_cast<float2*>(g_master);
-  hipLaunchKernelGGL(ste_zero_kernel, dim3(nblk), dim3(256), 0, s, g_master, 2 * N * K);
-  hipError_t e = hipGetLastError();
+  const bool vec = ((reinterpret_cast<uintptr_t>(g_hat) | reinterpret_cast<uintptr_t>(g_master)) & 15) == 0;
+  hipError_t e = hipSuccess;
   for (int t = T - 1; t >= 0 && e == hipSuccess; --t) {
     const uint8_t* ct = codes + (int64_t)t * nbytes;
-    hipLaunchKernelGGL(ste_reduce_kernel, dim3(nblk), dim3(kQatThreads), 0, s, ct, G, H, nbytes, part);
+    const bool first = t == T - 1;  // H is still zero: not read, only written
+    auto reduce = vec ? (first ? ste_reduce_kernel<true, true> : ste_reduce_kernel<true, false>)
+                      : (first ? ste_reduce_kernel<false, true> : ste_reduce_kernel<false, false>);
+    auto update = vec ? (first ? ste_update_kernel<true, true> : ste_update_kernel<true, false>)
+                      : (first ? ste_update_kernel<false, true> : ste_update_kernel<false, false>);
+    hipLaunchKernelGGL(reduce, dim3(nblk), dim3(kQatThreads), 0, s, ct, G, H, nelem, part);
     if ((e = hipGetLastError()) != hipSuccess) break;
-    hipLaunchKernelGGL(ste_finalize_kernel, dim3(1), dim3(64), 0, s, part, nblk, d);
-    if ((e = hipGetLastError()) != hipSuccess) break;
-    hipLaunchKernelGGL(ste_update_kernel, dim3(nblk), dim3(kQatThreads), 0, s, ct, scales + 2 * t, G, H, nbytes, d);
+    hipLaunchKernelGGL(update, dim3(nblk), dim3(kQatThreads), 0, s, ct, scales + 2 * t, G, H, nelem, part, nblk);
     e = hipGetLastError();
   }
   return qat_status(e);

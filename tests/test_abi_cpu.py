@@ -236,3 +236,54 @@ def test_group_call_validation(lib):
     ev = (ctypes.c_void_p * 4)(0x1000, 0x1000, None, 0x1000)
     assert lib.fairy2i_wl_matmul_group_timed(ctypes.byref(buf), P, None, ev) == binding.ERR_NULL
     assert lib.fairy2i_wl_matmul_group_timed(ctypes.byref(buf), P, None, None) == binding.ERR_NULL
+
+
+def test_cgemm_validation(lib):
+    """Both complex GEMM entry points reject bad operands, sizes and
+    workspaces before any GPU work; the planar workspace covers the three
+    bf16 planes of each operand (K padded to 64), the three float32 products
+    and the library's 32 MiB."""
+    op = binding.CgemmOperand
+    M, N, K = 70, 90, 100
+
+    def ops(a=None, b=None):
+        A = (op * 2)(op(P, K, binding.ACT_F32, 0, 0, 0), op(P, K, binding.ACT_F32, 0, 0, 0))
+        B = (op * 2)(op(P, K, binding.ACT_BF16, 0, 1, 0), op(P, K, binding.ACT_BF16, 0, 1, 0))
+        if a is not None:
+            A[0] = a
+        if b is not None:
+            B[0] = b
+        return A, B
+
+    Ks = (ctypes.c_int64 * 2)(K, 36)
+    for planar in (False, True):
+        def call(A, B, nseg=1, m=M, n=N, C=P, ldc=N, acc=0, ws=P, wsb=1 << 40):
+            if planar:
+                return lib.fairy2i_cgemm_gauss_planar(ctypes.byref(A), ctypes.byref(B), ctypes.byref(Ks), nseg, m, n,
+                                                      C, ldc, acc, ws, wsb, None)
+            return lib.fairy2i_cgemm_gauss(ctypes.byref(A), ctypes.byref(B), ctypes.byref(Ks), nseg, m, n, C, ldc,
+                                           acc, None)
+        assert call(*ops(), C=None) == binding.ERR_NULL
+        assert call(*ops(a=op(None, K, binding.ACT_F32, 0, 0, 0))) == binding.ERR_NULL
+        assert call(*ops(), nseg=0) == binding.ERR_SHAPE
+        assert call(*ops(), nseg=3) == binding.ERR_SHAPE
+        assert call(*ops(), m=0) == binding.ERR_SHAPE
+        assert call(*ops(), ldc=N - 1) == binding.ERR_SHAPE
+        assert call(*ops(), acc=2) == binding.ERR_SHAPE
+        assert call(*ops(a=op(P, K - 1, binding.ACT_F32, 0, 0, 0))) == binding.ERR_SHAPE    # ld < K
+        assert call(*ops(a=op(P, M - 1, binding.ACT_F32, 1, 0, 0))) == binding.ERR_SHAPE    # ld < rows
+        assert call(*ops(b=op(P, K, 7, 0, 0, 0))) == binding.ERR_SHAPE                      # dtype
+        assert call(*ops(b=op(P, K, binding.ACT_F32, 0, 2, 0))) == binding.ERR_SHAPE        # conj flag
+        assert call(*ops(b=op(P, K, binding.ACT_F32, 0, 0, 1))) == binding.ERR_SHAPE        # reserved
+        if planar:
+            assert call(*ops(), ws=None) == binding.ERR_WORKSPACE
+            need = lib.fairy2i_cgemm_gauss_planar_workspace_bytes(ctypes.byref(Ks), 1, M, N)
+            assert call(*ops(), wsb=need - 1) == binding.ERR_WORKSPACE
+    wsb = lib.fairy2i_cgemm_gauss_planar_workspace_bytes
+    a256 = lambda b: (b + 255) // 256 * 256
+    Kp = 192   # 100 + 36 padded to 64
+    assert wsb(ctypes.byref(Ks), 2, M, N) == (a256(3 * M * Kp * 2) + a256(3 * N * Kp * 2) + a256(3 * M * N * 4)
+                                              + (32 << 20))
+    assert wsb(ctypes.byref(Ks), 0, M, N) == 0
+    assert wsb(ctypes.byref(Ks), 1, 0, N) == 0
+    assert wsb(ctypes.byref((ctypes.c_int64 * 2)(0, 5)), 1, M, N) == 0

@@ -6,7 +6,8 @@ Bars:
   output bit-exact against a single rounding of the float64 value);
 * straight-through backward: relative L2 <= 1e-6 (the GPU keeps the running
   gradient in float32 between stages);
-* Gauss GEMM: exact for small-integer operands (every product and sum is an
+* Gauss GEMM (the single kernel and the planar path through the vendor
+  library, which round the operands alike): exact for small-integer operands (every product and sum is an
   integer below 2^24, so any wrong index, sign or lane shows); otherwise,
   element by element, within the bound of its roundings: the operands and
   the two sums Ar + Ai, Br + Bi rounded to bf16 (2^-9 each) and float32
@@ -108,6 +109,13 @@ def test_ste_backward_matches_oracle(gpu, N, K, T):
     assert rel_l2(host(got), want) <= 1e-6
     # repeat: bitwise equal (fixed-order reductions)
     np.testing.assert_array_equal(host(f2.qat_ste_backward(c, s, dev(G, gpu))), host(got))
+    # g_hat 8 bytes off 16-byte alignment: the one-value-at-a-time loads, same sums in the same order
+    import torch
+    buf = torch.empty(N * K + 1, dtype=torch.complex64, device=gpu)
+    buf[1:] = dev(G, gpu).reshape(-1)
+    g_off = buf[1:].view(N, K)
+    assert g_off.data_ptr() % 16 == 8
+    np.testing.assert_array_equal(host(f2.qat_ste_backward(c, s, g_off)), host(got))
 
 
 # ------------------------------------------------------------- Gauss GEMM ---
@@ -140,7 +148,8 @@ def logical(z, dtype, conj):
 
 @pytest.mark.parametrize("M,N,K", [(64, 64, 32), (100, 37, 70), (5, 130, 257), (256, 192, 1024)])
 @pytest.mark.parametrize("layout", [(0, 0), (1, 0), (0, 1), (1, 1)])
-def test_gauss_gemm_integers_exact(gpu, M, N, K, layout):
+@pytest.mark.parametrize("planar", [False, True])
+def test_gauss_gemm_integers_exact(gpu, M, N, K, layout, planar):
     """Small integers: every bf16 value, product and sum is exact, so the
     kernel must reproduce the complex product bit for bit."""
     import paper_2512_02901_amd as f2
@@ -150,20 +159,21 @@ def test_gauss_gemm_integers_exact(gpu, M, N, K, layout):
     for dt in (f2.ACT_BF16, f2.ACT_F32):
         for conj in ((0, 0), (1, 0), (0, 1)):
             C = f2.cgemm_gauss([(operand(A, dt, layout[0], gpu), layout[0], conj[0],
-                                 operand(B, dt, layout[1], gpu), layout[1], conj[1], K)], M, N)
+                                 operand(B, dt, layout[1], gpu), layout[1], conj[1], K)], M, N, planar=planar)
             want = (np.conj(A) if conj[0] else A) @ (np.conj(B) if conj[1] else B).T
             np.testing.assert_array_equal(host(C), want.astype(np.complex64))
 
 
 @pytest.mark.parametrize("M,N,K", [(64, 64, 64), (200, 130, 300), (512, 256, 2048)])
-def test_gauss_gemm_within_rounding_bound(gpu, M, N, K):
+@pytest.mark.parametrize("planar", [False, True])
+def test_gauss_gemm_within_rounding_bound(gpu, M, N, K, planar):
     import paper_2512_02901_amd as f2
     rng = np.random.default_rng(M + N + K)
     A, B = cplx(rng, M, K), cplx(rng, N, K)
     for dt in (f2.ACT_BF16, f2.ACT_F32):
         for lay in ((0, 0), (1, 1)):
             C = host(f2.cgemm_gauss([(operand(A, dt, lay[0], gpu), lay[0], 1, operand(B, dt, lay[1], gpu), lay[1], 0,
-                                      K)], M, N))
+                                      K)], M, N, planar=planar))
             a, b = logical(A, dt, 1), logical(B, dt, 0)
             want = a @ b.T
             br, bi = gemm_bound(a, b)
@@ -172,7 +182,8 @@ def test_gauss_gemm_within_rounding_bound(gpu, M, N, K):
             assert rel_l2(C, want) <= 1e-2
 
 
-def test_gauss_gemm_two_segments_and_accumulate(gpu):
+@pytest.mark.parametrize("planar", [False, True])
+def test_gauss_gemm_two_segments_and_accumulate(gpu, planar):
     import paper_2512_02901_amd as f2
     rng = np.random.default_rng(3)
     M, N, K0, K1 = 70, 90, 100, 36
@@ -181,7 +192,7 @@ def test_gauss_gemm_two_segments_and_accumulate(gpu):
     out = dev(C0.astype(np.complex64), gpu)
     f2.cgemm_gauss([(operand(A0, f2.ACT_BF16, 0, gpu), 0, 0, operand(B0, f2.ACT_BF16, 0, gpu), 0, 0, K0),
                     (operand(A1, f2.ACT_BF16, 1, gpu), 1, 1, operand(B1, f2.ACT_F32, 0, gpu), 0, 1, K1)],
-                   M, N, out=out, accumulate=True)
+                   M, N, out=out, accumulate=True, planar=planar)
     a0, b0 = logical(A0, f2.ACT_BF16, 0), logical(B0, f2.ACT_BF16, 0)
     a1, b1 = logical(A1, f2.ACT_BF16, 1), logical(B1, f2.ACT_F32, 1)
     want = C0.astype(np.complex64).astype(np.complex128) + a0 @ b0.T + a1 @ b1.T
@@ -192,7 +203,8 @@ def test_gauss_gemm_two_segments_and_accumulate(gpu):
     assert np.all(np.abs(got.imag - want.imag) <= i0 + i1 + 1e-6)
 
 
-def test_qat_layer_step_matches_oracle(gpu):
+@pytest.mark.parametrize("planar", [False, True])
+def test_qat_layer_step_matches_oracle(gpu, planar):
     """One training step of a widely-linear layer on the GPU: fake-quant
     forward of both masters, Y = X U^T + conj(X) W^T, then from G_Y the
     input gradient and the two weight gradients (one Gauss GEMM each) and
@@ -212,9 +224,9 @@ def test_qat_layer_step_matches_oracle(gpu):
     Wh, cw, sw = f2.qat_fake_quant(dW, T)
     Xb = to_bf16_pairs(X, gpu)
     GYb = to_bf16_pairs(GY, gpu)
-    Y = f2.cgemm_gauss([(Xb, 0, 0, Uh, 0, 0, K), (Xb, 0, 1, Wh, 0, 0, K)], Bt, N)
-    GX = f2.cgemm_gauss([(GYb, 0, 0, Uh, 1, 1, N), (GYb, 0, 1, Wh, 1, 0, N)], Bt, K)
-    GUW = [f2.cgemm_gauss([(GYb, 1, 0, Xb, 1, c, Bt)], N, K) for c in (1, 0)]
+    Y = f2.cgemm_gauss([(Xb, 0, 0, Uh, 0, 0, K), (Xb, 0, 1, Wh, 0, 0, K)], Bt, N, planar=planar)
+    GX = f2.cgemm_gauss([(GYb, 0, 0, Uh, 1, 1, N), (GYb, 0, 1, Wh, 1, 0, N)], Bt, K, planar=planar)
+    GUW = [f2.cgemm_gauss([(GYb, 1, 0, Xb, 1, c, Bt)], N, K, planar=planar) for c in (1, 0)]
     gU = f2.qat_ste_backward(cu, su, GUW[0])
     gW = f2.qat_ste_backward(cw, sw, GUW[1])
     torch.cuda.synchronize()
