@@ -647,6 +647,10 @@ def main():
                          "the JSON line then says so in `data`)")
     ap.add_argument("--prefill-only", action="store_true",
                     help="only run the two 2048-token prefill GEMMs (for hardware-counter runs)")
+    ap.add_argument("--qat-only", action="store_true",
+                    help="only run the QAT training-step leg (for profiler runs)")
+    ap.add_argument("--grouped-only", action="store_true",
+                    help="only run the per-group-scale stack leg, G = 256 (for profiler runs)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run 5 plain 256 MiB device copies (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -672,6 +676,13 @@ def main():
     f2.load()
     if args.prefill_only:
         print(json.dumps({"prefill": prefill_bench(f2, synth, torch, dev)}), flush=True)
+        return
+    if args.qat_only:
+        print(json.dumps({"qat_step": qat_bench(f2, synth, torch, dev)}), flush=True)
+        return
+    if args.grouped_only:
+        print(json.dumps({"stack_group256": grouped_stack_bench(f2, synth, torch, dev, 2, 256, args.steps,
+                                                                args.warmup)}), flush=True)
         return
     T = 2
     t0 = time.time()
