@@ -285,19 +285,20 @@ typedef struct fairy2i_wl_layer {
  * FAIRY2I_ACT_BF16 and B <= 16 (B <= 8 for T = 3, B <= 4 for T = 4); the
  * product then runs on the
  * fp8 x fp4 matrix cores.  Each token is scaled by a power of two 2^S so that
- * its largest magnitude m lies in [2^7, 2^8).  For B <= 2 a scaled value v is
- * split by magnitude into two bands (|v| >= 1, and |v| < 1 taken times 2^8),
+ * its largest magnitude m lies in [2^7, 2^8).  For B <= 4 (B <= 2 when T = 4)
+ * a scaled value v is split by magnitude into two bands (|v| >= 1, and |v| < 1 taken times 2^8),
  * and each band value u is written as two e4m3 digits, hi = e4m3(u) and
  * lo = e4m3((u - hi) * 2^5) (round to nearest even), u = hi + 2^-5 lo.  Every
  * value down to 2^-22 m is represented exactly, smaller ones to within
  * 2^-30 m.  The digit products are exact and are summed in float32 on the
  * matrix cores; y matches the exact product of the bf16 inputs to float32
- * rounding (relative L2 about 1e-7).  For 3 <= B <= 16 each value gets one
+ * rounding (relative L2 about 1e-7, also for tokens with 3000-sigma
+ * channels).  For 5 <= B <= 16 (3 <= B <= 4 when T = 4) each value gets one
  * (hi, lo) pair (four tokens per 16-column tile): still exact per value, but
  * the matrix core's narrow adder may drop the low bits of a small product
  * next to one near m in the same group of products, at most about 2^-13 of
- * the larger; relative L2 about 4e-6 for N(0,1) tokens and up to 1.5e-4
- * with a 300-sigma channel, inside the 1e-3 bar for bf16 activations.
+ * the larger; relative L2 about 3e-6 for N(0,1) tokens and up to 1.8e-4
+ * with a 3000-sigma channel, inside the 1e-3 bar for bf16 activations.
  * Per-group scales (group_size G > 0) are supported on this fp4 path only,
  * for every layer of the group or for none (G may differ between layers).
  * The products of each 256-code step then start from zero and are folded,

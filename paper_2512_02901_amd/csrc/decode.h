@@ -81,7 +81,8 @@ constexpr size_t kGroupCallBytes = 256;
 // claimed at run time, where the shortest groups sit).
 constexpr double kCoopStaticFrac = 0.65;
 
-int dec_ntile(int mode, int64_t B);
+int dec_f4_bands(int T, int64_t B);
+int dec_ntile(int mode, int64_t B, int T);
 int dec_ncols(int mode, int64_t B);
 // Tiles of 16 activation columns processed per pass of the register kernel.
 int dec_tiles_per_group(int T, int ntile);

@@ -681,15 +681,21 @@ namespace {
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 }  // namespace
 
-int dec_ntile(int mode, int64_t B) {
+// fp4 path: two digit bands per value (8 columns per token, two tokens per
+// tile; exact for any bf16 token) while the tokens fit the two-tile kernels
+// that exist for T (up to 2 tokens, and up to 4 for T <= 3), else one band
+// (4 columns per token, four tokens per tile).
+int dec_f4_bands(int T, int64_t B) { return (B <= 2 || (B <= 4 && T <= 3)) ? 2 : 1; }
+
+int dec_ntile(int mode, int64_t B, int T) {
   if (mode == kModeI8) return (int)((B + 7) / 8);
-  if (mode == kModeBf16F4) return B <= 2 ? 1 : (int)((B + 3) / 4);  // two bands up to 2 tokens, then one
+  if (mode == kModeBf16F4) return dec_f4_bands(T, B) == 2 ? (int)((B + 1) / 2) : (int)((B + 3) / 4);
   return (int)((B + 1) / 2);
 }
 
 int dec_ncols(int mode, int64_t B) {
   if (mode == kModeBf16) return B >= 2 ? 14 : 6;  // per token 6 digit columns, 8-column stride
-  if (mode == kModeBf16F4) return B == 1 ? 8 : 16;  // 8 digit columns per token (B <= 2), 4 (B >= 3)
+  if (mode == kModeBf16F4) return B == 1 ? 8 : 16;  // 8 columns per two-band token, 4 per one-band token
   return B >= 8 ? 16 : (int)(2 * B);
 }
 
@@ -698,9 +704,9 @@ DecHeader dec_header(int T, int mode, int64_t B, bool export_acc) {
   h.T = T;
   h.mode = mode;
   h.B = (int32_t)B;
-  h.ntile = dec_ntile(mode, B);
+  h.ntile = dec_ntile(mode, B, T);
   h.nc = dec_ncols(mode, B);
-  h.bands = (mode == kModeBf16F4 && B <= 2) ? 2 : 1;
+  h.bands = mode == kModeBf16F4 ? dec_f4_bands(T, B) : 1;
   // the fp4 path always runs its streaming kernel (one or two tiles)
   h.kernel = (!export_acc && (h.ntile == 1 || mode == kModeBf16F4)) ? kKernelStream : kKernelReg;
   return h;

@@ -754,7 +754,8 @@ void launch_stream_f4_g(const DecHeader& h, const DecLayer& inl, const DecLayer*
   }
   if constexpr (T <= 3) {
     if (h.ntile >= 2) {
-      launch_stream_f4<T, 4, 2, GS, 1>(h, inl, tab, s);
+      if (h.bands == 2) launch_stream_f4<T, 4, 2, GS, 2>(h, inl, tab, s);
+      else launch_stream_f4<T, 4, 2, GS, 1>(h, inl, tab, s);
       return;
     }
   }
@@ -779,7 +780,8 @@ void launch_stream_f4_t(const DecHeader& h, const DecLayer& inl, const DecLayer*
       return;
     }
     if (tab && h.coop && h.ntile == 2) {
-      launch_coop_f4<T, 2, 16, 1>(h, tab, s);
+      if (h.bands == 2) launch_coop_f4<T, 2, 16, 2>(h, tab, s);
+      else launch_coop_f4<T, 2, 16, 1>(h, tab, s);
       return;
     }
     if (tab && h.coop && kCoopSmallB) {
