@@ -16,14 +16,12 @@ constexpr int kCoopSlots = 4;     // steps in the cooperative kernel's ring
 // Cooperative fp4 kernel geometry by its activation tiles per call (NT = 1,
 // 2 or 4; three tiles run as four): waves per block (four for one tile, three
 // blocks per CU; eight for more, one block per CU, so that more row blocks
-// share each step's activation operand), tiles per wave (with four tiles two
-// waves share a row block, two tiles each) and row blocks per group.
+// share each step's activation operand), waves per row block (with four tiles
+// two: one for the U planes, one for the W planes) and row blocks per group.
 constexpr int coop_nt(int ntile) { return ntile >= 3 ? 4 : ntile; }
 constexpr int coop_waves(int nt) { return nt >= 2 ? 8 : 4; }
-constexpr int coop_tiles_per_wave(int nt) { return nt >= 4 ? 2 : nt; }
-constexpr int coop_row_blocks(int ntile) {
-  return coop_waves(coop_nt(ntile)) / (coop_nt(ntile) / coop_tiles_per_wave(coop_nt(ntile)));
-}
+constexpr int coop_plane_split(int nt) { return nt >= 4 ? 2 : 1; }
+constexpr int coop_row_blocks(int ntile) { return coop_waves(coop_nt(ntile)) / coop_plane_split(coop_nt(ntile)); }
 constexpr int kKernelReg = 0;     // codes staged in registers; any batch, accumulator export
 constexpr int kKernelStream = 1;  // codes streamed through an LDS ring; one activation tile
 constexpr int kRegKc4 = 2;        // 256-code steps per work item of the register kernel

@@ -320,6 +320,47 @@ __device__ inline void write_outputs_f4(const DecLayer& L, const DecHeader& h, i
     buf_store8(L.part, (uint32_t)L.nkc * h.B * L.N * 8, (uint32_t)(((kc * h.B + b) * L.N + row) * 8), v);
 }
 
+// Split planes (one-band tiles): the half of write_outputs_f4's sum that
+// matrix m (0: U with x, 1: W with conj(x)) contributes, stages in order,
+// without the token factor.
+template <int T>
+__device__ inline float2 partial_outputs_f4(int m, const v4f (&aS)[T], const v4f (&aI)[T], const float (&sc)[2][T][2]) {
+  float yr = 0.0f, yi = 0.0f;
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    float vS[2], vI[2];
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      vS[c] = fmaf(aS[t][2 + c], 1.0f / kLoScale, aS[t][c]);
+      vI[c] = fmaf(aI[t][2 + c], 1.0f / kLoScale, aI[t][c]);
+    }
+    const float pre0 = vS[0] - vI[0], pre1 = vS[1] - vI[1];
+    const float s_re = m == 0 ? sc[0][t][0] : sc[1][t][0], s_im = m == 0 ? sc[0][t][1] : sc[1][t][1];
+    if (m == 0) {
+      yr = fmaf(s_re, pre0, yr);
+      yr = fmaf(-s_im, vI[1], yr);
+      yi = fmaf(s_re, pre1, yi);
+      yi = fmaf(s_im, vI[0], yi);
+    } else {
+      yr = fmaf(s_re, pre0, yr);
+      yr = fmaf(s_im, vI[1], yr);
+      yi = fmaf(-s_re, pre1, yi);
+      yi = fmaf(s_im, vI[0], yi);
+    }
+  }
+  return make_float2(yr, yi);
+}
+
+// y of token slot g (lane group) of a one-band tile: (yr, yi) times the token factor.
+__device__ inline void store_outputs_f4(const DecLayer& L, const DecHeader& h, int row, bool row_ok, int lane,
+                                        int tile, float yr, float yi, const float (&xf)[4]) {
+  const int g = lane >> 4;
+  const int b = 4 * tile + g;
+  if (!row_ok || b >= h.B) return;
+  const float f = pick_factor<4>(xf, g);
+  buf_store8(L.y, (uint32_t)h.B * L.N * 8, (uint32_t)((b * L.N + row) * 8), make_float2(__fmul_rn(yr, f), __fmul_rn(yi, f)));
+}
+
 // ------------------------------------------------ per-group axis scales ---
 // With per-group scales (a pair (s_re, s_im) per stage, row and group of
 // 256 gsteps consecutive codes; scales [T][N][groups][2]) the MFMAs of a
@@ -948,6 +989,20 @@ __device__ inline void coop_read_x(const uint32_t (&a)[2][TS][2], v4i (&x)[2][TS
   }
 }
 
+// Four tiles: one 128-code half's eight reads and their wait (the halves one
+// after the other, so that only one half's operands are live).
+__device__ inline void coop_read_x4(const uint32_t (&a)[4][2], v4i (&x)[4][2]) {
+  __asm__ volatile(
+      "ds_read_b128 %0, %8\n\tds_read_b128 %1, %9\n\tds_read_b128 %2, %10\n\tds_read_b128 %3, %11\n\t"
+      "ds_read_b128 %4, %12\n\tds_read_b128 %5, %13\n\tds_read_b128 %6, %14\n\tds_read_b128 %7, %15\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(x[0][0]), "=&v"(x[0][1]), "=&v"(x[1][0]), "=&v"(x[1][1]), "=&v"(x[2][0]), "=&v"(x[2][1]),
+        "=&v"(x[3][0]), "=&v"(x[3][1])
+      : "v"(a[0][0]), "v"(a[0][1]), "v"(a[1][0]), "v"(a[1][1]), "v"(a[2][0]), "v"(a[2][1]), "v"(a[3][0]),
+        "v"(a[3][1])
+      : "memory");
+}
+
 template <int TS>
 __device__ inline void coop_wait_x(v4i (&x)[2][TS][2]) {
   if constexpr (TS == 1) {
@@ -960,19 +1015,24 @@ __device__ inline void coop_wait_x(v4i (&x)[2][TS][2]) {
   }
 }
 
-// TS activation tiles per wave: with NT = 4 two waves share a row block,
-// two tiles each, so a wave's accumulators stay at 64 registers; two blocks
-// per CU (eight waves, at most 256 registers per lane).
+// Every wave multiplies all NT activation tiles.  PS waves share a row
+// block, each taking P / PS of its code planes: with four tiles (PS = 2) one
+// wave takes the U planes and one the W planes, so a wave's accumulators
+// stay at 64 registers and each code byte is still loaded and expanded once;
+// the two halves of y meet in LDS at the end of a group.
 // NC columns per tile (8: one two-band token; 16), BANDS digit bands per token.
-template <int T, int NT, int TS, int NC, int BANDS>
+template <int T, int NT, int PS, int NC, int BANDS>
 __global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) void dec_coop_f4_kernel(DecHeader h,
                                                                       const DecLayer* __restrict__ tab) {
 #if defined(__HIP_DEVICE_COMPILE__)  // LDS-DMA and buffer-descriptor code: device pass only
   constexpr int P = 2 * T;
+  constexpr int TS = NT;                // tiles per wave
+  constexpr int PW = P / PS;            // code planes per wave
   constexpr int W = coop_waves(NT);
-  constexpr int SH = NT / TS;           // waves sharing a row block
-  constexpr int RBG = W / SH;           // row blocks per group
-  static_assert(NT % TS == 0 && W % SH == 0, "tiles split evenly over the waves of a row block");
+  constexpr int RBG = W / PS;           // row blocks per group
+  static_assert(P % PS == 0 && W % PS == 0, "planes split evenly over the waves of a row block");
+  static_assert(PS == 1 || (PS == 2 && BANDS == 1), "split planes: one-band tiles only");
+  static_assert(TS == 1 || TS == 2 || TS == 4, "one, two or four tiles");
   constexpr int NS = kCoopSlots;
   constexpr int XT = NC * 256;          // a tile's operand per step: NC columns x 256 codes
   constexpr int XS = NT * XT;           // a step's activation operand
@@ -980,7 +1040,7 @@ __global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) v
   constexpr int DMA = (NDMA + W - 1) / W;  // per wave (waves past the last load issue an empty one)
   constexpr int TPT = 4 / BANDS;        // tokens per 16 columns
   constexpr int CPT = 4 * BANDS;        // columns per token
-  constexpr int LOADS = P + DMA;        // vector memory ops per wave and step
+  constexpr int LOADS = PW + DMA;       // vector memory ops per wave and step
   constexpr int WAIT = (NS - 2) * LOADS;  // when step j is read, steps j+1 .. j+NS-2 may still load
   constexpr int WAITCNT = (WAIT & 0xF) | (0x7 << 4) | (0xF << 8) | (((WAIT >> 4) & 3) << 14);
   static_assert(WAIT < 64, "vmcnt holds at most 63");
@@ -990,6 +1050,8 @@ __global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) v
   // (an out-of-range load still writes its zeros to LDS)
   __shared__ __attribute__((aligned(16))) uint8_t spare[NDMA % W ? 1024 : 16];
   __shared__ CoopPost post;
+  // split planes: the W waves' partial outputs, [row block][tile][lane] (re, im)
+  __shared__ __attribute__((aligned(16))) float2 xch[PS == 2 ? RBG * TS * 64 : 1];
   const int lane = threadIdx.x & 63;
   const int g4 = lane >> 4, li = lane & 15;
   const int wave = uniform(threadIdx.x >> 6);
@@ -1012,8 +1074,8 @@ __global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) v
     if (q0 >= h.coop_groups) return;  // nothing left: the whole block leaves
     q1 = q0 + 1;
   }
-  const int wrb = wave / SH;              // this wave's row block within a group
-  const int t0 = (wave % SH) * TS;        // and its first activation tile
+  const int wrb = wave / PS;              // this wave's row block within a group
+  const int pw0 = (wave % PS) * PW;       // and its first code plane
 
   CoopCursor lc;
   {
@@ -1041,7 +1103,7 @@ __global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) v
   // first step of the block's last known group wave 0 also claims the next
   // group; the claim goes out before the slot's loads, so the wait for them
   // covers it.
-  auto issue = [&](int k, v4i (&cq)[P]) {
+  auto issue = [&](int k, v4i (&cq)[PW]) {
     if (dyn && wave == 0 && lc.live && lc.k4 == 0 && lc.q + 1 >= lc.qend) {
       // one lane's atomic without a divergent branch: the other lanes' offsets
       // are out of range, so their adds are dropped
@@ -1054,9 +1116,13 @@ __global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) v
     const uint32_t pb = (uint32_t)(T * lc.nrb * lc.nk4 * 1024) - (uint32_t)(T - 1) * 1024u;
     const uint32_t off = ok ? (uint32_t)((rb * lc.nk4 + lc.k4) * T) * 1024u + (uint32_t)lane * 16u : kOob;
 #pragma unroll
-    for (int p = 0; p < P; ++p)
-      cq[p] = __builtin_amdgcn_raw_buffer_load_b128(make_rsrc(uniform_ptr(lc.codes[p / T] + (p % T) * 1024), pb),
-                                                    off, 0, kNonTemporal);
+    for (int j = 0; j < PW; ++j) {
+      const int p = pw0 + j;
+      // a select, not an index: a cursor indexed by a run-time value would live in scratch memory
+      const uint8_t* cm = p < T ? lc.codes[0] : lc.codes[1];
+      cq[j] = __builtin_amdgcn_raw_buffer_load_b128(make_rsrc(uniform_ptr(cm + (p % T) * 1024), pb), off, 0,
+                                                    kNonTemporal);
+    }
     const uint32_t xtile = (uint32_t)(lc.nk4 * XT);
     const auto xr = make_rsrc(uniform_ptr(lc.xf), (uint32_t)(h.ntile * xtile));
 #pragma unroll
@@ -1077,25 +1143,25 @@ __global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) v
     Lo = load_layer(tab + oc.lidx);
     sload_scales<T>(uniform_ptr(Lo.scales[0]), uniform_ptr(Lo.scales[1]), esc);
 #pragma unroll
-    for (int t = 0; t < TS; ++t) sload_run<TPT>(uniform_ptr(Lo.xs) + TPT * (t0 + t), exf[t]);
+    for (int t = 0; t < TS; ++t) sload_run<TPT>(uniform_ptr(Lo.xs) + TPT * t, exf[t]);
   };
   load_out_layer();
 
   bool xvalid[TS];
 #pragma unroll
-  for (int t = 0; t < TS; ++t) xvalid[t] = li < NC && TPT * (t0 + t) + li / CPT < h.B;
+  for (int t = 0; t < TS; ++t) xvalid[t] = li < NC && TPT * t + li / CPT < h.B;
 
-  v4i cq[NS][P];
+  v4i cq[NS][PW];
 #pragma unroll
   for (int k = 0; k < NS - 1; ++k) {
     issue(k, cq[k]);
     if (lc.live) coop_advance(lc, tab, h, &post);
   }
-  v4f aS[TS][P], aI[TS][P];
+  v4f aS[TS][PW], aI[TS][PW];
 #pragma unroll
   for (int t = 0; t < TS; ++t)
 #pragma unroll
-    for (int p = 0; p < P; ++p) aS[t][p] = aI[t][p] = v4f{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < PW; ++j) aS[t][j] = aI[t][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
   auto step = [&](auto kconst) -> bool {
     constexpr int K = decltype(kconst)::value;
@@ -1125,35 +1191,39 @@ __global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) v
     issue(KN, cq[KN]);
     if (lc.live) coop_advance(lc, tab, h, &post);
     const v4i* cr = cq[K];
-    v4i xq[2][TS][2];
-    {
-      uint32_t xa[2][TS][2];
+    uint32_t xa[2][TS][2];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int t = 0; t < TS; ++t) {
-          const uint32_t a = xvalid[t] ? lds_addr(&ring[K][(t0 + t) * XT]) + (uint32_t)((g4 * NC + li) * 16) +
-                                             kb * (uint32_t)(2 * 64 * NC)
-                                       : lds_addr(zero16);
-          xa[kb][t][0] = a;
-          xa[kb][t][1] = a + (xvalid[t] ? (uint32_t)(64 * NC) : 0u);
-        }
-      coop_read_x<TS>(xa, xq);
-    }
+      for (int t = 0; t < TS; ++t) {
+        const uint32_t a = xvalid[t] ? lds_addr(&ring[K][t * XT]) + (uint32_t)((g4 * NC + li) * 16) +
+                                           kb * (uint32_t)(2 * 64 * NC)
+                                     : lds_addr(zero16);
+        xa[kb][t][0] = a;
+        xa[kb][t][1] = a + (xvalid[t] ? (uint32_t)(64 * NC) : 0u);
+      }
+    // the halves' operands: both read up front (one or two tiles), else one
+    // half at a time (four tiles)
+    v4i xq[TS == 4 ? 1 : 2][TS][2];
+    if constexpr (TS != 4) coop_read_x<TS>(xa, xq);
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
-      if (kb == 1) coop_wait_x<TS>(xq);
-      const v4i(&xr)[TS][2] = xq[kb];
+      if constexpr (TS == 4) {
+        coop_read_x4(xa[kb], xq[0]);
+      } else {
+        if (kb == 1) coop_wait_x<TS>(xq);
+      }
+      const v4i(&xr)[TS][2] = xq[TS == 4 ? 0 : kb];
 #pragma unroll
-      for (int p = 0; p < P; ++p) {
+      for (int j = 0; j < PW; ++j) {
         v8i bs, bi;
-        expand_f4((uint32_t)cr[p][2 * kb], (uint32_t)cr[p][2 * kb + 1], bs, bi);
+        expand_f4((uint32_t)cr[j][2 * kb], (uint32_t)cr[j][2 * kb + 1], bs, bi);
 #pragma unroll
         for (int t = 0; t < TS; ++t) {
           const v4i x0 = xr[t][0], x1 = xr[t][1];
           const v8i a = v8i{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
-          aS[t][p] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bs, aS[t][p], kFmtFp8, kFmtFp4, 0, 0, 0, 0);
-          aI[t][p] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bi, aI[t][p], kFmtFp8, kFmtFp4, 0, 0, 0, 0);
+          aS[t][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bs, aS[t][j], kFmtFp8, kFmtFp4, 0, 0, 0, 0);
+          aI[t][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bi, aI[t][j], kFmtFp8, kFmtFp4, 0, 0, 0, 0);
         }
         // one plane's expansion, then its MFMAs: bounds the registers the schedule keeps live
         __builtin_amdgcn_sched_group_barrier(0x002, 10, 0);
@@ -1164,12 +1234,40 @@ __global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) v
       const int rb = oc.g * RBG + wrb;
       const int row = rb * 16 + li;
       const bool row_ok = rb < oc.nrb && row < oc.N;
+      if constexpr (PS == 1) {
 #pragma unroll
-      for (int t = 0; t < TS; ++t) {
-        write_outputs_f4<T, BANDS>(Lo, h, 0, row, row_ok, lane, t0 + t, aS[t], aI[t], esc, exf[t]);
+        for (int t = 0; t < TS; ++t)
+          write_outputs_f4<T, BANDS>(Lo, h, 0, row, row_ok, lane, t, aS[t], aI[t], esc, exf[t]);
+      } else {
+        // the W wave posts its half of y in LDS, the U wave adds it and writes y
+        const int m = pw0 / T;
+        float2 part[TS];
 #pragma unroll
-        for (int p = 0; p < P; ++p) aS[t][p] = aI[t][p] = v4f{0.f, 0.f, 0.f, 0.f};
+        for (int t = 0; t < TS; ++t) part[t] = partial_outputs_f4<T>(m, aS[t], aI[t], esc);
+        const uint32_t xa = lds_addr(&xch[(wrb * TS) * 64 + lane]);
+        if (m == 1) {
+#pragma unroll
+          for (int t = 0; t < TS; ++t)
+            asm volatile("ds_write_b64 %0, %1 offset:%2" : : "v"(xa), "v"(part[t]), "i"(t * 512) : "memory");
+          asm volatile("s_waitcnt lgkmcnt(0)" : : : "memory");
+        }
+        __builtin_amdgcn_s_barrier();
+        if (m == 0) {
+#pragma unroll
+          for (int t = 0; t < TS; ++t) {
+            float2 o;
+            asm volatile("ds_read_b64 %0, %1 offset:%2\n\ts_waitcnt lgkmcnt(0)" : "=v"(o) : "v"(xa), "i"(t * 512)
+                         : "memory");
+            store_outputs_f4(Lo, h, row, row_ok, lane, t, part[t].x + o.x, part[t].y + o.y, exf[t]);
+          }
+        }
+        // the next group's posts come after the next step's barrier, which
+        // every U wave reaches only after these reads
       }
+#pragma unroll
+      for (int t = 0; t < TS; ++t)
+#pragma unroll
+        for (int j = 0; j < PW; ++j) aS[t][j] = aI[t][j] = v4f{0.f, 0.f, 0.f, 0.f};
     }
     const int lbefore = oc.lidx;
     if (dyn) {
@@ -1200,7 +1298,7 @@ __global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) v
 
 template <int T, int NT, int NC, int BANDS>
 void launch_coop_f4(const DecHeader& h, const DecLayer* tab, hipStream_t s) {
-  auto k = dec_coop_f4_kernel<T, NT, coop_tiles_per_wave(NT), NC, BANDS>;
+  auto k = dec_coop_f4_kernel<T, NT, coop_plane_split(NT), NC, BANDS>;
   static const int resident = resident_blocks(reinterpret_cast<const void*>(k), 64 * coop_waves(NT));
   hipLaunchKernelGGL(k, dim3((unsigned)resident), dim3(64 * coop_waves(NT)), 0, s, h, tab);
 }
