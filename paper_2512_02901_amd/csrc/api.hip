@@ -462,7 +462,7 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
   h.coop_groups = sitems;
   h.coop_dyn0 = sitems;
   h.coop_dyn_steps = ssteps;
-  if (h.coop && !h.grouped && min_nk4 > kCoopSlots) {
+  if (h.coop && min_nk4 > kCoopSlots) {
     const int64_t target = (int64_t)(kCoopStaticFrac * (double)ssteps);
     const int rbg = h.coop_rb;
     for (int32_t i = 0; i < n_layers; ++i) {

@@ -805,30 +805,44 @@ void launch_stream_f4_g(const DecHeader& h, const DecLayer& inl, const DecLayer*
   else launch_stream_f4<T, 4, 1, GS, 1>(h, inl, tab, s);
 }
 
-template <int T, int NT, int NC, int BANDS>
+template <int T, int NT, int NC, int BANDS, bool GS>
 void launch_coop_f4(const DecHeader& h, const DecLayer* tab, hipStream_t s);  // the block-cooperative kernel below
+
+// The cooperative kernel for one or two tiles (per-group scales or not).
+template <int T, bool GS>
+void launch_coop_f4_small(const DecHeader& h, const DecLayer* tab, hipStream_t s) {
+  if (h.ntile == 2) {
+    if (h.bands == 2) launch_coop_f4<T, 2, 16, 2, GS>(h, tab, s);
+    else launch_coop_f4<T, 2, 16, 1, GS>(h, tab, s);
+  } else if (h.nc <= 8) {
+    launch_coop_f4<T, 1, 8, 2, GS>(h, tab, s);
+  } else if (h.bands == 2) {
+    launch_coop_f4<T, 1, 16, 2, GS>(h, tab, s);
+  } else {
+    launch_coop_f4<T, 1, 16, 1, GS>(h, tab, s);
+  }
+}
 constexpr bool kCoopSmallB = true;  // one tile (1-4 tokens) on the cooperative kernel too
 
 template <int T>
 void launch_stream_f4_t(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
   if (h.grouped) {
+    if constexpr (T <= 2) {
+      if (tab && h.coop && h.ntile <= 2) {
+        launch_coop_f4_small<T, true>(h, tab, s);
+        return;
+      }
+    }
     launch_stream_f4_g<T, true>(h, inl, tab, s);
     return;
   }
   if constexpr (T <= 2) {
     if (tab && h.coop && h.ntile >= 3) {
-      launch_coop_f4<T, 4, 16, 1>(h, tab, s);
+      launch_coop_f4<T, 4, 16, 1, false>(h, tab, s);
       return;
     }
-    if (tab && h.coop && h.ntile == 2) {
-      if (h.bands == 2) launch_coop_f4<T, 2, 16, 2>(h, tab, s);
-      else launch_coop_f4<T, 2, 16, 1>(h, tab, s);
-      return;
-    }
-    if (tab && h.coop && kCoopSmallB) {
-      if (h.nc <= 8) launch_coop_f4<T, 1, 8, 2>(h, tab, s);
-      else if (h.bands == 2) launch_coop_f4<T, 1, 16, 2>(h, tab, s);
-      else launch_coop_f4<T, 1, 16, 1>(h, tab, s);
+    if (tab && h.coop && (h.ntile == 2 || kCoopSmallB)) {
+      launch_coop_f4_small<T, false>(h, tab, s);
       return;
     }
   }
@@ -1021,7 +1035,11 @@ __device__ inline void coop_wait_x(v4i (&x)[2][TS][2]) {
 // stay at 64 registers and each code byte is still loaded and expanded once;
 // the two halves of y meet in LDS at the end of a group.
 // NC columns per tile (8: one two-band token; 16), BANDS digit bands per token.
-template <int T, int NT, int PS, int NC, int BANDS>
+// GS: per-group scales (every layer of the call; one or two tiles): each
+// wave's row block has its step's scales loaded into the ring slot with the
+// step's operands, every step's products start from zero and are folded into
+// scaled float32 sums (as in the streaming kernel).
+template <int T, int NT, int PS, int NC, int BANDS, bool GS>
 __global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) void dec_coop_f4_kernel(DecHeader h,
                                                                       const DecLayer* __restrict__ tab) {
 #if defined(__HIP_DEVICE_COMPILE__)  // LDS-DMA and buffer-descriptor code: device pass only
@@ -1033,6 +1051,8 @@ __global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) v
   static_assert(P % PS == 0 && W % PS == 0, "planes split evenly over the waves of a row block");
   static_assert(PS == 1 || (PS == 2 && BANDS == 1), "split planes: one-band tiles only");
   static_assert(TS == 1 || TS == 2 || TS == 4, "one, two or four tiles");
+  static_assert(!GS || PS == 1, "per-group scales: one wave per row block");
+  constexpr int GSB = GS ? group_slot_bytes(T) : 16;  // a wave's scale bytes per step
   constexpr int NS = kCoopSlots;
   constexpr int XT = NC * 256;          // a tile's operand per step: NC columns x 256 codes
   constexpr int XS = NT * XT;           // a step's activation operand
@@ -1040,7 +1060,7 @@ __global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) v
   constexpr int DMA = (NDMA + W - 1) / W;  // per wave (waves past the last load issue an empty one)
   constexpr int TPT = 4 / BANDS;        // tokens per 16 columns
   constexpr int CPT = 4 * BANDS;        // columns per token
-  constexpr int LOADS = PW + DMA;       // vector memory ops per wave and step
+  constexpr int LOADS = PW + DMA + (GS ? 2 * group_loads(T) : 0);  // vector memory ops per wave and step
   constexpr int WAIT = (NS - 2) * LOADS;  // when step j is read, steps j+1 .. j+NS-2 may still load
   constexpr int WAITCNT = (WAIT & 0xF) | (0x7 << 4) | (0xF << 8) | (((WAIT >> 4) & 3) << 14);
   static_assert(WAIT < 64, "vmcnt holds at most 63");
@@ -1050,6 +1070,8 @@ __global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) v
   // (an out-of-range load still writes its zeros to LDS)
   __shared__ __attribute__((aligned(16))) uint8_t spare[NDMA % W ? 1024 : 16];
   __shared__ CoopPost post;
+  // per-group scales: [slot][wave] scale area of each step
+  __shared__ __attribute__((aligned(16))) uint8_t gring[GS ? NS : 1][GS ? W : 1][GSB];
   // split planes: the W waves' partial outputs, [row block][tile][lane] (re, im)
   __shared__ __attribute__((aligned(16))) float2 xch[PS == 2 ? RBG * TS * 64 : 1];
   const int lane = threadIdx.x & 63;
@@ -1103,7 +1125,20 @@ __global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) v
   // first step of the block's last known group wave 0 also claims the next
   // group; the claim goes out before the slot's loads, so the wait for them
   // covers it.
+  GroupCursor<T> gc;
+  int glidx = -1;  // the layer gc was entered for
   auto issue = [&](int k, v4i (&cq)[PW]) {
+    if constexpr (GS) {
+      if (lc.live && lc.k4 == 0) {
+        if (lc.lidx != glidx) {
+          group_enter_layer(gc, load_layer(tab + lc.lidx));
+          glidx = lc.lidx;
+        }
+        group_item(gc, lc.g * RBG + wrb, 0, lane);
+      }
+      group_issue<T>(gc, lc.live, lane, &gring[k][wave][0]);
+      group_step(gc);
+    }
     if (dyn && wave == 0 && lc.live && lc.k4 == 0 && lc.q + 1 >= lc.qend) {
       // one lane's atomic without a divergent branch: the other lanes' offsets
       // are out of range, so their adds are dropped
@@ -1162,6 +1197,14 @@ __global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) v
   for (int t = 0; t < TS; ++t)
 #pragma unroll
     for (int j = 0; j < PW; ++j) aS[t][j] = aI[t][j] = v4f{0.f, 0.f, 0.f, 0.f};
+  // per-group scales: the scaled sums of the current group
+  float Are[TS][PW][2], Aim[TS][PW][2];
+  if constexpr (GS) {
+#pragma unroll
+    for (int t = 0; t < TS; ++t)
+#pragma unroll
+      for (int j = 0; j < PW; ++j) Are[t][j][0] = Are[t][j][1] = Aim[t][j][0] = Aim[t][j][1] = 0.0f;
+  }
 
   auto step = [&](auto kconst) -> bool {
     constexpr int K = decltype(kconst)::value;
@@ -1222,19 +1265,35 @@ __global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) v
         for (int t = 0; t < TS; ++t) {
           const v4i x0 = xr[t][0], x1 = xr[t][1];
           const v8i a = v8i{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
-          aS[t][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bs, aS[t][j], kFmtFp8, kFmtFp4, 0, 0, 0, 0);
-          aI[t][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bi, aI[t][j], kFmtFp8, kFmtFp4, 0, 0, 0, 0);
+          // per-group scales: every step starts from zero
+          const v4f cS = (GS && kb == 0) ? v4f{0.f, 0.f, 0.f, 0.f} : aS[t][j];
+          const v4f cI = (GS && kb == 0) ? v4f{0.f, 0.f, 0.f, 0.f} : aI[t][j];
+          aS[t][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bs, cS, kFmtFp8, kFmtFp4, 0, 0, 0, 0);
+          aI[t][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, bi, cI, kFmtFp8, kFmtFp4, 0, 0, 0, 0);
         }
         // one plane's expansion, then its MFMAs: bounds the registers the schedule keeps live
         __builtin_amdgcn_sched_group_barrier(0x002, 10, 0);
         __builtin_amdgcn_sched_group_barrier(0x008, 2 * TS, 0);
       }
     }
+    if constexpr (GS) {
+      float gs[PW][2];
+      group_read<T>(&gring[K][wave][0], li, gs);
+#pragma unroll
+      for (int t = 0; t < TS; ++t) fold_group<PW>(aS[t], aI[t], gs, Are[t], Aim[t]);
+    }
     if (oc.k4 == oc.nk4 - 1) {
       const int rb = oc.g * RBG + wrb;
       const int row = rb * 16 + li;
       const bool row_ok = rb < oc.nrb && row < oc.N;
-      if constexpr (PS == 1) {
+      if constexpr (GS) {
+#pragma unroll
+        for (int t = 0; t < TS; ++t) {
+          write_outputs_f4_gs<T, BANDS>(Lo, h, 0, row, row_ok, lane, t, Are[t], Aim[t], exf[t]);
+#pragma unroll
+          for (int j = 0; j < PW; ++j) Are[t][j][0] = Are[t][j][1] = Aim[t][j][0] = Aim[t][j][1] = 0.0f;
+        }
+      } else if constexpr (PS == 1) {
 #pragma unroll
         for (int t = 0; t < TS; ++t)
           write_outputs_f4<T, BANDS>(Lo, h, 0, row, row_ok, lane, t, aS[t], aI[t], esc, exf[t]);
@@ -1296,9 +1355,9 @@ __global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) v
 #endif
 }
 
-template <int T, int NT, int NC, int BANDS>
+template <int T, int NT, int NC, int BANDS, bool GS>
 void launch_coop_f4(const DecHeader& h, const DecLayer* tab, hipStream_t s) {
-  auto k = dec_coop_f4_kernel<T, NT, coop_plane_split(NT), NC, BANDS>;
+  auto k = dec_coop_f4_kernel<T, NT, coop_plane_split(NT), NC, BANDS, GS>;
   static const int resident = resident_blocks(reinterpret_cast<const void*>(k), 64 * coop_waves(NT));
   hipLaunchKernelGGL(k, dim3((unsigned)resident), dim3(64 * coop_waves(NT)), 0, s, h, tab);
 }
