@@ -651,6 +651,8 @@ def main():
                     help="only run the QAT training-step leg (for profiler runs)")
     ap.add_argument("--grouped-only", action="store_true",
                     help="only run the per-group-scale stack leg, G = 256 (for profiler runs)")
+    ap.add_argument("--block-only", action="store_true",
+                    help="only run the decoder-block leg (for profiler runs)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run 5 plain 256 MiB device copies (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -679,6 +681,9 @@ def main():
         return
     if args.qat_only:
         print(json.dumps({"qat_step": qat_bench(f2, synth, torch, dev)}), flush=True)
+        return
+    if args.block_only:
+        print(json.dumps({"decoder_block": block_bench(f2, synth, torch, dev)}), flush=True)
         return
     if args.grouped_only:
         print(json.dumps({"stack_group256": grouped_stack_bench(f2, synth, torch, dev, 2, 256, args.steps,

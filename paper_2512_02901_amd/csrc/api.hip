@@ -84,16 +84,6 @@ fairy2i_status run_single_decode(DecLayer l, int32_t T, int32_t dtype, int64_t B
                                   acc, stream));
 }
 
-// Group table: header followed by the layer descriptors (the device copy is
-// read by the kernels at the same offsets).
-constexpr uint32_t kGroupMagic = 0xFA112101u;
-struct GroupTableHeader {
-  uint32_t magic, abi;
-  DecHeader h;
-  int32_t any_split, pad0_;
-  int64_t max_BN;
-};
-static_assert(sizeof(GroupTableHeader) % 16 == 0, "table header alignment");
 
 // ------------------------------------------------ allocation-free call ---
 // fairy2i_wl_matmul_noalloc runs fairy2i_wl_matmul with this array as its

@@ -14,6 +14,18 @@
 //   attn_combine  the slices of a head merged in slice order, bf16 out
 //   swiglu        silu(Re g) Re u + i silu(Im g) Im u, bf16 out
 //   add           the final residual add
+// For one token on the fp4 path with two digit bands (every block this
+// library plans, up to 8192 complex entries per token) the fused path runs
+// instead: 13 launches in place of 19.  The stage that consumes a
+// projection's output sums that projection's split-K partials itself, and
+// the stage that makes a projection's input writes its activation operand:
+//   operand (norm)  x (+ the o projection's output), RMSNorm, operand of
+//                   q k v (of gate and up)
+//   rope_append_sum q k v summed, rotary embedding, caches
+//   operand (bf16)  operand of a bf16 token (the attention output; SwiGLU's)
+//   swiglu_sum      gate and up summed, SwiGLU, bf16 out
+//   add_sum         down summed, the final residual add
+// so only the product kernels of the four group calls remain of them.
 // Complex vectors are float2 (re, im); a head owns dc = n / n_heads
 // consecutive complex entries (entry j: its real dims j and j + dc).  All
 // reductions run in a fixed order, so results are bitwise reproducible.
@@ -21,6 +33,8 @@
 #include <string.h>
 
 #include "common.h"
+#include "decode.h"
+#include "f4_operand.h"
 
 namespace fairy2i {
 
@@ -106,65 +120,81 @@ __global__ void rope_append_kernel(const float2* __restrict__ q, const float2* _
   v_cache[at] = v[i];
 }
 
-// One wave per (64-position slice, head).  Lane t scores position n0 + t as
-// Re(q^H k) * scale, reading its key with 16-byte loads and the query from
-// LDS (every lane reads the same address: a broadcast); then the slice's
-// maximum m, e_t = exp(s_t - m), l = sum e_t; then lane j forms
-// o_j = sum_t e_t v_{n0+t, j} over the slice (t wave-uniform, eight value loads
-// in flight).  Partial record per (head, slice): [m, l, o (2 dc floats)].
+// One block of four waves per (64-position slice, head).  Scores: four lanes
+// per position, each taking a quarter of the key row's 16-byte chunks (eight
+// loads in flight), summed across the four lanes, times scale; then the
+// slice's maximum m, e_t = exp(s_t - m) (kept in LDS) and l = sum e_t.
+// Values: wave w takes positions 16 w .. 16 w + 15, lane j (+ 64 r) entry j
+// of o = sum_t e_t v_t (eight value loads in flight), and the four waves'
+// sums are added in wave order.  Partial record per (head, slice):
+// [m, l, o (2 dc floats)].
+constexpr int kAttnThreads = 256;
 template <int R>  // complex entries per lane in the value pass: dc <= 64 R
-__global__ __launch_bounds__(64) void attn_partial_kernel(const float2* __restrict__ q_rot,
-                                                          const float2* __restrict__ k_cache,
-                                                          const float2* __restrict__ v_cache, int dc, int64_t n_ctx,
-                                                          int64_t max_ctx, float scale, float* __restrict__ part) {
-  __shared__ float4 qs[64 * R / 2];
-  const int h = blockIdx.y, sl = blockIdx.x, lane = threadIdx.x;
+__global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(const float2* __restrict__ q_rot,
+                                                                    const float2* __restrict__ k_cache,
+                                                                    const float2* __restrict__ v_cache, int dc,
+                                                                    int64_t n_ctx, int64_t max_ctx, float scale,
+                                                                    float* __restrict__ part) {
+  __shared__ float es[kAttnSlice];
+  __shared__ float redm[kAttnThreads / 64], redl[kAttnThreads / 64];
+  __shared__ float2 ow[kAttnThreads / 64][64 * R];
+  const int h = blockIdx.y, sl = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t n0 = (int64_t)sl * kAttnSlice;
   const int cnt = (int)min((int64_t)kAttnSlice, n_ctx - n0);
-  for (int j = lane; j < dc / 2; j += 64) qs[j] = reinterpret_cast<const float4*>(q_rot + h * dc)[j];
-  __syncthreads();
   const float2* kh = k_cache + (int64_t)h * max_ctx * dc;
   const float2* vh = v_cache + (int64_t)h * max_ctx * dc;
-  float s = -INFINITY;
-  if (lane < cnt) {
-    const float4* kp = reinterpret_cast<const float4*>(kh + (n0 + lane) * dc);
-    float acc = 0.0f;
-    for (int j0 = 0; j0 < dc / 2; j0 += 8) {
-      float4 kv[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) kv[u] = j0 + u < dc / 2 ? kp[j0 + u] : make_float4(0.f, 0.f, 0.f, 0.f);
+  const float4* qh = reinterpret_cast<const float4*>(q_rot + (int64_t)h * dc);
+  const int p = tid >> 2, qd = tid & 3, nf4 = dc / 2;
+  float acc = 0.0f;
+  if (p < cnt) {
+    const float4* kp = reinterpret_cast<const float4*>(kh + (n0 + p) * dc);
+    for (int j0 = qd; j0 < nf4; j0 += 32) {
+      float4 kv[8], qv[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        if (j0 + u < dc / 2) {
-          const float4 qv = qs[j0 + u];
-          acc = fmaf(qv.x, kv[u].x, acc);
-          acc = fmaf(qv.y, kv[u].y, acc);
-          acc = fmaf(qv.z, kv[u].z, acc);
-          acc = fmaf(qv.w, kv[u].w, acc);
-        }
+        const int j = j0 + 4 * u;
+        kv[u] = j < nf4 ? kp[j] : make_float4(0.f, 0.f, 0.f, 0.f);
+        qv[u] = j < nf4 ? qh[j] : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        acc = fmaf(qv[u].x, kv[u].x, acc);
+        acc = fmaf(qv[u].y, kv[u].y, acc);
+        acc = fmaf(qv[u].z, kv[u].z, acc);
+        acc = fmaf(qv[u].w, kv[u].w, acc);
       }
     }
-    s = acc * scale;
   }
-  const float m = wave_max(s);
-  const float e = lane < cnt ? expf(s - m) : 0.0f;
-  const float l = wave_sum(e);
+  acc += __shfl_xor(acc, 1);
+  acc += __shfl_xor(acc, 2);
+  const float s = p < cnt ? acc * scale : -INFINITY;
+  float m = wave_max(s);
+  if (lane == 0) redm[wave] = m;
+  __syncthreads();
+  m = fmaxf(fmaxf(redm[0], redm[1]), fmaxf(redm[2], redm[3]));
+  const float e = p < cnt ? expf(s - m) : 0.0f;
+  if (qd == 0) es[p] = e;
+  const float lw = wave_sum(qd == 0 ? e : 0.0f);
+  if (lane == 0) redl[wave] = lw;
+  __syncthreads();
+  const float l = ((redl[0] + redl[1]) + redl[2]) + redl[3];
   float2 o[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) o[r] = make_float2(0.f, 0.f);
-  for (int t0 = 0; t0 < cnt; t0 += 8) {
+  const int pb = 16 * wave;
+#pragma unroll
+  for (int t0 = 0; t0 < 16; t0 += 8) {
     float2 vv[8][R];
 #pragma unroll
     for (int u = 0; u < 8; ++u)
 #pragma unroll
       for (int r = 0; r < R; ++r) {
-        const int j = lane + 64 * r;
-        vv[u][r] = (t0 + u < cnt && j < dc) ? vh[(n0 + t0 + u) * dc + j] : make_float2(0.f, 0.f);
+        const int t = pb + t0 + u, j = lane + 64 * r;
+        vv[u][r] = (t < cnt && j < dc) ? vh[(n0 + t) * dc + j] : make_float2(0.f, 0.f);
       }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      // lanes t >= cnt hold e = 0, and t0 + u < 64
-      const float w = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(e), t0 + u));
+      const float w = es[pb + t0 + u];  // 0 past cnt
 #pragma unroll
       for (int r = 0; r < R; ++r) {
         o[r].x = fmaf(w, vv[u][r].x, o[r].x);
@@ -172,18 +202,22 @@ __global__ __launch_bounds__(64) void attn_partial_kernel(const float2* __restri
       }
     }
   }
+#pragma unroll
+  for (int r = 0; r < R; ++r) ow[wave][lane + 64 * r] = o[r];
+  __syncthreads();
   float* rec = part + ((int64_t)h * gridDim.x + sl) * (2 + 2 * dc);
-  if (lane == 0) {
+  if (tid == 0) {
     rec[0] = m;
     rec[1] = l;
   }
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const int j = lane + 64 * r;
-    if (j < dc) {
-      rec[2 + 2 * j] = o[r].x;
-      rec[3 + 2 * j] = o[r].y;
+  for (int j = tid; j < dc; j += kAttnThreads) {
+    float2 a = ow[0][j];
+    for (int w = 1; w < kAttnThreads / 64; ++w) {
+      a.x += ow[w][j].x;
+      a.y += ow[w][j].y;
     }
+    rec[2 + 2 * j] = a.x;
+    rec[3 + 2 * j] = a.y;
   }
 }
 
@@ -251,6 +285,286 @@ __global__ void add_kernel(const float2* __restrict__ a, const float2* __restric
   out[i] = make_float2(av.x + bv.x, av.y + bv.y);
 }
 
+// ---------------------------------------------------------- fused path ---
+// For one token on the fp4 path (two digit bands, one 8-column tile), the
+// block's elementwise stages also do the grouped call's other two launches:
+// the kernel that needs a layer's output sums that layer's split-K partials
+// itself (in slice order, the additions of the grouped call's reduction),
+// and the stage that makes a projection's input also writes that
+// projection's activation operand (token shift, digit pairs; f4_operand.h).
+
+// A projection's output: its split-K partials [nkc][N] or, with one slice,
+// the output itself.
+struct LayerOut {
+  const float2* part;
+  float2* y;
+  int32_t nkc, N;
+};
+
+// Entry i of NS projections' outputs: each output's slices added in order
+// from +0 (the additions of the grouped call's reduction), the loads of U
+// slices of every output in flight together; summed outputs are also written
+// where that reduction would write them.
+template <int NS, int U = 8>
+__device__ inline void layer_outs(const LayerOut (&o)[NS], int i, float2 (&r)[NS]) {
+  int mk = 1;
+#pragma unroll
+  for (int q = 0; q < NS; ++q) {
+    mk = max(mk, o[q].nkc);
+    r[q] = make_float2(0.0f, 0.0f);
+  }
+  for (int kc0 = 0; kc0 < mk; kc0 += U) {
+    float2 t[NS][U];
+#pragma unroll
+    for (int q = 0; q < NS; ++q)
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int kc = kc0 + u;
+        t[q][u] = o[q].nkc > 1 ? (kc < o[q].nkc ? o[q].part[(int64_t)kc * o[q].N + i] : make_float2(0.f, 0.f))
+                               : (kc == 0 ? o[q].y[i] : make_float2(0.f, 0.f));
+      }
+#pragma unroll
+    for (int q = 0; q < NS; ++q)
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (kc0 + u < max(o[q].nkc, 1)) {
+          r[q].x += t[q][u].x;
+          r[q].y += t[q][u].y;
+        }
+  }
+#pragma unroll
+  for (int q = 0; q < NS; ++q)
+    if (o[q].nkc > 1) o[q].y[i] = r[q];
+}
+
+// Up to three projections fed the same token: their operand buffers and
+// output factors, the operand's 256-code steps and the claim counter of
+// their group call (zeroed for the product kernel, as the grouped call's
+// own operand kernel does).
+struct OperandTargets {
+  int8_t* xf[3];
+  float* xs[3];
+  int32_t count, nk4;
+  uint32_t* ctr;
+};
+
+constexpr int kOpThreads = 512;
+constexpr int kOpMaxK = 16 * kOpThreads;  // complex entries of a token the operand kernel takes
+constexpr int kSrcNorm = 0, kSrcBf16 = 1;
+
+struct OperandArgs {
+  int32_t K;  // complex entries of the token
+  // kSrcNorm: v = x (+ the residual branch res); h_out = v; z = RMSNorm(v) gamma
+  const float2* x;
+  LayerOut res;      // res.y null: no residual branch
+  float2* h_out;
+  const float* gamma;
+  float eps;
+  uint16_t* z_out;  // the bf16 token
+  // kSrcBf16: the token as bf16 (re, im) words
+  const uint32_t* tok;
+  OperandTargets t;
+};
+
+// Entries tid + e kOpThreads (e < E) of a projection's output, every load of
+// U slices in flight together; the slices are added in order.
+template <int E>
+__device__ inline void gather_out(const LayerOut& o, int tid, int K, float2 (&acc)[E]) {
+  constexpr int U = E <= 4 ? 8 : (E <= 8 ? 4 : 2);
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc[e] = make_float2(0.0f, 0.0f);
+  if (o.nkc <= 1) {
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int i = tid + e * kOpThreads;
+      if (i < K) acc[e] = o.y[i];
+    }
+    return;
+  }
+  for (int kc0 = 0; kc0 < o.nkc; kc0 += U) {
+    float2 t[U][E];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const int i = tid + e * kOpThreads;
+        t[u][e] = (kc0 + u < o.nkc && i < K) ? o.part[(int64_t)(kc0 + u) * o.N + i] : make_float2(0.0f, 0.0f);
+      }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (kc0 + u < o.nkc)
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          acc[e].x += t[u][e].x;
+          acc[e].y += t[u][e].y;
+        }
+  }
+  // the sums start from +0 and add the slices in order, as the grouped
+  // call's reduction does; write them where that reduction would
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = tid + e * kOpThreads;
+    if (i < K) o.y[i] = acc[e];
+  }
+}
+
+// One block: the token's bf16 words in LDS (entry i of thread i mod
+// kOpThreads, E entries a thread: K <= E kOpThreads), their largest
+// magnitude, then the digits of every half run (8 codes) of the operand
+// (runs past K hold zeros) for each target.
+template <int SRC, int E>
+__global__ __launch_bounds__(kOpThreads) void block_operand_kernel(OperandArgs a) {
+  __shared__ __align__(16) uint32_t tokw[E * kOpThreads];
+  __shared__ float red[kOpThreads / 64];
+  __shared__ float sh_g;
+  const int K = a.K, tid = threadIdx.x, wave = tid >> 6;
+  uint32_t zw[E];
+  if constexpr (SRC == kSrcNorm) {
+    float2 v[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int i = tid + e * kOpThreads;
+      v[e] = i < K ? a.x[i] : make_float2(0.0f, 0.0f);
+    }
+    if (a.res.y) {
+      float2 w[E];
+      gather_out<E>(a.res, tid, K, w);
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        v[e].x += w[e].x;
+        v[e].y += w[e].y;
+      }
+    }
+    float ss = 0.0f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      ss = fmaf(v[e].x, v[e].x, ss);
+      ss = fmaf(v[e].y, v[e].y, ss);
+    }
+    ss = wave_sum(ss);
+    if ((tid & 63) == 0) red[wave] = ss;
+    __syncthreads();
+    float tot = 0.0f;
+    for (int w = 0; w < kOpThreads / 64; ++w) tot += red[w];
+    const float r = 1.0f / sqrtf(tot / (float)(2 * K) + a.eps);
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int i = tid + e * kOpThreads;
+      zw[e] = 0u;
+      if (i < K) {
+        if (a.h_out) a.h_out[i] = v[e];
+        zw[e] = (uint32_t)bf16_rne((v[e].x * r) * a.gamma[i]) | ((uint32_t)bf16_rne((v[e].y * r) * a.gamma[K + i]) << 16);
+      }
+    }
+    __syncthreads();  // red is reused below
+  } else {
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int i = tid + e * kOpThreads;
+      zw[e] = i < K ? a.tok[i] : 0u;
+    }
+  }
+  float m = 0.0f;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = tid + e * kOpThreads;
+    if (i < K) {
+      tokw[i] = zw[e];
+      if constexpr (SRC == kSrcNorm) reinterpret_cast<uint32_t*>(a.z_out)[i] = zw[e];
+      m = fmaxf(m, fmaxf(fabsf(__uint_as_float(zw[e] << 16)), fabsf(__uint_as_float(zw[e] & 0xFFFF0000u))));
+    }
+  }
+  m = wave_max(m);
+  if ((tid & 63) == 0) red[wave] = m;
+  __syncthreads();
+  if (tid == 0) {
+    float g = 0.0f;
+    for (int w = 0; w < kOpThreads / 64; ++w) g = fmaxf(g, red[w]);
+    sh_g = g;
+  }
+  __syncthreads();
+  const float g = sh_g;
+  const int S = f4_token_shift(g);
+  if (tid == 0) {
+    for (int t = 0; t < a.t.count; ++t) a.t.xs[t][0] = g > 0.0f ? ldexpf(1.0f, -S) : 0.0f;
+    if (a.t.ctr) *a.t.ctr = 0u;
+  }
+  const int nhalf = a.t.nk4 * 32;  // half runs of 8 codes in the operand (nhalf <= 2 E kOpThreads / 8)
+  for (int hr = tid; hr < nhalf; hr += kOpThreads) {
+    uint32_t w8[8];
+    if (8 * hr < K) {  // K % 8 == 0: the half run is in range or past K entirely
+      const uint4 p0 = *reinterpret_cast<const uint4*>(&tokw[8 * hr]);
+      const uint4 p1 = *reinterpret_cast<const uint4*>(&tokw[8 * hr + 4]);
+      w8[0] = p0.x; w8[1] = p0.y; w8[2] = p0.z; w8[3] = p0.w;
+      w8[4] = p1.x; w8[5] = p1.y; w8[6] = p1.z; w8[7] = p1.w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) w8[e] = 0u;
+    }
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      float xv[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) xv[e] = __uint_as_float(c ? (w8[e] & 0xFFFF0000u) : (w8[e] << 16));
+      uint32_t out[2][2][2];
+      f4_unit_digits(xv, S, 2, out);
+      for (int t = 0; t < a.t.count; ++t)
+        f4_store_unit(reinterpret_cast<uint8_t*>(a.t.xf[t]), hr >> 1, 8, 0, c, hr & 1, 2, out);
+    }
+  }
+}
+
+template <int SRC>
+void launch_operand(const OperandArgs& a, hipStream_t s) {
+  const dim3 g(1), b(kOpThreads);
+  if (a.K <= 4 * kOpThreads) hipLaunchKernelGGL((block_operand_kernel<SRC, 4>), g, b, 0, s, a);
+  else if (a.K <= 8 * kOpThreads) hipLaunchKernelGGL((block_operand_kernel<SRC, 8>), g, b, 0, s, a);
+  else hipLaunchKernelGGL((block_operand_kernel<SRC, 16>), g, b, 0, s, a);
+}
+
+// rope_append_kernel on the summed q, k and v partials (also written out).
+__global__ void rope_append_sum_kernel(LayerOut q, LayerOut k, LayerOut v, int n, int dc, int64_t pos,
+                                       int64_t max_ctx, double base, float2* __restrict__ q_rot,
+                                       float2* __restrict__ k_cache, float2* __restrict__ v_cache) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const LayerOut o[3] = {q, k, v};
+  float2 r[3];
+  layer_outs<3>(o, i, r);
+  const float2 qv = r[0], kv = r[1], vv = r[2];
+  const int h = i / dc, j = i - h * dc;
+  const double ang = (double)pos * pow(base, -2.0 * (double)j / (double)(2 * dc));
+  double s, c;
+  sincos(ang, &s, &c);
+  const float cf = (float)c, sf = (float)s;
+  q_rot[i] = make_float2(fmaf(qv.x, cf, -qv.y * sf), fmaf(qv.x, sf, qv.y * cf));
+  const int64_t at = ((int64_t)h * max_ctx + pos) * dc + j;
+  k_cache[at] = make_float2(fmaf(kv.x, cf, -kv.y * sf), fmaf(kv.x, sf, kv.y * cf));
+  v_cache[at] = vv;
+}
+
+// out = h1 + d, d summed from its partials (and written out).
+__global__ void add_sum_kernel(const float2* __restrict__ h1, LayerOut d, int n, float2* __restrict__ out) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const LayerOut o[1] = {d};
+  float2 r[1];
+  layer_outs<1, 24>(o, i, r);
+  const float2 av = h1[i], bv = r[0];
+  out[i] = make_float2(av.x + bv.x, av.y + bv.y);
+}
+
+// act = bf16(silu(g) u) per component, g and u summed from their partials
+// (and written out).
+__global__ void swiglu_sum_kernel(LayerOut g, LayerOut u, int n, uint32_t* __restrict__ act) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const LayerOut o[2] = {g, u};
+  float2 r[2];
+  layer_outs<2>(o, i, r);
+  act[i] = (uint32_t)bf16_rne(silu(r[0].x) * r[1].x) | ((uint32_t)bf16_rne(silu(r[0].y) * r[1].y) << 16);
+}
+
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 // Plan: header, then the four group tables (q k v; o; gate up; down).
@@ -261,7 +575,7 @@ struct BlockPlanHeader {
   int64_t n, n_ff, max_ctx;
   int32_t n_heads, T;
   float eps;
-  int32_t pad0_;
+  int32_t fused;  // one-token fp4 groups: the fused path runs
   double rope_base;
   const float* norm_attn;
   const float* norm_mlp;
@@ -363,6 +677,95 @@ bool block_layout(const fairy2i_block_desc* d, BlockLayout& L) {
 
 inline fairy2i_status hip_st(hipError_t e) { return e == hipSuccess ? FAIRY2I_OK : FAIRY2I_ERR_HIP; }
 
+void launch_attention(const BlockPlanHeader* hdr, float2* kc, float2* vc, int64_t pos, hipStream_t s) {
+  const int n = (int)hdr->n, H = hdr->n_heads, dc = n / H;
+  const int64_t n_ctx = pos + 1;
+  const int slices = (int)((n_ctx + kAttnSlice - 1) / kAttnSlice);
+  const float scale = (float)(1.0 / sqrt((double)(2 * dc)));
+  if (dc <= 64)
+    hipLaunchKernelGGL(attn_partial_kernel<1>, dim3(slices, H), dim3(kAttnThreads), 0, s, hdr->q_rot, kc, vc, dc, n_ctx,
+                       hdr->max_ctx, scale, hdr->part);
+  else
+    hipLaunchKernelGGL(attn_partial_kernel<4>, dim3(slices, H), dim3(kAttnThreads), 0, s, hdr->q_rot, kc, vc, dc, n_ctx,
+                       hdr->max_ctx, scale, hdr->part);
+  hipLaunchKernelGGL(attn_combine_kernel, dim3(H), dim3(64), 0, s, hdr->part, slices, dc, hdr->o);
+}
+
+// The fused path: the four product launches and eight block kernels.
+fairy2i_status block_decode_fused(const void* plan, const void* plan_device, const float2* xin, float2* kc,
+                                  float2* vc, int64_t pos, float2* out, hipStream_t s) {
+  const auto* hdr = static_cast<const BlockPlanHeader*>(plan);
+  const int n = (int)hdr->n, f = (int)hdr->n_ff, dc = n / hdr->n_heads;
+  auto gtab = [&](int gi) {
+    return reinterpret_cast<const GroupTableHeader*>(static_cast<const char*>(plan) + hdr->table_off[gi]);
+  };
+  auto layer = [&](int gi, int i) -> const DecLayer& { return reinterpret_cast<const DecLayer*>(gtab(gi) + 1)[i]; };
+  auto out_of = [&](int gi, int i) {
+    const DecLayer& l = layer(gi, i);
+    return LayerOut{l.part, l.y, l.nkc, l.N};
+  };
+  auto targets = [&](int gi) {
+    OperandTargets t{};
+    t.count = gtab(gi)->h.n_layers;
+    for (int i = 0; i < t.count; ++i) {
+      t.xf[i] = layer(gi, i).xf;
+      t.xs[i] = layer(gi, i).xs;
+    }
+    t.nk4 = layer(gi, 0).nk4;
+    t.ctr = gtab(gi)->h.coop_ctr;
+    return t;
+  };
+  auto product = [&](int gi) {
+    DecLayer none{};
+    const auto* td = reinterpret_cast<const DecLayer*>(static_cast<const char*>(plan_device) + hdr->table_off[gi] +
+                                                        sizeof(GroupTableHeader));
+    launch_f4_product(gtab(gi)->h, none, td, s);
+  };
+  OperandArgs a{};
+  // attention input: RMSNorm of x, operand of q, k, v
+  a.K = n;
+  a.x = xin;
+  a.gamma = hdr->norm_attn;
+  a.eps = hdr->eps;
+  a.z_out = hdr->z;
+  a.t = targets(0);
+  launch_operand<kSrcNorm>(a, s);
+  product(0);
+  hipLaunchKernelGGL(rope_append_sum_kernel, dim3((n + 255) / 256), dim3(256), 0, s, out_of(0, 0), out_of(0, 1),
+                     out_of(0, 2), n, dc, pos, hdr->max_ctx, hdr->rope_base, hdr->q_rot, kc, vc);
+  launch_attention(hdr, kc, vc, pos, s);
+  // output projection input: the attention output as it stands
+  a = OperandArgs{};
+  a.K = n;
+  a.tok = reinterpret_cast<const uint32_t*>(hdr->o);
+  a.t = targets(1);
+  launch_operand<kSrcBf16>(a, s);
+  product(1);
+  // MLP input: h1 = x + attention branch, its RMSNorm; operand of gate and up
+  a = OperandArgs{};
+  a.K = n;
+  a.x = xin;
+  a.res = out_of(1, 0);
+  a.h_out = hdr->h1;
+  a.gamma = hdr->norm_mlp;
+  a.eps = hdr->eps;
+  a.z_out = hdr->z2;
+  a.t = targets(2);
+  launch_operand<kSrcNorm>(a, s);
+  product(2);
+  // down projection input: SwiGLU of gate and up
+  hipLaunchKernelGGL(swiglu_sum_kernel, dim3((f + 255) / 256), dim3(256), 0, s, out_of(2, 0), out_of(2, 1), f,
+                     reinterpret_cast<uint32_t*>(hdr->act));
+  a = OperandArgs{};
+  a.K = f;
+  a.tok = reinterpret_cast<const uint32_t*>(hdr->act);
+  a.t = targets(3);
+  launch_operand<kSrcBf16>(a, s);
+  product(3);
+  hipLaunchKernelGGL(add_sum_kernel, dim3((n + 255) / 256), dim3(256), 0, s, hdr->h1, out_of(3, 0), n, out);
+  return hip_st(hipGetLastError());
+}
+
 }  // namespace
 
 }  // namespace fairy2i
@@ -437,6 +840,11 @@ fairy2i_status fairy2i_block_build_plan(const fairy2i_block_desc* desc, void* wo
     hdr->table_bytes[gi] = tb;
     off += align256(tb);
   }
+  hdr->fused = desc->n <= kOpMaxK && desc->n_ff <= kOpMaxK;
+  for (int gi = 0; gi < kGroups; ++gi) {
+    const DecHeader& h = reinterpret_cast<const GroupTableHeader*>(pl + hdr->table_off[gi])->h;
+    if (h.mode != kModeBf16F4 || h.B != 1 || h.bands != 2 || h.nc != 8 || h.ntile != 1) hdr->fused = 0;
+  }
   return FAIRY2I_OK;
 }
 
@@ -469,18 +877,19 @@ fairy2i_status fairy2i_block_decode(const void* plan, const void* plan_device, c
   float2* vc = reinterpret_cast<float2*>(v_cache);
   hipError_t e;
   fairy2i_status st;
+  const float scale = (float)(1.0 / sqrt((double)(2 * dc)));
+  if (hdr->fused) return block_decode_fused(plan, plan_device, xin, kc, vc, pos, reinterpret_cast<float2*>(out), s);
   hipLaunchKernelGGL(add_rmsnorm_kernel, dim3(1), dim3(kNormThreads), 0, s, xin, nullptr, nullptr, hdr->norm_attn,
                      hdr->eps, n, hdr->z);
   if ((e = hipGetLastError()) != hipSuccess) return hip_st(e);
   if ((st = group(0)) != FAIRY2I_OK) return st;
   hipLaunchKernelGGL(rope_append_kernel, dim3((n + 255) / 256), dim3(256), 0, s, hdr->q, hdr->k, hdr->v, n, dc, pos,
                      hdr->max_ctx, hdr->rope_base, hdr->q_rot, kc, vc);
-  const float scale = (float)(1.0 / sqrt((double)(2 * dc)));
   if (dc <= 64)
-    hipLaunchKernelGGL(attn_partial_kernel<1>, dim3(slices, H), dim3(64), 0, s, hdr->q_rot, kc, vc, dc, n_ctx,
+    hipLaunchKernelGGL(attn_partial_kernel<1>, dim3(slices, H), dim3(kAttnThreads), 0, s, hdr->q_rot, kc, vc, dc, n_ctx,
                        hdr->max_ctx, scale, hdr->part);
   else
-    hipLaunchKernelGGL(attn_partial_kernel<4>, dim3(slices, H), dim3(64), 0, s, hdr->q_rot, kc, vc, dc, n_ctx,
+    hipLaunchKernelGGL(attn_partial_kernel<4>, dim3(slices, H), dim3(kAttnThreads), 0, s, hdr->q_rot, kc, vc, dc, n_ctx,
                        hdr->max_ctx, scale, hdr->part);
   hipLaunchKernelGGL(attn_combine_kernel, dim3(H), dim3(64), 0, s, hdr->part, slices, dc, hdr->o);
   if ((e = hipGetLastError()) != hipSuccess) return hip_st(e);

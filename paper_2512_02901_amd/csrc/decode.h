@@ -79,6 +79,18 @@ constexpr size_t kGroupCallBytes = 256;
 // claimed at run time, where the shortest groups sit).
 constexpr double kCoopStaticFrac = 0.65;
 
+// Group table of fairy2i_wl_group_build_table: this header followed by the
+// layer descriptors (the device copy is read by the kernels at the same
+// offsets).
+constexpr uint32_t kGroupMagic = 0xFA112101u;
+struct GroupTableHeader {
+  uint32_t magic, abi;
+  DecHeader h;
+  int32_t any_split, pad0_;
+  int64_t max_BN;
+};
+static_assert(sizeof(GroupTableHeader) % 16 == 0, "table header alignment");
+
 int dec_f4_bands(int T, int64_t B);
 int dec_ntile(int mode, int64_t B, int T);
 int dec_ncols(int mode, int64_t B);

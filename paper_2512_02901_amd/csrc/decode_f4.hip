@@ -5,71 +5,20 @@
 // straight out of their packed words, the activations as e4m3 digits.
 #include "common.h"
 #include "decode_dev.h"
+#include "f4_operand.h"
 
 namespace fairy2i {
 
 namespace {
 
 // ------------------------------------------------- prep, fp4 code path ---
-// Activation operand of the fp8 x fp4 product.  Each bf16 token b is scaled
-// by 2^S_b, S_b chosen so that its largest magnitude m lands in [2^7, 2^8).
-// A scaled value v (|v| < 2^8) is written as a pair of e4m3 digits
-//     hi = e4m3(v),   lo = e4m3((v - hi) * 2^5)      (round to nearest even),
-// v = hi + 2^-5 lo: hi holds the leading 4 significant bits, lo the next 4,
-// so the pair is exact whenever lo lands on the e4m3 grid (|v| >= 2^-7).
-//
-// The matrix cores multiply the digits exactly but add the products of an
-// MFMA in small groups with a narrow adder: a product more than about 2^13
-// below the largest product of its group loses the bits below that window
-// (measured with an in-bounds probe of v_mfma_f32_16x16x128_f8f6f4; groups of
-// values within 2^10 of each other are summed exactly).  So the values are
-// split into two bands by magnitude: |v| >= 1 goes to the first pair, whose
-// hi digits then span at most 2^8 .. 2^-3 and are summed exactly; smaller
-// values go, times 2^8, to a second pair.  Every value down to 2^-15 (2^-22 m)
-// is represented exactly, smaller ones to within 2^-23; the narrow adder can
-// only shave the lo digits and the second band, by at most about 2^-17 m per
-// group of products.  (One pair for all values would need half the columns,
-// but there a value near m drops the low bits of its small neighbours: 1.5e-4
-// relative L2 on tokens with a 300-sigma channel.)
-// A token owns 8 operand columns, 8 t' .. 8 t' + 7 for token t' of its tile
-// (two tokens per 16-column tile): column 4 band + j holds, for that band,
-// j = 0: hi of Re x, 1: hi of Im x, 2: lo of Re x, 3: lo of Im x.  The
-// output factor of token b is 2^-S_b (0 for an all-zero token).
-// With more tokens per call (B >= 3) a token gets one band only: columns
-// 4 t' + j for token t' of the tile (four tokens per tile), every value as
-// one (hi, lo) pair.  A bf16 value is then still written exactly (its 8
-// significant bits fit the pair down to 2^-14), but the narrow adder can
-// drop the low bits of small products that share an MFMA group with a
-// value near m: at most about 2^-13 of the group's largest product, 1.5e-4
-// relative L2 measured on tokens with a 300-sigma channel, against the
-// 1e-3 bar for bf16 activations.
+// Activation operand of the fp8 x fp4 product: see f4_operand.h (token
+// shift, two-band / one-band e4m3 digit pairs, operand layout).
 constexpr int kPrepF4Threads = 512;
 constexpr int kPrepUnroll = 4;     // loads a prep thread issues before using them
 constexpr int kPrepF4Blocks = 4;   // blocks per layer (tiles x K slices): each slice finds the token maxima itself
-constexpr float kLoScale = 32.0f;     // lo digit = residual of hi times 2^5
-constexpr float kBand2Scale = 256.0f;  // second band: values below 1, times 2^8
 constexpr int kTokensPerTile = 2;      // two bands: 8 operand columns per token
 constexpr int kMaxTokensPerTile = 4;   // one band: 4 operand columns per token
-
-// The (hi, lo) digit words of four values, |v| < 2^8 (byte i = value i):
-// hi = e4m3(v), lo = e4m3((v - hi) 2^5), e4m3 being OCP fp8 (1 sign bit, 4
-// exponent bits with bias 7, 3 mantissa bits, largest finite 448), rounded
-// to nearest with ties to even by the hardware conversion v_cvt_pk_fp8_f32;
-// its inverse gives hi back as a float, and v - hi is exact in float32.
-// The largest digit is 2^8 (hi of a value next to 2^8, or lo of a value
-// near 2^7), well inside e4m3's range.
-__device__ inline void digit_words(const float (&v)[4], uint32_t& hi, uint32_t& lo) {
-  int h = __builtin_amdgcn_cvt_pk_fp8_f32(v[0], v[1], 0, false);
-  h = __builtin_amdgcn_cvt_pk_fp8_f32(v[2], v[3], h, true);
-  const float r0 = (v[0] - __builtin_amdgcn_cvt_f32_fp8(h, 0)) * kLoScale;
-  const float r1 = (v[1] - __builtin_amdgcn_cvt_f32_fp8(h, 1)) * kLoScale;
-  const float r2 = (v[2] - __builtin_amdgcn_cvt_f32_fp8(h, 2)) * kLoScale;
-  const float r3 = (v[3] - __builtin_amdgcn_cvt_f32_fp8(h, 3)) * kLoScale;
-  int l = __builtin_amdgcn_cvt_pk_fp8_f32(r0, r1, 0, false);
-  l = __builtin_amdgcn_cvt_pk_fp8_f32(r2, r3, l, true);
-  hi = (uint32_t)h;
-  lo = (uint32_t)l;
-}
 
 // One block per (activation tile, layer): the largest magnitude of each of
 // the tile's tokens, then the digits of every value.
@@ -124,12 +73,7 @@ __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_kernel(DecHeader h
     const int tk = threadIdx.x, b = tpt * tile + tk;
     float g = 0.0f;
     for (int w = 0; w < kPrepF4Threads / 64; ++w) g = fmaxf(g, red[w][tk]);
-    int S = 0;
-    if (g > 0.0f) {
-      int ex;
-      frexpf(g, &ex);  // g in [2^(ex-1), 2^ex), so g * 2^(8 - ex) in [2^7, 2^8)
-      S = 8 - ex;
-    }
+    const int S = f4_token_shift(g);
     sh_S[tk] = S;
     if (blockIdx.z == 0 && tk < ntok && b < h.B) L.xs[b] = g > 0.0f ? ldexpf(1.0f, -S) : 0.0f;
   }
@@ -172,38 +116,12 @@ __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_kernel(DecHeader h
       if (idx >= uhi) break;
       const int hf = idx & 1, c = (idx >> 1) & 1, tk = (idx >> 2) % ntok, r = (idx >> 2) / ntok;
       uint32_t out[2][2][2] = {};  // [band][hi, lo][word]: bytes e = 0..7 of the half chunk
-      {
-        const int S = sh_S[tk];
-        float x[8];
-        bool small[8];
+      float xv[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const uint32_t bits = c ? (wu[u][e] & 0xFFFF0000u) : (wu[u][e] << 16);
-          x[e] = ldexpf(__uint_as_float(bits), S);  // exact: |x| < 2^8
-          small[e] = bands == 2 && fabsf(x[e]) < 1.0f;  // one band: every value in the first
-        }
-        for (int bd = 0; bd < bands; ++bd) {
-#pragma unroll
-          for (int w = 0; w < 2; ++w) {
-            float v[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int e = 4 * w + i;
-              v[i] = bd == 0 ? (small[e] ? 0.0f : x[e]) : (small[e] ? x[e] * kBand2Scale : 0.0f);
-            }
-            uint32_t hi, lo;
-            digit_words(v, hi, lo);
-            out[bd][0][w] = hi;
-            out[bd][1][w] = lo;
-          }
-        }
-      }
+      for (int e = 0; e < 8; ++e) xv[e] = __uint_as_float(c ? (wu[u][e] & 0xFFFF0000u) : (wu[u][e] << 16));
+      f4_unit_digits(xv, sh_S[tk], bands, out);
       // column cpt tk + 4 band + 2 digit + c of run r; this half is bytes 8 hf .. 8 hf + 7 of its chunk
-      for (int bd = 0; bd < bands; ++bd)
-#pragma unroll
-        for (int dg = 0; dg < 2; ++dg)
-          *reinterpret_cast<uint2*>(dst + ((int64_t)r * h.nc + cpt * tk + 4 * bd + 2 * dg + c) * 16 + 8 * hf) =
-              make_uint2(out[bd][dg][0], out[bd][dg][1]);
+      f4_store_unit(dst, r, h.nc, cpt * tk, c, hf, bands, out);
     }
   }
 }
@@ -589,13 +507,35 @@ __global__ __launch_bounds__((64 * F4Ring<T, NT * XW, GS>::WAVES)) void dec_stre
   // the block's items: those starting in an equal share of the call's steps
   // (the table lists layers by decreasing item length, so a block claims its
   // longest items first and its range ends with short ones)
+  // (both searches of the table advance a level per round trip, and both
+  // layers are loaded together: the prologue is a chain of memory latencies)
   int64_t b0, b1;
+  int la = 0;  // layer holding the block's first step
+  DecLayer La = inl;
   {
     const int64_t s0 = (int64_t)blockIdx.x * h.total_steps / gridDim.x;
     const int64_t s1 = ((int64_t)blockIdx.x + 1) * h.total_steps / gridDim.x;
     if (tab) {
-      b0 = item_at_step(load_layer(tab + find_layer_by_step(tab, h.n_layers, s0)), s0, h);
-      b1 = item_at_step(load_layer(tab + find_layer_by_step(tab, h.n_layers, s1 < h.total_steps ? s1 : s0)), s1, h);
+      const int64_t s1c = s1 < h.total_steps ? s1 : s0;
+      int lo0 = 0, hi0 = h.n_layers - 1, lo1 = 0, hi1 = h.n_layers - 1;
+      while (lo0 < hi0 || lo1 < hi1) {
+        const int m0 = (lo0 + hi0 + 1) >> 1, m1 = (lo1 + hi1 + 1) >> 1;
+        const int64_t v0 = tab[m0].step0, v1 = tab[m1].step0;
+        const int64_t u0 = uniform64(v0), u1 = uniform64(v1);
+        if (lo0 < hi0) {
+          if (u0 <= s0) lo0 = m0;
+          else hi0 = m0 - 1;
+        }
+        if (lo1 < hi1) {
+          if (u1 <= s1c) lo1 = m1;
+          else hi1 = m1 - 1;
+        }
+      }
+      la = lo0;
+      La = load_layer(tab + lo0);
+      const DecLayer Lb = load_layer(tab + lo1);
+      b0 = item_at_step(La, s0, h);
+      b1 = item_at_step(Lb, s1, h);
     } else {
       b0 = item_at_step(inl, s0, h);
       b1 = item_at_step(inl, s1, h);
@@ -619,8 +559,13 @@ __global__ __launch_bounds__((64 * F4Ring<T, NT * XW, GS>::WAVES)) void dec_stre
   ItemQueue iq;
   iq.n = 0;
   {
-    const int lidx = tab ? find_layer(tab, h.n_layers, i0) : 0;
-    const DecLayer L0 = tab ? load_layer(tab + lidx) : inl;
+    // the wave's first item is mostly in the layer already loaded
+    int lidx = la;
+    DecLayer L0 = La;
+    if (tab && (i0 < La.item0 || i0 >= La.item0 + (int64_t)La.nrb * La.nkc)) {
+      lidx = find_layer(tab, h.n_layers, i0);
+      L0 = load_layer(tab + lidx);
+    }
     lc.lidx = oc.lidx = lidx;
     lc.item = oc.item = i0;
     load_enter_layer(lc, L0, h);

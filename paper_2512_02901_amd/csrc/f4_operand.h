@@ -1,0 +1,122 @@
+// Activation operand of the fp8 x fp4 decode product (Sec. 3.4, Algorithm 1:
+// the activations enter the matrix cores against the code planes).  Shared by
+// the operand kernels of the grouped decode call and of the decoder block.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+namespace fairy2i {
+
+namespace {
+
+// Activation operand of the fp8 x fp4 product.  Each bf16 token b is scaled
+// by 2^S_b, S_b chosen so that its largest magnitude m lands in [2^7, 2^8).
+// A scaled value v (|v| < 2^8) is written as a pair of e4m3 digits
+//     hi = e4m3(v),   lo = e4m3((v - hi) * 2^5)      (round to nearest even),
+// v = hi + 2^-5 lo: hi holds the leading 4 significant bits, lo the next 4,
+// so the pair is exact whenever lo lands on the e4m3 grid (|v| >= 2^-7).
+//
+// The matrix cores multiply the digits exactly but add the products of an
+// MFMA in small groups with a narrow adder: a product more than about 2^13
+// below the largest product of its group loses the bits below that window
+// (measured with an in-bounds probe of v_mfma_f32_16x16x128_f8f6f4; groups of
+// values within 2^10 of each other are summed exactly).  So the values are
+// split into two bands by magnitude: |v| >= 1 goes to the first pair, whose
+// hi digits then span at most 2^8 .. 2^-3 and are summed exactly; smaller
+// values go, times 2^8, to a second pair.  Every value down to 2^-15 (2^-22 m)
+// is represented exactly, smaller ones to within 2^-23; the narrow adder can
+// only shave the lo digits and the second band, by at most about 2^-17 m per
+// group of products.  (One pair for all values would need half the columns,
+// but there a value near m drops the low bits of its small neighbours: 1.5e-4
+// relative L2 on tokens with a 300-sigma channel.)
+// A token owns 8 operand columns, 8 t' .. 8 t' + 7 for token t' of its tile
+// (two tokens per 16-column tile): column 4 band + j holds, for that band,
+// j = 0: hi of Re x, 1: hi of Im x, 2: lo of Re x, 3: lo of Im x.  The
+// output factor of token b is 2^-S_b (0 for an all-zero token).
+// With more tokens per call (B >= 3) a token gets one band only: columns
+// 4 t' + j for token t' of the tile (four tokens per tile), every value as
+// one (hi, lo) pair.  A bf16 value is then still written exactly (its 8
+// significant bits fit the pair down to 2^-14), but the narrow adder can
+// drop the low bits of small products that share an MFMA group with a
+// value near m: at most about 2^-13 of the group's largest product, 1.5e-4
+// relative L2 measured on tokens with a 300-sigma channel, against the
+// 1e-3 bar for bf16 activations.
+constexpr float kLoScale = 32.0f;     // lo digit = residual of hi times 2^5
+constexpr float kBand2Scale = 256.0f;  // second band: values below 1, times 2^8
+
+// The (hi, lo) digit words of four values, |v| < 2^8 (byte i = value i):
+// hi = e4m3(v), lo = e4m3((v - hi) 2^5), e4m3 being OCP fp8 (1 sign bit, 4
+// exponent bits with bias 7, 3 mantissa bits, largest finite 448), rounded
+// to nearest with ties to even by the hardware conversion v_cvt_pk_fp8_f32;
+// its inverse gives hi back as a float, and v - hi is exact in float32.
+// The largest digit is 2^8 (hi of a value next to 2^8, or lo of a value
+// near 2^7), well inside e4m3's range.
+__device__ inline void digit_words(const float (&v)[4], uint32_t& hi, uint32_t& lo) {
+  int h = __builtin_amdgcn_cvt_pk_fp8_f32(v[0], v[1], 0, false);
+  h = __builtin_amdgcn_cvt_pk_fp8_f32(v[2], v[3], h, true);
+  const float r0 = (v[0] - __builtin_amdgcn_cvt_f32_fp8(h, 0)) * kLoScale;
+  const float r1 = (v[1] - __builtin_amdgcn_cvt_f32_fp8(h, 1)) * kLoScale;
+  const float r2 = (v[2] - __builtin_amdgcn_cvt_f32_fp8(h, 2)) * kLoScale;
+  const float r3 = (v[3] - __builtin_amdgcn_cvt_f32_fp8(h, 3)) * kLoScale;
+  int l = __builtin_amdgcn_cvt_pk_fp8_f32(r0, r1, 0, false);
+  l = __builtin_amdgcn_cvt_pk_fp8_f32(r2, r3, l, true);
+  hi = (uint32_t)h;
+  lo = (uint32_t)l;
+}
+
+// Shift S of a token whose largest magnitude is g > 0: g 2^S lies in
+// [2^7, 2^8); 0 for an all-zero token.  Its output factor is 2^-S (0 if g = 0).
+__device__ inline int f4_token_shift(float g) {
+  int S = 0;
+  if (g > 0.0f) {
+    int ex;
+    frexpf(g, &ex);  // g in [2^(ex-1), 2^ex)
+    S = 8 - ex;
+  }
+  return S;
+}
+
+// Digit words of eight consecutive values of one component of a token (xv:
+// its bf16 values as floats), scaled by 2^S: out[band][0 = hi, 1 = lo][w],
+// word w holding values 4 w .. 4 w + 3.  Two bands: |v| >= 1 in the first,
+// smaller values times 2^8 in the second; one band: every value in the first.
+__device__ inline void f4_unit_digits(const float (&xv)[8], int S, int bands, uint32_t (&out)[2][2][2]) {
+  float x[8];
+  bool small[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    x[e] = ldexpf(xv[e], S);  // exact: |x| < 2^8
+    small[e] = bands == 2 && fabsf(x[e]) < 1.0f;
+  }
+  for (int bd = 0; bd < bands; ++bd) {
+#pragma unroll
+    for (int w = 0; w < 2; ++w) {
+      float v[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int e = 4 * w + i;
+        v[i] = bd == 0 ? (small[e] ? 0.0f : x[e]) : (small[e] ? x[e] * kBand2Scale : 0.0f);
+      }
+      digit_words(v, out[bd][0][w], out[bd][1][w]);
+    }
+  }
+}
+
+// Operand layout [run][nc columns][16 codes] bytes per activation tile: the
+// unit's words go to column col0 + 4 band + 2 digit + c of run r (col0 = the
+// token's first column, c = 0 for Re, 1 for Im), bytes 8 hf .. 8 hf + 7 of
+// the 16-code chunk (hf: which half of the run's codes the unit holds).
+__device__ inline void f4_store_unit(uint8_t* dst, int64_t r, int nc, int col0, int c, int hf, int bands,
+                                     const uint32_t (&out)[2][2][2]) {
+  for (int bd = 0; bd < bands; ++bd)
+#pragma unroll
+    for (int dg = 0; dg < 2; ++dg)
+      *reinterpret_cast<uint2*>(dst + (r * nc + col0 + 4 * bd + 2 * dg + c) * 16 + 8 * hf) =
+          make_uint2(out[bd][dg][0], out[bd][dg][1]);
+}
+
+}  // namespace
+
+}  // namespace fairy2i
