@@ -208,3 +208,34 @@ def test_block_llama_shape(gpu):
     err = rel_l2(y, yo)
     print(f"LLaMA block: end-to-end rel-L2 {err:.2e}, bf16 flips {flips}")
     assert err <= TOL_END
+
+
+def test_block_general_path_wide_heads(gpu):
+    """The unfused path: an FFN of 8256 complex entries, past the fused
+    path's 8192 (separate norm, preparation, reduction and SwiGLU kernels),
+    with 2 heads of 256 real dims (the attention kernel's wide variant),
+    quantised on the GPU; 70 cached positions."""
+    import torch
+    import paper_2512_02901_amd as f2
+    n, f, H, T, max_ctx, pos = 256, 8256, 2, 2, 80, 70
+    dl, cl = {}, {}
+    for i, (name, (N, K)) in enumerate(shapes(n, f).items()):
+        A = synth.torch_llama_weight(2 * N, 2 * K, 8500 + i, gpu)
+        U, W = f2.to_widely_linear(A)
+        cu, su = f2.quantize(U, T)
+        cw, sw = f2.quantize(W, T)
+        dl[name] = (f2.repack_tiled_fp4(cu), su, f2.repack_tiled_fp4(cw), sw)
+        cl[name] = (oracle.unpack(host(cu), K), host(su), oracle.unpack(host(cw), K), host(sw))
+        del A, U, W
+    x, na, nm, kc, vc = make_inputs(n, H, max_ctx, pos, 86)
+    blk = f2.WlBlock(dl, dev(na, gpu), dev(nm, gpu), n=n, n_ff=f, n_heads=H, T=T, max_ctx=max_ctx)
+    dk, dv = dev(kc, gpu), dev(vc, gpu)
+    y = host(blk.decode(dev(x, gpu), dk, dv, pos))
+    torch.cuda.synchronize()
+    flips = check_stages(blk, cl, x, na, nm, kc, host(dk), host(dv), pos, H, y)
+    yo, _, _, _ = ob.block_decode(x, cl, na, nm, kc, vc, pos, H)
+    err = rel_l2(y, yo)
+    print(f"general path: end-to-end rel-L2 {err:.2e}, bf16 flips {flips}")
+    assert err <= TOL_END
+    y2 = host(blk.decode(dev(x, gpu), dev(kc, gpu), dev(vc, gpu), pos))
+    np.testing.assert_array_equal(y.view(np.uint32), y2.view(np.uint32))
