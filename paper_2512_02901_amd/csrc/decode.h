@@ -14,12 +14,13 @@ constexpr int kModeBf16F4 = 2;  // bf16 activations as e4m3 digit pairs in two m
 
 constexpr int kCoopSlots = 4;     // steps in the cooperative kernel's ring
 // Cooperative fp4 kernel geometry by its activation tiles per call (NT = 1,
-// 2 or 4; three tiles run as four): waves per block (four for one tile, three
-// blocks per CU; eight for more, one block per CU, so that more row blocks
-// share each step's activation operand), waves per row block (with four tiles
-// two: one for the U planes, one for the W planes) and row blocks per group.
+// 2 or 4; three tiles run as four): waves per block (four for one or two
+// tiles, three or two blocks per CU, whose barriers are independent; eight
+// for four tiles, one block per CU, so that more row blocks share each
+// step's activation operand), waves per row block (with four tiles two: one
+// for the U planes, one for the W planes) and row blocks per group.
 constexpr int coop_nt(int ntile) { return ntile >= 3 ? 4 : ntile; }
-constexpr int coop_waves(int nt) { return nt >= 2 ? 8 : 4; }
+constexpr int coop_waves(int nt) { return nt >= 4 ? 8 : 4; }
 constexpr int coop_plane_split(int nt) { return nt >= 4 ? 2 : 1; }
 constexpr int coop_row_blocks(int ntile) { return coop_waves(coop_nt(ntile)) / coop_plane_split(coop_nt(ntile)); }
 constexpr int kKernelReg = 0;     // codes staged in registers; any batch, accumulator export
