@@ -79,6 +79,7 @@ fairy2i_status run_single_decode(DecLayer l, int32_t T, int32_t dtype, int64_t B
   h.n_layers = 1;
   h.total_items = (int64_t)l.nrb * l.nkc;
   h.total_steps = (int64_t)l.nrb * l.nk4;
+  h.max_nk4 = l.nk4;
   const int64_t acc_elems = acc ? (int64_t)2 * T * 2 * B * l.N * 2 : 0;
   return hip_status(launch_decode(h, l, nullptr, l.nkc > 1, B * (int64_t)l.N, acc != nullptr, acc_elems,
                                   acc, stream));
@@ -428,6 +429,7 @@ fairy2i_status fairy2i_wl_group_build_table(const fairy2i_wl_layer* layers, int3
     sitems += groups;
     ssteps += groups * l.nk4;
     if (l.nk4 < min_nk4) min_nk4 = l.nk4;
+    if (l.nk4 > h.max_nk4) h.max_nk4 = l.nk4;
     if (l.nkc > 1) any_split = 1;
     if (B * (int64_t)l.N > max_BN) max_BN = B * (int64_t)l.N;
     tab[i] = l;

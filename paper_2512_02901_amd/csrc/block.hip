@@ -489,29 +489,9 @@ __global__ __launch_bounds__(kOpThreads) void block_operand_kernel(OperandArgs a
     for (int t = 0; t < a.t.count; ++t) a.t.xs[t][0] = g > 0.0f ? ldexpf(1.0f, -S) : 0.0f;
     if (a.t.ctr) *a.t.ctr = 0u;
   }
-  const int nhalf = a.t.nk4 * 32;  // half runs of 8 codes in the operand (nhalf <= 2 E kOpThreads / 8)
-  for (int hr = tid; hr < nhalf; hr += kOpThreads) {
-    uint32_t w8[8];
-    if (8 * hr < K) {  // K % 8 == 0: the half run is in range or past K entirely
-      const uint4 p0 = *reinterpret_cast<const uint4*>(&tokw[8 * hr]);
-      const uint4 p1 = *reinterpret_cast<const uint4*>(&tokw[8 * hr + 4]);
-      w8[0] = p0.x; w8[1] = p0.y; w8[2] = p0.z; w8[3] = p0.w;
-      w8[4] = p1.x; w8[5] = p1.y; w8[6] = p1.z; w8[7] = p1.w;
-    } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) w8[e] = 0u;
-    }
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      float xv[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) xv[e] = __uint_as_float(c ? (w8[e] & 0xFFFF0000u) : (w8[e] << 16));
-      uint32_t out[2][2][2];
-      f4_unit_digits(xv, S, 2, out);
-      for (int t = 0; t < a.t.count; ++t)
-        f4_store_unit(reinterpret_cast<uint8_t*>(a.t.xf[t]), hr >> 1, 8, 0, c, hr & 1, 2, out);
-    }
-  }
+  uint8_t* const dst[3] = {reinterpret_cast<uint8_t*>(a.t.xf[0]), reinterpret_cast<uint8_t*>(a.t.xf[1]),
+                           reinterpret_cast<uint8_t*>(a.t.xf[2])};
+  f4_encode_token<kOpThreads, 3>(tokw, K, S, a.t.nk4, dst, a.t.count);
 }
 
 template <int SRC>

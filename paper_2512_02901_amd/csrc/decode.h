@@ -57,7 +57,7 @@ struct DecHeader {
   int32_t kernel;  // kKernelReg or kKernelStream
   int32_t grouped;  // every layer has per-group scales (fp4 path only)
   int32_t bands;    // fp4 path: activation digit bands per token (2: 8 columns, 1: 4 columns)
-  int32_t pad_;
+  int32_t max_nk4;  // the most 256-code steps of a layer of the call
   int64_t total_items;
   int64_t total_steps;  // 256-code steps of all work items
   int64_t total_ssteps; // block-cooperative kernel: steps of all row-block groups

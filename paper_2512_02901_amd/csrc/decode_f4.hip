@@ -126,6 +126,54 @@ __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_kernel(DecHeader h
   }
 }
 
+// One token (two bands, one 8-column tile): one block per layer reads the
+// token once into LDS (E entries per thread, K <= E kPrepF4Threads), reduces
+// its largest magnitude and writes the digits from LDS: one round of loads
+// where the general kernel above takes two.
+template <int E>
+__global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_token_kernel(DecHeader h, DecLayer inl,
+                                                                           const DecLayer* __restrict__ tab) {
+  const DecLayer L = tab ? load_layer(tab + blockIdx.x) : inl;
+  if (h.coop_ctr && blockIdx.x == 0 && threadIdx.x == 0) *h.coop_ctr = 0u;
+  __shared__ __attribute__((aligned(16))) uint32_t tokw[E * kPrepF4Threads];
+  __shared__ float red[kPrepF4Threads / 64];
+  __shared__ float sh_g;
+  const int K = L.K, tid = threadIdx.x, wave = tid >> 6;
+  const bool al4 = (reinterpret_cast<uintptr_t>(L.x) & 3) == 0;
+  const uint32_t* x32 = static_cast<const uint32_t*>(L.x);
+  const uint16_t* x16 = static_cast<const uint16_t*>(L.x);
+  uint32_t w[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = tid + e * kPrepF4Threads;
+    w[e] = 0u;
+    if (i < K) w[e] = al4 ? x32[i] : ((uint32_t)x16[2 * i] | ((uint32_t)x16[2 * i + 1] << 16));
+  }
+  float m = 0.0f;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = tid + e * kPrepF4Threads;
+    if (i < K) {
+      tokw[i] = w[e];
+      m = fmaxf(m, fmaxf(fabsf(__uint_as_float(w[e] << 16)), fabsf(__uint_as_float(w[e] & 0xFFFF0000u))));
+    }
+  }
+  for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+  if ((tid & 63) == 0) red[wave] = m;
+  __syncthreads();
+  if (tid == 0) {
+    float g = 0.0f;
+    for (int v = 0; v < kPrepF4Threads / 64; ++v) g = fmaxf(g, red[v]);
+    sh_g = g;
+  }
+  __syncthreads();
+  const float g = sh_g;
+  const int S = f4_token_shift(g);
+  if (tid == 0) L.xs[0] = g > 0.0f ? ldexpf(1.0f, -S) : 0.0f;
+  uint8_t* const dst[1] = {reinterpret_cast<uint8_t*>(L.xf)};
+  f4_encode_token<kPrepF4Threads, 1>(tokw, K, S, L.nk4, dst, 1);
+}
+
 // ------------------------------------------- streaming kernel, fp4 codes ---
 // The same ring, cursors and work items as above, for codes in the fp4 tiled
 // layout and bf16 activations as two e4m3 digits per value (hi, lo; see the
@@ -1311,6 +1359,22 @@ void launch_coop_f4(const DecHeader& h, const DecLayer* tab, hipStream_t s) {
 
 void launch_f4_prep(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
   // one token: one block per layer (its work is a latency chain, not throughput)
+  if (h.B == 1 && h.bands == 2 && h.nc == 8 && h.ntile == 1 && h.max_nk4 > 0) {
+    const dim3 g((unsigned)h.n_layers), b(kPrepF4Threads);
+    const int kmax = h.max_nk4 * 256;  // entries of the longest token, padded to whole steps
+    if (kmax <= 4 * kPrepF4Threads) {
+      hipLaunchKernelGGL(dec_prep_f4_token_kernel<4>, g, b, 0, s, h, inl, tab);
+      return;
+    }
+    if (kmax <= 8 * kPrepF4Threads) {
+      hipLaunchKernelGGL(dec_prep_f4_token_kernel<8>, g, b, 0, s, h, inl, tab);
+      return;
+    }
+    if (kmax <= 16 * kPrepF4Threads) {
+      hipLaunchKernelGGL(dec_prep_f4_token_kernel<16>, g, b, 0, s, h, inl, tab);
+      return;
+    }
+  }
   const int slices = (h.B == 1 || h.ntile >= kPrepF4Blocks) ? 1 : kPrepF4Blocks / h.ntile;
   hipLaunchKernelGGL(dec_prep_f4_kernel, dim3(h.ntile, h.n_layers, slices), dim3(kPrepF4Threads), 0, s, h, inl, tab);
 }

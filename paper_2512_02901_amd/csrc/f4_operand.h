@@ -117,6 +117,40 @@ __device__ inline void f4_store_unit(uint8_t* dst, int64_t r, int nc, int col0, 
           make_uint2(out[bd][dg][0], out[bd][dg][1]);
 }
 
+// The operand of one token for a one-token call (two bands, one 8-column
+// tile) from its bf16 (re, im) words tokw[0, K) (in LDS; K % 8 == 0) and its
+// shift S: every half run of the nk4 256-code steps (runs past K hold zeros)
+// by the block's NT threads, written to each of the ndst <= MAXD operand
+// buffers.
+template <int NT, int MAXD>
+__device__ inline void f4_encode_token(const uint32_t* tokw, int K, int S, int nk4, uint8_t* const (&dst)[MAXD],
+                                       int ndst) {
+  const int nhalf = nk4 * 32;
+  for (int hr = (int)threadIdx.x; hr < nhalf; hr += NT) {
+    uint32_t w8[8];
+    if (8 * hr < K) {  // the half run is in range or past K entirely
+      const uint4 p0 = *reinterpret_cast<const uint4*>(&tokw[8 * hr]);
+      const uint4 p1 = *reinterpret_cast<const uint4*>(&tokw[8 * hr + 4]);
+      w8[0] = p0.x; w8[1] = p0.y; w8[2] = p0.z; w8[3] = p0.w;
+      w8[4] = p1.x; w8[5] = p1.y; w8[6] = p1.z; w8[7] = p1.w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) w8[e] = 0u;
+    }
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      float xv[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) xv[e] = __uint_as_float(c ? (w8[e] & 0xFFFF0000u) : (w8[e] << 16));
+      uint32_t out[2][2][2];
+      f4_unit_digits(xv, S, 2, out);
+#pragma unroll
+      for (int t = 0; t < MAXD; ++t)
+        if (t < ndst) f4_store_unit(dst[t], hr >> 1, 8, 0, c, hr & 1, 2, out);
+    }
+  }
+}
+
 }  // namespace
 
 }  // namespace fairy2i
