@@ -38,21 +38,37 @@ FAIRY2I_HD inline void sa_split(double v, int* limb, uint32_t* lo, uint32_t* mid
   *hi = (uint32_t)(sh == 0 ? 0 : (M >> (64 - sh)));
 }
 
+// Loops over the words run with constant indices (fully unrolled on the
+// device), so the words stay in registers: every word a position selects is
+// picked by comparison, never by a computed index.
+#ifdef __HIP_DEVICE_COMPILE__
+#define SA_UNROLL _Pragma("unroll")
+#else
+#define SA_UNROLL
+#endif
+
 // Round (sum of limbs) * 2^-1074 / n to the nearest float32, ties to even.
 // `limbs` may be unnormalised (each < 2^63); n >= 1 and n <= 2^31.
 FAIRY2I_HD inline float sa_mean_to_f32(const uint64_t* limbs, uint64_t n) {
   uint32_t w[SA_LIMBS + 1];
   uint64_t carry = 0;
+  SA_UNROLL
   for (int i = 0; i < SA_LIMBS; ++i) {
     const uint64_t v = limbs[i] + carry;
     w[i] = (uint32_t)v;
     carry = v >> 32;
   }
   w[SA_LIMBS] = (uint32_t)carry;
-  int h = SA_LIMBS;
-  while (h >= 0 && w[h] == 0) --h;
+  int h = -1;  // highest nonzero word
+  SA_UNROLL
+  for (int i = 0; i <= SA_LIMBS; ++i)
+    if (w[i] != 0) h = i;
   if (h < 0) return 0.0f;
-  const int bitlen = 32 * h + (32 - __builtin_clz(w[h]));
+  uint32_t wh = 0;
+  SA_UNROLL
+  for (int i = 0; i <= SA_LIMBS; ++i)
+    if (i == h) wh = w[i];
+  const int bitlen = 32 * h + (32 - __builtin_clz(wh));
   // S64 = top 64 bits of the sum (bit bitlen-1 becomes bit 63), sticky = any
   // bit below them is set.
   uint64_t S64;
@@ -63,12 +79,18 @@ FAIRY2I_HD inline float sa_mean_to_f32(const uint64_t* limbs, uint64_t n) {
     S64 = S << (-shift);
   } else {
     const int ws = shift >> 5, bs = shift & 31;
-    const uint64_t lo64 = (uint64_t)w[ws] | ((uint64_t)w[ws + 1] << 32);
-    const uint64_t top = (ws + 2 <= SA_LIMBS) ? (uint64_t)w[ws + 2] : 0ull;
+    uint32_t a0 = 0, a1 = 0, a2 = 0;  // words ws, ws + 1, ws + 2 (0 past the top)
+    SA_UNROLL
+    for (int i = 0; i <= SA_LIMBS; ++i) {
+      if (i == ws) a0 = w[i];
+      if (i == ws + 1) a1 = w[i];
+      if (i == ws + 2) a2 = w[i];
+      if (i < ws && w[i] != 0) sticky = true;
+    }
+    const uint64_t lo64 = (uint64_t)a0 | ((uint64_t)a1 << 32);
+    const uint64_t top = (uint64_t)a2;
     S64 = bs == 0 ? lo64 : ((lo64 >> bs) | (top << (64 - bs)));
-    if (bs != 0 && (w[ws] & ((1u << bs) - 1u)) != 0) sticky = true;
-    for (int i = 0; i < ws; ++i)
-      if (w[i] != 0) sticky = true;
+    if (bs != 0 && (a0 & ((1u << bs) - 1u)) != 0) sticky = true;
   }
   // value = (S64 + frac) * 2^shift * 2^-1074 / n = (q + delta) * 2^E
   const uint64_t q = S64 / n;
