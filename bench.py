@@ -38,6 +38,7 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 INT8_PEAK_TOPS = 5000.0        # MI355X dense int8 MFMA, TOPS
+FP8_PEAK_TOPS = 5000.0         # MI355X dense fp8 MFMA, TFLOP/s (the e4m3 x e2m1 product is counted against it)
 PROFILES = os.path.join(ROOT, "profiles")
 PRODUCT_KERNEL_SRC = os.path.join(ROOT, "paper_2512_02901_amd", "csrc", "decode_f4.hip")
 
@@ -388,6 +389,26 @@ def traffic_record():
         return None
 
 
+def mfma_probe(f2, torch, dev, kind, iters, reps=10):
+    """Sustained rate of one MFMA instruction on this GPU (back-to-back
+    independent MFMAs, four waves per SIMD, no memory traffic), in TOPS:
+    the measured counterpart of the nominal peak, at the clock the chip
+    holds under matrix-core load."""
+    blocks = 4 * torch.cuda.get_device_properties(dev).multi_processor_count  # 16 waves per CU
+    sink = torch.empty(blocks * 256, dtype=torch.int32, device=dev)
+    ops = f2.probe_mfma(kind, blocks, iters, sink)
+    warm_up(lambda: f2.probe_mfma(kind, blocks, iters, sink), torch, 3, min_s=0.3)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        f2.probe_mfma(kind, blocks, iters, sink)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    return {"tops": round(ops / (us * 1e-6) / 1e12, 1), "us_per_launch": round(us, 1), "blocks": blocks,
+            "iters": iters}
+
+
 def prefill_bench(f2, synth, torch, dev, T=2, tokens=2048, reps=20):
     out = {}
     for name, (rows, cols) in (("q", synth.LLAMA2_7B_PROJ["q"]), ("gate", synth.LLAMA2_7B_PROJ["gate"])):
@@ -429,6 +450,16 @@ def prefill_bench(f2, synth, torch, dev, T=2, tokens=2048, reps=20):
         # context, not the product: the same dense int8 op count as one plain library GEMM
         # ((2 tokens) x K x (4TN), torch._int_mm), timed the same way
         out[name]["library_int8_gemm"] = library_int8_gemm(torch, dev, 2 * tokens, K, 4 * T * N, reps)
+    probe = mfma_probe(f2, torch, dev, f2.PROBE_MFMA_I8, 4096)
+    probe["frac_nominal_peak"] = round(probe["tops"] / INT8_PEAK_TOPS, 4)
+    probe["instruction"] = "v_mfma_i32_16x16x64_i8 (the GEMM's)"
+    out["mfma_i8_probe"] = probe
+    p32 = mfma_probe(f2, torch, dev, f2.PROBE_MFMA_I8_32X32, 4096)
+    p32["frac_nominal_peak"] = round(p32["tops"] / INT8_PEAK_TOPS, 4)
+    p32["instruction"] = "v_mfma_i32_32x32x32_i8"
+    out["mfma_i8_32x32_probe"] = p32
+    for name in ("q", "gate"):
+        out[name]["frac_measured_i8_peak"] = round(out[name]["tops"] / probe["tops"], 4)
     return out
 
 
@@ -785,7 +816,12 @@ def main():
                              "useful_tops": round(g["tops"] * 0.5, 1), "us": g["us"],
                              "workload": "2048 tokens x gate/up shape (real 11008x4096, complex 5504x2048), "
                                          "T=2, int8 activations",
+                             "frac_measured_i8_peak": g["frac_measured_i8_peak"],
+                             "mfma_i8_probe": pf["mfma_i8_probe"], "mfma_i8_32x32_probe": pf["mfma_i8_32x32_probe"],
                              "q": pf["q"], "gate": pf["gate"]}
+        probe = mfma_probe(f2, torch, dev, f2.PROBE_MFMA_F8F4, 4096)
+        probe["frac_nominal_peak"] = round(probe["tops"] / FP8_PEAK_TOPS, 4)
+        result["mfma_f8f4_probe"] = probe
         result["quantizer"] = quantizer_bench(f2, synth, torch, dev)
 
     if not args.no_cpu_baseline:

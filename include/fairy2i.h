@@ -614,6 +614,29 @@ fairy2i_status fairy2i_cpu_lut_wl_matmul(const uint8_t* codes_U, const float* sc
                                          float* y, int32_t* acc,
                                          void* workspace, size_t workspace_bytes, int32_t n_threads);
 
+/*
+ * Matrix-core rate probe, for the roofline figures (not part of the method):
+ * the sustained rate of the prefill GEMM's instruction (kind
+ * FAIRY2I_PROBE_MFMA_I8: v_mfma_i32_16x16x64_i8, 32768 operations), of the
+ * decode product's (FAIRY2I_PROBE_MFMA_F8F4: v_mfma_scale_f32_16x16x128_f8f6f4
+ * with e4m3 x e2m1 operands, 65536 operations) or of the larger int8 shape
+ * (FAIRY2I_PROBE_MFMA_I8_32X32: v_mfma_i32_32x32x32_i8, 65536 operations) on
+ * this GPU at the clock it holds under that load.  Launches `blocks` blocks
+ * of 256 threads on `stream`; every wave issues `iters` x 8 independent
+ * MFMAs (x 4 for the 32 x 32 shape) with no memory traffic and writes one
+ * int32 of their sums to sink[block * 256 + thread]
+ * (device memory, blocks * 256 words, contents meaningless).  *ops (host)
+ * receives the operations one launch performs; the caller times the launch.
+ * Errors: FAIRY2I_ERR_NULL; FAIRY2I_ERR_UNSUPPORTED for another kind;
+ * FAIRY2I_ERR_SHAPE unless 1 <= blocks <= 2^20 and 1 <= iters <= 2^24;
+ * FAIRY2I_ERR_HIP if the launch fails.
+ */
+#define FAIRY2I_PROBE_MFMA_I8 0
+#define FAIRY2I_PROBE_MFMA_F8F4 1
+#define FAIRY2I_PROBE_MFMA_I8_32X32 2
+fairy2i_status fairy2i_probe_mfma(int32_t kind, int32_t blocks, int32_t iters, int32_t* sink, double* ops,
+                                  void* stream);
+
 #ifdef __cplusplus
 }
 #endif

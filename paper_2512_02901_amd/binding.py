@@ -60,6 +60,7 @@ _SIGNATURES = {
     "fairy2i_cgemm_gauss_planar_workspace_bytes": (_c_size, [_c_p, _c_i32, _c_i64, _c_i64]),
     "fairy2i_cgemm_gauss_planar": (_c_i32, [_c_p, _c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_i64, _c_i32, _c_p,
                                             _c_size, _c_p]),
+    "fairy2i_probe_mfma": (_c_i32, [_c_i32, _c_i32, _c_i32, _c_p, _c_p, _c_p]),
     "fairy2i_cpu_lut_workspace_bytes": (_c_size, [_c_i32, _c_i64, _c_i64, _c_i32]),
     "fairy2i_cpu_lut_wl_matmul": (_c_i32, [_c_p, _c_p, _c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_p, _c_i64,
                                            _c_p, _c_p, _c_p, _c_size, _c_i32]),
@@ -150,6 +151,26 @@ def _require(t, dtype, name, device=None):
 
 
 # ------------------------------------------------------------------ API ---
+
+PROBE_MFMA_I8 = 0    # v_mfma_i32_16x16x64_i8 (the prefill GEMM's instruction)
+PROBE_MFMA_F8F4 = 1  # v_mfma_scale_f32_16x16x128_f8f6f4, e4m3 x e2m1 (the decode product's)
+PROBE_MFMA_I8_32X32 = 2  # v_mfma_i32_32x32x32_i8
+
+
+def probe_mfma(kind: int, blocks: int, iters: int, sink) -> float:
+    """Launch the matrix-core rate probe on the current stream of sink's
+    device (sink: int32 device tensor of at least blocks * 256 words);
+    returns the operations of the launch, for the caller to time."""
+    torch = _torch()
+    lib = load()
+    _require(sink, torch.int32, "sink")
+    if sink.numel() < blocks * 256:
+        raise ValueError("sink needs blocks * 256 words")
+    ops = ctypes.c_double()
+    _check(lib.fairy2i_probe_mfma(kind, blocks, iters, _ptr(sink), ctypes.byref(ops), _stream_ptr(sink)),
+           "fairy2i_probe_mfma")
+    return ops.value
+
 
 def to_widely_linear(A):
     """A: float32 [2N, 2K] device tensor -> (U, W) complex64 [N, K]."""

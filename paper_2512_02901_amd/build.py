@@ -39,6 +39,8 @@ EXTRA = {
     # atomic optimizer would read each result back at once, waiting for every
     # load in flight)
     "decode_f4.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"],
+    # accumulators in VGPRs: the probe loops are then the MFMAs alone
+    "probe.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
 }
 
 

@@ -287,3 +287,17 @@ def test_cgemm_validation(lib):
     assert wsb(ctypes.byref(Ks), 0, M, N) == 0
     assert wsb(ctypes.byref(Ks), 1, 0, N) == 0
     assert wsb(ctypes.byref((ctypes.c_int64 * 2)(0, 5)), 1, M, N) == 0
+
+
+def test_probe_mfma_validation(lib):
+    """The matrix-core rate probe rejects bad arguments before any launch and
+    names the operations of a launch only when it launches."""
+    ops = ctypes.c_double(-1.0)
+    probe = lib.fairy2i_probe_mfma
+    assert probe(binding.PROBE_MFMA_I8, 4, 8, None, ctypes.byref(ops), None) == binding.ERR_NULL
+    assert probe(binding.PROBE_MFMA_I8, 4, 8, P, None, None) == binding.ERR_NULL
+    assert probe(7, 4, 8, P, ctypes.byref(ops), None) == binding.ERR_UNSUPPORTED
+    assert probe(binding.PROBE_MFMA_F8F4, 0, 8, P, ctypes.byref(ops), None) == binding.ERR_SHAPE
+    assert probe(binding.PROBE_MFMA_F8F4, 4, 0, P, ctypes.byref(ops), None) == binding.ERR_SHAPE
+    assert probe(binding.PROBE_MFMA_I8, (1 << 20) + 1, 8, P, ctypes.byref(ops), None) == binding.ERR_SHAPE
+    assert ops.value == -1.0
