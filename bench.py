@@ -241,9 +241,12 @@ def qat_bench(f2, synth, torch, dev, T=2, tokens=4096, reps=10):
     """One quantisation-aware training step of a q-shaped widely-linear layer
     (masters U, W complex 2048 x 2048, T stages) on `tokens` bf16 tokens:
     fake-quant forward of both masters, Y = X U^T + conj(X) W^T, the input
-    gradient and both weight gradients (Gauss GEMMs), and the
-    straight-through gradients of the masters.  Synthetic LLaMA-shaped
-    masters, N(0,1) tokens and output gradients."""
+    gradient and both weight gradients, and the straight-through gradients
+    of the masters.  The products run in the layer's real form (R from
+    W^ once per step, three plain bf16 GEMMs, the weight gradients read off
+    G_R); the same step with Gauss's complex GEMMs (planar path, and the
+    single-kernel path for the GEMMs alone) is reported next to it.
+    Synthetic LLaMA-shaped masters, N(0,1) tokens and output gradients."""
     rows, cols = synth.LLAMA2_7B_PROJ["q"]
     N, K = rows // 2, cols // 2
     A = synth.torch_llama_weight(rows, cols, 6000, dev)
@@ -257,8 +260,13 @@ def qat_bench(f2, synth, torch, dev, T=2, tokens=4096, reps=10):
     GX = torch.empty(tokens, K, dtype=torch.complex64, device=dev)
     GU = torch.empty(N, K, dtype=torch.complex64, device=dev)
     GW = torch.empty(N, K, dtype=torch.complex64, device=dev)
+    R = torch.empty(2 * N, 2 * K, dtype=torch.bfloat16, device=dev)
+    GR = torch.empty(2 * N, 2 * K, dtype=torch.float32, device=dev)
+    Xr, GYr = X.view(tokens, 2 * K), GY.view(tokens, 2 * N)
+    Yr, GXr = torch.view_as_real(Y).view(tokens, 2 * N), torch.view_as_real(GX).view(tokens, 2 * K)
+    lt_ws = torch.empty(f2.load().fairy2i_gemm_bf16_workspace_bytes(), dtype=torch.uint8, device=dev)
     state = {}
-    # the GEMMs run on the planar path (bf16 planes, one batched library GEMM); one workspace for all
+    # the Gauss GEMMs on the planar path (bf16 planes, one batched library GEMM); one workspace for all
     ws = torch.empty(max(f2.cgemm_gauss_planar_workspace_bytes(kk, m, n)
                          for kk, m, n in (([K, K], tokens, N), ([N, N], tokens, K), ([tokens], N, K))),
                      dtype=torch.uint8, device=dev)
@@ -271,29 +279,32 @@ def qat_bench(f2, synth, torch, dev, T=2, tokens=4096, reps=10):
         state["u"] = f2.qat_fake_quant(U, T)
         state["w"] = f2.qat_fake_quant(W, T)
 
-    def fwd():
-        gemm([(X, 0, 0, state["u"][0], 0, 0, K), (X, 0, 1, state["w"][0], 0, 0, K)], tokens, N, Y)
-
-    def bwd_x():
-        gemm([(GY, 0, 0, state["u"][0], 1, 1, N), (GY, 0, 1, state["w"][0], 1, 0, N)], tokens, K, GX)
-
-    def bwd_w():
-        gemm([(GY, 1, 0, X, 1, 1, tokens)], N, K, GU)
-        gemm([(GY, 1, 0, X, 1, 0, tokens)], N, K, GW)
-
     def ste():
         f2.qat_ste_backward(state["u"][1], state["u"][2], GU)
         f2.qat_ste_backward(state["w"][1], state["w"][2], GW)
 
-    phases = [("fake_quant", fq), ("forward_gemm", fwd), ("input_grad_gemm", bwd_x), ("weight_grad_gemms", bwd_w),
-              ("ste_backward", ste)]
-    fq()
-    for _, fn in phases:
-        fn()
-    warm_up(lambda: [fn() for _, fn in phases], torch, 3)
-    out = {"workload": f"one QAT step of a q-shaped layer (complex {N}x{K}, T={T}), {tokens} bf16 tokens",
-           "gemm_path": "planar: bf16 planes (Re, Im, Re+Im) by this library's kernels, the three real products "
-                        "as one batched hipBLASLt GEMM, combine kernel"}
+    # real form
+    def r_fwd():
+        f2.wl_realify(state["u"][0], state["w"][0], out=R)
+        f2.gemm_bf16(Xr, R, transB=True, out=Yr, workspace=lt_ws)
+
+    def r_bwd_x():
+        f2.gemm_bf16(GYr, R, out=GXr, workspace=lt_ws)
+
+    def r_bwd_w():
+        f2.gemm_bf16(GYr, Xr, transA=True, out=GR, workspace=lt_ws)
+        f2.wl_unrealify_grad(GR, N, K, out=(GU, GW))
+
+    # Gauss's complex GEMMs
+    def g_fwd():
+        gemm([(X, 0, 0, state["u"][0], 0, 0, K), (X, 0, 1, state["w"][0], 0, 0, K)], tokens, N, Y)
+
+    def g_bwd_x():
+        gemm([(GY, 0, 0, state["u"][0], 1, 1, N), (GY, 0, 1, state["w"][0], 1, 0, N)], tokens, K, GX)
+
+    def g_bwd_w():
+        gemm([(GY, 1, 0, X, 1, 1, tokens)], N, K, GU)
+        gemm([(GY, 1, 0, X, 1, 0, tokens)], N, K, GW)
 
     def timed(fn):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -304,25 +315,41 @@ def qat_bench(f2, synth, torch, dev, T=2, tokens=4096, reps=10):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / reps * 1e3
 
-    total = 0.0
-    for name, fn in phases:
-        us = timed(fn)
-        out[name + "_us"] = round(us, 1)
-        total += us
-    out["step_us"] = round(total, 1)
-    # each GEMM phase: 3 real products of 2 M N K flops per complex MAC; "effective" counts the 8 flops of a
-    # complex MAC done with four products
-    macs = {"forward_gemm": 2 * tokens * N * K, "input_grad_gemm": 2 * tokens * N * K,
-            "weight_grad_gemms": 2 * N * K * tokens}
+    def run(phases):
+        fq()
+        for _, fn in phases:
+            fn()
+        warm_up(lambda: [fn() for _, fn in phases], torch, 3)
+        res = {}
+        for name, fn in phases:
+            res[name + "_us"] = round(timed(fn), 1)
+        res["step_us"] = round(sum(res.values()), 1)
+        return res
+
+    out = {"workload": f"one QAT step of a q-shaped layer (complex {N}x{K}, T={T}), {tokens} bf16 tokens",
+           "gemm_path": "real form: R (bf16 2N x 2K) from W^ each step, Y = X R^T, G_X = G_Y R, G_R = G_Y^T X as "
+                        "plain bf16 hipBLASLt GEMMs, G_U and G_W read off G_R"}
+    out.update(run([("fake_quant", fq), ("forward_gemm", r_fwd), ("input_grad_gemm", r_bwd_x),
+                    ("weight_grad_gemms", r_bwd_w), ("ste_backward", ste)]))
+    # per GEMM phase (M N K = tokens x 2048 x 2048): the real form executes one real product of
+    # 2 M (2N) (2K) = 8 M N K flops; the layer's two complex products are 16 M N K flops counted as 8 per
+    # complex MAC ("effective"); Gauss executes 3 real products of 2 M N (2K) = 12 M N K flops
+    macs = {"forward_gemm": tokens * N * K, "input_grad_gemm": tokens * N * K, "weight_grad_gemms": N * K * tokens}
     gemm_us = sum(out[k + "_us"] for k in macs)
-    out["gemm_exec_TFLOPs"] = round(6 * sum(macs.values()) / gemm_us / 1e6, 1)
-    out["gemm_effective_TFLOPs"] = round(8 * sum(macs.values()) / gemm_us / 1e6, 1)
+    out["gemm_exec_TFLOPs"] = round(8 * sum(macs.values()) / gemm_us / 1e6, 1)
+    out["gemm_effective_TFLOPs"] = round(16 * sum(macs.values()) / gemm_us / 1e6, 1)
     out["gemm_frac_bf16_peak"] = round(out["gemm_exec_TFLOPs"] / 2500.0, 4)
-    # the same three GEMM phases on the single-kernel path, for comparison
+    gauss = run([("fake_quant", fq), ("forward_gemm", g_fwd), ("input_grad_gemm", g_bwd_x),
+                 ("weight_grad_gemms", g_bwd_w), ("ste_backward", ste)])
+    g_us = sum(gauss[k + "_us"] for k in macs)
+    gauss["gemm_exec_TFLOPs"] = round(12 * sum(macs.values()) / g_us / 1e6, 1)
+    gauss["gemm_effective_TFLOPs"] = round(16 * sum(macs.values()) / g_us / 1e6, 1)
+    out["gauss_planar"] = gauss
+    # the same three GEMM phases on the single-kernel Gauss path, for comparison
     mode["planar"] = False
-    warm_up(lambda: [fn() for name, fn in phases if name in macs], torch, 3)
-    out["single_kernel_gemms_us"] = round(sum(timed(fn) for name, fn in phases if name in macs), 1)
-    del U, W, X, GY, Y, GX, GU, GW, state, ws
+    warm_up(lambda: [fn() for fn in (g_fwd, g_bwd_x, g_bwd_w)], torch, 3)
+    out["gauss_single_kernel_gemms_us"] = round(sum(timed(fn) for fn in (g_fwd, g_bwd_x, g_bwd_w)), 1)
+    del U, W, X, GY, Y, GX, GU, GW, R, GR, state, ws, lt_ws
     torch.cuda.empty_cache()
     return out
 

@@ -580,6 +580,61 @@ fairy2i_status fairy2i_cgemm_gauss_planar(const fairy2i_cgemm_operand* A, const 
                                           void* stream);
 
 /*
+ * Real form of the layer's training products (Sec. 3.1, Eq. UW-from-R read
+ * backwards, with Eq. realify-ops).  y = U x + W conj(x) is the real map of
+ * (Re, Im) pairs whose 2 x 2 block for output n and input k is
+ *   [ Re U + Re W   Im W - Im U ]
+ *   [ Im U + Im W   Re U - Re W ]
+ * fairy2i_wl_realify writes it as R: bf16 [2N][2K] row-major, entry
+ * (2n + a, 2k + b) = block (a, b) of (n, k), each the exact sum or
+ * difference of the two inputs rounded once (nearest even).  U, W: [N][K]
+ * complex, float32 pairs (dtype FAIRY2I_ACT_F32) or bf16 pairs
+ * (FAIRY2I_ACT_BF16), device memory.  With tokens stored as (re, im) pairs,
+ * a [M][K] complex matrix is a real M x 2K matrix in place, and the three
+ * products of a training step are plain real GEMMs (fairy2i_gemm_bf16):
+ *   Y   [M][N] complex = X R^T     (forward; X bf16 pairs)
+ *   G_X [M][K] complex = G_Y R     (G_Y rounded to bf16 pairs first)
+ *   G_R [2N][2K] float = G_Y^T X
+ * and fairy2i_wl_unrealify_grad reads G_U = G_Y^T conj(X) and
+ * G_W = G_Y^T X (complex64 [N][K], device) off G_R's blocks:
+ *   Re G_U = G_R[2n][2k] + G_R[2n+1][2k+1], Im G_U = G_R[2n+1][2k] - G_R[2n][2k+1],
+ *   Re G_W = G_R[2n][2k] - G_R[2n+1][2k+1], Im G_W = G_R[2n][2k+1] + G_R[2n+1][2k].
+ * These are the products fairy2i_cgemm_gauss computes with Gauss's three
+ * real products per complex product; the real form needs four real products'
+ * work for both segments instead of six, and no operand planes.
+ * fairy2i_f32_to_bf16: out[i] = in[i] rounded to bf16 (nearest even),
+ * n values, device memory.
+ * Errors: FAIRY2I_ERR_NULL; FAIRY2I_ERR_DTYPE; FAIRY2I_ERR_SHAPE for
+ * non-positive sizes or N K > 2^30 (realify, unrealify), n <= 0
+ * (f32_to_bf16); FAIRY2I_ERR_HIP if a launch fails.
+ */
+fairy2i_status fairy2i_wl_realify(const void* U, const void* W, int32_t dtype, int64_t N, int64_t K, void* R,
+                                  void* stream);
+fairy2i_status fairy2i_wl_unrealify_grad(const float* G_R, int64_t N, int64_t K, float* G_U, float* G_W,
+                                         void* stream);
+fairy2i_status fairy2i_f32_to_bf16(const float* in, int64_t n, void* out, void* stream);
+
+/*
+ * Plain real GEMM on the matrix cores, for the real form above (the
+ * vendor library, hipBLASLt, bf16 operands, float32 accumulation and
+ * output): C = op(A) op(B), every matrix row-major in device memory:
+ * op(A) is M x K, A itself (transA = 0, lda >= K) or the transpose of a
+ * stored K x M matrix (transA = 1, lda >= M); op(B) is K x N, B itself
+ * (transB = 0, ldb >= N) or the transpose of a stored N x K matrix
+ * (transB = 1, ldb >= K); C: float32 M x N, ldc >= N, overwritten.
+ * workspace: device buffer of at least fairy2i_gemm_bf16_workspace_bytes()
+ * bytes for the library.  The library's first heuristic choice per problem
+ * shape is kept for the process.
+ * Errors: FAIRY2I_ERR_NULL; FAIRY2I_ERR_SHAPE (sizes, transposition flags,
+ * leading dimensions); FAIRY2I_ERR_WORKSPACE; FAIRY2I_ERR_UNSUPPORTED if the
+ * library offers no algorithm; FAIRY2I_ERR_HIP.
+ */
+size_t fairy2i_gemm_bf16_workspace_bytes(void);
+fairy2i_status fairy2i_gemm_bf16(const void* A, int64_t lda, int32_t transA, const void* B, int64_t ldb,
+                                 int32_t transB, int64_t M, int64_t N, int64_t K, float* C, int64_t ldc,
+                                 void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * CPU table-lookup product for int8 activations (Sec. 3.4, the paragraph on
  * lookup tables for CPU inference): every four consecutive codes of a row
  * (one byte of the canonical packed layout) index a 256-entry table of their

@@ -61,6 +61,12 @@ _SIGNATURES = {
     "fairy2i_cgemm_gauss_planar": (_c_i32, [_c_p, _c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_i64, _c_i32, _c_p,
                                             _c_size, _c_p]),
     "fairy2i_probe_mfma": (_c_i32, [_c_i32, _c_i32, _c_i32, _c_p, _c_p, _c_p]),
+    "fairy2i_wl_realify": (_c_i32, [_c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_p]),
+    "fairy2i_wl_unrealify_grad": (_c_i32, [_c_p, _c_i64, _c_i64, _c_p, _c_p, _c_p]),
+    "fairy2i_f32_to_bf16": (_c_i32, [_c_p, _c_i64, _c_p, _c_p]),
+    "fairy2i_gemm_bf16_workspace_bytes": (_c_size, []),
+    "fairy2i_gemm_bf16": (_c_i32, [_c_p, _c_i64, _c_i32, _c_p, _c_i64, _c_i32, _c_i64, _c_i64, _c_i64, _c_p, _c_i64,
+                                   _c_p, _c_size, _c_p]),
     "fairy2i_cpu_lut_workspace_bytes": (_c_size, [_c_i32, _c_i64, _c_i64, _c_i32]),
     "fairy2i_cpu_lut_wl_matmul": (_c_i32, [_c_p, _c_p, _c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_p, _c_i64,
                                            _c_p, _c_p, _c_p, _c_size, _c_i32]),
@@ -151,6 +157,95 @@ def _require(t, dtype, name, device=None):
 
 
 # ------------------------------------------------------------------ API ---
+
+def wl_realify(U, W, out=None):
+    """U, W: [N, K] complex64 or bf16 [N, K, 2] device tensors -> R: bf16
+    [2N, 2K], the layer's real map with (re, im) rows and columns
+    interleaved (fairy2i_wl_realify; out: such a tensor to write)."""
+    torch = _torch()
+    lib = load()
+    if U.dtype == torch.complex64:
+        dt = ACT_F32
+        N, K = U.shape
+    else:
+        dt = ACT_BF16
+        N, K = U.shape[0], U.shape[1]
+    for t, n in ((U, "U"), (W, "W")):
+        _require(t, U.dtype, n, U.device)
+        if t.shape != U.shape or (dt == ACT_BF16 and (t.dim() != 3 or t.shape[2] != 2 or t.dtype != torch.bfloat16)):
+            raise ValueError(f"{n} must be [N, K] complex64 or [N, K, 2] bf16")
+    R = torch.empty((2 * N, 2 * K), dtype=torch.bfloat16, device=U.device) if out is None else out
+    _require(R, torch.bfloat16, "out", U.device)
+    if tuple(R.shape) != (2 * N, 2 * K):
+        raise ValueError("out must be [2N, 2K]")
+    _check(lib.fairy2i_wl_realify(_ptr(U), _ptr(W), dt, N, K, _ptr(R), _stream_ptr(U)), "fairy2i_wl_realify")
+    return R
+
+
+def wl_unrealify_grad(G_R, N, K, out=None):
+    """G_R: float32 [2N, 2K] -> (G_U, G_W) complex64 [N, K] (out: a pair
+    of such tensors to write)."""
+    torch = _torch()
+    lib = load()
+    _require(G_R, torch.float32, "G_R")
+    if tuple(G_R.shape) != (2 * N, 2 * K):
+        raise ValueError("G_R must be [2N, 2K]")
+    if out is None:
+        G_U = torch.empty((N, K), dtype=torch.complex64, device=G_R.device)
+        G_W = torch.empty_like(G_U)
+    else:
+        G_U, G_W = out
+        for t, n in ((G_U, "G_U"), (G_W, "G_W")):
+            _require(t, torch.complex64, n, G_R.device)
+            if tuple(t.shape) != (N, K):
+                raise ValueError(f"{n} must be [N, K]")
+    _check(lib.fairy2i_wl_unrealify_grad(_ptr(G_R), N, K, _ptr(G_U), _ptr(G_W), _stream_ptr(G_R)),
+           "fairy2i_wl_unrealify_grad")
+    return G_U, G_W
+
+
+def f32_to_bf16(x, out=None):
+    """float32 (or complex64, as its float pairs) device tensor -> bf16 of
+    the same number of values, nearest even; complex input gives [..., 2]."""
+    torch = _torch()
+    lib = load()
+    _require(x, None, "x")
+    xf = torch.view_as_real(x) if x.dtype == torch.complex64 else x
+    if xf.dtype != torch.float32:
+        raise TypeError("x must be float32 or complex64")
+    if out is None:
+        out = torch.empty(xf.shape, dtype=torch.bfloat16, device=x.device)
+    _require(out, torch.bfloat16, "out", x.device)
+    if out.numel() != xf.numel():
+        raise ValueError("out must hold as many values as x")
+    _check(lib.fairy2i_f32_to_bf16(ctypes.c_void_p(xf.data_ptr()), xf.numel(), _ptr(out), _stream_ptr(x)),
+           "fairy2i_f32_to_bf16")
+    return out
+
+
+def gemm_bf16(A, B, transA=False, transB=False, out=None, workspace=None):
+    """C (float32 M x N) = op(A) op(B) for bf16 row-major 2-D device tensors
+    (fairy2i_gemm_bf16); op(X) is X or X^T."""
+    torch = _torch()
+    lib = load()
+    _require(A, torch.bfloat16, "A")
+    _require(B, torch.bfloat16, "B", A.device)
+    if A.dim() != 2 or B.dim() != 2:
+        raise ValueError("A and B must be 2-D")
+    M, K = (A.shape[1], A.shape[0]) if transA else (A.shape[0], A.shape[1])
+    Kb, N = (B.shape[1], B.shape[0]) if transB else (B.shape[0], B.shape[1])
+    if Kb != K:
+        raise ValueError("inner dimensions differ")
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float32, device=A.device)
+    _require(out, torch.float32, "out", A.device)
+    if tuple(out.shape) != (M, N):
+        raise ValueError("out must be M x N")
+    ws, wsb = _workspace(lib.fairy2i_gemm_bf16_workspace_bytes(), workspace, A.device)
+    _check(lib.fairy2i_gemm_bf16(_ptr(A), A.shape[1], int(transA), _ptr(B), B.shape[1], int(transB), M, N, K,
+                                 _ptr(out), N, _ptr(ws), wsb, _stream_ptr(A)), "fairy2i_gemm_bf16")
+    return out
+
 
 PROBE_MFMA_I8 = 0    # v_mfma_i32_16x16x64_i8 (the prefill GEMM's instruction)
 PROBE_MFMA_F8F4 = 1  # v_mfma_scale_f32_16x16x128_f8f6f4, e4m3 x e2m1 (the decode product's)

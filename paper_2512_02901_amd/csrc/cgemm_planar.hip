@@ -137,21 +137,42 @@ bool lt_ok(hipblasStatus_t s) { return s == HIPBLAS_STATUS_SUCCESS; }
 // P[z] (row-major M x N) = Aplanes[z] (M x Kp) Bplanes[z] (N x Kp)^T for z < 3.
 // Column-major view: P[z]^T (N x M, ld N) = Bplanes[z]^T (op T of a Kp x N
 // matrix, ld Kp) times Aplanes[z]^T (a Kp x M matrix, ld Kp).
+// The current device's handle (created on first use) in *h.
+fairy2i_status lt_handle(int* dev, hipblasLtHandle_t* h) {
+  if (hipGetDevice(dev) != hipSuccess) return FAIRY2I_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_lt_mutex);
+  auto it = g_lt_handles.find(*dev);
+  if (it == g_lt_handles.end()) {
+    if (!lt_ok(hipblasLtCreate(h))) return FAIRY2I_ERR_HIP;
+    g_lt_handles[*dev] = *h;
+  } else {
+    *h = it->second;
+  }
+  return FAIRY2I_OK;
+}
+
+// The library's first heuristic choice for a problem, or false.
+bool lt_pick(hipblasLtHandle_t h, const LtDescs& d, hipblasLtMatmulAlgo_t* algo) {
+  hipblasLtMatmulPreference_t pref = nullptr;
+  const uint64_t wsb = kLtWorkspaceBytes;
+  hipblasLtMatmulHeuristicResult_t res[1];
+  int found = 0;
+  const bool ok =
+      lt_ok(hipblasLtMatmulPreferenceCreate(&pref)) &&
+      lt_ok(hipblasLtMatmulPreferenceSetAttribute(pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES, &wsb, sizeof(wsb))) &&
+      lt_ok(hipblasLtMatmulAlgoGetHeuristic(h, d.op, d.a, d.b, d.c, d.c, pref, 1, res, &found));
+  if (pref) hipblasLtMatmulPreferenceDestroy(pref);
+  if (!ok || found < 1 || res[0].workspaceSize > kLtWorkspaceBytes) return false;
+  *algo = res[0].algo;
+  return true;
+}
+
 fairy2i_status lt_products(const uint16_t* Ap, const uint16_t* Bp, float* P, int64_t M, int64_t N, int64_t Kp,
                            void* lt_ws, hipStream_t s) {
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return FAIRY2I_ERR_HIP;
   hipblasLtHandle_t h = nullptr;
-  {
-    std::lock_guard<std::mutex> lock(g_lt_mutex);
-    auto it = g_lt_handles.find(dev);
-    if (it == g_lt_handles.end()) {
-      if (!lt_ok(hipblasLtCreate(&h))) return FAIRY2I_ERR_HIP;
-      g_lt_handles[dev] = h;
-    } else {
-      h = it->second;
-    }
-  }
+  const fairy2i_status hs = lt_handle(&dev, &h);
+  if (hs != FAIRY2I_OK) return hs;
   LtDescs d;
   const int32_t opT = HIPBLAS_OP_T, opN = HIPBLAS_OP_N;
   const int32_t batch = 3;
@@ -179,23 +200,58 @@ fairy2i_status lt_products(const uint16_t* Ap, const uint16_t* Bp, float* P, int
     if (it != g_lt_algos.end()) {
       algo = it->second;
     } else {
-      hipblasLtMatmulPreference_t pref = nullptr;
-      const uint64_t wsb = kLtWorkspaceBytes;
-      hipblasLtMatmulHeuristicResult_t res[1];
-      int found = 0;
-      const bool ok =
-          lt_ok(hipblasLtMatmulPreferenceCreate(&pref)) &&
-          lt_ok(hipblasLtMatmulPreferenceSetAttribute(pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES, &wsb,
-                                                      sizeof(wsb))) &&
-          lt_ok(hipblasLtMatmulAlgoGetHeuristic(h, d.op, d.a, d.b, d.c, d.c, pref, 1, res, &found));
-      if (pref) hipblasLtMatmulPreferenceDestroy(pref);
-      if (!ok || found < 1 || res[0].workspaceSize > kLtWorkspaceBytes) return FAIRY2I_ERR_UNSUPPORTED;
-      algo = res[0].algo;
+      if (!lt_pick(h, d, &algo)) return FAIRY2I_ERR_UNSUPPORTED;
       g_lt_algos[key] = algo;
     }
   }
   const float one = 1.0f, zero = 0.0f;
   if (!lt_ok(hipblasLtMatmul(h, d.op, &one, Bp, d.a, Ap, d.b, &zero, P, d.c, P, d.c, &algo, lt_ws,
+                             kLtWorkspaceBytes, s)))
+    return FAIRY2I_ERR_HIP;
+  return FAIRY2I_OK;
+}
+
+// C (row-major M x N, ld ldc, float32) = op(A) op(B), A and B bf16
+// row-major: op(A) = A (M x K, ld lda) or A^T (A stored K x M), op(B) = B
+// (K x N, ld ldb) or B^T (B stored N x K).  Column-major view for the
+// library: C^T (N x M, ld ldc) = op(B)^T op(A)^T, where the stored B is, read
+// column-major, op(B)^T itself (no transpose) or its transpose, and A alike.
+std::map<std::tuple<int, int64_t, int64_t, int64_t, int, int, int64_t, int64_t, int64_t>, hipblasLtMatmulAlgo_t>
+    g_lt_gemm_algos;
+
+fairy2i_status lt_gemm(const uint16_t* A, int64_t lda, int transA, const uint16_t* B, int64_t ldb, int transB,
+                       int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, void* lt_ws, hipStream_t s) {
+  int dev = 0;
+  hipblasLtHandle_t h = nullptr;
+  const fairy2i_status hs = lt_handle(&dev, &h);
+  if (hs != FAIRY2I_OK) return hs;
+  LtDescs d;
+  const int32_t opa = transB ? HIPBLAS_OP_T : HIPBLAS_OP_N;  // the library's A is our B
+  const int32_t opb = transA ? HIPBLAS_OP_T : HIPBLAS_OP_N;  // and its B our A
+  // stored shapes, column-major: B is N x K (no transpose) or K x N; A is K x M or M x K
+  const uint64_t ar = transB ? (uint64_t)K : (uint64_t)N, ac = transB ? (uint64_t)N : (uint64_t)K;
+  const uint64_t br = transA ? (uint64_t)M : (uint64_t)K, bc = transA ? (uint64_t)K : (uint64_t)M;
+  if (!lt_ok(hipblasLtMatmulDescCreate(&d.op, HIPBLAS_COMPUTE_32F, HIP_R_32F)) ||
+      !lt_ok(hipblasLtMatmulDescSetAttribute(d.op, HIPBLASLT_MATMUL_DESC_TRANSA, &opa, sizeof(opa))) ||
+      !lt_ok(hipblasLtMatmulDescSetAttribute(d.op, HIPBLASLT_MATMUL_DESC_TRANSB, &opb, sizeof(opb))) ||
+      !lt_ok(hipblasLtMatrixLayoutCreate(&d.a, HIP_R_16BF, ar, ac, ldb)) ||
+      !lt_ok(hipblasLtMatrixLayoutCreate(&d.b, HIP_R_16BF, br, bc, lda)) ||
+      !lt_ok(hipblasLtMatrixLayoutCreate(&d.c, HIP_R_32F, (uint64_t)N, (uint64_t)M, ldc)))
+    return FAIRY2I_ERR_HIP;
+  hipblasLtMatmulAlgo_t algo;
+  {
+    std::lock_guard<std::mutex> lock(g_lt_mutex);
+    const auto key = std::make_tuple(dev, M, N, K, transA, transB, lda, ldb, ldc);
+    auto it = g_lt_gemm_algos.find(key);
+    if (it != g_lt_gemm_algos.end()) {
+      algo = it->second;
+    } else {
+      if (!lt_pick(h, d, &algo)) return FAIRY2I_ERR_UNSUPPORTED;
+      g_lt_gemm_algos[key] = algo;
+    }
+  }
+  const float one = 1.0f, zero = 0.0f;
+  if (!lt_ok(hipblasLtMatmul(h, d.op, &one, B, d.a, A, d.b, &zero, C, d.c, C, d.c, &algo, lt_ws,
                              kLtWorkspaceBytes, s)))
     return FAIRY2I_ERR_HIP;
   return FAIRY2I_OK;
@@ -287,6 +343,20 @@ fairy2i_status fairy2i_cgemm_gauss_planar(const fairy2i_cgemm_operand* A, const 
   hipLaunchKernelGGL(gauss_combine_kernel, dim3((unsigned)bx, (unsigned)by), dim3(256), 0, s, P, M, N,
                      reinterpret_cast<float2*>(C), ldc, accumulate);
   return hipGetLastError() == hipSuccess ? FAIRY2I_OK : FAIRY2I_ERR_HIP;
+}
+
+size_t fairy2i_gemm_bf16_workspace_bytes(void) { return kLtWorkspaceBytes; }
+
+fairy2i_status fairy2i_gemm_bf16(const void* A, int64_t lda, int32_t transA, const void* B, int64_t ldb,
+                                 int32_t transB, int64_t M, int64_t N, int64_t K, float* C, int64_t ldc,
+                                 void* workspace, size_t workspace_bytes, void* stream) {
+  if (!A || !B || !C) return FAIRY2I_ERR_NULL;
+  if ((transA != 0 && transA != 1) || (transB != 0 && transB != 1)) return FAIRY2I_ERR_SHAPE;
+  if (M <= 0 || N <= 0 || K <= 0 || ldc < N) return FAIRY2I_ERR_SHAPE;
+  if (lda < (transA ? M : K) || ldb < (transB ? K : N)) return FAIRY2I_ERR_SHAPE;
+  if (!workspace || workspace_bytes < kLtWorkspaceBytes) return FAIRY2I_ERR_WORKSPACE;
+  return lt_gemm(static_cast<const uint16_t*>(A), lda, transA, static_cast<const uint16_t*>(B), ldb, transB, M, N,
+                 K, C, ldc, workspace, static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

@@ -1,0 +1,137 @@
+// Real form of a widely-linear layer for training (Sec. 3.1, Eq. UW-from-R
+// read backwards, with Eq. realify-ops): y = U x + W conj(x) is one real
+// linear map of the stacked (Re, Im) pairs, whose 2 x 2 block for output n
+// and input k is
+//     [ Re U + Re W    Im W - Im U ]
+//     [ Im U + Im W    Re U - Re W ]
+// (R11 = Re U + Re W, R12 = Im W - Im U, R21 = Im U + Im W, R22 = Re U - Re W
+// of the half-split real matrix).  With R stored interleaved (row 2n + a,
+// column 2k + b for the (a, b) entry of that block) and tokens stored as
+// (re, im) pairs, the three products of a training step are plain real
+// GEMMs of the same data in place:
+//     Y   = X R^T        (M x 2N  =  M x 2K  .  2K x 2N)
+//     G_X = G_Y R        (the gradient through the real map)
+//     G_R = G_Y^T X      (2N x 2K)
+// and G_U = G_Y^T conj(X), G_W = G_Y^T X are read off G_R's blocks:
+//     Re G_U = G_R[2n][2k] + G_R[2n+1][2k+1],  Im G_U = G_R[2n+1][2k] - G_R[2n][2k+1],
+//     Re G_W = G_R[2n][2k] - G_R[2n+1][2k+1],  Im G_W = G_R[2n][2k+1] + G_R[2n+1][2k].
+// Against Gauss's three complex products per segment (six real products of
+// M x N x K for the two segments) this is four real products' work, and the
+// operands need no planes.
+#include "common.h"
+
+namespace fairy2i {
+
+namespace {
+
+__device__ inline uint16_t bf16_rne_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// a double holding a sum of two float32 values exactly, rounded once to bf16
+// (nearest even): the float32 rounding of the double first is exact when
+// the double's value needs at most 24 bits, which two float32 summands do
+// not guarantee, so the rounding is done from the double directly.
+__device__ inline uint16_t bf16_from_double(double v) {
+  const float f = (float)v;  // nearest float32
+  // if the float32 rounding already lost bits, the bf16 tie-break could go
+  // the wrong way: correct by the sign of the remainder
+  const double r = v - (double)f;
+  uint32_t u = __float_as_uint(f);
+  const uint32_t low = u & 0xFFFFu;
+  uint32_t hi = u >> 16;
+  if (low > 0x8000u || (low == 0x8000u && (r > 0.0 ? (f > 0.0f) : (r < 0.0 ? (f < 0.0f) : (hi & 1u))))) {
+    hi += 1u;
+  }
+  return (uint16_t)hi;
+}
+
+__device__ inline float2 load_c(const void* p, int32_t dtype, int64_t i) {
+  if (dtype == FAIRY2I_ACT_BF16) {
+    const uint32_t w = static_cast<const uint32_t*>(p)[i];
+    return make_float2(__uint_as_float(w << 16), __uint_as_float(w & 0xFFFF0000u));
+  }
+  return static_cast<const float2*>(p)[i];
+}
+
+// One thread per (n, k): the block's four entries as two 32-bit words, one
+// in row 2n and one in row 2n + 1.
+__global__ __launch_bounds__(256) void realify_kernel(const void* __restrict__ U, const void* __restrict__ W,
+                                                      int32_t dtype, int64_t N, int64_t K,
+                                                      uint32_t* __restrict__ R) {
+  const int64_t total = N * K;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t n = i / K, k = i - n * K;
+    const float2 u = load_c(U, dtype, i), w = load_c(W, dtype, i);
+    const double ur = u.x, ui = u.y, wr = w.x, wi = w.y;
+    const uint32_t top = (uint32_t)bf16_from_double(ur + wr) | ((uint32_t)bf16_from_double(wi - ui) << 16);
+    const uint32_t bot = (uint32_t)bf16_from_double(ui + wi) | ((uint32_t)bf16_from_double(ur - wr) << 16);
+    R[(2 * n) * K + k] = top;      // row 2n: columns 2k, 2k + 1 (K words per row)
+    R[(2 * n + 1) * K + k] = bot;  // row 2n + 1
+  }
+}
+
+// One thread per (n, k): G_U and G_W from the block of G_R (float32 sums).
+__global__ __launch_bounds__(256) void unrealify_grad_kernel(const float2* __restrict__ GR, int64_t N, int64_t K,
+                                                             float2* __restrict__ GU, float2* __restrict__ GW) {
+  const int64_t total = N * K;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t n = i / K, k = i - n * K;
+    const float2 t = GR[(2 * n) * K + k];      // (G_R[2n][2k], G_R[2n][2k+1])
+    const float2 b = GR[(2 * n + 1) * K + k];  // (G_R[2n+1][2k], G_R[2n+1][2k+1])
+    GU[i] = make_float2(t.x + b.y, b.x - t.y);
+    GW[i] = make_float2(t.x - b.y, t.y + b.x);
+  }
+}
+
+__global__ __launch_bounds__(256) void f32_to_bf16_kernel(const float* __restrict__ in, int64_t n,
+                                                          uint16_t* __restrict__ out) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    out[i] = bf16_rne_bits(in[i]);
+}
+
+inline unsigned grid_for(int64_t n) {
+  int64_t b = (n + 255) / 256;
+  if (b > 65536) b = 65536;
+  return (unsigned)(b < 1 ? 1 : b);
+}
+
+}  // namespace
+
+}  // namespace fairy2i
+
+using namespace fairy2i;
+
+extern "C" {
+
+fairy2i_status fairy2i_wl_realify(const void* U, const void* W, int32_t dtype, int64_t N, int64_t K, void* R,
+                                  void* stream) {
+  if (!U || !W || !R) return FAIRY2I_ERR_NULL;
+  if (dtype != FAIRY2I_ACT_F32 && dtype != FAIRY2I_ACT_BF16) return FAIRY2I_ERR_DTYPE;
+  if (N <= 0 || K <= 0 || N > ((int64_t)1 << 30) / K) return FAIRY2I_ERR_SHAPE;
+  hipLaunchKernelGGL(realify_kernel, dim3(grid_for(N * K)), dim3(256), 0, static_cast<hipStream_t>(stream), U, W,
+                     dtype, N, K, static_cast<uint32_t*>(R));
+  return hipGetLastError() == hipSuccess ? FAIRY2I_OK : FAIRY2I_ERR_HIP;
+}
+
+fairy2i_status fairy2i_wl_unrealify_grad(const float* G_R, int64_t N, int64_t K, float* G_U, float* G_W,
+                                         void* stream) {
+  if (!G_R || !G_U || !G_W) return FAIRY2I_ERR_NULL;
+  if (N <= 0 || K <= 0 || N > ((int64_t)1 << 30) / K) return FAIRY2I_ERR_SHAPE;
+  hipLaunchKernelGGL(unrealify_grad_kernel, dim3(grid_for(N * K)), dim3(256), 0, static_cast<hipStream_t>(stream),
+                     reinterpret_cast<const float2*>(G_R), N, K, reinterpret_cast<float2*>(G_U),
+                     reinterpret_cast<float2*>(G_W));
+  return hipGetLastError() == hipSuccess ? FAIRY2I_OK : FAIRY2I_ERR_HIP;
+}
+
+fairy2i_status fairy2i_f32_to_bf16(const float* in, int64_t n, void* out, void* stream) {
+  if (!in || !out) return FAIRY2I_ERR_NULL;
+  if (n <= 0) return FAIRY2I_ERR_SHAPE;
+  hipLaunchKernelGGL(f32_to_bf16_kernel, dim3(grid_for(n)), dim3(256), 0, static_cast<hipStream_t>(stream), in, n,
+                     static_cast<uint16_t*>(out));
+  return hipGetLastError() == hipSuccess ? FAIRY2I_OK : FAIRY2I_ERR_HIP;
+}
+
+}  // extern "C"

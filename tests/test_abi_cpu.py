@@ -301,3 +301,30 @@ def test_probe_mfma_validation(lib):
     assert probe(binding.PROBE_MFMA_F8F4, 4, 0, P, ctypes.byref(ops), None) == binding.ERR_SHAPE
     assert probe(binding.PROBE_MFMA_I8, (1 << 20) + 1, 8, P, ctypes.byref(ops), None) == binding.ERR_SHAPE
     assert ops.value == -1.0
+
+
+def test_real_form_validation(lib):
+    """The real-form entries reject bad arguments before any launch."""
+    assert lib.fairy2i_wl_realify(None, P, binding.ACT_F32, 4, 4, P, None) == binding.ERR_NULL
+    assert lib.fairy2i_wl_realify(P, P, binding.ACT_I8, 4, 4, P, None) == binding.ERR_DTYPE
+    assert lib.fairy2i_wl_realify(P, P, binding.ACT_F32, 0, 4, P, None) == binding.ERR_SHAPE
+    assert lib.fairy2i_wl_realify(P, P, binding.ACT_BF16, 1 << 16, 1 << 15, P, None) == binding.ERR_SHAPE
+    assert lib.fairy2i_wl_unrealify_grad(P, 4, 4, None, P, None) == binding.ERR_NULL
+    assert lib.fairy2i_wl_unrealify_grad(P, 4, -1, P, P, None) == binding.ERR_SHAPE
+    assert lib.fairy2i_f32_to_bf16(P, 0, P, None) == binding.ERR_SHAPE
+    assert lib.fairy2i_f32_to_bf16(None, 8, P, None) == binding.ERR_NULL
+    wsb = lib.fairy2i_gemm_bf16_workspace_bytes()
+    assert wsb >= 1 << 20
+
+    def g(A=P, lda=64, ta=0, B=P, ldb=32, tb=0, M=16, N=32, K=64, C=P, ldc=32, ws=P, n=None):
+        return lib.fairy2i_gemm_bf16(A, lda, ta, B, ldb, tb, M, N, K, C, ldc, ws, wsb if n is None else n, None)
+    assert g(C=None) == binding.ERR_NULL
+    assert g(ta=2) == binding.ERR_SHAPE
+    assert g(M=0) == binding.ERR_SHAPE
+    assert g(lda=63) == binding.ERR_SHAPE            # op(A) = A: lda >= K
+    assert g(ta=1, lda=15) == binding.ERR_SHAPE      # A stored K x M: lda >= M
+    assert g(ldb=31) == binding.ERR_SHAPE            # op(B) = B: ldb >= N
+    assert g(tb=1, ldb=63) == binding.ERR_SHAPE      # B stored N x K: ldb >= K
+    assert g(ldc=31) == binding.ERR_SHAPE
+    assert g(n=wsb - 1) == binding.ERR_WORKSPACE
+    assert g(ws=None) == binding.ERR_WORKSPACE

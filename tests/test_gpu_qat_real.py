@@ -1,0 +1,165 @@
+"""GPU parity of the real form of the layer's training products
+(fairy2i_wl_realify, fairy2i_gemm_bf16, fairy2i_wl_unrealify_grad,
+fairy2i_f32_to_bf16) against the CPU oracle.
+
+Bars:
+* R bit-exact: the oracle's real map of the pair, R_lin(U) + R_conj(W)
+  (Eq. realify-ops, half-split blocks), interleaved and rounded once from
+  float64 to bf16; the cases include sums whose float32 rounding lands on a
+  bf16 tie the exact value is not on (rounding through float32 would go the
+  wrong way);
+* the bf16 rounding of float32 gradients bit-exact;
+* the three products (Y = X R^T, G_X = G_Y R, G_R = G_Y^T X read off as
+  G_U, G_W) within relative L2 1e-5 of the oracle's layer forward and
+  backward (complex128) on the exact layer R's bf16 values represent,
+  recovered by the oracle's Eq. (UW-from-R) map: only the float32
+  accumulation of the GEMMs differs (2K or M terms, about 1e-7 each)."""
+import numpy as np
+import pytest
+
+import oracle
+from oracle import qat as oq
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-5
+
+
+def dev(a, gpu):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).to(gpu)
+
+
+def host(t):
+    return t.detach().cpu().numpy()
+
+
+def rel_l2(got, want):
+    got = np.asarray(got, dtype=np.complex128)
+    want = np.asarray(want, dtype=np.complex128)
+    den = np.linalg.norm(want)
+    return np.linalg.norm(got - want) / (den if den > 0 else 1.0)
+
+
+def bf16_once(v):
+    """float64 -> bf16 bits, nearest with ties to even, one rounding
+    (normal range)."""
+    v = np.asarray(v, dtype=np.float64)
+    u = v.view(np.uint64)
+    a = u & np.uint64(0x7FFFFFFFFFFFFFFF)
+    r = (a + np.uint64((1 << 44) - 1) + ((a >> np.uint64(45)) & np.uint64(1))) >> np.uint64(45)
+    b = r - np.uint64((1023 - 127) << 7)
+    out = np.where(a == 0, np.uint64(0), b) | ((u >> np.uint64(48)) & np.uint64(0x8000))
+    return out.astype(np.uint16)
+
+
+def bits_to_f64(bits):
+    return (np.asarray(bits, dtype=np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def interleave(R):
+    """Half-split [[R11, R12], [R21, R22]] (2N x 2K) -> rows 2n + a and
+    columns 2k + b holding block (a, b) of (n, k)."""
+    N, K = R.shape[0] // 2, R.shape[1] // 2
+    out = np.empty_like(R)
+    out[0::2, 0::2] = R[:N, :K]
+    out[0::2, 1::2] = R[:N, K:]
+    out[1::2, 0::2] = R[N:, :K]
+    out[1::2, 1::2] = R[N:, K:]
+    return out
+
+
+def half_split(Ri):
+    N, K = Ri.shape[0] // 2, Ri.shape[1] // 2
+    return np.block([[Ri[0::2, 0::2], Ri[0::2, 1::2]], [Ri[1::2, 0::2], Ri[1::2, 1::2]]])
+
+
+def cplx(rng, *shape):
+    return rng.standard_normal(shape) + 1j * rng.standard_normal(shape)
+
+
+def bf16_pairs(z, gpu):
+    import torch
+    z = np.asarray(z, dtype=np.complex128)
+    bits = np.stack([bf16_once(z.real), bf16_once(z.imag)], axis=-1)
+    return dev(bits.view(np.int16), gpu).view(torch.bfloat16)
+
+
+def bf16_value(z):
+    z = np.asarray(z, dtype=np.complex128)
+    return bits_to_f64(bf16_once(z.real)) + 1j * bits_to_f64(bf16_once(z.imag))
+
+
+def tie_pairs():
+    """(u, w) float32 pairs whose exact sum or difference lies just off a
+    bf16 tie that float32 rounding lands on."""
+    e = 2.0 ** -30
+    return [(1 + 2 ** -8, e), (1 + 2 ** -7 + 2 ** -8, -e), (-(1 + 2 ** -8), -e), (3 * (1 + 2 ** -8), 3 * e),
+            (1 + 2 ** -8, 0.0), (1 + 2 ** -7 + 2 ** -8, 0.0)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("N,K", [(64, 96), (33, 45)])
+def test_realify_bit_exact(gpu, N, K, dtype):
+    import torch
+    import paper_2512_02901_amd as f2
+    rng = np.random.default_rng(N * 100 + K)
+    U = cplx(rng, N, K).astype(np.complex64)
+    W = cplx(rng, N, K).astype(np.complex64)
+    if dtype == "f32":
+        for j, (a, b) in enumerate(tie_pairs()):
+            U[j, 0] = np.complex64(complex(a, a))   # Re: Ur + Wr and Ur - Wr; Im: Wi - Ui, Ui + Wi
+            W[j, 0] = np.complex64(complex(b, b))
+        R = f2.wl_realify(dev(U, gpu), dev(W, gpu))
+        Uv, Wv = U.astype(np.complex128), W.astype(np.complex128)
+    else:
+        Uv, Wv = bf16_value(U), bf16_value(W)
+        R = f2.wl_realify(bf16_pairs(U, gpu), bf16_pairs(W, gpu))
+    torch.cuda.synchronize()
+    want = bf16_once(interleave(oracle.realify_lin(Uv) + oracle.realify_conj(Wv)))
+    got = host(R.view(torch.int16)).view(np.uint16)
+    np.testing.assert_array_equal(got, want)
+
+
+def test_f32_to_bf16_bit_exact(gpu):
+    import torch
+    import paper_2512_02901_amd as f2
+    rng = np.random.default_rng(5)
+    x = (rng.standard_normal((37, 29)) * np.exp(rng.uniform(-20, 20, (37, 29)))).astype(np.float32)
+    x[0, :4] = [1 + 2 ** -8, 1 + 2 ** -7 + 2 ** -8, -(1 + 2 ** -8), 0.0]
+    out = f2.f32_to_bf16(dev(x, gpu))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(out.view(torch.int16)).view(np.uint16), bf16_once(x.astype(np.float64)))
+
+
+@pytest.mark.parametrize("Bt,N,K", [(96, 128, 256), (77, 33, 45)])
+def test_real_form_products_match_oracle(gpu, Bt, N, K):
+    """Forward, input gradient and weight gradients of one layer through the
+    real form, against the oracle's layer on the layer R's bf16 values
+    represent."""
+    import torch
+    import paper_2512_02901_amd as f2
+    rng = np.random.default_rng(Bt + N + K)
+    U = (cplx(rng, N, K) * 0.05).astype(np.complex64)
+    W = (cplx(rng, N, K) * 0.05).astype(np.complex64)
+    X = cplx(rng, Bt, K)
+    GY = cplx(rng, Bt, N).astype(np.complex64)
+    R = f2.wl_realify(dev(U, gpu), dev(W, gpu))
+    Xb = bf16_pairs(X, gpu).reshape(Bt, 2 * K)
+    GYb = f2.f32_to_bf16(dev(GY, gpu)).reshape(Bt, 2 * N)
+    Y = f2.gemm_bf16(Xb, R, transB=True)
+    GX = f2.gemm_bf16(GYb, R)
+    GR = f2.gemm_bf16(GYb, Xb, transA=True)
+    GU, GW = f2.wl_unrealify_grad(GR, N, K)
+    torch.cuda.synchronize()
+    Rv = bits_to_f64(host(R.view(torch.int16)).view(np.uint16))
+    Uq, Wq = oracle.to_widely_linear_f64(half_split(Rv))
+    Xq, GYq = bf16_value(X), bf16_value(GY)
+    Y_o = oq.layer_forward(Uq, Wq, Xq)
+    GX_o, GU_o, GW_o = oq.layer_backward(Uq, Wq, Xq, GYq)
+    y = host(Y).astype(np.float64)
+    gx = host(GX).astype(np.float64)
+    assert rel_l2(y[:, 0::2] + 1j * y[:, 1::2], Y_o) <= TOL
+    assert rel_l2(gx[:, 0::2] + 1j * gx[:, 1::2], GX_o) <= TOL
+    assert rel_l2(host(GU), GU_o) <= TOL
+    assert rel_l2(host(GW), GW_o) <= TOL
