@@ -170,20 +170,21 @@ __global__ __launch_bounds__(kQatThreads) void ste_reduce_kernel(const uint8_t* 
     float2 g[16], h[16];
     const int n = ste_unit<VEC>(codes_t, G, u, nelem, c, g);
     if constexpr (!FIRST) ste_h16<VEC>(H, u, n, h);
+    // every entry predicated, no early exit: a fully unrolled loop with
+    // constant indices keeps g and h in registers
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      if (e >= n) break;
       const uint32_t k = (c >> (2 * e)) & 3u;
       const double gq_re = FIRST ? (double)g[e].x : (double)g[e].x - (double)h[e].x;
       const double gq_im = FIRST ? (double)g[e].y : (double)g[e].y - (double)h[e].y;
       const double sg = (k & 2u) ? -1.0 : 1.0;  // codes 2, 3 are -1, -i
-      if (k & 1u) {
-        s_im += sg * gq_im;
-        ++n_im;
-      } else {
-        s_re += sg * gq_re;
-        ++n_re;
-      }
+      // selects, not a branch on which sum to bump (that also puts the pair
+      // in scratch memory)
+      const bool on = e < n, odd = (k & 1u) != 0u;
+      s_im = (on && odd) ? s_im + sg * gq_im : s_im;
+      s_re = (on && !odd) ? s_re + sg * gq_re : s_re;
+      n_im += (on && odd) ? 1ull : 0ull;
+      n_re += (on && !odd) ? 1ull : 0ull;
     }
   }
   const double a = block_sum_double(s_re, shd);
@@ -198,12 +199,18 @@ __global__ __launch_bounds__(kQatThreads) void ste_reduce_kernel(const uint8_t* 
   }
 }
 
-template <bool VEC, bool FIRST>
+// NEXT: the update also forms the next (lower) stage's reduction from the H
+// it has just written (codes_n: that stage's codes), with the same threads,
+// units and order as ste_reduce_kernel, into part_n: one pass over G and H
+// instead of two per stage.
+template <bool VEC, bool FIRST, bool NEXT>
 __global__ __launch_bounds__(kQatThreads) void ste_update_kernel(const uint8_t* __restrict__ codes_t,
                                                                  const float* __restrict__ scales_t,
                                                                  const float2* __restrict__ G,
                                                                  float2* __restrict__ H, int64_t nelem,
-                                                                 const StePart* __restrict__ part, int nblk) {
+                                                                 const StePart* __restrict__ part, int nblk,
+                                                                 const uint8_t* __restrict__ codes_n,
+                                                                 StePart* __restrict__ part_n) {
   // d[axis] = (sum of the reduction blocks' partial sums) / n, formed by every
   // block alike: thread i sums partials i, i + 256, ... in order, then the
   // block's fixed-order tree, so every block (and every run) gets the same d
@@ -223,12 +230,16 @@ __global__ __launch_bounds__(kQatThreads) void ste_update_kernel(const uint8_t* 
   nb = block_sum_u64(nb, shn);
   const double s_re = (double)scales_t[0], s_im = (double)scales_t[1];
   const double d_re = na ? a / (double)na : 0.0, d_im = nb ? b / (double)nb : 0.0;
+  double x_re = 0.0, x_im = 0.0;  // the next stage's sums
+  unsigned long long xn_re = 0, xn_im = 0;
   const int64_t nunits = (nelem + 15) / 16;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < nunits; u += stride) {
-    uint32_t c;
+    uint32_t c, cn = 0u;
     float2 g[16], h[16];
     const int n = ste_unit<VEC>(codes_t, G, u, nelem, c, g);
+    if constexpr (NEXT)
+      for (int bb = 0; bb < (n + 3) / 4; ++bb) cn |= (uint32_t)codes_n[4 * u + bb] << (8 * bb);
     if constexpr (FIRST) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) h[e] = make_float2(0.0f, 0.0f);
@@ -246,13 +257,41 @@ __global__ __launch_bounds__(kQatThreads) void ste_update_kernel(const uint8_t* 
       const double nr = (double)h[e].x + (s_re * gq_re + b_re * d_re);
       const double ni = (double)h[e].y + (s_im * gq_im + b_im * d_im);
       o[e] = make_float2((float)nr, (float)ni);
+      if constexpr (NEXT) {
+        // the next stage's G_Q from the stored (float32) H, as its own reduction would read it
+        if (e < n) {
+          const uint32_t kn = (cn >> (2 * e)) & 3u;
+          const double sn = (kn & 2u) ? -1.0 : 1.0;
+          if (kn & 1u) {
+            x_im += sn * ((double)g[e].y - (double)o[e].y);
+            ++xn_im;
+          } else {
+            x_re += sn * ((double)g[e].x - (double)o[e].x);
+            ++xn_re;
+          }
+        }
+      }
     }
     if (VEC && n == 16) {
       float4* q = reinterpret_cast<float4*>(H + 16 * u);
 #pragma unroll
       for (int i = 0; i < 8; ++i) q[i] = make_float4(o[2 * i].x, o[2 * i].y, o[2 * i + 1].x, o[2 * i + 1].y);
     } else {
-      for (int e = 0; e < n; ++e) H[16 * u + e] = o[e];
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        if (e < n) H[16 * u + e] = o[e];  // constant indices: o stays in registers
+    }
+  }
+  if constexpr (NEXT) {
+    const double xa = block_sum_double(x_re, shd);
+    const double xb = block_sum_double(x_im, shd);
+    const unsigned long long xna = block_sum_u64(xn_re, shn);
+    const unsigned long long xnb = block_sum_u64(xn_im, shn);
+    if (threadIdx.x == 0) {
+      part_n[blockIdx.x].sum[0] = xa;
+      part_n[blockIdx.x].sum[1] = xb;
+      part_n[blockIdx.x].n[0] = xna;
+      part_n[blockIdx.x].n[1] = xnb;
     }
   }
 }
@@ -477,7 +516,7 @@ fairy2i_status fairy2i_qat_fake_quant(const float* M, int64_t N, int64_t K, int3
 
 size_t fairy2i_qat_ste_workspace_bytes(int64_t N, int64_t K) {
   if (N <= 0 || K <= 0 || (K % 4) != 0) return 0;
-  return (size_t)qat_blocks((N * K + 15) / 16) * sizeof(StePart);
+  return 2 * (size_t)qat_blocks((N * K + 15) / 16) * sizeof(StePart);  // this stage's partials and the next's
 }
 
 fairy2i_status fairy2i_qat_ste_backward(const uint8_t* codes, const float* scales, int32_t T, int64_t N, int64_t K,
@@ -495,17 +534,34 @@ fairy2i_status fairy2i_qat_ste_backward(const uint8_t* codes, const float* scale
   auto* H = reinterpret_cast<float2*>(g_master);
   const bool vec = ((reinterpret_cast<uintptr_t>(g_hat) | reinterpret_cast<uintptr_t>(g_master)) & 15) == 0;
   hipError_t e = hipSuccess;
+  // the last stage's reduction reads G only (H is still zero); every update
+  // but the first stage's also forms the next stage's reduction
+  StePart* cur = part;
+  StePart* nxt = part + nblk;
+  {
+    const uint8_t* ct = codes + (int64_t)(T - 1) * nbytes;
+    if (vec) hipLaunchKernelGGL((ste_reduce_kernel<true, true>), dim3(nblk), dim3(kQatThreads), 0, s, ct, G, H, nelem, cur);
+    else hipLaunchKernelGGL((ste_reduce_kernel<false, true>), dim3(nblk), dim3(kQatThreads), 0, s, ct, G, H, nelem, cur);
+    e = hipGetLastError();
+  }
   for (int t = T - 1; t >= 0 && e == hipSuccess; --t) {
     const uint8_t* ct = codes + (int64_t)t * nbytes;
+    const uint8_t* cn = t > 0 ? codes + (int64_t)(t - 1) * nbytes : nullptr;
     const bool first = t == T - 1;  // H is still zero: not read, only written
-    auto reduce = vec ? (first ? ste_reduce_kernel<true, true> : ste_reduce_kernel<true, false>)
-                      : (first ? ste_reduce_kernel<false, true> : ste_reduce_kernel<false, false>);
-    auto update = vec ? (first ? ste_update_kernel<true, true> : ste_update_kernel<true, false>)
-                      : (first ? ste_update_kernel<false, true> : ste_update_kernel<false, false>);
-    hipLaunchKernelGGL(reduce, dim3(nblk), dim3(kQatThreads), 0, s, ct, G, H, nelem, part);
-    if ((e = hipGetLastError()) != hipSuccess) break;
-    hipLaunchKernelGGL(update, dim3(nblk), dim3(kQatThreads), 0, s, ct, scales + 2 * t, G, H, nelem, part, nblk);
+    const bool next = t > 0;
+    using K = void (*)(const uint8_t*, const float*, const float2*, float2*, int64_t, const StePart*, int,
+                       const uint8_t*, StePart*);
+    const K kernels[2][2][2] = {
+        {{ste_update_kernel<false, false, false>, ste_update_kernel<false, false, true>},
+         {ste_update_kernel<false, true, false>, ste_update_kernel<false, true, true>}},
+        {{ste_update_kernel<true, false, false>, ste_update_kernel<true, false, true>},
+         {ste_update_kernel<true, true, false>, ste_update_kernel<true, true, true>}}};
+    hipLaunchKernelGGL(kernels[vec][first][next], dim3(nblk), dim3(kQatThreads), 0, s, ct, scales + 2 * t, G, H,
+                       nelem, cur, nblk, cn, nxt);
     e = hipGetLastError();
+    StePart* tmp = cur;
+    cur = nxt;
+    nxt = tmp;
   }
   return qat_status(e);
 }
