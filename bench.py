@@ -283,9 +283,14 @@ def qat_bench(f2, synth, torch, dev, T=2, tokens=4096, reps=10):
         f2.qat_ste_backward(state["u"][1], state["u"][2], GU)
         f2.qat_ste_backward(state["w"][1], state["w"][2], GW)
 
-    # real form
+    # real form: the quantiser's codes and scales are all the step needs (R is formed from them directly, W^
+    # is not written); the straight-through backward takes the same codes and scales
+    def r_quant():
+        state["u"] = (None, *f2.quantize(U, T))
+        state["w"] = (None, *f2.quantize(W, T))
+
     def r_fwd():
-        f2.wl_realify(state["u"][0], state["w"][0], out=R)
+        f2.wl_realify_codes(state["u"][1], state["u"][2], state["w"][1], state["w"][2], out=R)
         f2.gemm_bf16(Xr, R, transB=True, out=Yr, workspace=lt_ws)
 
     def r_bwd_x():
@@ -316,7 +321,7 @@ def qat_bench(f2, synth, torch, dev, T=2, tokens=4096, reps=10):
         return e0.elapsed_time(e1) / reps * 1e3
 
     def run(phases):
-        fq()
+        phases[0][1]()
         for _, fn in phases:
             fn()
         warm_up(lambda: [fn() for _, fn in phases], torch, 3)
@@ -327,9 +332,10 @@ def qat_bench(f2, synth, torch, dev, T=2, tokens=4096, reps=10):
         return res
 
     out = {"workload": f"one QAT step of a q-shaped layer (complex {N}x{K}, T={T}), {tokens} bf16 tokens",
-           "gemm_path": "real form: R (bf16 2N x 2K) from W^ each step, Y = X R^T, G_X = G_Y R, G_R = G_Y^T X as "
-                        "plain bf16 hipBLASLt GEMMs, G_U and G_W read off G_R"}
-    out.update(run([("fake_quant", fq), ("forward_gemm", r_fwd), ("input_grad_gemm", r_bwd_x),
+           "gemm_path": "real form: the masters quantised (codes and scales), R (bf16 2N x 2K) formed from them "
+                        "each step, Y = X R^T, G_X = G_Y R, G_R = G_Y^T X as plain bf16 hipBLASLt GEMMs, G_U and "
+                        "G_W read off G_R"}
+    out.update(run([("fake_quant", r_quant), ("forward_gemm", r_fwd), ("input_grad_gemm", r_bwd_x),
                     ("weight_grad_gemms", r_bwd_w), ("ste_backward", ste)]))
     # per GEMM phase (M N K = tokens x 2048 x 2048): the real form executes one real product of
     # 2 M (2N) (2K) = 8 M N K flops; the layer's two complex products are 16 M N K flops counted as 8 per

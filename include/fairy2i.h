@@ -602,14 +602,25 @@ fairy2i_status fairy2i_cgemm_gauss_planar(const fairy2i_cgemm_operand* A, const 
  * These are the products fairy2i_cgemm_gauss computes with Gauss's three
  * real products per complex product; the real form needs four real products'
  * work for both segments instead of six, and no operand planes.
+ * fairy2i_wl_realify_codes writes the same R straight from the quantised
+ * pair (canonical packed codes uint8 [T][N][K/4] and scales float32 [T][2]
+ * of U and of W, as fairy2i_quantize writes them; K % 4 == 0, R 16-byte
+ * aligned): each entry of U^ and W^ is Eq. (res-sum) summed over the stages
+ * in increasing order in double, each block entry formed from those and
+ * rounded once to bf16 (no float32 U^, W^ in between, so a training step
+ * that needs W^ only for its products can skip writing and reading it).
  * fairy2i_f32_to_bf16: out[i] = in[i] rounded to bf16 (nearest even),
  * n values, device memory.
- * Errors: FAIRY2I_ERR_NULL; FAIRY2I_ERR_DTYPE; FAIRY2I_ERR_SHAPE for
- * non-positive sizes or N K > 2^30 (realify, unrealify), n <= 0
- * (f32_to_bf16); FAIRY2I_ERR_HIP if a launch fails.
+ * Errors: FAIRY2I_ERR_NULL; FAIRY2I_ERR_DTYPE; FAIRY2I_ERR_STAGES;
+ * FAIRY2I_ERR_SHAPE for non-positive sizes or N K > 2^30 (realify,
+ * realify_codes, unrealify), K % 4 != 0 or a misaligned R (realify_codes),
+ * n <= 0 (f32_to_bf16); FAIRY2I_ERR_HIP if a launch fails.
  */
 fairy2i_status fairy2i_wl_realify(const void* U, const void* W, int32_t dtype, int64_t N, int64_t K, void* R,
                                   void* stream);
+fairy2i_status fairy2i_wl_realify_codes(const uint8_t* codes_U, const float* scales_U, const uint8_t* codes_W,
+                                        const float* scales_W, int32_t T, int64_t N, int64_t K, void* R,
+                                        void* stream);
 fairy2i_status fairy2i_wl_unrealify_grad(const float* G_R, int64_t N, int64_t K, float* G_U, float* G_W,
                                          void* stream);
 fairy2i_status fairy2i_f32_to_bf16(const float* in, int64_t n, void* out, void* stream);

@@ -10,7 +10,7 @@ from .binding import (ACT_BF16, ACT_F32, ACT_I8, LAYOUT_D3, LAYOUT_TILED, LAYOUT
                       cpu_lut_workspace_bytes, cgemm_gauss, cgemm_gauss_planar_workspace_bytes, int8_accumulators, load, qat_fake_quant,
                       probe_mfma, qat_ste_backward, quantize, quantize_grouped,
                       quantize_act_int8, repack_tiled, repack_tiled_bytes, repack_tiled_fp4, to_widely_linear,
-                      wl_matmul, wl_matmul_noalloc, wl_matmul_workspace_bytes, wl_realify, wl_unrealify_grad,
+                      wl_matmul, wl_matmul_noalloc, wl_matmul_workspace_bytes, wl_realify, wl_realify_codes, wl_unrealify_grad,
                       f32_to_bf16, gemm_bf16)
 
 __all__ = [
@@ -19,6 +19,6 @@ __all__ = [
     "Fairy2iError", "WlBlock", "WlGroup", "ACT_F32", "ACT_BF16", "ACT_I8", "LAYOUT_D3", "LAYOUT_TILED",
     "LAYOUT_TILED_FP4", "MAX_STAGES", "MAX_DECODE_BATCH", "cpu_lut_wl_matmul", "cpu_lut_workspace_bytes",
     "qat_fake_quant", "qat_ste_backward", "cgemm_gauss", "cgemm_gauss_planar_workspace_bytes",
-    "probe_mfma", "PROBE_MFMA_I8", "PROBE_MFMA_F8F4", "PROBE_MFMA_I8_32X32", "wl_realify", "wl_unrealify_grad",
+    "probe_mfma", "PROBE_MFMA_I8", "PROBE_MFMA_F8F4", "PROBE_MFMA_I8_32X32", "wl_realify", "wl_realify_codes", "wl_unrealify_grad",
     "f32_to_bf16", "gemm_bf16",
 ]

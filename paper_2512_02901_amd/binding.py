@@ -62,6 +62,7 @@ _SIGNATURES = {
                                             _c_size, _c_p]),
     "fairy2i_probe_mfma": (_c_i32, [_c_i32, _c_i32, _c_i32, _c_p, _c_p, _c_p]),
     "fairy2i_wl_realify": (_c_i32, [_c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_p]),
+    "fairy2i_wl_realify_codes": (_c_i32, [_c_p, _c_p, _c_p, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_p]),
     "fairy2i_wl_unrealify_grad": (_c_i32, [_c_p, _c_i64, _c_i64, _c_p, _c_p, _c_p]),
     "fairy2i_f32_to_bf16": (_c_i32, [_c_p, _c_i64, _c_p, _c_p]),
     "fairy2i_gemm_bf16_workspace_bytes": (_c_size, []),
@@ -179,6 +180,32 @@ def wl_realify(U, W, out=None):
     if tuple(R.shape) != (2 * N, 2 * K):
         raise ValueError("out must be [2N, 2K]")
     _check(lib.fairy2i_wl_realify(_ptr(U), _ptr(W), dt, N, K, _ptr(R), _stream_ptr(U)), "fairy2i_wl_realify")
+    return R
+
+
+def wl_realify_codes(codes_U, scales_U, codes_W, scales_W, out=None):
+    """The layer's real map R (bf16 [2N, 2K]) straight from the quantised
+    pair: canonical codes uint8 [T, N, K/4] and scales float32 [T, 2] of U
+    and of W (fairy2i_wl_realify_codes)."""
+    torch = _torch()
+    lib = load()
+    _require(codes_U, torch.uint8, "codes_U")
+    T, N, K4 = codes_U.shape
+    d = codes_U.device
+    _require(codes_W, torch.uint8, "codes_W", d)
+    for t, n in ((scales_U, "scales_U"), (scales_W, "scales_W")):
+        _require(t, torch.float32, n, d)
+        if tuple(t.shape) != (T, 2):
+            raise ValueError(f"{n} must be [T, 2]")
+    if tuple(codes_W.shape) != (T, N, K4):
+        raise ValueError("codes_W must match codes_U")
+    K = 4 * K4
+    R = torch.empty((2 * N, 2 * K), dtype=torch.bfloat16, device=d) if out is None else out
+    _require(R, torch.bfloat16, "out", d)
+    if tuple(R.shape) != (2 * N, 2 * K):
+        raise ValueError("out must be [2N, 2K]")
+    _check(lib.fairy2i_wl_realify_codes(_ptr(codes_U), _ptr(scales_U), _ptr(codes_W), _ptr(scales_W), T, N, K,
+                                        _ptr(R), _stream_ptr(codes_U)), "fairy2i_wl_realify_codes")
     return R
 
 

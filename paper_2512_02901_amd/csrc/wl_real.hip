@@ -30,14 +30,13 @@ __device__ inline uint16_t bf16_rne_bits(float f) {
   return (uint16_t)(u >> 16);
 }
 
-// a double holding a sum of two float32 values exactly, rounded once to bf16
-// (nearest even): the float32 rounding of the double first is exact when
-// the double's value needs at most 24 bits, which two float32 summands do
-// not guarantee, so the rounding is done from the double directly.
+// A double rounded once to bf16 (nearest even).  Rounding to float32 first
+// and then to bf16 goes wrong only where the float32 value is a bf16 tie
+// that the double is not on (every bf16 tie is a float32 value, so
+// elsewhere the float32 value lies on the same side of every tie as the
+// double); there the sign of the float32 rounding's remainder decides.
 __device__ inline uint16_t bf16_from_double(double v) {
   const float f = (float)v;  // nearest float32
-  // if the float32 rounding already lost bits, the bf16 tie-break could go
-  // the wrong way: correct by the sign of the remainder
   const double r = v - (double)f;
   uint32_t u = __float_as_uint(f);
   const uint32_t low = u & 0xFFFFu;
@@ -86,6 +85,49 @@ __global__ __launch_bounds__(256) void unrealify_grad_kernel(const float2* __res
   }
 }
 
+// R straight from the codes (Eq. ifairy-dequant, Eq. res-sum): one thread
+// per packed byte, i.e. four entries (n, 4 j .. 4 j + 3) of U and of W, each
+// summed over the stages in increasing order in double (as the fake-quant
+// dequantisation does), their block entries formed in double and rounded
+// once to bf16; a 16-byte store per row of the block pair.
+__global__ __launch_bounds__(256) void realify_codes_kernel(const uint8_t* __restrict__ cu,
+                                                            const float* __restrict__ su,
+                                                            const uint8_t* __restrict__ cw,
+                                                            const float* __restrict__ sw, int T, int64_t N,
+                                                            int64_t K, uint4* __restrict__ R) {
+  const int64_t nbytes = N * K / 4, kb = K / 4;
+  for (int64_t bi = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; bi < nbytes;
+       bi += (int64_t)gridDim.x * blockDim.x) {
+    double ur[4] = {0.0, 0.0, 0.0, 0.0}, ui[4] = {0.0, 0.0, 0.0, 0.0};
+    double wr[4] = {0.0, 0.0, 0.0, 0.0}, wi[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+    for (int t = 0; t < FAIRY2I_MAX_STAGES; ++t) {
+      if (t >= T) break;
+      const uint32_t bu = cu[(int64_t)t * nbytes + bi], bw = cw[(int64_t)t * nbytes + bi];
+      const double sur = (double)su[2 * t], sui = (double)su[2 * t + 1];
+      const double swr = (double)sw[2 * t], swi = (double)sw[2 * t + 1];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t ku = (bu >> (2 * e)) & 3u, kw = (bw >> (2 * e)) & 3u;
+        // i^k: 0 -> +1, 1 -> +i, 2 -> -1, 3 -> -i
+        ur[e] = ku == 0u ? ur[e] + sur : (ku == 2u ? ur[e] - sur : ur[e]);
+        ui[e] = ku == 1u ? ui[e] + sui : (ku == 3u ? ui[e] - sui : ui[e]);
+        wr[e] = kw == 0u ? wr[e] + swr : (kw == 2u ? wr[e] - swr : wr[e]);
+        wi[e] = kw == 1u ? wi[e] + swi : (kw == 3u ? wi[e] - swi : wi[e]);
+      }
+    }
+    uint32_t top[4], bot[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      top[e] = (uint32_t)bf16_from_double(ur[e] + wr[e]) | ((uint32_t)bf16_from_double(wi[e] - ui[e]) << 16);
+      bot[e] = (uint32_t)bf16_from_double(ui[e] + wi[e]) | ((uint32_t)bf16_from_double(ur[e] - wr[e]) << 16);
+    }
+    const int64_t n = bi / kb, j = bi - n * kb;
+    R[(2 * n) * kb + j] = make_uint4(top[0], top[1], top[2], top[3]);  // row 2n: K words, K / 4 uint4
+    R[(2 * n + 1) * kb + j] = make_uint4(bot[0], bot[1], bot[2], bot[3]);
+  }
+}
+
 __global__ __launch_bounds__(256) void f32_to_bf16_kernel(const float* __restrict__ in, int64_t n,
                                                           uint16_t* __restrict__ out) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
@@ -113,6 +155,18 @@ fairy2i_status fairy2i_wl_realify(const void* U, const void* W, int32_t dtype, i
   if (N <= 0 || K <= 0 || N > ((int64_t)1 << 30) / K) return FAIRY2I_ERR_SHAPE;
   hipLaunchKernelGGL(realify_kernel, dim3(grid_for(N * K)), dim3(256), 0, static_cast<hipStream_t>(stream), U, W,
                      dtype, N, K, static_cast<uint32_t*>(R));
+  return hipGetLastError() == hipSuccess ? FAIRY2I_OK : FAIRY2I_ERR_HIP;
+}
+
+fairy2i_status fairy2i_wl_realify_codes(const uint8_t* codes_U, const float* scales_U, const uint8_t* codes_W,
+                                        const float* scales_W, int32_t T, int64_t N, int64_t K, void* R,
+                                        void* stream) {
+  if (!codes_U || !scales_U || !codes_W || !scales_W || !R) return FAIRY2I_ERR_NULL;
+  if (T < 1 || T > FAIRY2I_MAX_STAGES) return FAIRY2I_ERR_STAGES;
+  if (N <= 0 || K <= 0 || K % 4 != 0 || N > ((int64_t)1 << 30) / K) return FAIRY2I_ERR_SHAPE;
+  if (reinterpret_cast<uintptr_t>(R) & 15) return FAIRY2I_ERR_SHAPE;
+  hipLaunchKernelGGL(realify_codes_kernel, dim3(grid_for(N * K / 4)), dim3(256), 0, static_cast<hipStream_t>(stream),
+                     codes_U, scales_U, codes_W, scales_W, T, N, K, static_cast<uint4*>(R));
   return hipGetLastError() == hipSuccess ? FAIRY2I_OK : FAIRY2I_ERR_HIP;
 }
 

@@ -328,3 +328,13 @@ def test_real_form_validation(lib):
     assert g(ldc=31) == binding.ERR_SHAPE
     assert g(n=wsb - 1) == binding.ERR_WORKSPACE
     assert g(ws=None) == binding.ERR_WORKSPACE
+
+
+def test_realify_codes_validation(lib):
+    rc = lib.fairy2i_wl_realify_codes
+    assert rc(None, P, P, P, 2, 4, 8, P, None) == binding.ERR_NULL
+    assert rc(P, P, P, P, 0, 4, 8, P, None) == binding.ERR_STAGES
+    assert rc(P, P, P, P, 5, 4, 8, P, None) == binding.ERR_STAGES
+    assert rc(P, P, P, P, 2, 4, 6, P, None) == binding.ERR_SHAPE        # K % 4
+    assert rc(P, P, P, P, 2, 0, 8, P, None) == binding.ERR_SHAPE
+    assert rc(P, P, P, P, 2, 4, 8, ctypes.c_void_p(0x1008), None) == binding.ERR_SHAPE   # R not 16-byte aligned

@@ -1,13 +1,14 @@
 """GPU parity of the real form of the layer's training products
-(fairy2i_wl_realify, fairy2i_gemm_bf16, fairy2i_wl_unrealify_grad,
-fairy2i_f32_to_bf16) against the CPU oracle.
+(fairy2i_wl_realify, fairy2i_wl_realify_codes, fairy2i_gemm_bf16,
+fairy2i_wl_unrealify_grad, fairy2i_f32_to_bf16) against the CPU oracle.
 
 Bars:
 * R bit-exact: the oracle's real map of the pair, R_lin(U) + R_conj(W)
   (Eq. realify-ops, half-split blocks), interleaved and rounded once from
   float64 to bf16; the cases include sums whose float32 rounding lands on a
   bf16 tie the exact value is not on (rounding through float32 would go the
-  wrong way);
+  wrong way); from codes and scales, the same with U, W the oracle's
+  Eq. (res-sum) dequantisation;
 * the bf16 rounding of float32 gradients bit-exact;
 * the three products (Y = X R^T, G_X = G_Y R, G_R = G_Y^T X read off as
   G_U, G_W) within relative L2 1e-5 of the oracle's layer forward and
@@ -163,3 +164,21 @@ def test_real_form_products_match_oracle(gpu, Bt, N, K):
     assert rel_l2(gx[:, 0::2] + 1j * gx[:, 1::2], GX_o) <= TOL
     assert rel_l2(host(GU), GU_o) <= TOL
     assert rel_l2(host(GW), GW_o) <= TOL
+
+
+@pytest.mark.parametrize("T,N,K", [(2, 48, 64), (3, 17, 36), (1, 8, 4)])
+def test_realify_codes_bit_exact(gpu, T, N, K):
+    """R straight from the quantised pair: the oracle's Eq. (res-sum)
+    dequantisation of both matrices (float64), realified and rounded once."""
+    import torch
+    import paper_2512_02901_amd as f2
+    import synth
+    A = synth.llama_weight(2 * N, 2 * K, (T, N, K))
+    U, W = oracle.to_widely_linear(A)
+    cu, su = oracle.quantize(U, T)
+    cw, sw = oracle.quantize(W, T)
+    R = f2.wl_realify_codes(dev(oracle.pack(cu), gpu), dev(su, gpu), dev(oracle.pack(cw), gpu), dev(sw, gpu))
+    torch.cuda.synchronize()
+    Uq, Wq = oracle.dequantize(cu, su), oracle.dequantize(cw, sw)
+    want = bf16_once(interleave(oracle.realify_lin(Uq) + oracle.realify_conj(Wq)))
+    np.testing.assert_array_equal(host(R.view(torch.int16)).view(np.uint16), want)
