@@ -635,12 +635,24 @@ fairy2i_status fairy2i_f32_to_bf16(const float* in, int64_t n, void* out, void* 
  * (transB = 1, ldb >= K); C: float32 M x N, ldc >= N, overwritten.
  * workspace: device buffer of at least fairy2i_gemm_bf16_workspace_bytes()
  * bytes for the library.  The library's first heuristic choice per problem
- * shape is kept for the process.
+ * shape is kept for the process, unless fairy2i_gemm_bf16_tune chose one.
  * Errors: FAIRY2I_ERR_NULL; FAIRY2I_ERR_SHAPE (sizes, transposition flags,
  * leading dimensions); FAIRY2I_ERR_WORKSPACE; FAIRY2I_ERR_UNSUPPORTED if the
  * library offers no algorithm; FAIRY2I_ERR_HIP.
  */
 size_t fairy2i_gemm_bf16_workspace_bytes(void);
+/*
+ * Tuning for fairy2i_gemm_bf16 (same arguments, C overwritten): times up to
+ * 16 of the library's candidate algorithms for the problem on `stream`
+ * (each run 2 + 5 times) and keeps the fastest for later calls of the same
+ * problem in this process; *best_us (host, may be NULL) receives its time
+ * per call.  This call SYNCHRONISES the stream (outside any graph capture);
+ * without it a problem gets the library's first heuristic choice.
+ * Errors: as fairy2i_gemm_bf16.
+ */
+fairy2i_status fairy2i_gemm_bf16_tune(const void* A, int64_t lda, int32_t transA, const void* B, int64_t ldb,
+                                      int32_t transB, int64_t M, int64_t N, int64_t K, float* C, int64_t ldc,
+                                      void* workspace, size_t workspace_bytes, float* best_us, void* stream);
 fairy2i_status fairy2i_gemm_bf16(const void* A, int64_t lda, int32_t transA, const void* B, int64_t ldb,
                                  int32_t transB, int64_t M, int64_t N, int64_t K, float* C, int64_t ldc,
                                  void* workspace, size_t workspace_bytes, void* stream);

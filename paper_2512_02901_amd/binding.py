@@ -66,6 +66,8 @@ _SIGNATURES = {
     "fairy2i_wl_unrealify_grad": (_c_i32, [_c_p, _c_i64, _c_i64, _c_p, _c_p, _c_p]),
     "fairy2i_f32_to_bf16": (_c_i32, [_c_p, _c_i64, _c_p, _c_p]),
     "fairy2i_gemm_bf16_workspace_bytes": (_c_size, []),
+    "fairy2i_gemm_bf16_tune": (_c_i32, [_c_p, _c_i64, _c_i32, _c_p, _c_i64, _c_i32, _c_i64, _c_i64, _c_i64, _c_p,
+                                        _c_i64, _c_p, _c_size, _c_p, _c_p]),
     "fairy2i_gemm_bf16": (_c_i32, [_c_p, _c_i64, _c_i32, _c_p, _c_i64, _c_i32, _c_i64, _c_i64, _c_i64, _c_p, _c_i64,
                                    _c_p, _c_size, _c_p]),
     "fairy2i_cpu_lut_workspace_bytes": (_c_size, [_c_i32, _c_i64, _c_i64, _c_i32]),
@@ -250,9 +252,11 @@ def f32_to_bf16(x, out=None):
     return out
 
 
-def gemm_bf16(A, B, transA=False, transB=False, out=None, workspace=None):
+def gemm_bf16(A, B, transA=False, transB=False, out=None, workspace=None, tune=False):
     """C (float32 M x N) = op(A) op(B) for bf16 row-major 2-D device tensors
-    (fairy2i_gemm_bf16); op(X) is X or X^T."""
+    (fairy2i_gemm_bf16); op(X) is X or X^T.  tune=True first times the
+    library's candidate algorithms for this problem (fairy2i_gemm_bf16_tune,
+    which synchronises) and keeps the fastest."""
     torch = _torch()
     lib = load()
     _require(A, torch.bfloat16, "A")
@@ -269,6 +273,10 @@ def gemm_bf16(A, B, transA=False, transB=False, out=None, workspace=None):
     if tuple(out.shape) != (M, N):
         raise ValueError("out must be M x N")
     ws, wsb = _workspace(lib.fairy2i_gemm_bf16_workspace_bytes(), workspace, A.device)
+    if tune:
+        _check(lib.fairy2i_gemm_bf16_tune(_ptr(A), A.shape[1], int(transA), _ptr(B), B.shape[1], int(transB), M, N,
+                                          K, _ptr(out), N, _ptr(ws), wsb, None, _stream_ptr(A)),
+               "fairy2i_gemm_bf16_tune")
     _check(lib.fairy2i_gemm_bf16(_ptr(A), A.shape[1], int(transA), _ptr(B), B.shape[1], int(transB), M, N, K,
                                  _ptr(out), N, _ptr(ws), wsb, _stream_ptr(A)), "fairy2i_gemm_bf16")
     return out

@@ -219,13 +219,9 @@ fairy2i_status lt_products(const uint16_t* Ap, const uint16_t* Bp, float* P, int
 std::map<std::tuple<int, int64_t, int64_t, int64_t, int, int, int64_t, int64_t, int64_t>, hipblasLtMatmulAlgo_t>
     g_lt_gemm_algos;
 
-fairy2i_status lt_gemm(const uint16_t* A, int64_t lda, int transA, const uint16_t* B, int64_t ldb, int transB,
-                       int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, void* lt_ws, hipStream_t s) {
-  int dev = 0;
-  hipblasLtHandle_t h = nullptr;
-  const fairy2i_status hs = lt_handle(&dev, &h);
-  if (hs != FAIRY2I_OK) return hs;
-  LtDescs d;
+// The descriptors of one such problem.
+bool lt_gemm_descs(LtDescs& d, int64_t lda, int transA, int64_t ldb, int transB, int64_t M, int64_t N, int64_t K,
+                   int64_t ldc) {
   const int32_t opa = transB ? HIPBLAS_OP_T : HIPBLAS_OP_N;  // the library's A is our B
   const int32_t opb = transA ? HIPBLAS_OP_T : HIPBLAS_OP_N;  // and its B our A
   // stored shapes, column-major: B is N x K (no transpose) or K x N; A is K x M or M x K
@@ -237,7 +233,18 @@ fairy2i_status lt_gemm(const uint16_t* A, int64_t lda, int transA, const uint16_
       !lt_ok(hipblasLtMatrixLayoutCreate(&d.a, HIP_R_16BF, ar, ac, ldb)) ||
       !lt_ok(hipblasLtMatrixLayoutCreate(&d.b, HIP_R_16BF, br, bc, lda)) ||
       !lt_ok(hipblasLtMatrixLayoutCreate(&d.c, HIP_R_32F, (uint64_t)N, (uint64_t)M, ldc)))
-    return FAIRY2I_ERR_HIP;
+    return false;
+  return true;
+}
+
+fairy2i_status lt_gemm(const uint16_t* A, int64_t lda, int transA, const uint16_t* B, int64_t ldb, int transB,
+                       int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, void* lt_ws, hipStream_t s) {
+  int dev = 0;
+  hipblasLtHandle_t h = nullptr;
+  const fairy2i_status hs = lt_handle(&dev, &h);
+  if (hs != FAIRY2I_OK) return hs;
+  LtDescs d;
+  if (!lt_gemm_descs(d, lda, transA, ldb, transB, M, N, K, ldc)) return FAIRY2I_ERR_HIP;
   hipblasLtMatmulAlgo_t algo;
   {
     std::lock_guard<std::mutex> lock(g_lt_mutex);
@@ -254,6 +261,69 @@ fairy2i_status lt_gemm(const uint16_t* A, int64_t lda, int transA, const uint16_
   if (!lt_ok(hipblasLtMatmul(h, d.op, &one, B, d.a, A, d.b, &zero, C, d.c, C, d.c, &algo, lt_ws,
                              kLtWorkspaceBytes, s)))
     return FAIRY2I_ERR_HIP;
+  return FAIRY2I_OK;
+}
+
+// Up to kTuneCandidates of the library's algorithms for the problem, each
+// run twice and then timed over kTuneRuns runs on the stream; the fastest
+// is kept for later calls with the same problem.
+constexpr int kTuneCandidates = 16;
+constexpr int kTuneRuns = 5;
+
+fairy2i_status lt_gemm_tune(const uint16_t* A, int64_t lda, int transA, const uint16_t* B, int64_t ldb, int transB,
+                            int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, void* lt_ws, hipStream_t s,
+                            float* best_us) {
+  int dev = 0;
+  hipblasLtHandle_t h = nullptr;
+  const fairy2i_status hs = lt_handle(&dev, &h);
+  if (hs != FAIRY2I_OK) return hs;
+  LtDescs d;
+  if (!lt_gemm_descs(d, lda, transA, ldb, transB, M, N, K, ldc)) return FAIRY2I_ERR_HIP;
+  hipblasLtMatmulPreference_t pref = nullptr;
+  const uint64_t wsb = kLtWorkspaceBytes;
+  hipblasLtMatmulHeuristicResult_t res[kTuneCandidates];
+  int found = 0;
+  const bool ok =
+      lt_ok(hipblasLtMatmulPreferenceCreate(&pref)) &&
+      lt_ok(hipblasLtMatmulPreferenceSetAttribute(pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES, &wsb, sizeof(wsb))) &&
+      lt_ok(hipblasLtMatmulAlgoGetHeuristic(h, d.op, d.a, d.b, d.c, d.c, pref, kTuneCandidates, res, &found));
+  if (pref) hipblasLtMatmulPreferenceDestroy(pref);
+  if (!ok || found < 1) return FAIRY2I_ERR_UNSUPPORTED;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) {
+    if (e0) (void)hipEventDestroy(e0);
+    return FAIRY2I_ERR_HIP;
+  }
+  const float one = 1.0f, zero = 0.0f;
+  int best = -1;
+  float best_ms = 0.0f;
+  for (int i = 0; i < found; ++i) {
+    if (res[i].workspaceSize > kLtWorkspaceBytes) continue;
+    bool run_ok = true;
+    for (int r = 0; r < 2 && run_ok; ++r)
+      run_ok = lt_ok(hipblasLtMatmul(h, d.op, &one, B, d.a, A, d.b, &zero, C, d.c, C, d.c, &res[i].algo, lt_ws,
+                                     kLtWorkspaceBytes, s));
+    if (!run_ok || hipEventRecord(e0, s) != hipSuccess) continue;
+    for (int r = 0; r < kTuneRuns && run_ok; ++r)
+      run_ok = lt_ok(hipblasLtMatmul(h, d.op, &one, B, d.a, A, d.b, &zero, C, d.c, C, d.c, &res[i].algo, lt_ws,
+                                     kLtWorkspaceBytes, s));
+    float ms = 0.0f;
+    if (!run_ok || hipEventRecord(e1, s) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
+        hipEventElapsedTime(&ms, e0, e1) != hipSuccess)
+      continue;
+    if (best < 0 || ms < best_ms) {
+      best = i;
+      best_ms = ms;
+    }
+  }
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  if (best < 0) return FAIRY2I_ERR_UNSUPPORTED;
+  {
+    std::lock_guard<std::mutex> lock(g_lt_mutex);
+    g_lt_gemm_algos[std::make_tuple(dev, M, N, K, transA, transB, lda, ldb, ldc)] = res[best].algo;
+  }
+  if (best_us) *best_us = best_ms * 1e3f / kTuneRuns;
   return FAIRY2I_OK;
 }
 
@@ -346,6 +416,18 @@ fairy2i_status fairy2i_cgemm_gauss_planar(const fairy2i_cgemm_operand* A, const 
 }
 
 size_t fairy2i_gemm_bf16_workspace_bytes(void) { return kLtWorkspaceBytes; }
+
+fairy2i_status fairy2i_gemm_bf16_tune(const void* A, int64_t lda, int32_t transA, const void* B, int64_t ldb,
+                                      int32_t transB, int64_t M, int64_t N, int64_t K, float* C, int64_t ldc,
+                                      void* workspace, size_t workspace_bytes, float* best_us, void* stream) {
+  if (!A || !B || !C) return FAIRY2I_ERR_NULL;
+  if ((transA != 0 && transA != 1) || (transB != 0 && transB != 1)) return FAIRY2I_ERR_SHAPE;
+  if (M <= 0 || N <= 0 || K <= 0 || ldc < N) return FAIRY2I_ERR_SHAPE;
+  if (lda < (transA ? M : K) || ldb < (transB ? K : N)) return FAIRY2I_ERR_SHAPE;
+  if (!workspace || workspace_bytes < kLtWorkspaceBytes) return FAIRY2I_ERR_WORKSPACE;
+  return lt_gemm_tune(static_cast<const uint16_t*>(A), lda, transA, static_cast<const uint16_t*>(B), ldb, transB, M,
+                      N, K, C, ldc, workspace, static_cast<hipStream_t>(stream), best_us);
+}
 
 fairy2i_status fairy2i_gemm_bf16(const void* A, int64_t lda, int32_t transA, const void* B, int64_t ldb,
                                  int32_t transB, int64_t M, int64_t N, int64_t K, float* C, int64_t ldc,

@@ -328,6 +328,10 @@ def test_real_form_validation(lib):
     assert g(ldc=31) == binding.ERR_SHAPE
     assert g(n=wsb - 1) == binding.ERR_WORKSPACE
     assert g(ws=None) == binding.ERR_WORKSPACE
+    tune = lib.fairy2i_gemm_bf16_tune
+    assert tune(P, 64, 0, P, 32, 0, 16, 32, 64, None, 32, P, wsb, None, None) == binding.ERR_NULL
+    assert tune(P, 63, 0, P, 32, 0, 16, 32, 64, P, 32, P, wsb, None, None) == binding.ERR_SHAPE
+    assert tune(P, 64, 0, P, 32, 0, 16, 32, 64, P, 32, P, wsb - 1, None, None) == binding.ERR_WORKSPACE
 
 
 def test_realify_codes_validation(lib):

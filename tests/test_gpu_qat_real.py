@@ -133,11 +133,12 @@ def test_f32_to_bf16_bit_exact(gpu):
     np.testing.assert_array_equal(host(out.view(torch.int16)).view(np.uint16), bf16_once(x.astype(np.float64)))
 
 
-@pytest.mark.parametrize("Bt,N,K", [(96, 128, 256), (77, 33, 45)])
-def test_real_form_products_match_oracle(gpu, Bt, N, K):
+@pytest.mark.parametrize("Bt,N,K,tune", [(96, 128, 256, False), (77, 33, 45, False), (64, 96, 160, True)])
+def test_real_form_products_match_oracle(gpu, Bt, N, K, tune):
     """Forward, input gradient and weight gradients of one layer through the
     real form, against the oracle's layer on the layer R's bf16 values
-    represent."""
+    represent (tune: each GEMM first picks its algorithm by timing the
+    library's candidates, then runs with it)."""
     import torch
     import paper_2512_02901_amd as f2
     rng = np.random.default_rng(Bt + N + K)
@@ -148,9 +149,9 @@ def test_real_form_products_match_oracle(gpu, Bt, N, K):
     R = f2.wl_realify(dev(U, gpu), dev(W, gpu))
     Xb = bf16_pairs(X, gpu).reshape(Bt, 2 * K)
     GYb = f2.f32_to_bf16(dev(GY, gpu)).reshape(Bt, 2 * N)
-    Y = f2.gemm_bf16(Xb, R, transB=True)
-    GX = f2.gemm_bf16(GYb, R)
-    GR = f2.gemm_bf16(GYb, Xb, transA=True)
+    Y = f2.gemm_bf16(Xb, R, transB=True, tune=tune)
+    GX = f2.gemm_bf16(GYb, R, tune=tune)
+    GR = f2.gemm_bf16(GYb, Xb, transA=True, tune=tune)
     GU, GW = f2.wl_unrealify_grad(GR, N, K)
     torch.cuda.synchronize()
     Rv = bits_to_f64(host(R.view(torch.int16)).view(np.uint16))
