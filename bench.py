@@ -724,6 +724,8 @@ def main():
                     help="only run the per-group-scale stack leg, G = 256 (for profiler runs)")
     ap.add_argument("--block-only", action="store_true",
                     help="only run the decoder-block leg (for profiler runs)")
+    ap.add_argument("--batch-only", type=int, default=0, metavar="B",
+                    help="only run the fp4 stack with B tokens per layer, 2..16 (for profiler runs)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run 5 plain 256 MiB device copies (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -762,6 +764,16 @@ def main():
         return
     T = 2
     t0 = time.time()
+    if args.batch_only:
+        if not 2 <= args.batch_only <= 16:
+            print("--batch-only takes 2..16 tokens per layer", file=sys.stderr)
+            sys.exit(2)
+        _, packed, _, _, _, fp4_layers = build_stack(f2, synth, torch, dev, T, random_codes=args.random_codes)
+        msb, _, prodb, _ = batch_stack_fp4(f2, torch, dev, T, fp4_layers, args.batch_only, args.steps, args.warmup)
+        print(json.dumps({f"stack_B{args.batch_only}": {
+            "ms_per_step": round(msb, 4), "GBs": round(packed / (msb * 1e-3) / 1e9, 1),
+            "product_us": round(prodb * 1e3, 1), "random_codes": args.random_codes}}), flush=True)
+        return
     grp, packed, algo, layers, grp_tiled, fp4_layers = build_stack(f2, synth, torch, dev, T,
                                                                    random_codes=args.random_codes,
                                                                    with_tiled=not args.no_extras)

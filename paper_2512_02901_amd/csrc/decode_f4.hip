@@ -996,18 +996,29 @@ __device__ inline void coop_read_x(const uint32_t (&a)[2][TS][2], v4i (&x)[2][TS
   }
 }
 
-// Four tiles: one 128-code half's eight reads and their wait (the halves one
-// after the other, so that only one half's operands are live).
+// Four tiles: one 128-code half's eight reads (the halves one after the
+// other, so that only one half's operands are live), issued without a wait;
+// coop_wait_x4<t> then waits for tile t alone (LDS reads complete in order),
+// so a tile's MFMAs start while the later tiles' reads are still served.
+// After a step's barrier every wave of the block reads the whole operand at
+// once, which keeps the LDS busy for several hundred cycles.  Tile t's
+// registers pass through its wait as in/out operands, which keeps every use
+// of them after that wait.
 __device__ inline void coop_read_x4(const uint32_t (&a)[4][2], v4i (&x)[4][2]) {
   __asm__ volatile(
       "ds_read_b128 %0, %8\n\tds_read_b128 %1, %9\n\tds_read_b128 %2, %10\n\tds_read_b128 %3, %11\n\t"
-      "ds_read_b128 %4, %12\n\tds_read_b128 %5, %13\n\tds_read_b128 %6, %14\n\tds_read_b128 %7, %15\n\t"
-      "s_waitcnt lgkmcnt(0)"
+      "ds_read_b128 %4, %12\n\tds_read_b128 %5, %13\n\tds_read_b128 %6, %14\n\tds_read_b128 %7, %15"
       : "=&v"(x[0][0]), "=&v"(x[0][1]), "=&v"(x[1][0]), "=&v"(x[1][1]), "=&v"(x[2][0]), "=&v"(x[2][1]),
         "=&v"(x[3][0]), "=&v"(x[3][1])
       : "v"(a[0][0]), "v"(a[0][1]), "v"(a[1][0]), "v"(a[1][1]), "v"(a[2][0]), "v"(a[2][1]), "v"(a[3][0]),
         "v"(a[3][1])
       : "memory");
+}
+
+template <int t>
+__device__ inline void coop_wait_x4(v4i (&x)[2]) {
+  static_assert(t >= 0 && t < 4, "four tiles");
+  __asm__ volatile("s_waitcnt lgkmcnt(%2)" : "+v"(x[0]), "+v"(x[1]) : "i"(6 - 2 * t) : "memory");
 }
 
 template <int TS>
@@ -1249,13 +1260,23 @@ __global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) v
       } else {
         if (kb == 1) coop_wait_x<TS>(xq);
       }
-      const v4i(&xr)[TS][2] = xq[TS == 4 ? 0 : kb];
+      v4i(&xr)[TS][2] = xq[TS == 4 ? 0 : kb];
 #pragma unroll
       for (int j = 0; j < PW; ++j) {
         v8i bs, bi;
         expand_f4((uint32_t)cr[j][2 * kb], (uint32_t)cr[j][2 * kb + 1], bs, bi);
 #pragma unroll
         for (int t = 0; t < TS; ++t) {
+          if constexpr (TS == 4) {
+            if (j == 0) {
+              // the earlier tiles' MFMAs stay ahead of this tile's wait
+              if (t > 0) __builtin_amdgcn_sched_barrier(0);
+              if (t == 0) coop_wait_x4<0>(xr[0]);
+              else if (t == 1) coop_wait_x4<1>(xr[1]);
+              else if (t == 2) coop_wait_x4<2>(xr[2]);
+              else coop_wait_x4<3>(xr[3]);
+            }
+          }
           const v4i x0 = xr[t][0], x1 = xr[t][1];
           const v8i a = v8i{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
           // per-group scales: every step starts from zero
