@@ -735,6 +735,10 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
+    if args.batch_only and not 2 <= args.batch_only <= 16:
+        print("--batch-only takes 2..16 tokens per layer", file=sys.stderr)
+        sys.exit(2)
+
     import torch
     if args.calibrate_copy:
         src = torch.ones(256 << 20, dtype=torch.uint8, device="cuda:0")
@@ -765,9 +769,6 @@ def main():
     T = 2
     t0 = time.time()
     if args.batch_only:
-        if not 2 <= args.batch_only <= 16:
-            print("--batch-only takes 2..16 tokens per layer", file=sys.stderr)
-            sys.exit(2)
         _, packed, _, _, _, fp4_layers = build_stack(f2, synth, torch, dev, T, random_codes=args.random_codes)
         msb, _, prodb, _ = batch_stack_fp4(f2, torch, dev, T, fp4_layers, args.batch_only, args.steps, args.warmup)
         print(json.dumps({f"stack_B{args.batch_only}": {
