@@ -968,11 +968,12 @@ __device__ inline void coop_advance(CoopCursor& c, const DecLayer* tab, const De
 }
 
 // A step's activation reads for one wave: both 128-code halves (kb) of TS
-// tiles, two 16-byte reads each, issued together; the asm waits only for the
-// first half's reads, and coop_wait_x for the rest, so the second half's LDS
-// latency hides behind the first half's MFMAs.  The second half's registers
-// pass through coop_wait_x as in/out operands, which keeps every use of them
-// after that wait.
+// tiles, two 16-byte reads each, issued together; with one tile the asm waits
+// for the first half's reads, with two the first half's tiles are waited for
+// one at a time (coop_wait_tile, as with four tiles), and coop_wait_x waits
+// for the rest, so the second half's LDS latency hides behind the first
+// half's MFMAs.  Registers that a later wait covers pass through it as
+// in/out operands, which keeps every use of them after that wait.
 template <int TS>
 __device__ inline void coop_read_x(const uint32_t (&a)[2][TS][2], v4i (&x)[2][TS][2]) {
   static_assert(TS == 1 || TS == 2, "one or two tiles per wave");
@@ -986,8 +987,7 @@ __device__ inline void coop_read_x(const uint32_t (&a)[2][TS][2], v4i (&x)[2][TS
   } else {
     __asm__ volatile(
         "ds_read_b128 %0, %8\n\tds_read_b128 %1, %9\n\tds_read_b128 %2, %10\n\tds_read_b128 %3, %11\n\t"
-        "ds_read_b128 %4, %12\n\tds_read_b128 %5, %13\n\tds_read_b128 %6, %14\n\tds_read_b128 %7, %15\n\t"
-        "s_waitcnt lgkmcnt(4)"
+        "ds_read_b128 %4, %12\n\tds_read_b128 %5, %13\n\tds_read_b128 %6, %14\n\tds_read_b128 %7, %15"
         : "=&v"(x[0][0][0]), "=&v"(x[0][0][1]), "=&v"(x[0][1][0]), "=&v"(x[0][1][1]), "=&v"(x[1][0][0]),
           "=&v"(x[1][0][1]), "=&v"(x[1][1][0]), "=&v"(x[1][1][1])
         : "v"(a[0][0][0]), "v"(a[0][0][1]), "v"(a[0][1][0]), "v"(a[0][1][1]), "v"(a[1][0][0]), "v"(a[1][0][1]),
@@ -998,7 +998,7 @@ __device__ inline void coop_read_x(const uint32_t (&a)[2][TS][2], v4i (&x)[2][TS
 
 // Four tiles: one 128-code half's eight reads (the halves one after the
 // other, so that only one half's operands are live), issued without a wait;
-// coop_wait_x4<t> then waits for tile t alone (LDS reads complete in order),
+// coop_wait_tile<6 - 2t> then waits for tile t alone (LDS reads complete in order),
 // so a tile's MFMAs start while the later tiles' reads are still served.
 // After a step's barrier every wave of the block reads the whole operand at
 // once, which keeps the LDS busy for several hundred cycles.  Tile t's
@@ -1015,10 +1015,12 @@ __device__ inline void coop_read_x4(const uint32_t (&a)[4][2], v4i (&x)[4][2]) {
       : "memory");
 }
 
-template <int t>
-__device__ inline void coop_wait_x4(v4i (&x)[2]) {
-  static_assert(t >= 0 && t < 4, "four tiles");
-  __asm__ volatile("s_waitcnt lgkmcnt(%2)" : "+v"(x[0]), "+v"(x[1]) : "i"(6 - 2 * t) : "memory");
+
+// Wait until at most N of the LDS reads issued before are outstanding (one
+// tile's two registers covered).
+template <int N>
+__device__ inline void coop_wait_tile(v4i (&x)[2]) {
+  __asm__ volatile("s_waitcnt lgkmcnt(%2)" : "+v"(x[0]), "+v"(x[1]) : "i"(N) : "memory");
 }
 
 template <int TS>
@@ -1257,8 +1259,10 @@ __global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) v
     for (int kb = 0; kb < 2; ++kb) {
       if constexpr (TS == 4) {
         coop_read_x4(xa[kb], xq[0]);
-      } else {
-        if (kb == 1) coop_wait_x<TS>(xq);
+      } else if (kb == 1) {
+        // the first half's MFMAs stay ahead of the second half's wait
+        __builtin_amdgcn_sched_barrier(0);
+        coop_wait_x<TS>(xq);
       }
       v4i(&xr)[TS][2] = xq[TS == 4 ? 0 : kb];
 #pragma unroll
@@ -1271,10 +1275,17 @@ __global__ __launch_bounds__(64 * coop_waves(NT), coop_waves(NT) == 8 ? 1 : 2) v
             if (j == 0) {
               // the earlier tiles' MFMAs stay ahead of this tile's wait
               if (t > 0) __builtin_amdgcn_sched_barrier(0);
-              if (t == 0) coop_wait_x4<0>(xr[0]);
-              else if (t == 1) coop_wait_x4<1>(xr[1]);
-              else if (t == 2) coop_wait_x4<2>(xr[2]);
-              else coop_wait_x4<3>(xr[3]);
+              if (t == 0) coop_wait_tile<6>(xr[0]);
+              else if (t == 1) coop_wait_tile<4>(xr[1]);
+              else if (t == 2) coop_wait_tile<2>(xr[2]);
+              else coop_wait_tile<0>(xr[3]);
+            }
+          } else if constexpr (TS == 2) {
+            // the first half's tiles (the second half's four reads were issued after them)
+            if (kb == 0 && j == 0) {
+              if (t > 0) __builtin_amdgcn_sched_barrier(0);
+              if (t == 0) coop_wait_tile<6>(xr[0]);
+              else coop_wait_tile<4>(xr[1]);
             }
           }
           const v4i x0 = xr[t][0], x1 = xr[t][1];
