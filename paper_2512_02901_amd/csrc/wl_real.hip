@@ -35,16 +35,16 @@ __device__ inline uint16_t bf16_rne_bits(float f) {
 // that the double is not on (every bf16 tie is a float32 value, so
 // elsewhere the float32 value lies on the same side of every tie as the
 // double); there the sign of the float32 rounding's remainder decides.
+// (Selects, no branches: at a float32 tie f is not zero, so a nonzero
+// remainder rounds away from zero exactly when it has f's sign.)
 __device__ inline uint16_t bf16_from_double(double v) {
   const float f = (float)v;  // nearest float32
   const double r = v - (double)f;
-  uint32_t u = __float_as_uint(f);
+  const uint32_t u = __float_as_uint(f);
   const uint32_t low = u & 0xFFFFu;
-  uint32_t hi = u >> 16;
-  if (low > 0x8000u || (low == 0x8000u && (r > 0.0 ? (f > 0.0f) : (r < 0.0 ? (f < 0.0f) : (hi & 1u))))) {
-    hi += 1u;
-  }
-  return (uint16_t)hi;
+  const uint32_t hi = u >> 16;
+  const uint32_t away = r != 0.0 ? (uint32_t)((r > 0.0) == (f > 0.0f)) : (hi & 1u);
+  return (uint16_t)(hi + ((uint32_t)(low > 0x8000u) | ((uint32_t)(low == 0x8000u) & away)));
 }
 
 __device__ inline float2 load_c(const void* p, int32_t dtype, int64_t i) {
@@ -62,7 +62,8 @@ __global__ __launch_bounds__(256) void realify_kernel(const void* __restrict__ U
                                                       uint32_t* __restrict__ R) {
   const int64_t total = N * K;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t n = i / K, k = i - n * K;
+    // N K <= 2^30 (checked by the host): 32-bit division
+    const int64_t n = (int64_t)((uint32_t)i / (uint32_t)K), k = i - n * K;
     const float2 u = load_c(U, dtype, i), w = load_c(W, dtype, i);
     const double ur = u.x, ui = u.y, wr = w.x, wi = w.y;
     const uint32_t top = (uint32_t)bf16_from_double(ur + wr) | ((uint32_t)bf16_from_double(wi - ui) << 16);
@@ -77,7 +78,7 @@ __global__ __launch_bounds__(256) void unrealify_grad_kernel(const float2* __res
                                                              float2* __restrict__ GU, float2* __restrict__ GW) {
   const int64_t total = N * K;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t n = i / K, k = i - n * K;
+    const int64_t n = (int64_t)((uint32_t)i / (uint32_t)K), k = i - n * K;  // N K <= 2^30
     const float2 t = GR[(2 * n) * K + k];      // (G_R[2n][2k], G_R[2n][2k+1])
     const float2 b = GR[(2 * n + 1) * K + k];  // (G_R[2n+1][2k], G_R[2n+1][2k+1])
     GU[i] = make_float2(t.x + b.y, b.x - t.y);
@@ -89,7 +90,10 @@ __global__ __launch_bounds__(256) void unrealify_grad_kernel(const float2* __res
 // per packed byte, i.e. four entries (n, 4 j .. 4 j + 3) of U and of W, each
 // summed over the stages in increasing order in double (as the fake-quant
 // dequantisation does), their block entries formed in double and rounded
-// once to bf16; a 16-byte store per row of the block pair.
+// once to bf16; a 16-byte store per row of the block pair.  A stage adds
+// s c with c in {1, 0, -1} as one fused multiply-add: the same rounding as
+// adding or subtracting s, or nothing (a sum never holds -0, and the scales
+// are not negative), without a branch on the code.
 __global__ __launch_bounds__(256) void realify_codes_kernel(const uint8_t* __restrict__ cu,
                                                             const float* __restrict__ su,
                                                             const uint8_t* __restrict__ cw,
@@ -108,12 +112,14 @@ __global__ __launch_bounds__(256) void realify_codes_kernel(const uint8_t* __res
       const double swr = (double)sw[2 * t], swi = (double)sw[2 * t + 1];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const uint32_t ku = (bu >> (2 * e)) & 3u, kw = (bw >> (2 * e)) & 3u;
-        // i^k: 0 -> +1, 1 -> +i, 2 -> -1, 3 -> -i
-        ur[e] = ku == 0u ? ur[e] + sur : (ku == 2u ? ur[e] - sur : ur[e]);
-        ui[e] = ku == 1u ? ui[e] + sui : (ku == 3u ? ui[e] - sui : ui[e]);
-        wr[e] = kw == 0u ? wr[e] + swr : (kw == 2u ? wr[e] - swr : wr[e]);
-        wi[e] = kw == 1u ? wi[e] + swi : (kw == 3u ? wi[e] - swi : wi[e]);
+        const int ku = (int)((bu >> (2 * e)) & 3u), kw = (int)((bw >> (2 * e)) & 3u);
+        // i^k: 0 -> +1, 1 -> +i, 2 -> -1, 3 -> -i: real part 1 - k for even k, imaginary part 2 - k for odd k
+        const int cur = (1 - ku) & ((ku & 1) - 1), cui = (2 - ku) & -(ku & 1);
+        const int cwr = (1 - kw) & ((kw & 1) - 1), cwi = (2 - kw) & -(kw & 1);
+        ur[e] = fma(sur, (double)cur, ur[e]);
+        ui[e] = fma(sui, (double)cui, ui[e]);
+        wr[e] = fma(swr, (double)cwr, wr[e]);
+        wi[e] = fma(swi, (double)cwi, wi[e]);
       }
     }
     uint32_t top[4], bot[4];
@@ -122,7 +128,7 @@ __global__ __launch_bounds__(256) void realify_codes_kernel(const uint8_t* __res
       top[e] = (uint32_t)bf16_from_double(ur[e] + wr[e]) | ((uint32_t)bf16_from_double(wi[e] - ui[e]) << 16);
       bot[e] = (uint32_t)bf16_from_double(ui[e] + wi[e]) | ((uint32_t)bf16_from_double(ur[e] - wr[e]) << 16);
     }
-    const int64_t n = bi / kb, j = bi - n * kb;
+    const int64_t n = (int64_t)((uint32_t)bi / (uint32_t)kb), j = bi - n * kb;  // N K / 4 <= 2^28
     R[(2 * n) * kb + j] = make_uint4(top[0], top[1], top[2], top[3]);  // row 2n: K words, K / 4 uint4
     R[(2 * n + 1) * kb + j] = make_uint4(bot[0], bot[1], bot[2], bot[3]);
   }
