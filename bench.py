@@ -724,6 +724,8 @@ def main():
                     help="only run the per-group-scale stack leg, G = 256 (for profiler runs)")
     ap.add_argument("--block-only", action="store_true",
                     help="only run the decoder-block leg (for profiler runs)")
+    ap.add_argument("--quantizer-only", action="store_true",
+                    help="only run the offline quantisation leg, q and gate shapes (for profiler runs)")
     ap.add_argument("--batch-only", type=int, default=0, metavar="B",
                     help="only run the fp4 stack with B tokens per layer, 2..16 (for profiler runs)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -758,6 +760,9 @@ def main():
         return
     if args.qat_only:
         print(json.dumps({"qat_step": qat_bench(f2, synth, torch, dev)}), flush=True)
+        return
+    if args.quantizer_only:
+        print(json.dumps({"quantizer": quantizer_bench(f2, synth, torch, dev)}), flush=True)
         return
     if args.block_only:
         print(json.dumps({"decoder_block": block_bench(f2, synth, torch, dev)}), flush=True)
