@@ -126,22 +126,24 @@ __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_kernel(DecHeader h
   }
 }
 
-// One token (two bands, one 8-column tile): one block per layer reads the
-// token once into LDS (E entries per thread, K <= E kPrepF4Threads), reduces
-// its largest magnitude and writes the digits from LDS: one round of loads
-// where the general kernel above takes two.
+// One or two tokens with two bands (one tile of 8 or 16 columns): one block
+// per layer and token reads the token once into LDS (E entries per thread,
+// K <= E kPrepF4Threads), reduces its largest magnitude and writes its 8
+// digit columns from LDS: one round of loads where the general kernel above
+// takes two.
 template <int E>
 __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_token_kernel(DecHeader h, DecLayer inl,
                                                                            const DecLayer* __restrict__ tab) {
   const DecLayer L = tab ? load_layer(tab + blockIdx.x) : inl;
-  if (h.coop_ctr && blockIdx.x == 0 && threadIdx.x == 0) *h.coop_ctr = 0u;
+  const int b = blockIdx.y;  // the token
+  if (h.coop_ctr && blockIdx.x == 0 && b == 0 && threadIdx.x == 0) *h.coop_ctr = 0u;
   __shared__ __attribute__((aligned(16))) uint32_t tokw[E * kPrepF4Threads];
   __shared__ float red[kPrepF4Threads / 64];
   __shared__ float sh_g;
   const int K = L.K, tid = threadIdx.x, wave = tid >> 6;
   const bool al4 = (reinterpret_cast<uintptr_t>(L.x) & 3) == 0;
-  const uint32_t* x32 = static_cast<const uint32_t*>(L.x);
-  const uint16_t* x16 = static_cast<const uint16_t*>(L.x);
+  const uint32_t* x32 = static_cast<const uint32_t*>(L.x) + (int64_t)b * K;
+  const uint16_t* x16 = static_cast<const uint16_t*>(L.x) + (int64_t)b * 2 * K;
   uint32_t w[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) {
@@ -169,9 +171,9 @@ __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_token_kernel(DecHe
   __syncthreads();
   const float g = sh_g;
   const int S = f4_token_shift(g);
-  if (tid == 0) L.xs[0] = g > 0.0f ? ldexpf(1.0f, -S) : 0.0f;
+  if (tid == 0) L.xs[b] = g > 0.0f ? ldexpf(1.0f, -S) : 0.0f;
   uint8_t* const dst[1] = {reinterpret_cast<uint8_t*>(L.xf)};
-  f4_encode_token<kPrepF4Threads, 1>(tokw, K, S, L.nk4, dst, 1);
+  f4_encode_token<kPrepF4Threads, 1>(tokw, K, S, L.nk4, dst, 1, h.nc, 8 * b);
 }
 
 // ------------------------------------------- streaming kernel, fp4 codes ---
@@ -1390,9 +1392,10 @@ void launch_coop_f4(const DecHeader& h, const DecLayer* tab, hipStream_t s) {
 }  // namespace
 
 void launch_f4_prep(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
-  // one token: one block per layer (its work is a latency chain, not throughput)
-  if (h.B == 1 && h.bands == 2 && h.nc == 8 && h.ntile == 1 && h.max_nk4 > 0) {
-    const dim3 g((unsigned)h.n_layers), b(kPrepF4Threads);
+  // one or two tokens: one block per layer and token (its work is a latency
+  // chain, not throughput)
+  if (h.B <= 2 && h.bands == 2 && h.nc == 8 * h.B && h.ntile == 1 && h.max_nk4 > 0) {
+    const dim3 g((unsigned)h.n_layers, (unsigned)h.B), b(kPrepF4Threads);
     const int kmax = h.max_nk4 * 256;  // entries of the longest token, padded to whole steps
     if (kmax <= 4 * kPrepF4Threads) {
       hipLaunchKernelGGL(dec_prep_f4_token_kernel<4>, g, b, 0, s, h, inl, tab);

@@ -117,14 +117,14 @@ __device__ inline void f4_store_unit(uint8_t* dst, int64_t r, int nc, int col0, 
           make_uint2(out[bd][dg][0], out[bd][dg][1]);
 }
 
-// The operand of one token for a one-token call (two bands, one 8-column
-// tile) from its bf16 (re, im) words tokw[0, K) (in LDS; K % 8 == 0) and its
-// shift S: every half run of the nk4 256-code steps (runs past K hold zeros)
-// by the block's NT threads, written to each of the ndst <= MAXD operand
-// buffers.
+// The operand of one token with two bands (8 columns, col0 .. col0 + 7 of
+// an nc-column tile) from its bf16 (re, im) words tokw[0, K) (in LDS;
+// K % 8 == 0) and its shift S: every half run of the nk4 256-code steps
+// (runs past K hold zeros) by the block's NT threads, written to each of the
+// ndst <= MAXD operand buffers.
 template <int NT, int MAXD>
 __device__ inline void f4_encode_token(const uint32_t* tokw, int K, int S, int nk4, uint8_t* const (&dst)[MAXD],
-                                       int ndst) {
+                                       int ndst, int nc = 8, int col0 = 0) {
   const int nhalf = nk4 * 32;
   for (int hr = (int)threadIdx.x; hr < nhalf; hr += NT) {
     uint32_t w8[8];
@@ -146,7 +146,7 @@ __device__ inline void f4_encode_token(const uint32_t* tokw, int K, int S, int n
       f4_unit_digits(xv, S, 2, out);
 #pragma unroll
       for (int t = 0; t < MAXD; ++t)
-        if (t < ndst) f4_store_unit(dst[t], hr >> 1, 8, 0, c, hr & 1, 2, out);
+        if (t < ndst) f4_store_unit(dst[t], hr >> 1, nc, col0, c, hr & 1, 2, out);
     }
   }
 }
