@@ -126,16 +126,18 @@ __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_kernel(DecHeader h
   }
 }
 
-// One or two tokens with two bands (one tile of 8 or 16 columns): one block
-// per layer and token reads the token once into LDS (E entries per thread,
-// K <= E kPrepF4Threads), reduces its largest magnitude and writes its 8
-// digit columns from LDS: one round of loads where the general kernel above
-// takes two.
+// Up to four tokens with two bands (one 8-column tile for one token, else
+// 16-column tiles of two): one block per layer and token slot reads the token
+// once into LDS (E entries per thread, K <= E kPrepF4Threads), reduces its
+// largest magnitude and writes its 8 digit columns from LDS: one round of
+// loads where the general kernel above takes two.  A slot past the last
+// token writes zero digits, as the general kernel does.
 template <int E>
 __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_token_kernel(DecHeader h, DecLayer inl,
                                                                            const DecLayer* __restrict__ tab) {
   const DecLayer L = tab ? load_layer(tab + blockIdx.x) : inl;
-  const int b = blockIdx.y;  // the token
+  const int b = blockIdx.y;  // the token slot: tile b / 2, columns 8 (b % 2) .. +7 of 16 (8 columns for one token)
+  const bool live = b < h.B;
   if (h.coop_ctr && blockIdx.x == 0 && b == 0 && threadIdx.x == 0) *h.coop_ctr = 0u;
   __shared__ __attribute__((aligned(16))) uint32_t tokw[E * kPrepF4Threads];
   __shared__ float red[kPrepF4Threads / 64];
@@ -149,7 +151,7 @@ __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_token_kernel(DecHe
   for (int e = 0; e < E; ++e) {
     const int i = tid + e * kPrepF4Threads;
     w[e] = 0u;
-    if (i < K) w[e] = al4 ? x32[i] : ((uint32_t)x16[2 * i] | ((uint32_t)x16[2 * i + 1] << 16));
+    if (live && i < K) w[e] = al4 ? x32[i] : ((uint32_t)x16[2 * i] | ((uint32_t)x16[2 * i + 1] << 16));
   }
   float m = 0.0f;
 #pragma unroll
@@ -171,9 +173,9 @@ __global__ __launch_bounds__(kPrepF4Threads) void dec_prep_f4_token_kernel(DecHe
   __syncthreads();
   const float g = sh_g;
   const int S = f4_token_shift(g);
-  if (tid == 0) L.xs[b] = g > 0.0f ? ldexpf(1.0f, -S) : 0.0f;
-  uint8_t* const dst[1] = {reinterpret_cast<uint8_t*>(L.xf)};
-  f4_encode_token<kPrepF4Threads, 1>(tokw, K, S, L.nk4, dst, 1, h.nc, 8 * b);
+  if (tid == 0 && live) L.xs[b] = g > 0.0f ? ldexpf(1.0f, -S) : 0.0f;
+  uint8_t* const dst[1] = {reinterpret_cast<uint8_t*>(L.xf) + (int64_t)(b >> 1) * L.nk4 * 16 * h.nc * 16};
+  f4_encode_token<kPrepF4Threads, 1>(tokw, K, S, L.nk4, dst, 1, h.nc, h.nc == 8 ? 0 : 8 * (b & 1));
 }
 
 // ------------------------------------------- streaming kernel, fp4 codes ---
@@ -1392,10 +1394,10 @@ void launch_coop_f4(const DecHeader& h, const DecLayer* tab, hipStream_t s) {
 }  // namespace
 
 void launch_f4_prep(const DecHeader& h, const DecLayer& inl, const DecLayer* tab, hipStream_t s) {
-  // one or two tokens: one block per layer and token (its work is a latency
-  // chain, not throughput)
-  if (h.B <= 2 && h.bands == 2 && h.nc == 8 * h.B && h.ntile == 1 && h.max_nk4 > 0) {
-    const dim3 g((unsigned)h.n_layers, (unsigned)h.B), b(kPrepF4Threads);
+  // up to four two-band tokens: one block per layer and token slot (its work
+  // is a latency chain, not throughput)
+  if (h.B <= 4 && h.bands == 2 && h.nc == (h.B == 1 ? 8 : 16) && h.ntile == (h.B + 1) / 2 && h.max_nk4 > 0) {
+    const dim3 g((unsigned)h.n_layers, (unsigned)(h.B == 1 ? 1 : 2 * h.ntile)), b(kPrepF4Threads);
     const int kmax = h.max_nk4 * 256;  // entries of the longest token, padded to whole steps
     if (kmax <= 4 * kPrepF4Threads) {
       hipLaunchKernelGGL(dec_prep_f4_token_kernel<4>, g, b, 0, s, h, inl, tab);
